@@ -1,0 +1,199 @@
+/*
+ * cqsa.h -- C ABI of the Stream-CQSA hot path for AMD MI355X (gfx950).
+ *
+ * Stream-CQSA (arxiv 2604.20819) splits an exact attention call into c**itr
+ * independent subsequence tasks by cyclic-quorum-set (CQS) decomposition
+ * (Section 3, Eq. 1; Section 3.3), runs a masked flash-style inner kernel on
+ * every task, and recomposes the per-task softmax statistics exactly in
+ * full-token coordinates (App. A.1, Eq. "merge"); the backward recomputes the
+ * probabilities from the global log-sum-exp (App. A.1, Eq. "globallse").
+ * The depth is the smallest one whose modelled device footprint fits the
+ * budget (Section 3.4).
+ *
+ * Conventions shared by every call
+ *   - Every call returns cqsa_status: 0 on success, a negative code on error.
+ *     No C++ exception or abort crosses this boundary.  On error the contents
+ *     of outputs are unspecified and cqsa_last_error() describes the failure.
+ *   - Tensors are dense row-major [B, L, H, d] (d fastest); the caller owns
+ *     them.  LSE and the softmax statistics are [B, H, L] fp32.
+ *   - Outputs O, dQ, dK, dV are fp32 and LSE is the natural-log log-sum-exp
+ *     of the scaled scores (Section 4.1: statistics, merge and output are
+ *     fp32; App. A.1: lse = m + log l).
+ *   - Inputs are fp32, fp16 or bf16; head dimension d is 64 or 128.
+ *   - Calls on device-resident outputs are ordered on `hip_stream` (a
+ *     hipStream_t; NULL = the null stream) and return without waiting;
+ *     a call with any host-resident output blocks until it is complete.
+ *   - The library is thread-safe for distinct plans and streams; a plan is
+ *     immutable after creation and may be shared.
+ */
+#ifndef CQSA_H
+#define CQSA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  CQSA_OK = 0,
+  CQSA_ERR_INVALID_ARG = -1, /* bad pointer, shape, dtype or option; no device work done */
+  CQSA_ERR_UNSUPPORTED = -2, /* valid but not built (e.g. d not in {64,128}) */
+  CQSA_ERR_BUDGET = -3,      /* no depth <= max_depth fits the device budget */
+  CQSA_ERR_DEVICE_OOM = -4,  /* a device allocation failed */
+  CQSA_ERR_HIP = -5,         /* a HIP runtime call failed (no device, launch error, ...) */
+  CQSA_ERR_INTERNAL = -6
+} cqsa_status;
+
+typedef enum { CQSA_F32 = 0, CQSA_F16 = 1, CQSA_BF16 = 2 } cqsa_dtype;
+typedef enum { CQSA_MEM_HOST = 0, CQSA_MEM_DEVICE = 1 } cqsa_mem;
+
+/* A caller-owned tensor: `data` points at element [0,0,0,0] of a dense
+ * row-major [B, L, H, d] array of `dtype`, in host memory (pinned memory is
+ * recommended, pageable works) or device memory as `where` says. */
+typedef struct {
+  void* data;
+  cqsa_dtype dtype;
+  cqsa_mem where;
+  int64_t B, L, H, d;
+} cqsa_tensor;
+
+#define CQSA_MAX_INTEREST 16
+
+/* Planning options.  cqsa_plan_opts_default() fills the defaults noted here. */
+typedef struct {
+  int32_t B;                 /* batch size (1) */
+  cqsa_dtype dtype;          /* input dtype (CQSA_BF16) */
+  int32_t c;                 /* chunk count, c = l(l-1)+1 (7) */
+  int32_t l;                 /* interest-set size (3) */
+  int32_t interest[CQSA_MAX_INTEREST]; /* perfect (c,l,1) difference set ({0,1,3}); App. C */
+  int32_t depth;             /* -1: automatic (smallest fitting depth >= min_depth); >= 0: forced (-1) */
+  int32_t min_depth;         /* first depth the automatic search tries (1, the paper's auto*) */
+  int32_t max_depth;         /* last depth the automatic search tries (4) */
+  int32_t n_slots;           /* staging slots in flight, >= 1 (2) */
+  int32_t inputs_on_device;  /* 1: Q, K, V (and dO) are device-resident; 0: host-resident (1) */
+  int32_t acc_on_device;     /* 1: accumulator/outputs on device; 0: on host, merged by host threads (1) */
+  int32_t with_backward;     /* 1: the footprint must also fit cqsa_backward (0) */
+} cqsa_plan_opts;
+
+/* One contiguous run of a task's tokens: global tokens
+ * [global_start, global_start + length) all carrying group `bits`. */
+typedef struct {
+  int64_t global_start;
+  int64_t length;
+  uint32_t bits;
+} cqsa_run;
+
+/* Read-only view of one task (Alg. 3 entry).  Pointers stay valid until the
+ * plan is destroyed.  Local token order equals global order (App. A.3).
+ * Group bit numbering: at level t (1-based) the chunk (q_t + interest[j]) mod c,
+ * j = 1..l-1, carries bit (t-1)*(l-1) + (j-1); the owner chunk q_t carries none.
+ * A local pair (q, k) is kept iff (bits[q] & bits[k]) == 0 (App. A.2), and, when
+ * causal, global(k) <= global(q). */
+typedef struct {
+  int64_t index;             /* position in the plan's task list (lexicographic quorum order) */
+  int32_t depth;
+  const int32_t* quorum;     /* `depth` entries q_1..q_depth */
+  int64_t L_local;           /* tokens in the task */
+  int32_t n_runs;
+  const cqsa_run* runs;      /* ascending global order */
+  int64_t n_blocks;          /* ceil(L_local / 64) */
+  const uint32_t* block_or;  /* per 64-token local block: OR of the bits (App. A.2) */
+  const uint32_t* block_and; /* per 64-token local block: AND of the bits */
+} cqsa_task;
+
+typedef struct cqsa_plan_s cqsa_plan_t;
+
+/* Per-call statistics (cqsa_last_stats).  Stage times are filled only when
+ * timing is enabled (cqsa_set_timing); they come from HIP events recorded on
+ * the stream each stage runs on. */
+typedef struct {
+  int32_t depth;
+  int64_t num_tasks;
+  uint64_t modelled_device_bytes;   /* the plan's footprint model */
+  uint64_t workspace_bytes;         /* device bytes the library held for the call */
+  uint64_t h2d_bytes, d2h_bytes, d2d_bytes; /* bytes staged across the host link / on device */
+  int64_t inner_launches;           /* inner-kernel launches (forward or backward) */
+  double ms_wall;                   /* first enqueue to completion, device clock */
+  double ms_stage;                  /* sum of staging copy spans */
+  double ms_inner;                  /* sum of inner forward (or backward) kernel spans */
+  double ms_merge;                  /* sum of recompose (device) or host-merge spans */
+  double ms_finalize;               /* finalize (forward) or preprocess (backward) span */
+  double ms_d2h;                    /* sum of statistics device-to-host spans */
+  int64_t tiles_full, tiles_clear, tiles_mixed; /* 128x128 tile census of the plan */
+} cqsa_run_stats;
+
+/* Fill `o` with the defaults listed in cqsa_plan_opts. */
+void cqsa_plan_opts_default(cqsa_plan_opts* o);
+
+/* Plan a call on L tokens, H heads, head dim d (Section 3.4; Alg. 3).
+ * device_budget_bytes = 0 means uncapped.  opts = NULL uses the defaults.
+ * Validates (c, l, interest) as a perfect difference set (App. C).  With an
+ * automatic depth, returns the smallest depth in [min_depth, max_depth] whose
+ * modelled device footprint fits the budget, else CQSA_ERR_BUDGET; a forced
+ * depth is planned even if it does not fit (the footprint is still reported).
+ * Host only: no device work.  *out receives a plan the caller must destroy. */
+cqsa_status cqsa_plan(int64_t L, int32_t H, int32_t d, int32_t causal,
+                      uint64_t device_budget_bytes, const cqsa_plan_opts* opts,
+                      cqsa_plan_t** out);
+int32_t cqsa_plan_depth(const cqsa_plan_t* plan);          /* -1 if plan is NULL */
+int64_t cqsa_plan_num_tasks(const cqsa_plan_t* plan);      /* -1 if plan is NULL */
+/* Fill *out with task t's view; CQSA_ERR_INVALID_ARG if t is out of range. */
+cqsa_status cqsa_plan_get_task(const cqsa_plan_t* plan, int64_t t, cqsa_task* out);
+/* Modelled peak device bytes of a call under this plan: caller tensors that are
+ * device-resident plus everything the library allocates. 0 if plan is NULL. */
+uint64_t cqsa_plan_modelled_device_bytes(const cqsa_plan_t* plan);
+/* Pooled 128x128 tile census over causal-retained tiles of every task (App. A.2). */
+cqsa_status cqsa_plan_tile_census(const cqsa_plan_t* plan, int64_t* full, int64_t* clear,
+                                  int64_t* mixed);
+void cqsa_plan_destroy(cqsa_plan_t* plan);                 /* NULL is a no-op */
+
+/* Decomposed forward (Alg. 1 computed with the max-shifted merge of App. A.1).
+ * Q, K, V: inputs matching the plan (B, L, H, d, dtype, and residency
+ * inputs_on_device).  O: fp32 [B, L, H, d], where = acc_on_device ? device : host.
+ * LSE: fp32 [B, H, L] in `lse_where` memory (must equal O's residency).
+ * scale <= 0 selects 1/sqrt(d) (Section 3.1).  Device-resident outputs are
+ * written in stream order on hip_stream; host-resident outputs are complete
+ * on return. */
+cqsa_status cqsa_forward(const cqsa_plan_t* plan, const cqsa_tensor* Q, const cqsa_tensor* K,
+                         const cqsa_tensor* V, cqsa_tensor* O, float* LSE, cqsa_mem lse_where,
+                         float scale, void* hip_stream);
+
+/* Decomposed backward in the global-LSE form (App. A.1, Eq. "globallse"),
+ * equal to Alg. 2.  Q, K, V, dO: inputs matching the plan; O, LSE: the
+ * forward's outputs; dQ, dK, dV: fp32 [B, L, H, d], overwritten.  This build
+ * supports device-resident tensors only (CQSA_ERR_UNSUPPORTED otherwise) and a
+ * plan made with with_backward = 1 or an uncapped budget. */
+cqsa_status cqsa_backward(const cqsa_plan_t* plan, const cqsa_tensor* Q, const cqsa_tensor* K,
+                          const cqsa_tensor* V, const cqsa_tensor* O, const float* LSE,
+                          cqsa_mem lse_where, const cqsa_tensor* dO, cqsa_tensor* dQ,
+                          cqsa_tensor* dK, cqsa_tensor* dV, float scale, void* hip_stream);
+
+/* Route the library's device workspace through a caller allocator (e.g. a
+ * framework's caching allocator).  alloc(bytes, ctx) returns device memory or
+ * NULL (reported as CQSA_ERR_DEVICE_OOM); release(ptr, ctx) frees it.  Passing
+ * NULL functions restores the built-in cached hipMalloc workspace. */
+cqsa_status cqsa_set_allocator(void* (*alloc)(size_t bytes, void* ctx),
+                               void (*release)(void* ptr, void* ctx), void* ctx);
+
+/* Enable (1) or disable (0) per-stage HIP-event timing for later calls on
+ * this thread. */
+cqsa_status cqsa_set_timing(int32_t enable);
+
+/* Statistics of the last cqsa_forward/cqsa_backward on this thread; waits for
+ * that call's timing events to complete. */
+cqsa_status cqsa_last_stats(cqsa_run_stats* out);
+
+/* Free the built-in workspace cache of the current device. */
+cqsa_status cqsa_release_workspace(void);
+
+/* Thread-local description of the last error; valid until the next call on
+ * this thread.  Never NULL. */
+const char* cqsa_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CQSA_H */

@@ -1,0 +1,398 @@
+// Inner forward kernels: masked flash-style attention over one CQS task.
+//
+// Each work group owns a 128-query strip of one (batch, head) and walks the
+// task's 64-key tiles with an online softmax, emitting the local statistics
+// (unnormalised acc, row max m, row sum l) that the max-shifted merge of
+// App. A.1 (Eq. "merge") recomposes across tasks.
+//
+// Tile verdicts (App. A.2): from the 64-token block summaries a (strip, key
+// tile) pair is fully masked (AND(rows) & AND(cols) != 0, or causally empty),
+// clear (OR(rows) & OR(cols) == 0 and causally full) or mixed; fully masked
+// tiles are never loaded, clear tiles run without any mask work, and only
+// mixed tiles apply the per-element test bits[q] & bits[k] == 0.  Because
+// tokens are gathered in ascending order, the causal test is on local indices.
+//
+// gfx950 design: S^T = K Q^T on v_mfma_f32_32x32x16 so each lane owns one
+// query column and its row statistics stay in-lane (one permlane32 swap per
+// tile); P^T feeds O^T = V^T P^T directly from registers, and V^T operands come
+// from row-major LDS through ds_read_b64_tr_b16.  Running maxima are rounded
+// up to integers in the log2 domain, so every rescale is an exact power of two
+// and 16-bit P is rounded identically whichever task, or the undecomposed
+// call, produced it.
+#include "hip_common.hpp"
+#include "kernels.hpp"
+
+namespace cqsa {
+
+__device__ __forceinline__ uint32_t run_bits(const DevRun* runs, int n, int64_t local) {
+  for (int i = 0; i < n; ++i)
+    if (local < runs[i].local_start + runs[i].length) return runs[i].bits;
+  return 0u;
+}
+
+template <typename E, int D, int MODE>
+__global__ void __launch_bounds__(256, 2) attn_fwd_mfma(const FwdArgs a) {
+  constexpr int BM = 128, BN = 64;
+  constexpr int KP = D * 2 + 16;  // K row pitch (bytes): conflict-free 16-byte reads
+  constexpr int VP = D * 2 + 64;  // V row pitch (bytes): conflict-free transpose reads
+  constexpr int KBYTES = BN * KP, VBYTES = BN * VP, STAGE = KBYTES + VBYTES;
+  constexpr int DK = D / 16;             // k-steps of S^T = K Q^T
+  constexpr int DB = D / 32;             // 32-wide d blocks of O^T
+  constexpr int CHUNKS = D / 8;          // 16-byte chunks per row
+  constexpr int RPP = 256 / CHUNKS;      // rows per load pass
+  constexpr int PASSES = BN / RPP;
+  typedef typename E::vec8 vec8;
+
+  __shared__ __attribute__((aligned(16))) char smem[2 * STAGE];
+  __shared__ uint32_t kbits_s[2][BN];
+  __shared__ DevRun runs_s[kMaxRuns];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5;
+  const int L = a.L;
+  const int64_t nstrips = (L + BM - 1) / BM;
+  const int64_t work = xcd_remap(blockIdx.x, nstrips * a.H * a.B);
+  const int strip = int(work % nstrips);
+  const int h = int((work / nstrips) % a.H);
+  const int b = int(work / (nstrips * a.H));
+
+  for (int i = tid; i < a.n_runs; i += 256) runs_s[i] = ((const DevRun*)a.runs)[i];
+
+  const int64_t rs = int64_t(a.H) * D;  // elements between consecutive tokens
+  const int64_t base = (int64_t(b) * a.seq_rows + a.row0) * rs + int64_t(h) * D;
+  const uint16_t* Qg = (const uint16_t*)a.q + base;
+  const uint16_t* Kg = (const uint16_t*)a.k + base;
+  const uint16_t* Vg = (const uint16_t*)a.v + base;
+  const float c = a.scale_log2;
+  const bool causal = a.causal != 0;
+
+  const int q0w = strip * BM + wave * 32;  // first query of this wave
+  const int myq = q0w + (lane & 31);
+  const bool qvalid = myq < L;
+
+  vec8 qf[DK];
+#pragma unroll
+  for (int ks = 0; ks < DK; ++ks) {
+    u32x4 u = {0u, 0u, 0u, 0u};
+    if (qvalid) u = *(const u32x4*)(Qg + int64_t(myq) * rs + ks * 16 + half * 8);
+    qf[ks] = bitcast_u4<vec8>(u);
+  }
+
+  // block summaries of the strip and of this wave's queries
+  const int lastq_wg = (strip * BM + BM < L ? strip * BM + BM : L) - 1;
+  const int qb0 = strip * 2, qb1 = lastq_wg / 64;
+  const uint32_t qor = a.blk_or[qb0] | a.blk_or[qb1];
+  const uint32_t qand = a.blk_and[qb0] & a.blk_and[qb1];
+  const bool wave_live = q0w < L;
+  const int wq1 = wave_live ? (q0w + 31 < L ? q0w + 31 : L - 1) : 0;
+  const uint32_t wor = wave_live ? a.blk_or[q0w / 64] : 0u;
+  const uint32_t wand = wave_live ? a.blk_and[q0w / 64] : 0u;
+
+  const int nkt = (L + BN - 1) / BN;
+  auto full_wg = [&](int kt) -> bool {
+    if (causal && kt * BN > lastq_wg) return true;
+    return (qand & a.blk_and[kt]) != 0u;
+  };
+  auto next_live = [&](int kt) -> int {
+    while (kt < nkt) {
+      if (causal && kt * BN > lastq_wg) return nkt;
+      if (!full_wg(kt)) return kt;
+      ++kt;
+    }
+    return nkt;
+  };
+
+  u32x4 kreg[PASSES], vreg[PASSES];
+  auto gload = [&](int kt) {
+#pragma unroll
+    for (int p = 0; p < PASSES; ++p) {
+      const int row = p * RPP + tid / CHUNKS, ch = tid % CHUNKS;
+      const int key = kt * BN + row;
+      u32x4 zk = {0u, 0u, 0u, 0u}, zv = {0u, 0u, 0u, 0u};
+      if (key < L) {
+        zk = *(const u32x4*)(Kg + int64_t(key) * rs + ch * 8);
+        zv = *(const u32x4*)(Vg + int64_t(key) * rs + ch * 8);
+      }
+      kreg[p] = zk;
+      vreg[p] = zv;
+    }
+  };
+  auto sstore = [&](int buf, int kt) {
+    char* kb = smem + buf * STAGE;
+    char* vb = kb + KBYTES;
+#pragma unroll
+    for (int p = 0; p < PASSES; ++p) {
+      const int row = p * RPP + tid / CHUNKS, ch = tid % CHUNKS;
+      *(u32x4*)(kb + row * KP + ch * 16) = kreg[p];
+      *(u32x4*)(vb + row * VP + ch * 16) = vreg[p];
+    }
+    // group bits of the tile's keys, only when the CQS mask can bite here
+    if ((qor & a.blk_or[kt]) != 0u && tid < BN) {
+      const int key = kt * BN + tid;
+      kbits_s[buf][tid] = key < L ? run_bits(runs_s, a.n_runs, key) : 0u;
+    }
+  };
+
+  f32x16 o[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) o[db][r] = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;
+
+  __syncthreads();  // runs_s visible
+  const uint32_t qbits = qvalid ? run_bits(runs_s, a.n_runs, myq) : 0u;
+
+  int kt = next_live(0);
+  if (kt < nkt) {
+    gload(kt);
+    sstore(0, kt);
+  }
+  int buf = 0;
+  while (kt < nkt) {
+    const int kn = next_live(kt + 1);
+    if (kn < nkt) gload(kn);
+    __syncthreads();
+
+    // ---- compute on tile kt (wave-uniform verdict) ----
+    const uint32_t kor = a.blk_or[kt], kand = a.blk_and[kt];
+    const int k0 = kt * BN, k1 = (k0 + BN - 1 < L ? k0 + BN - 1 : L - 1);
+    const bool wfull = !wave_live || (wand & kand) != 0u || (causal && k0 > wq1);
+    if (!wfull) {
+      const bool wclear = (wor & kor) == 0u && (!causal || k1 <= q0w) && (k0 + BN <= L);
+      const bool use_bits = (qor & kor) != 0u;
+      const char* Kb = smem + buf * STAGE;
+      const char* Vb = Kb + KBYTES;
+      f32x16 s[2];
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s[kb][r] = 0.f;
+#pragma unroll
+        for (int ks = 0; ks < DK; ++ks) {
+          const u32x4 ka = *(const u32x4*)(Kb + (32 * kb + (lane & 31)) * KP + (16 * ks + 8 * half) * 2);
+          s[kb] = mfma32<E>(bitcast_u4<vec8>(ka), qf[ks], s[kb]);
+        }
+      }
+      if (!wclear) {
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int kl = 32 * kb + 8 * (r >> 2) + 4 * half + (r & 3);
+            const int key = k0 + kl;
+            bool keep = key < L && (!causal || key <= myq);
+            if (use_bits) keep = keep && ((kbits_s[buf][kl] & qbits) == 0u);
+            if (!keep) s[kb][r] = -INFINITY;
+          }
+      }
+      float smax = -INFINITY;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) smax = fmaxf(smax, s[kb][r]);
+      smax = fmaxf(smax, swap_halves(smax));
+      const float mnew = fmaxf(m_run, ceilf(smax * c));
+      const float msafe = mnew == -INFINITY ? 0.f : mnew;
+      const float alpha = fast_exp2(m_run - msafe);
+      m_run = mnew;
+      l_run *= alpha;
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
+      float psum = 0.f;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float p = fast_exp2(fmaf(s[kb][r], c, -msafe));
+          s[kb][r] = p;
+          psum += p;
+        }
+      l_run += psum;
+#pragma unroll
+      for (int ks2 = 0; ks2 < 4; ++ks2) {
+        const int kb = ks2 >> 1, sub = ks2 & 1;
+        float pv[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) pv[e] = s[kb][8 * sub + e];
+        const vec8 pb = pack8<E>(pv);
+        const int row = 32 * kb + 16 * sub + 4 * half + ((lane & 15) >> 2);
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+          const int col = 32 * db + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+          const char* p0 = Vb + row * VP + col * 2;
+          const vec8 va = lds_tr_pair<E>(p0, p0 + 8 * VP);
+          o[db] = mfma32<E>(va, pb, o[db]);
+        }
+      }
+    }
+    // ---- stage the next tile into the other buffer ----
+    if (kn < nkt) sstore(buf ^ 1, kn);
+    buf ^= 1;
+    kt = kn;
+  }
+
+  const float l_tot = l_run + swap_halves(l_run);
+  if (!qvalid) return;
+  if (MODE == kModeStats) {
+    float* accp = a.acc + (int64_t(b) * L + myq) * rs + int64_t(h) * D;
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        f32x4 v = {o[db][4 * i], o[db][4 * i + 1], o[db][4 * i + 2], o[db][4 * i + 3]};
+        *(f32x4*)(accp + 32 * db + 8 * i + 4 * half) = v;
+      }
+    if (half == 0) {
+      const int64_t si = (int64_t(b) * a.H + h) * L + myq;
+      a.m[si] = m_run;
+      a.l[si] = l_tot;
+    }
+  } else {
+    const float inv = 1.f / l_tot;
+    float* op = a.acc + (int64_t(b) * a.out_rows + myq) * rs + int64_t(h) * D;
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        f32x4 v = {o[db][4 * i] * inv, o[db][4 * i + 1] * inv, o[db][4 * i + 2] * inv,
+                   o[db][4 * i + 3] * inv};
+        *(f32x4*)(op + 32 * db + 8 * i + 4 * half) = v;
+      }
+    if (half == 0) {
+      const int64_t si = (int64_t(b) * a.H + h) * a.out_rows + myq;
+      a.m[si] = (m_run + __log2f(l_tot)) * 0.69314718055994530942f;
+    }
+  }
+}
+
+// fp32 inputs: plain VALU flash loop (8 threads per query, d/8 dims each).
+// Same statistics convention as the MFMA kernel (log2 domain, integer max).
+template <int D, int MODE>
+__global__ void __launch_bounds__(256) attn_fwd_f32(const FwdArgs a) {
+  constexpr int QPB = 32, BN = 32, SL = D / 8;
+  __shared__ float ks_[BN][D + 1];
+  __shared__ float vs_[BN][D + 1];
+  __shared__ uint32_t kbits_s[BN];
+  __shared__ DevRun runs_s[kMaxRuns];
+  const int tid = threadIdx.x, sub = tid & 7, ql = tid >> 3;
+  const int L = a.L;
+  const int64_t nstrips = (L + QPB - 1) / QPB;
+  const int64_t work = blockIdx.x;
+  const int strip = int(work % nstrips);
+  const int h = int((work / nstrips) % a.H);
+  const int b = int(work / (nstrips * a.H));
+  for (int i = tid; i < a.n_runs; i += 256) runs_s[i] = ((const DevRun*)a.runs)[i];
+  const int64_t rs = int64_t(a.H) * D;
+  const int64_t base = (int64_t(b) * a.seq_rows + a.row0) * rs + int64_t(h) * D;
+  const float* Qg = (const float*)a.q + base;
+  const float* Kg = (const float*)a.k + base;
+  const float* Vg = (const float*)a.v + base;
+  const float c = a.scale_log2;
+  const int myq = strip * QPB + ql;
+  const bool qvalid = myq < L;
+  float q[SL], o[SL];
+#pragma unroll
+  for (int i = 0; i < SL; ++i) {
+    q[i] = qvalid ? Qg[int64_t(myq) * rs + sub * SL + i] : 0.f;
+    o[i] = 0.f;
+  }
+  __syncthreads();
+  const uint32_t qbits = qvalid ? run_bits(runs_s, a.n_runs, myq) : 0u;
+  float m_run = -INFINITY, l_run = 0.f;
+  const int nkt = (L + BN - 1) / BN;
+  for (int kt = 0; kt < nkt; ++kt) {
+    __syncthreads();
+    for (int i = tid; i < BN * D; i += 256) {
+      const int r = i / D, dd = i % D, key = kt * BN + r;
+      ks_[r][dd] = key < L ? Kg[int64_t(key) * rs + dd] : 0.f;
+      vs_[r][dd] = key < L ? Vg[int64_t(key) * rs + dd] : 0.f;
+    }
+    if (tid < BN) {
+      const int key = kt * BN + tid;
+      kbits_s[tid] = key < L ? run_bits(runs_s, a.n_runs, key) : 0xFFFFFFFFu;
+    }
+    __syncthreads();
+    float s[BN];
+    float smax = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < BN; ++j) {
+      float part = 0.f;
+#pragma unroll
+      for (int i = 0; i < SL; ++i) part = fmaf(q[i], ks_[j][sub * SL + i], part);
+      part += __shfl_xor(part, 1);
+      part += __shfl_xor(part, 2);
+      part += __shfl_xor(part, 4);
+      const int key = kt * BN + j;
+      const bool keep = key < L && (!a.causal || key <= myq) && (kbits_s[j] & qbits) == 0u;
+      s[j] = keep ? part : -INFINITY;
+      smax = fmaxf(smax, s[j]);
+    }
+    const float mnew = fmaxf(m_run, ceilf(smax * c));
+    const float msafe = mnew == -INFINITY ? 0.f : mnew;
+    const float alpha = exp2f(m_run - msafe);
+    m_run = mnew;
+    l_run *= alpha;
+#pragma unroll
+    for (int i = 0; i < SL; ++i) o[i] *= alpha;
+#pragma unroll
+    for (int j = 0; j < BN; ++j) {
+      const float p = exp2f(fmaf(s[j], c, -msafe));
+      l_run += p;
+#pragma unroll
+      for (int i = 0; i < SL; ++i) o[i] = fmaf(p, vs_[j][sub * SL + i], o[i]);
+    }
+  }
+  if (!qvalid) return;
+  if (MODE == kModeStats) {
+    float* accp = a.acc + (int64_t(b) * L + myq) * rs + int64_t(h) * D + sub * SL;
+#pragma unroll
+    for (int i = 0; i < SL; ++i) accp[i] = o[i];
+    if (sub == 0) {
+      const int64_t si = (int64_t(b) * a.H + h) * L + myq;
+      a.m[si] = m_run;
+      a.l[si] = l_run;
+    }
+  } else {
+    const float inv = 1.f / l_run;
+    float* op = a.acc + (int64_t(b) * a.out_rows + myq) * rs + int64_t(h) * D + sub * SL;
+#pragma unroll
+    for (int i = 0; i < SL; ++i) op[i] = o[i] * inv;
+    if (sub == 0) {
+      const int64_t si = (int64_t(b) * a.H + h) * a.out_rows + myq;
+      a.m[si] = (m_run + log2f(l_run)) * 0.69314718055994530942f;
+    }
+  }
+}
+
+template <typename E, int D>
+static hipError_t launch_mfma(FwdMode mode, const FwdArgs& a, hipStream_t s) {
+  const int64_t n = ((a.L + 127) / 128) * int64_t(a.H) * a.B;
+  if (n == 0) return hipSuccess;
+  if (mode == kModeStats)
+    hipLaunchKernelGGL((attn_fwd_mfma<E, D, kModeStats>), dim3(unsigned(n)), dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL((attn_fwd_mfma<E, D, kModeFinal>), dim3(unsigned(n)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+template <int D>
+static hipError_t launch_f32(FwdMode mode, const FwdArgs& a, hipStream_t s) {
+  const int64_t n = ((a.L + 31) / 32) * int64_t(a.H) * a.B;
+  if (n == 0) return hipSuccess;
+  if (mode == kModeStats)
+    hipLaunchKernelGGL((attn_fwd_f32<D, kModeStats>), dim3(unsigned(n)), dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL((attn_fwd_f32<D, kModeFinal>), dim3(unsigned(n)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_fwd(cqsa_dtype dt, int d, FwdMode mode, const FwdArgs& a, hipStream_t s) {
+  if (a.n_runs > kMaxRuns) return hipErrorInvalidValue;
+  if (dt == CQSA_BF16) return d == 128 ? launch_mfma<BF16, 128>(mode, a, s) : launch_mfma<BF16, 64>(mode, a, s);
+  if (dt == CQSA_F16) return d == 128 ? launch_mfma<F16, 128>(mode, a, s) : launch_mfma<F16, 64>(mode, a, s);
+  return d == 128 ? launch_f32<128>(mode, a, s) : launch_f32<64>(mode, a, s);
+}
+
+}  // namespace cqsa

@@ -1,0 +1,147 @@
+// C-ABI entry points for planning (host only; no HIP calls).
+#include <algorithm>
+#include <cstring>
+#include <exception>
+#include <new>
+#include <string>
+
+#include "errors.hpp"
+#include "plan.hpp"
+
+using namespace cqsa;
+
+namespace cqsa {
+std::string& error_slot() {
+  thread_local std::string s;
+  return s;
+}
+}  // namespace cqsa
+
+extern "C" {
+
+void cqsa_plan_opts_default(cqsa_plan_opts* o) {
+  if (!o) return;
+  std::memset(o, 0, sizeof(*o));
+  o->B = 1;
+  o->dtype = CQSA_BF16;
+  o->c = 7;
+  o->l = 3;
+  o->interest[0] = 0;
+  o->interest[1] = 1;
+  o->interest[2] = 3;
+  o->depth = -1;
+  o->min_depth = 1;
+  o->max_depth = 4;
+  o->n_slots = 2;
+  o->inputs_on_device = 1;
+  o->acc_on_device = 1;
+  o->with_backward = 0;
+}
+
+cqsa_status cqsa_plan(int64_t L, int32_t H, int32_t d, int32_t causal,
+                      uint64_t device_budget_bytes, const cqsa_plan_opts* opts,
+                      cqsa_plan_t** out) {
+  clear_error();
+  if (!out) return fail(CQSA_ERR_INVALID_ARG, "cqsa_plan: out is NULL");
+  *out = nullptr;
+  try {
+    cqsa_plan_opts o;
+    if (opts)
+      o = *opts;
+    else
+      cqsa_plan_opts_default(&o);
+    std::string err;
+    cqsa_status s = validate_plan_args(L, H, d, o, &err);
+    if (s != CQSA_OK) return fail(s, "cqsa_plan: " + err);
+    Geometry g{L, H, d, causal ? 1 : 0};
+    auto* p = new cqsa_plan_s();
+    p->g = g;
+    p->budget = device_budget_bytes;
+    p->opts = o;
+    auto fits = [&](const Footprint& f) {
+      return device_budget_bytes == 0 || f.peak <= device_budget_bytes;
+    };
+    if (o.depth >= 0) {
+      p->depth = o.depth;
+      p->tasks = build_tasks(L, o, o.depth);
+      p->fp = footprint(g, o, o.depth, p->tasks);
+    } else {
+      bool found = false;
+      for (int32_t dep = o.min_depth; dep <= o.max_depth; ++dep) {
+        std::vector<Task> tasks = build_tasks(L, o, dep);
+        Footprint f = footprint(g, o, dep, tasks);
+        if (fits(f)) {
+          p->depth = dep;
+          p->tasks = std::move(tasks);
+          p->fp = f;
+          found = true;
+          break;
+        }
+      }
+      if (!found) {
+        delete p;
+        return fail(CQSA_ERR_BUDGET,
+                    "cqsa_plan: no depth in [min_depth, max_depth] fits the device budget");
+      }
+    }
+    p->max_L_local = 0;
+    size_t max_runs = 0;
+    for (const Task& t : p->tasks) {
+      p->max_L_local = std::max(p->max_L_local, t.L_local);
+      max_runs = std::max(max_runs, t.runs.size());
+    }
+    if (max_runs > 128) {
+      delete p;
+      return fail(CQSA_ERR_UNSUPPORTED, "cqsa_plan: a task has more than 128 runs (depth too large)");
+    }
+    pack_tables(p->tasks, &p->packed, &p->table_off);
+    *out = p;
+    return CQSA_OK;
+  } catch (const std::bad_alloc&) {
+    return fail(CQSA_ERR_INTERNAL, "cqsa_plan: host allocation failed");
+  } catch (const std::exception& e) {
+    return fail(CQSA_ERR_INTERNAL, std::string("cqsa_plan: ") + e.what());
+  }
+}
+
+int32_t cqsa_plan_depth(const cqsa_plan_t* p) { return p ? p->depth : -1; }
+
+int64_t cqsa_plan_num_tasks(const cqsa_plan_t* p) { return p ? int64_t(p->tasks.size()) : -1; }
+
+cqsa_status cqsa_plan_get_task(const cqsa_plan_t* p, int64_t t, cqsa_task* out) {
+  clear_error();
+  if (!p || !out) return fail(CQSA_ERR_INVALID_ARG, "cqsa_plan_get_task: NULL argument");
+  if (t < 0 || t >= int64_t(p->tasks.size()))
+    return fail(CQSA_ERR_INVALID_ARG, "cqsa_plan_get_task: task index out of range");
+  const Task& k = p->tasks[size_t(t)];
+  out->index = t;
+  out->depth = p->depth;
+  out->quorum = k.quorum.data();
+  out->L_local = k.L_local;
+  out->n_runs = int32_t(k.abi_runs.size());
+  out->runs = k.abi_runs.data();
+  out->n_blocks = int64_t(k.blk_or.size());
+  out->block_or = k.blk_or.data();
+  out->block_and = k.blk_and.data();
+  return CQSA_OK;
+}
+
+uint64_t cqsa_plan_modelled_device_bytes(const cqsa_plan_t* p) { return p ? p->fp.peak : 0; }
+
+cqsa_status cqsa_plan_tile_census(const cqsa_plan_t* p, int64_t* full, int64_t* clear,
+                                  int64_t* mixed) {
+  clear_error();
+  if (!p || !full || !clear || !mixed)
+    return fail(CQSA_ERR_INVALID_ARG, "cqsa_plan_tile_census: NULL argument");
+  std::call_once(p->census_once, [p] { tile_census(p->tasks, p->census); });
+  *full = p->census[0];
+  *clear = p->census[1];
+  *mixed = p->census[2];
+  return CQSA_OK;
+}
+
+void cqsa_plan_destroy(cqsa_plan_t* p) { delete p; }
+
+const char* cqsa_last_error(void) { return last_error_cstr(); }
+
+}  // extern "C"

@@ -1,0 +1,122 @@
+// Device-side building blocks for the gfx950 (CDNA4) kernels.
+//
+// MFMA lane layouts used throughout (wave64, v_mfma_f32_32x32x16_{bf16,f16}):
+//   A (M x K = 32 x 16): lane l holds row l%32, k = 8*(l/32) .. +8
+//   B (K x N = 16 x 32): lane l holds column l%32, k = 8*(l/32) .. +8
+//   C/D (32 x 32 fp32):  lane l holds column l%32; register r holds row
+//                        8*(r/4) + 4*(l/32) + (r%4)
+// ds_read_b64_tr_b16 (LDS transpose read), per group of 16 lanes: lane i of
+// the group receives element (i%4) of the 4 x 16-bit words read by source
+// lane 4*e + i/4, for e = 0..3.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace cqsa {
+
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+typedef __attribute__((__vector_size__(8 * sizeof(_Float16)))) _Float16 f16x8;
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
+typedef __attribute__((__vector_size__(4 * sizeof(short)))) short i16x4;
+typedef __attribute__((__vector_size__(4 * sizeof(uint32_t)))) uint32_t u32x4;
+typedef __attribute__((__vector_size__(2 * sizeof(uint32_t)))) uint32_t u32x2;
+
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+
+// Input element tags.
+struct BF16 {
+  typedef bf16x8 vec8;
+};
+struct F16 {
+  typedef f16x8 vec8;
+};
+
+template <typename E>
+__device__ __forceinline__ f32x16 mfma32(const typename E::vec8& a, const typename E::vec8& b,
+                                         const f32x16& c);
+template <>
+__device__ __forceinline__ f32x16 mfma32<BF16>(const bf16x8& a, const bf16x8& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+template <>
+__device__ __forceinline__ f32x16 mfma32<F16>(const f16x8& a, const f16x8& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+}
+
+// Convert 8 fp32 values to a packed 16-bit operand (round to nearest even).
+template <typename E>
+__device__ __forceinline__ typename E::vec8 pack8(const float* x);
+template <>
+__device__ __forceinline__ bf16x8 pack8<BF16>(const float* x) {
+  bf16x8 r;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) r[i] = (__bf16)x[i];
+  return r;
+}
+template <>
+__device__ __forceinline__ f16x8 pack8<F16>(const float* x) {
+  f16x8 r;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) r[i] = (_Float16)x[i];
+  return r;
+}
+
+template <typename V>
+__device__ __forceinline__ V bitcast_u4(const u32x4& u) {
+  return __builtin_bit_cast(V, u);
+}
+
+// Two LDS transpose reads forming one 8-element 16-bit MFMA operand.
+template <typename E>
+__device__ __forceinline__ typename E::vec8 lds_tr_pair(const char* p0, const char* p1) {
+  i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p0);
+  i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p1);
+  u32x4 u;
+  u32x2 a = __builtin_bit_cast(u32x2, lo), b = __builtin_bit_cast(u32x2, hi);
+  u[0] = a[0];
+  u[1] = a[1];
+  u[2] = b[0];
+  u[3] = b[1];
+  return __builtin_bit_cast(typename E::vec8, u);
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Value held by lane l^32 (the other half of the wave).
+__device__ __forceinline__ float swap_halves(float v) {
+  auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(uint32_t, v),
+                                            __builtin_bit_cast(uint32_t, v), false, false);
+  uint32_t lane = __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+  return __builtin_bit_cast(float, lane < 32 ? r[1] : r[0]);
+}
+
+__device__ __forceinline__ int lane_id() {
+  return (int)__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+}
+
+// One maximal run of a task on the device (see plan.hpp).
+struct DevRun {
+  int64_t local_start;
+  int64_t global_start;
+  int64_t length;
+  uint32_t bits;
+  uint32_t pad;
+};
+
+// Work-group id remapped so that consecutive work items land on the same XCD
+// (the dispatcher deals work groups round-robin over the 8 XCDs, each with its
+// own L2): work item w = xcd * per_xcd + slot.
+__device__ __forceinline__ int64_t xcd_remap(int64_t id, int64_t n) {
+  constexpr int64_t kXcd = 8;
+  const int64_t per = n / kXcd, rem = n % kXcd;
+  const int64_t xcd = id % kXcd, slot = id / kXcd;
+  // the first `rem` XCDs own per+1 items
+  const int64_t base = xcd * per + (xcd < rem ? xcd : rem);
+  const int64_t cap = per + (xcd < rem ? 1 : 0);
+  if (slot < cap) return base + slot;
+  return id;  // unreachable when the grid has exactly n groups
+}
+
+}  // namespace cqsa

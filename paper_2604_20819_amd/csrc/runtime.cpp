@@ -1,0 +1,214 @@
+// Runtime shared by the drivers: per-device streams, workspace caching,
+// the caller-allocator hook, per-stage timing, and the C-ABI entry points
+// that are not planning or compute.
+#include "runtime.hpp"
+
+#include <cmath>
+#include <cstring>
+
+namespace cqsa {
+
+namespace {
+std::mutex g_ctx_mu;
+DevCtx g_ctx[64];
+std::mutex g_hook_mu;
+void* (*g_alloc)(size_t, void*) = nullptr;
+void (*g_release)(void*, void*) = nullptr;
+void* g_hook_ctx = nullptr;
+thread_local bool t_timing = false;
+thread_local CallRecord t_record;
+}  // namespace
+
+DevCtx* device_ctx(cqsa_status* st) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess || dev < 0 || dev >= 64) {
+    *st = hip_fail(e == hipSuccess ? hipErrorInvalidDevice : e, "hipGetDevice");
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> g(g_ctx_mu);
+  DevCtx* c = &g_ctx[dev];
+  if (!c->ready) {
+    c->device = dev;
+    if ((e = hipStreamCreateWithFlags(&c->copy, hipStreamNonBlocking)) != hipSuccess ||
+        (e = hipStreamCreateWithFlags(&c->d2h, hipStreamNonBlocking)) != hipSuccess ||
+        (e = hipEventCreateWithFlags(&c->ws_free, hipEventDisableTiming)) != hipSuccess) {
+      *st = hip_fail(e, "creating library streams");
+      return nullptr;
+    }
+    c->ready = true;
+  }
+  *st = CQSA_OK;
+  return c;
+}
+
+cqsa_status acquire_workspace(DevCtx* c, size_t bytes, Workspace* ws) {
+  ws->bytes = bytes;
+  ws->from_hook = false;
+  ws->ptr = nullptr;
+  if (bytes == 0) return CQSA_OK;
+  {
+    std::lock_guard<std::mutex> g(g_hook_mu);
+    if (g_alloc) {
+      ws->ptr = g_alloc(bytes, g_hook_ctx);
+      ws->from_hook = true;
+      if (!ws->ptr) return fail(CQSA_ERR_DEVICE_OOM, "caller allocator returned NULL");
+      return CQSA_OK;
+    }
+  }
+  if (c->ws_bytes < bytes) {
+    if (c->ws) {
+      hipError_t e = hipDeviceSynchronize();
+      if (e != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
+      (void)hipFree(c->ws);
+      c->ws = nullptr;
+      c->ws_bytes = 0;
+      c->ws_free_valid = false;
+    }
+    hipError_t e = hipMalloc(&c->ws, bytes);
+    if (e != hipSuccess) {
+      c->ws = nullptr;
+      (void)hipGetLastError();
+      return fail(CQSA_ERR_DEVICE_OOM, "hipMalloc of the workspace failed");
+    }
+    c->ws_bytes = bytes;
+  }
+  ws->ptr = c->ws;
+  return CQSA_OK;
+}
+
+void release_workspace(DevCtx* c, Workspace* ws, hipStream_t s) {
+  if (!ws->ptr) return;
+  if (ws->from_hook) {
+    // the caller's allocator is not stream ordered for our side streams
+    (void)hipStreamSynchronize(s);
+    std::lock_guard<std::mutex> g(g_hook_mu);
+    if (g_release) g_release(ws->ptr, g_hook_ctx);
+  }
+  ws->ptr = nullptr;
+  (void)c;
+}
+
+cqsa_status acquire_pinned(DevCtx* c, size_t bytes, void** out) {
+  if (c->pin_bytes < bytes) {
+    if (c->pin) {
+      (void)hipDeviceSynchronize();
+      (void)hipHostFree(c->pin);
+      c->pin = nullptr;
+      c->pin_bytes = 0;
+    }
+    hipError_t e = hipHostMalloc(&c->pin, bytes, hipHostMallocDefault);
+    if (e != hipSuccess) {
+      c->pin = nullptr;
+      (void)hipGetLastError();
+      return fail(CQSA_ERR_INTERNAL, "hipHostMalloc of the host staging buffer failed");
+    }
+    c->pin_bytes = bytes;
+  }
+  *out = c->pin;
+  return CQSA_OK;
+}
+
+void CallRecord::reset() {
+  for (hipEvent_t e : owned) (void)hipEventDestroy(e);
+  owned.clear();
+  for (auto& v : spans) v.clear();
+  wall0 = wall1 = nullptr;
+  host_merge_ms = 0.0;
+  std::memset(&stats, 0, sizeof(stats));
+  timing = t_timing;
+}
+
+hipEvent_t CallRecord::make() {
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  owned.push_back(e);
+  return e;
+}
+
+CallRecord& call_record() { return t_record; }
+bool timing_enabled() { return t_timing; }
+
+cqsa_status check_tensor(const cqsa_tensor* t, const char* name, const cqsa_plan_t* p,
+                         cqsa_dtype want, cqsa_mem where) {
+  std::string n(name);
+  if (!t) return fail(CQSA_ERR_INVALID_ARG, n + " is NULL");
+  if (!t->data) return fail(CQSA_ERR_INVALID_ARG, n + ".data is NULL");
+  if (t->dtype != want) return fail(CQSA_ERR_INVALID_ARG, n + " has the wrong dtype");
+  if (t->where != where)
+    return fail(CQSA_ERR_INVALID_ARG, n + " residency differs from the plan");
+  if (t->B != p->opts.B || t->L != p->g.L || t->H != p->g.H || t->d != p->g.d)
+    return fail(CQSA_ERR_INVALID_ARG, n + " shape differs from the plan");
+  return CQSA_OK;
+}
+
+}  // namespace cqsa
+
+using namespace cqsa;
+
+extern "C" {
+
+cqsa_status cqsa_set_allocator(void* (*alloc)(size_t, void*), void (*release)(void*, void*),
+                               void* ctx) {
+  clear_error();
+  if ((alloc == nullptr) != (release == nullptr))
+    return fail(CQSA_ERR_INVALID_ARG, "cqsa_set_allocator: give both functions or neither");
+  std::lock_guard<std::mutex> g(g_hook_mu);
+  g_alloc = alloc;
+  g_release = release;
+  g_hook_ctx = ctx;
+  return CQSA_OK;
+}
+
+cqsa_status cqsa_set_timing(int32_t enable) {
+  clear_error();
+  t_timing = enable != 0;
+  return CQSA_OK;
+}
+
+cqsa_status cqsa_last_stats(cqsa_run_stats* out) {
+  clear_error();
+  if (!out) return fail(CQSA_ERR_INVALID_ARG, "cqsa_last_stats: out is NULL");
+  CallRecord& r = t_record;
+  cqsa_run_stats s = r.stats;
+  if (r.timing && r.wall1) {
+    hipError_t e = hipEventSynchronize(r.wall1);
+    if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+    auto span = [](hipEvent_t a, hipEvent_t b) {
+      float ms = 0.f;
+      if (hipEventSynchronize(b) != hipSuccess) return 0.0;
+      if (hipEventElapsedTime(&ms, a, b) != hipSuccess) return 0.0;
+      return double(ms);
+    };
+    s.ms_wall = span(r.wall0, r.wall1);
+    double* dst[kStCount] = {&s.ms_stage, &s.ms_inner, &s.ms_merge, &s.ms_finalize, &s.ms_d2h};
+    for (int k = 0; k < kStCount; ++k) {
+      double acc = 0.0;
+      for (auto& pr : r.spans[k]) acc += span(pr.first, pr.second);
+      *dst[k] = acc;
+    }
+    s.ms_merge += r.host_merge_ms;
+  }
+  *out = s;
+  return CQSA_OK;
+}
+
+cqsa_status cqsa_release_workspace(void) {
+  clear_error();
+  cqsa_status st;
+  DevCtx* c = device_ctx(&st);
+  if (!c) return st;
+  std::lock_guard<std::mutex> g(c->mu);
+  hipError_t e = hipDeviceSynchronize();
+  if (e != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
+  if (c->ws) (void)hipFree(c->ws);
+  c->ws = nullptr;
+  c->ws_bytes = 0;
+  c->ws_free_valid = false;
+  if (c->pin) (void)hipHostFree(c->pin);
+  c->pin = nullptr;
+  c->pin_bytes = 0;
+  return CQSA_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,80 @@
+// Per-device runtime state and helpers shared by the forward and backward
+// drivers (internal).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <chrono>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "cqsa.h"
+#include "errors.hpp"
+#include "plan.hpp"
+
+namespace cqsa {
+
+// Library-owned streams and caches of one device.  All streams use the
+// default priority.
+struct DevCtx {
+  int device = -1;
+  bool ready = false;
+  hipStream_t copy = nullptr;   // staging copies (H2D or D2D)
+  hipStream_t d2h = nullptr;    // statistics device -> host
+  hipEvent_t ws_free = nullptr; // recorded after the last call's last use of the workspace
+  bool ws_free_valid = false;
+  void* ws = nullptr;           // cached device workspace (built-in allocator)
+  size_t ws_bytes = 0;
+  void* pin = nullptr;          // cached pinned host staging for host accumulation
+  size_t pin_bytes = 0;
+  std::vector<hipEvent_t> sync_events;  // reusable non-timing events
+  std::mutex mu;
+};
+
+DevCtx* device_ctx(cqsa_status* st);  // context of the current device (created on first use)
+
+// Workspace of one call: from the caller allocator when one is installed,
+// else the cached per-device buffer.
+struct Workspace {
+  void* ptr = nullptr;
+  size_t bytes = 0;
+  bool from_hook = false;
+};
+cqsa_status acquire_workspace(DevCtx* c, size_t bytes, Workspace* ws);
+void release_workspace(DevCtx* c, Workspace* ws, hipStream_t s);
+cqsa_status acquire_pinned(DevCtx* c, size_t bytes, void** out);
+
+// Event pairs for the optional per-stage timing of the last call.
+enum Stage { kStStage = 0, kStInner, kStMerge, kStFinal, kStD2H, kStCount };
+struct CallRecord {
+  bool timing = false;
+  std::vector<hipEvent_t> owned;                       // destroyed on reset
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> spans[kStCount];
+  hipEvent_t wall0 = nullptr, wall1 = nullptr;
+  double host_merge_ms = 0.0;
+  cqsa_run_stats stats{};
+  void reset();
+  hipEvent_t make();                                    // timing event owned by the record
+};
+CallRecord& call_record();
+bool timing_enabled();
+
+// Checks shared by forward and backward.
+cqsa_status check_tensor(const cqsa_tensor* t, const char* name, const cqsa_plan_t* p,
+                         cqsa_dtype want, cqsa_mem where);
+
+inline cqsa_status hip_fail(hipError_t e, const char* what) {
+  return fail(CQSA_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+#define CQSA_HIP(expr)                                                   \
+  do {                                                                   \
+    hipError_t e_ = (expr);                                              \
+    if (e_ != hipSuccess) {                                              \
+      if (e_ == hipErrorOutOfMemory) return fail(CQSA_ERR_DEVICE_OOM, #expr); \
+      return hip_fail(e_, #expr);                                        \
+    }                                                                    \
+  } while (0)
+
+}  // namespace cqsa

@@ -1,0 +1,45 @@
+"""Shared helpers of the GPU parity tests (no test functions here)."""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2604_20819_amd as cq
+from paper_2604_20819_amd import synth
+
+
+def need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("needs a GPU")
+
+
+def say(*a):
+    """Name the case before GPU work starts (flushed, so a crash still shows it)."""
+    print("[case]", *a, file=sys.stderr, flush=True)
+
+
+def run_forward(Q, K, V, causal, depth=-1, budget=0, n_slots=2, host=False, scale=0.0):
+    """Run cqsa_forward; Q, K, V are CPU tensors.  host=True keeps inputs and
+    outputs in pinned host memory (streamed path).  Returns CPU (O, LSE, plan)."""
+    B, L, H, d = Q.shape
+    dt = {torch.float32: "f32", torch.float16: "f16", torch.bfloat16: "bf16"}[Q.dtype]
+    opts = cq.make_opts(B=B, dtype=dt, depth=depth, n_slots=n_slots,
+                        inputs_on_device=not host, acc_on_device=not host)
+    plan = cq.cqsa_plan(L, H, d, causal, budget, opts)
+    if host:
+        q, k, v = (x.pin_memory() for x in (Q, K, V))
+        O = torch.empty((B, L, H, d), dtype=torch.float32, pin_memory=True)
+        LSE = torch.empty((B, H, L), dtype=torch.float32, pin_memory=True)
+    else:
+        q, k, v = (x.cuda() for x in (Q, K, V))
+        O = torch.empty((B, L, H, d), dtype=torch.float32, device="cuda")
+        LSE = torch.empty((B, H, L), dtype=torch.float32, device="cuda")
+    cq.cqsa_forward(plan, q, k, v, O, LSE, scale)
+    torch.cuda.synchronize()
+    return O.cpu(), LSE.cpu(), plan
+
+
+def rel_l2(x, ref):
+    x = np.asarray(x, dtype=np.float64); ref = np.asarray(ref, dtype=np.float64)
+    return float(np.linalg.norm((x - ref).ravel()) / np.linalg.norm(ref.ravel()))

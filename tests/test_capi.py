@@ -1,0 +1,140 @@
+"""C-ABI tests that need no GPU: the library loads and exports every symbol
+include/cqsa.h declares; planning through the ABI is bit-exact against the
+independent oracle planner; argument validation; the footprint model picks
+the depths the workload definitions call for."""
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2604_20819_amd as cq
+from oracle import planner as oplan
+from tests.conftest import ROOT
+
+
+def _declared_symbols():
+    text = open(os.path.join(ROOT, "include", "cqsa.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(cqsa_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = cq.lib()
+    syms = _declared_symbols()
+    assert "cqsa_forward" in syms and "cqsa_backward" in syms and "cqsa_plan" in syms
+    for s in syms:
+        assert hasattr(lib, s), s
+        assert s in cq._SIGS, s
+
+
+@pytest.mark.parametrize("N,itr,c", [(7, 1, 7), (49, 2, 7), (100, 1, 7), (100, 2, 7),
+                                      (343, 3, 7), (1000, 2, 7), (65536, 1, 7), (5000, 2, 7),
+                                      (90, 2, 13), (13, 1, 13), (30, 1, 3), (10, 0, 7)])
+def test_planner_matches_oracle(N, itr, c):
+    I = oplan.PAPER_INTEREST_SETS[c] if c in oplan.PAPER_INTEREST_SETS else (0, 1)
+    p = cq.cqsa_plan(N, 1, 64, False, 0, cq.make_opts(c=c, interest=I, depth=itr))
+    ref = oplan.build_tasks(N, c, itr, I)
+    assert p.depth == itr and p.num_tasks == len(ref) == c ** itr
+    for t, rt in enumerate(ref):
+        got = p.task(t)
+        assert got["quorum"] == tuple(rt["quorum"])
+        assert got["L_local"] == len(rt["tokens"])
+        assert got["runs"] == oplan.runs(rt)
+        bor, band = oplan.block_summaries(rt["bits"])
+        assert got["block_or"] == bor.tolist() and got["block_and"] == band.tolist()
+
+
+@pytest.mark.parametrize("N,itr", [(65536, 1), (65536, 2), (20000, 3)])
+def test_census_matches_oracle(N, itr):
+    p = cq.cqsa_plan(N, 1, 64, True, 0, cq.make_opts(depth=itr))
+    f, c, m, _ = oplan.tile_census(oplan.build_tasks(N, 7, itr, (0, 1, 3)))
+    assert p.tile_census() == (f, c, m)
+
+
+@pytest.mark.parametrize("kw,budget,msg", [
+    (dict(interest=(0, 1, 2)), 0, "difference set"),
+    (dict(c=8), 0, "l(l-1)+1"),
+    (dict(n_slots=0), 0, "n_slots"),
+    (dict(depth=-2), 0, "depth"),
+    (dict(min_depth=3, max_depth=2), 0, "min_depth"),
+])
+def test_plan_rejects_bad_options(kw, budget, msg):
+    with pytest.raises(cq.CqsaError) as e:
+        cq.cqsa_plan(1000, 2, 64, False, budget, cq.make_opts(**kw))
+    assert e.value.status == -1 and msg in str(e.value)
+
+
+def test_plan_rejects_bad_geometry():
+    with pytest.raises(cq.CqsaError) as e:
+        cq.cqsa_plan(0, 2, 64, False, 0)
+    assert e.value.status == -1
+    with pytest.raises(cq.CqsaError) as e:
+        cq.cqsa_plan(100, 2, 96, False, 0)
+    assert e.value.status == -2
+    with pytest.raises(cq.CqsaError) as e:
+        cq.cqsa_plan(100, 2, 64, False, 0, cq.make_opts(depth=9))
+    assert e.value.status == -2
+
+
+def test_budget_too_small():
+    with pytest.raises(cq.CqsaError) as e:
+        cq.cqsa_plan(1 << 20, 8, 128, False, 1 << 20, cq.make_opts(max_depth=3))
+    assert e.value.status == -3
+
+
+GB = 10 ** 9
+# (L, H, d, causal, budget, opts, expected depth) for the five workloads
+WORKLOADS = [
+    (1024, 1, 64, False, 0, dict(dtype="f32", depth=1), 1),
+    (32768, 16, 128, False, 0, dict(dtype="bf16", depth=1), 1),
+    (131072, 32, 128, True, 8 * GB, dict(dtype="f16"), 2),
+    (65536, 16, 128, True, 16 * GB, dict(B=2, dtype="bf16", with_backward=True), 1),
+    (1048576, 8, 128, False, 4 * GB, dict(dtype="bf16", inputs_on_device=False,
+                                          acc_on_device=False), 2),
+]
+
+
+@pytest.mark.parametrize("L,H,d,causal,budget,kw,want", WORKLOADS)
+def test_workload_depths(L, H, d, causal, budget, kw, want):
+    p = cq.cqsa_plan(L, H, d, causal, budget, cq.make_opts(**kw))
+    assert p.depth == want
+    if budget:
+        assert p.modelled_device_bytes <= budget
+        if want > 1:
+            # the next shallower depth must not fit (smallest feasible depth, Section 3.4)
+            q = cq.cqsa_plan(L, H, d, causal, 0, cq.make_opts(depth=want - 1, **kw))
+            assert q.modelled_device_bytes > budget
+
+
+def test_footprint_model_closed_form():
+    """Footprint of the bf16 L=32768 H=16 d=128 depth-1 plan, recomputed here
+    from the workspace layout the header documents."""
+    L, H, d, B = 32768, 16, 128, 1
+    p = cq.cqsa_plan(L, H, d, False, 0, cq.make_opts(depth=1))
+    al = lambda x: (x + 255) // 256 * 256
+    Lmax = max(p.task(t)["L_local"] for t in range(p.num_tasks))
+    rows = B * Lmax * H
+    slot = 3 * al(rows * d * 2) + al(rows * d * 4) + 2 * al(rows * 4)
+    resident = 3 * al(B * L * H * d * 2) + al(B * L * H * d * 4) + al(B * L * H * 4)
+    tables = sum(al(len(p.task(t)["runs"]) * 32) + 2 * al(len(p.task(t)["block_or"]) * 4)
+                 for t in range(p.num_tasks))
+    want = resident + 2 * slot + al(B * H * L * 4) + tables
+    assert p.modelled_device_bytes == want
+
+
+def test_forward_argument_errors_without_device_work():
+    torch = pytest.importorskip("torch")
+    p = cq.cqsa_plan(64, 1, 64, False, 0, cq.make_opts(dtype="f32", depth=1,
+                                                        inputs_on_device=False,
+                                                        acc_on_device=False))
+    Q = torch.zeros(1, 64, 1, 64)
+    O = torch.zeros(1, 64, 1, 64)
+    LSE = torch.zeros(1, 1, 64)
+    bad = torch.zeros(1, 63, 1, 64)
+    with pytest.raises(cq.CqsaError) as e:
+        cq.cqsa_forward(p, Q, Q, bad, O, LSE)
+    assert e.value.status == -1 and "shape" in str(e.value)
+    with pytest.raises(cq.CqsaError) as e:
+        cq.cqsa_forward(p, Q, Q, Q.half(), O, LSE)
+    assert e.value.status == -1 and "dtype" in str(e.value)

@@ -1,0 +1,151 @@
+"""GPU parity of the decomposed forward (HIP path through the C ABI) against
+the float64 oracle, and decomposed against undecomposed.
+
+Tolerances
+  * fp32 inputs: max |O - O_f64| <= 1e-5 (required for the fp32 exactness case).
+  * 16-bit inputs: max |O - O_f64| <= 1e-2 (required), and a relative-L2 bound
+    derived from the arithmetic: P is rounded to the input type before the PV
+    product (unit roundoff 2^-9 for bf16, 2^-12 for fp16), which gives
+    rel-L2 of order 1e-3 (bf16) / 2e-4 (fp16); the tests allow 4e-3 / 6e-4.
+  * LSE uses fp32 statistics only: |LSE - LSE_f64| <= 1e-4 (16-bit scores are
+    exact products accumulated in fp32).
+  * decomposed vs undecomposed (depth 0) on the same inputs: rel-L2 <= 1e-3.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import dense
+from paper_2604_20819_amd import synth
+from tests.gpu_util import need_gpu, rel_l2, run_forward, say
+
+pytestmark = pytest.mark.gpu
+
+REL = {"bf16": 4e-3, "f16": 6e-4, "f32": 1e-6}
+
+
+def _check_vs_oracle(O, LSE, Q, K, V, causal, dt, rows=None, atol=None):
+    Of, LSEf = dense.attention_forward(synth.as_f64(Q), synth.as_f64(K), synth.as_f64(V),
+                                       causal, rows=rows)
+    if rows is None:
+        Og, LSEg = O.double().numpy(), LSE.double().numpy()
+    else:
+        Og = np.stack([O[:, r, h].double().numpy() for h, r in enumerate(rows)], axis=2)
+        LSEg = np.stack([LSE[:, h, r].double().numpy() for h, r in enumerate(rows)], axis=1)
+    err = np.abs(Og - Of).max()
+    rl = rel_l2(Og, Of)
+    lerr = np.abs(LSEg - LSEf).max()
+    say(f"max_abs={err:.3e} rel_l2={rl:.3e} lse_abs={lerr:.3e}")
+    assert np.isfinite(Og).all() and np.isfinite(LSEg).all()
+    if atol is not None:
+        assert err <= atol
+    elif dt == "f32":
+        assert err <= 1e-5
+    else:
+        assert err <= 1e-2
+    assert rl <= REL[dt]
+    assert lerr <= 1e-4
+    return rl
+
+
+def test_fp32_exactness_case():
+    """B=1, H=1, d=64, L=1024, non-causal, fp32, depth 1 forced, all rows."""
+    need_gpu()
+    say("fp32 L=1024 H=1 d=64 depth=1")
+    Q, K, V = synth.make_inputs(20819 + 1, 1, 1024, 1, 64, "f32")
+    O, LSE, plan = run_forward(Q, K, V, causal=False, depth=1)
+    assert plan.depth == 1 and plan.num_tasks == 7
+    _check_vs_oracle(O, LSE, Q, K, V, False, "f32")
+
+
+GRID = [(dt, d, causal, L, depth)
+        for dt in ("bf16", "f16") for d in (64, 128) for causal in (False, True)
+        for L, depth in ((1, 0), (1, 1), (100, 1), (1000, 0), (1000, 1), (2049, 2))]
+
+
+@pytest.mark.parametrize("dt,d,causal,L,depth", GRID)
+def test_small_grid_vs_oracle(dt, d, causal, L, depth):
+    need_gpu()
+    say(f"grid dt={dt} d={d} causal={causal} L={L} depth={depth}")
+    Q, K, V = synth.make_inputs(7 + L + d, 2, L, 3, d, dt)
+    O, LSE, plan = run_forward(Q, K, V, causal, depth=depth)
+    assert plan.depth == depth
+    _check_vs_oracle(O, LSE, Q, K, V, causal, dt)
+
+
+@pytest.mark.parametrize("d,causal", [(64, True), (128, False)])
+def test_fp32_grid(d, causal):
+    need_gpu()
+    for L, depth in ((77, 0), (700, 1), (1500, 2)):
+        say(f"fp32 grid d={d} causal={causal} L={L} depth={depth}")
+        Q, K, V = synth.make_inputs(11 + L, 1, L, 2, d, "f32")
+        O, LSE, _ = run_forward(Q, K, V, causal, depth=depth)
+        _check_vs_oracle(O, LSE, Q, K, V, causal, "f32")
+
+
+@pytest.mark.parametrize("dt,causal", [("bf16", False), ("bf16", True), ("f16", True)])
+def test_decomposed_matches_undecomposed(dt, causal):
+    need_gpu()
+    say(f"decomposed vs undecomposed dt={dt} causal={causal}")
+    Q, K, V = synth.make_inputs(99, 1, 4100, 4, 128, dt)
+    O0, L0, _ = run_forward(Q, K, V, causal, depth=0)
+    for depth in (1, 2, 3):
+        O1, L1, _ = run_forward(Q, K, V, causal, depth=depth)
+        r = rel_l2(O1.numpy(), O0.numpy())
+        say(f"depth {depth}: rel_l2 vs depth 0 = {r:.3e}")
+        assert r <= 1e-3
+        assert np.abs(L1.numpy() - L0.numpy()).max() <= 1e-5
+
+
+def test_single_slot_and_many_slots_agree():
+    need_gpu()
+    Q, K, V = synth.make_inputs(5, 1, 3000, 2, 128, "bf16")
+    say("slots 1 vs 3")
+    O1, L1, _ = run_forward(Q, K, V, True, depth=2, n_slots=1)
+    O3, L3, _ = run_forward(Q, K, V, True, depth=2, n_slots=3)
+    assert torch.equal(O1, O3) and torch.equal(L1, L3)
+
+
+def test_overflowing_scores_stay_finite():
+    """Scores of order 200 (lse far above ln(FLT_MAX) ~ 88.72): the max-shifted
+    path must stay finite and exact (App. A.1)."""
+    need_gpu()
+    say("overflow scores")
+    Q, K, V = synth.make_inputs(3, 1, 1500, 2, 128, "bf16")
+    Q = (Q.float() * 4).to(torch.bfloat16)
+    K = (K.float() * 4).to(torch.bfloat16)
+    O, LSE, _ = run_forward(Q, K, V, False, depth=1)
+    assert LSE.max().item() > 88.72
+    # near one-hot softmax rows: O is of the size of V itself, and rounding P
+    # to bf16 (unit roundoff 2^-9) bounds the error by about 2^-9 * max|V|
+    atol = 2.0 ** -8 * float(V.float().abs().max())
+    _check_vs_oracle(O, LSE, Q, K, V, False, "bf16", atol=atol)
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+def test_host_resident_streamed_small(dt):
+    need_gpu()
+    say(f"host streamed small {dt}")
+    Q, K, V = synth.make_inputs(17, 2, 3001, 2, 64, dt)
+    O, LSE, plan = run_forward(Q, K, V, True, depth=2, host=True)
+    assert plan.depth == 2
+    _check_vs_oracle(O, LSE, Q, K, V, True, dt)
+    Od, Ld, _ = run_forward(Q, K, V, True, depth=2)
+    assert rel_l2(O.numpy(), Od.numpy()) <= 1e-6
+
+
+def test_bf16_L32768_single_level():
+    """B=1, H=16, d=128, L=32768, non-causal bf16, depth 1: 2048 sampled rows
+    per head against float64; all rows against the undecomposed kernel."""
+    need_gpu()
+    say("bf16 L=32768 H=16 depth 1")
+    B, L, H, d = 1, 32768, 16, 128
+    Q, K, V = synth.make_inputs(20819 + 2, B, L, H, d, "bf16")
+    O, LSE, plan = run_forward(Q, K, V, False, depth=1)
+    assert plan.depth == 1 and plan.num_tasks == 7
+    rows = synth.sample_rows(20819 + 2, L, 2048, H)
+    _check_vs_oracle(O, LSE, Q, K, V, False, "bf16", rows=rows)
+    O0, L0, _ = run_forward(Q, K, V, False, depth=0)
+    r = rel_l2(O.numpy(), O0.numpy())
+    say(f"rel_l2 vs depth 0 = {r:.3e}")
+    assert r <= 1e-3
