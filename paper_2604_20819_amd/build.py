@@ -24,7 +24,7 @@ COMMON = [
 ]
 SOURCES = [
     "plan.cpp", "capi_plan.cpp", "runtime.cpp", "fwd_driver.cpp", "bwd_driver.cpp",
-    "attn_fwd.hip", "merge.hip", "attn_bwd.hip",
+    "attn_fwd.hip", "merge.hip", "attn_bwd.hip", "stage.hip",
 ]
 
 

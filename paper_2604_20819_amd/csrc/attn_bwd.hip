@@ -1,2 +1,432 @@
-// Inner backward kernels (placeholder).
+// Inner backward kernels over one CQS task, in the global-LSE form of App. A.1
+// (Eq. "globallse"): P[q,k] = exp(alpha s[q,k] - lse_global[q]) on the pairs the
+// task keeps, D[q] = rowsum(dO * O), dS = P * (dP - D), and
+//   dV = P^T dO,  dK = alpha dS^T Q  (key-parallel kernel, 4 products)
+//   dQ = alpha dS K                  (query-parallel kernel, 3 products)
+// The paper shows this equals Alg. 2; because every (query, key) pair is kept
+// by exactly one task, task gradients add, and each kernel's epilogue adds its
+// task-local rows straight into the global fp32 gradients (tasks are ordered
+// on one stream and a task holds each token once, so no atomics are needed).
+//
+// Tile verdicts, masks and ascending-order causal tests follow the forward.
+// Fully masked tiles are skipped before any load: a skipped tile leaves
+// P = 0 and therefore dS = 0 (App. A.2, "Skipping fully-masked tiles").
+//
+// gfx950 layouts: the dQ kernel works on S^T (lane = query) like the forward
+// and reads K^T operands with ds_read_b64_tr_b16; the dK/dV kernel works on S
+// (lane = key), keeps the wave's K and V rows as register operands, and reads
+// dO^T and Q^T operands from row-major LDS tiles with the transpose read.
 #include "hip_common.hpp"
+#include "kernels.hpp"
+
+namespace cqsa {
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+template <typename E, int D>
+__global__ void __launch_bounds__(256, (D == 128 ? 1 : 2)) attn_bwd_dq(const BwdArgs a) {
+  constexpr int BM = 128, BN = 64;
+  constexpr int KP = D * 2 + 64;  // K tile: transpose reads and row reads
+  constexpr int VP = D * 2 + 16;  // V tile: row reads
+  constexpr int KBYTES = BN * KP, VBYTES = BN * VP, STAGE = KBYTES + VBYTES;
+  constexpr int DK = D / 16, DB = D / 32, CHUNKS = D / 8, RPP = 256 / CHUNKS, PASSES = BN / RPP;
+  typedef typename E::vec8 vec8;
+
+  __shared__ __attribute__((aligned(16))) char smem[2 * STAGE];
+  __shared__ uint32_t kbits_s[2][BN];
+  __shared__ DevRun runs_s[kMaxRuns];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5;
+  const int L = a.L;
+  const int64_t nstrips = (L + BM - 1) / BM;
+  const int64_t work = xcd_remap(blockIdx.x, nstrips * a.H * a.B);
+  const int strip = int(work % nstrips);
+  const int h = int((work / nstrips) % a.H);
+  const int b = int(work / (nstrips * a.H));
+  for (int i = tid; i < a.n_runs; i += 256) runs_s[i] = ((const DevRun*)a.runs)[i];
+
+  const int64_t rs = int64_t(a.H) * D;
+  const int64_t base = int64_t(b) * L * rs + int64_t(h) * D;
+  const uint16_t* Qg = (const uint16_t*)a.q + base;
+  const uint16_t* Kg = (const uint16_t*)a.k + base;
+  const uint16_t* Vg = (const uint16_t*)a.v + base;
+  const uint16_t* Og = (const uint16_t*)a.dO + base;
+  const float c = a.scale_log2;
+  const bool causal = a.causal != 0;
+
+  const int q0w = strip * BM + wave * 32;
+  const int myq = q0w + (lane & 31);
+  const bool qvalid = myq < L;
+  vec8 qf[DK], of[DK];
+#pragma unroll
+  for (int ks = 0; ks < DK; ++ks) {
+    u32x4 u = {0u, 0u, 0u, 0u}, w = {0u, 0u, 0u, 0u};
+    if (qvalid) {
+      u = *(const u32x4*)(Qg + int64_t(myq) * rs + ks * 16 + half * 8);
+      w = *(const u32x4*)(Og + int64_t(myq) * rs + ks * 16 + half * 8);
+    }
+    qf[ks] = bitcast_u4<vec8>(u);
+    of[ks] = bitcast_u4<vec8>(w);
+  }
+
+  const int lastq_wg = (strip * BM + BM < L ? strip * BM + BM : L) - 1;
+  const int qb0 = strip * 2, qb1 = lastq_wg / 64;
+  const uint32_t qor = a.blk_or[qb0] | a.blk_or[qb1];
+  const uint32_t qand = a.blk_and[qb0] & a.blk_and[qb1];
+  const bool wave_live = q0w < L;
+  const int wq1 = wave_live ? (q0w + 31 < L ? q0w + 31 : L - 1) : 0;
+  const uint32_t wor = wave_live ? a.blk_or[q0w / 64] : 0u;
+  const uint32_t wand = wave_live ? a.blk_and[q0w / 64] : 0u;
+  const int nkt = (L + BN - 1) / BN;
+  auto next_live = [&](int kt) -> int {
+    for (; kt < nkt; ++kt) {
+      if (causal && kt * BN > lastq_wg) return nkt;
+      if ((qand & a.blk_and[kt]) == 0u) return kt;
+    }
+    return nkt;
+  };
+
+  u32x4 kreg[PASSES], vreg[PASSES];
+  auto gload = [&](int kt) {
+#pragma unroll
+    for (int p = 0; p < PASSES; ++p) {
+      const int row = p * RPP + tid / CHUNKS, ch = tid % CHUNKS, key = kt * BN + row;
+      u32x4 zk = {0u, 0u, 0u, 0u}, zv = {0u, 0u, 0u, 0u};
+      if (key < L) {
+        zk = *(const u32x4*)(Kg + int64_t(key) * rs + ch * 8);
+        zv = *(const u32x4*)(Vg + int64_t(key) * rs + ch * 8);
+      }
+      kreg[p] = zk;
+      vreg[p] = zv;
+    }
+  };
+  auto sstore = [&](int buf, int kt) {
+    char* kb = smem + buf * STAGE;
+    char* vb = kb + KBYTES;
+#pragma unroll
+    for (int p = 0; p < PASSES; ++p) {
+      const int row = p * RPP + tid / CHUNKS, ch = tid % CHUNKS;
+      *(u32x4*)(kb + row * KP + ch * 16) = kreg[p];
+      *(u32x4*)(vb + row * VP + ch * 16) = vreg[p];
+    }
+    if ((qor & a.blk_or[kt]) != 0u && tid < BN) {
+      const int key = kt * BN + tid;
+      kbits_s[buf][tid] = key < L ? run_bits(runs_s, a.n_runs, key) : 0u;
+    }
+  };
+
+  f32x16 dq[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) dq[db][r] = 0.f;
+
+  __syncthreads();
+  const uint32_t qbits = qvalid ? run_bits(runs_s, a.n_runs, myq) : 0u;
+  const int64_t gq = qvalid ? run_global(runs_s, a.n_runs, myq) : 0;
+  const int64_t si = (int64_t(b) * a.H + h) * a.Lg + gq;
+  const float lse2 = qvalid ? a.lse[si] * kLog2e : 0.f;
+  const float Dq = qvalid ? a.D[si] : 0.f;
+
+  int kt = next_live(0);
+  if (kt < nkt) {
+    gload(kt);
+    sstore(0, kt);
+  }
+  int buf = 0;
+  while (kt < nkt) {
+    const int kn = next_live(kt + 1);
+    if (kn < nkt) gload(kn);
+    __syncthreads();
+    const uint32_t kor = a.blk_or[kt], kand = a.blk_and[kt];
+    const int k0 = kt * BN, k1 = (k0 + BN - 1 < L ? k0 + BN - 1 : L - 1);
+    const bool wfull = !wave_live || (wand & kand) != 0u || (causal && k0 > wq1);
+    if (!wfull) {
+      const bool wclear = (wor & kor) == 0u && (!causal || k1 <= q0w) && (k0 + BN <= L);
+      const bool use_bits = (qor & kor) != 0u;
+      const char* Kb = smem + buf * STAGE;
+      const char* Vb = Kb + KBYTES;
+      f32x16 s[2], dp[2];
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          s[kb][r] = 0.f;
+          dp[kb][r] = 0.f;
+        }
+        const int row = 32 * kb + (lane & 31);
+#pragma unroll
+        for (int ks = 0; ks < DK; ++ks) {
+          const u32x4 ka = *(const u32x4*)(Kb + row * KP + (16 * ks + 8 * half) * 2);
+          s[kb] = mfma32<E>(bitcast_u4<vec8>(ka), qf[ks], s[kb]);
+          const u32x4 va = *(const u32x4*)(Vb + row * VP + (16 * ks + 8 * half) * 2);
+          dp[kb] = mfma32<E>(bitcast_u4<vec8>(va), of[ks], dp[kb]);
+        }
+      }
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          float p = fast_exp2(fmaf(s[kb][r], c, -lse2));
+          if (!wclear) {
+            const int kl = 32 * kb + 8 * (r >> 2) + 4 * half + (r & 3);
+            const int key = k0 + kl;
+            bool keep = key < L && (!causal || key <= myq);
+            if (use_bits) keep = keep && ((kbits_s[buf][kl] & qbits) == 0u);
+            if (!keep) p = 0.f;
+          }
+          s[kb][r] = p * (dp[kb][r] - Dq);  // dS^T
+        }
+#pragma unroll
+      for (int ks2 = 0; ks2 < 4; ++ks2) {
+        const int kb = ks2 >> 1, sub = ks2 & 1;
+        float pv[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) pv[e] = s[kb][8 * sub + e];
+        const vec8 bs = pack8<E>(pv);
+        const int row = 32 * kb + 16 * sub + 4 * half + ((lane & 15) >> 2);
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+          const int col = 32 * db + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+          const char* p0 = Kb + row * KP + col * 2;
+          dq[db] = mfma32<E>(lds_tr_pair<E>(p0, p0 + 8 * KP), bs, dq[db]);
+        }
+      }
+    }
+    if (kn < nkt) sstore(buf ^ 1, kn);
+    buf ^= 1;
+    kt = kn;
+  }
+  if (!qvalid) return;
+  float* dst = a.dq + (int64_t(b) * a.Lg + gq) * rs + int64_t(h) * D;
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      f32x4* p = (f32x4*)(dst + 32 * db + 8 * i + 4 * half);
+      f32x4 v = *p;
+      v[0] += a.scale * dq[db][4 * i];
+      v[1] += a.scale * dq[db][4 * i + 1];
+      v[2] += a.scale * dq[db][4 * i + 2];
+      v[3] += a.scale * dq[db][4 * i + 3];
+      *p = v;
+    }
+}
+
+template <typename E, int D>
+__global__ void __launch_bounds__(256, (D == 128 ? 1 : 2)) attn_bwd_dkdv(const BwdArgs a) {
+  constexpr int BK = 128, BQ = 64;
+  constexpr int P2 = D * 2 + 64;  // Q and dO tiles: transpose reads and row reads
+  constexpr int DK = D / 16, DB = D / 32, CHUNKS = D / 8, RPP = 256 / CHUNKS, PASSES = BQ / RPP;
+  typedef typename E::vec8 vec8;
+
+  __shared__ __attribute__((aligned(16))) char qs[BQ * P2];
+  __shared__ __attribute__((aligned(16))) char os[BQ * P2];
+  __shared__ __attribute__((aligned(16))) float lse_s[BQ];
+  __shared__ __attribute__((aligned(16))) float d_s[BQ];
+  __shared__ uint32_t qbits_s[BQ];
+  __shared__ DevRun runs_s[kMaxRuns];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5;
+  const int L = a.L;
+  const int64_t nstrips = (L + BK - 1) / BK;
+  const int64_t work = xcd_remap(blockIdx.x, nstrips * a.H * a.B);
+  const int strip = int(work % nstrips);
+  const int h = int((work / nstrips) % a.H);
+  const int b = int(work / (nstrips * a.H));
+  for (int i = tid; i < a.n_runs; i += 256) runs_s[i] = ((const DevRun*)a.runs)[i];
+
+  const int64_t rs = int64_t(a.H) * D;
+  const int64_t base = int64_t(b) * L * rs + int64_t(h) * D;
+  const uint16_t* Qg = (const uint16_t*)a.q + base;
+  const uint16_t* Kg = (const uint16_t*)a.k + base;
+  const uint16_t* Vg = (const uint16_t*)a.v + base;
+  const uint16_t* Og = (const uint16_t*)a.dO + base;
+  const float c = a.scale_log2;
+  const bool causal = a.causal != 0;
+
+  const int k0w = strip * BK + wave * 32;
+  const int mykey = k0w + (lane & 31);
+  const bool kvalid = mykey < L;
+  vec8 kf[DK], vf[DK];
+#pragma unroll
+  for (int ks = 0; ks < DK; ++ks) {
+    u32x4 u = {0u, 0u, 0u, 0u}, w = {0u, 0u, 0u, 0u};
+    if (kvalid) {
+      u = *(const u32x4*)(Kg + int64_t(mykey) * rs + ks * 16 + half * 8);
+      w = *(const u32x4*)(Vg + int64_t(mykey) * rs + ks * 16 + half * 8);
+    }
+    kf[ks] = bitcast_u4<vec8>(u);
+    vf[ks] = bitcast_u4<vec8>(w);
+  }
+
+  const int lastk_wg = (strip * BK + BK < L ? strip * BK + BK : L) - 1;
+  const int kb0 = strip * 2, kb1 = lastk_wg / 64;
+  const uint32_t kor = a.blk_or[kb0] | a.blk_or[kb1];
+  const uint32_t kand = a.blk_and[kb0] & a.blk_and[kb1];
+  const bool wave_live = k0w < L;
+  const int wk1 = wave_live ? (k0w + 31 < L ? k0w + 31 : L - 1) : 0;
+  const uint32_t wor = wave_live ? a.blk_or[k0w / 64] : 0u;
+  const uint32_t wand = wave_live ? a.blk_and[k0w / 64] : 0u;
+  const int nqt = (L + BQ - 1) / BQ;
+  const int first_key = strip * BK;
+  auto next_live = [&](int qt) -> int {
+    for (; qt < nqt; ++qt) {
+      if (causal && qt * BQ + BQ - 1 < first_key) continue;
+      if ((kand & a.blk_and[qt]) == 0u) return qt;
+    }
+    return nqt;
+  };
+
+  f32x16 dk[DB], dv[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      dk[db][r] = 0.f;
+      dv[db][r] = 0.f;
+    }
+
+  __syncthreads();
+  const uint32_t kbits = kvalid ? run_bits(runs_s, a.n_runs, mykey) : 0u;
+  const int64_t stat_base = (int64_t(b) * a.H + h) * a.Lg;
+
+  for (int qt = next_live(causal ? first_key / BQ : 0); qt < nqt; qt = next_live(qt + 1)) {
+    __syncthreads();  // every wave is done with the previous tile
+#pragma unroll
+    for (int p = 0; p < PASSES; ++p) {
+      const int row = p * RPP + tid / CHUNKS, ch = tid % CHUNKS, q = qt * BQ + row;
+      u32x4 zq = {0u, 0u, 0u, 0u}, zo = {0u, 0u, 0u, 0u};
+      if (q < L) {
+        zq = *(const u32x4*)(Qg + int64_t(q) * rs + ch * 8);
+        zo = *(const u32x4*)(Og + int64_t(q) * rs + ch * 8);
+      }
+      *(u32x4*)(qs + row * P2 + ch * 16) = zq;
+      *(u32x4*)(os + row * P2 + ch * 16) = zo;
+    }
+    const uint32_t qor = a.blk_or[qt], qand = a.blk_and[qt];
+    if (tid < BQ) {
+      const int q = qt * BQ + tid;
+      if (q < L) {
+        const int64_t g = run_global(runs_s, a.n_runs, q);
+        lse_s[tid] = a.lse[stat_base + g] * kLog2e;
+        d_s[tid] = a.D[stat_base + g];
+        qbits_s[tid] = run_bits(runs_s, a.n_runs, q);
+      } else {
+        lse_s[tid] = INFINITY;  // P = 0 for rows past the task
+        d_s[tid] = 0.f;
+        qbits_s[tid] = 0u;
+      }
+    }
+    __syncthreads();
+    const int q0 = qt * BQ;
+    const bool wfull = !wave_live || (wand & qand) != 0u || (causal && q0 + BQ - 1 < k0w);
+    if (wfull) continue;
+    const bool wclear = (wor & qor) == 0u && (!causal || q0 >= wk1);
+    const bool use_bits = (kor & qor) != 0u;
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+      f32x16 s, dp;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        s[r] = 0.f;
+        dp[r] = 0.f;
+      }
+      const int row = 32 * qb + (lane & 31);
+#pragma unroll
+      for (int ks = 0; ks < DK; ++ks) {
+        const u32x4 qa = *(const u32x4*)(qs + row * P2 + (16 * ks + 8 * half) * 2);
+        s = mfma32<E>(bitcast_u4<vec8>(qa), kf[ks], s);
+        const u32x4 oa = *(const u32x4*)(os + row * P2 + (16 * ks + 8 * half) * 2);
+        dp = mfma32<E>(bitcast_u4<vec8>(oa), vf[ks], dp);
+      }
+      float pr[16];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int ql = 32 * qb + 8 * i + 4 * half;
+        const f32x4 l4 = *(const f32x4*)(lse_s + ql);
+        const f32x4 d4 = *(const f32x4*)(d_s + ql);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int r = 4 * i + j;
+          float p = fast_exp2(fmaf(s[r], c, -l4[j]));
+          if (!wclear) {
+            const int q = q0 + ql + j;
+            bool keep = (!causal || mykey <= q);
+            if (use_bits) keep = keep && ((qbits_s[ql + j] & kbits) == 0u);
+            if (!keep) p = 0.f;
+          }
+          pr[r] = p;
+          s[r] = p * (dp[r] - d4[j]);  // dS
+        }
+      }
+#pragma unroll
+      for (int sub = 0; sub < 2; ++sub) {
+        const vec8 bp = pack8<E>(pr + 8 * sub);
+        float dsv[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) dsv[e] = s[8 * sub + e];
+        const vec8 bs = pack8<E>(dsv);
+        const int trow = 32 * qb + 16 * sub + 4 * half + ((lane & 15) >> 2);
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+          const int col = 32 * db + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+          const char* po = os + trow * P2 + col * 2;
+          dv[db] = mfma32<E>(lds_tr_pair<E>(po, po + 8 * P2), bp, dv[db]);
+          const char* pq = qs + trow * P2 + col * 2;
+          dk[db] = mfma32<E>(lds_tr_pair<E>(pq, pq + 8 * P2), bs, dk[db]);
+        }
+      }
+    }
+  }
+  if (!kvalid) return;
+  const int64_t gk = run_global(runs_s, a.n_runs, mykey);
+  float* dkp = a.dk + (int64_t(b) * a.Lg + gk) * rs + int64_t(h) * D;
+  float* dvp = a.dv + (int64_t(b) * a.Lg + gk) * rs + int64_t(h) * D;
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int off = 32 * db + 8 * i + 4 * half;
+      f32x4 x = *(f32x4*)(dkp + off), y = *(f32x4*)(dvp + off);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        x[j] += a.scale * dk[db][4 * i + j];
+        y[j] += dv[db][4 * i + j];
+      }
+      *(f32x4*)(dkp + off) = x;
+      *(f32x4*)(dvp + off) = y;
+    }
+}
+
+template <typename E, int D>
+static hipError_t launch_dq_t(const BwdArgs& a, hipStream_t s) {
+  const int64_t n = ((a.L + 127) / 128) * int64_t(a.H) * a.B;
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL((attn_bwd_dq<E, D>), dim3(unsigned(n)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+template <typename E, int D>
+static hipError_t launch_dkdv_t(const BwdArgs& a, hipStream_t s) {
+  const int64_t n = ((a.L + 127) / 128) * int64_t(a.H) * a.B;
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL((attn_bwd_dkdv<E, D>), dim3(unsigned(n)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd_dq(cqsa_dtype dt, int d, const BwdArgs& a, hipStream_t s) {
+  if (a.n_runs > kMaxRuns) return hipErrorInvalidValue;
+  if (dt == CQSA_BF16) return d == 128 ? launch_dq_t<BF16, 128>(a, s) : launch_dq_t<BF16, 64>(a, s);
+  if (dt == CQSA_F16) return d == 128 ? launch_dq_t<F16, 128>(a, s) : launch_dq_t<F16, 64>(a, s);
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_bwd_dkdv(cqsa_dtype dt, int d, const BwdArgs& a, hipStream_t s) {
+  if (a.n_runs > kMaxRuns) return hipErrorInvalidValue;
+  if (dt == CQSA_BF16) return d == 128 ? launch_dkdv_t<BF16, 128>(a, s) : launch_dkdv_t<BF16, 64>(a, s);
+  if (dt == CQSA_F16) return d == 128 ? launch_dkdv_t<F16, 128>(a, s) : launch_dkdv_t<F16, 64>(a, s);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace cqsa

@@ -24,12 +24,6 @@
 
 namespace cqsa {
 
-__device__ __forceinline__ uint32_t run_bits(const DevRun* runs, int n, int64_t local) {
-  for (int i = 0; i < n; ++i)
-    if (local < runs[i].local_start + runs[i].length) return runs[i].bits;
-  return 0u;
-}
-
 template <typename E, int D, int MODE>
 __global__ void __launch_bounds__(256, 2) attn_fwd_mfma(const FwdArgs a) {
   constexpr int BM = 128, BN = 64;

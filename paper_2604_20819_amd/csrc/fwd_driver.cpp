@@ -309,12 +309,25 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
       }
       const char* srcs[3] = {(const char*)Q->data, (const char*)K->data, (const char*)V->data};
       char* dsts[3] = {S.q, S.k, S.v};
-      for (int x = 0; x < 3; ++x)
-        for (const Run& r : task.runs)
-          for (int64_t b = 0; b < B; ++b)
-            CQSA_HIP(hipMemcpyAsync(dsts[x] + (b * Li + r.local_start) * row_bytes,
-                                    srcs[x] + (b * L + r.global_start) * row_bytes,
-                                    r.length * row_bytes, kind, C->copy));
+      if (in_dev) {
+        // device inputs: one gather kernel over the runs of all three tensors
+        StageArgs sa{};
+        for (int x = 0; x < 3; ++x) {
+          sa.src[x] = srcs[x];
+          sa.dst[x] = dsts[x];
+        }
+        sa.n_tensors = 3; sa.row_bytes = int64_t(row_bytes); sa.Li = Li; sa.Lg = L;
+        sa.B = int32_t(B); sa.runs = d_tab + to.runs; sa.n_runs = int32_t(task.runs.size());
+        CQSA_HIP(launch_stage(sa, C->copy));
+      } else {
+        // host inputs: one asynchronous H2D copy per run and batch element
+        for (int x = 0; x < 3; ++x)
+          for (const Run& r : task.runs)
+            for (int64_t b = 0; b < B; ++b)
+              CQSA_HIP(hipMemcpyAsync(dsts[x] + (b * Li + r.local_start) * row_bytes,
+                                      srcs[x] + (b * L + r.global_start) * row_bytes,
+                                      r.length * row_bytes, kind, C->copy));
+      }
       const uint64_t moved = uint64_t(3) * B * Li * row_bytes;
       if (in_dev)
         rec.stats.d2d_bytes += moved;

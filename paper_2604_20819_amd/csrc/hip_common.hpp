@@ -105,6 +105,19 @@ struct DevRun {
   uint32_t pad;
 };
 
+// Group bits and global index of a task-local token (runs sorted by local start).
+__device__ __forceinline__ uint32_t run_bits(const DevRun* runs, int n, int64_t local) {
+  for (int i = 0; i < n; ++i)
+    if (local < runs[i].local_start + runs[i].length) return runs[i].bits;
+  return 0u;
+}
+__device__ __forceinline__ int64_t run_global(const DevRun* runs, int n, int64_t local) {
+  for (int i = 0; i < n; ++i)
+    if (local < runs[i].local_start + runs[i].length)
+      return runs[i].global_start + (local - runs[i].local_start);
+  return 0;
+}
+
 // Work-group id remapped so that consecutive work items land on the same XCD
 // (the dispatcher deals work groups round-robin over the 8 XCDs, each with its
 // own L2): work item w = xcd * per_xcd + slot.

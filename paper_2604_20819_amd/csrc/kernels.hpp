@@ -50,10 +50,52 @@ struct MergeArgs {
   int32_t B, H, d;
 };
 
+// Inner backward kernels over one staged task (App. A.1, Eq. "globallse").
+struct BwdArgs {
+  const void* q;        // [B, L, H, d] staged task rows (seq_rows = L)
+  const void* k;
+  const void* v;
+  const void* dO;
+  int32_t L;            // task length
+  int32_t B, H;
+  int32_t causal;
+  float scale_log2;     // softmax scale * log2(e)
+  float scale;          // softmax scale (dQ = scale dS K, dK = scale dS^T Q)
+  const void* runs;     // DevRun[n_runs]
+  int32_t n_runs;
+  const uint32_t* blk_or;
+  const uint32_t* blk_and;
+  const float* lse;     // [B, H, Lg] global natural-log LSE from the forward
+  const float* D;       // [B, H, Lg] global rowsum(dO * O)
+  int64_t Lg;           // global sequence length
+  float* dq;            // [B, Lg, H, d] global fp32 gradients (scatter-added)
+  float* dk;
+  float* dv;
+};
+
+// Copy the rows of a task's runs from up to four [B, Lg, H, d] tensors into
+// task-local [B, Li, H, d] staging buffers (device to device).
+struct StageArgs {
+  const void* src[4];
+  void* dst[4];
+  int32_t n_tensors;
+  int64_t row_bytes;    // H * d * elem
+  int64_t Li, Lg;
+  int32_t B;
+  const void* runs;     // DevRun[n_runs]
+  int32_t n_runs;
+};
+
 hipError_t launch_fwd(cqsa_dtype dt, int d, FwdMode mode, const FwdArgs& a, hipStream_t s);
 hipError_t launch_acc_init(float* acc, float* m, float* l, int64_t n_acc, int64_t n_stat,
                            hipStream_t s);
 hipError_t launch_recompose(const MergeArgs& a, hipStream_t s);
+hipError_t launch_stage(const StageArgs& a, hipStream_t s);
+hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t s);
+hipError_t launch_bwd_preprocess(const void* dO, const float* O, float* D, cqsa_dtype dt,
+                                 int64_t B, int64_t L, int64_t H, int d, hipStream_t s);
+hipError_t launch_bwd_dkdv(cqsa_dtype dt, int d, const BwdArgs& a, hipStream_t s);
+hipError_t launch_bwd_dq(cqsa_dtype dt, int d, const BwdArgs& a, hipStream_t s);
 hipError_t launch_finalize(float* acc, float* m, const float* l, int64_t B, int64_t L, int64_t H,
                            int d, hipStream_t s);
 
