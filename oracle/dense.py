@@ -30,7 +30,7 @@ def _scale(d, scale):
     return 1.0 / np.sqrt(d) if scale is None else float(scale)
 
 
-def attention_forward(Q, K, V, causal, scale=None, rows=None, row_chunk=64):
+def attention_forward(Q, K, V, causal, scale=None, rows=None, row_chunk=16):
     """Dense forward on a subset of query rows.
 
     Q, K, V: [B, L, H, d].  rows: None (all rows) or an int array of query

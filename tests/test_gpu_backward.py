@@ -13,6 +13,7 @@ import concurrent.futures
 import numpy as np
 import pytest
 import torch
+from threadpoolctl import threadpool_limits
 
 import paper_2604_20819_amd as cq
 from oracle import dense
@@ -53,7 +54,7 @@ def oracle_grads(Q, K, V, dO, causal, workers=8):
         for i in range(3):
             out[i][sl] = g[i]
 
-    with concurrent.futures.ThreadPoolExecutor(workers) as ex:
+    with threadpool_limits(1), concurrent.futures.ThreadPoolExecutor(workers) as ex:
         list(ex.map(one, [(b, h) for b in range(B) for h in range(H)]))
     return out
 

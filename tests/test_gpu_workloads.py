@@ -1,0 +1,120 @@
+"""Full-size GPU parity of the two budget-capped forward workloads.
+
+* fp16 causal, B=1 H=32 d=128 L=131072, 8 GB device budget: the planner must
+  recurse to depth >= 2; 2048 sampled query rows per head against float64, all
+  rows against the undecomposed kernel (which fits at this size).
+* streamed out-of-core, bf16 non-causal, B=1 H=8 d=128 L=1048576, inputs and
+  outputs in pinned host memory, 4 GB device budget (the accumulator is merged
+  on the host); 4096 sampled query rows per head against float64, and the
+  host-link traffic is checked against the plan.
+Tolerances as in test_gpu_forward: max |O - O_f64| <= 1e-2 and a relative-L2
+bound from the 16-bit rounding of P (4e-3 bf16, 6e-4 fp16).
+"""
+import concurrent.futures
+
+import numpy as np
+import pytest
+import torch
+from threadpoolctl import threadpool_limits
+
+import paper_2604_20819_amd as cq
+from oracle import dense
+from paper_2604_20819_amd import synth
+from tests.gpu_util import need_gpu, rel_l2, run_forward, say
+
+pytestmark = pytest.mark.gpu
+GB = 10 ** 9
+
+
+def oracle_rows(Q, K, V, causal, rows, workers=16, chunk=64):
+    """Dense float64 forward on per-head sampled rows.  Work items are
+    (head, 64-row chunk) pairs run on `workers` threads with one BLAS thread
+    each (numpy releases the GIL inside matmul and exp)."""
+    B, L, H, d = Q.shape
+    R = len(rows[0])
+    O = np.zeros((B, R, H, d))
+    LSE = np.zeros((B, H, R))
+    kv = {}
+
+    def head(h):
+        if h not in kv:
+            kv[h] = (synth.as_f64(Q[:, :, h:h + 1]), synth.as_f64(K[:, :, h:h + 1]),
+                     synth.as_f64(V[:, :, h:h + 1]))
+        return kv[h]
+
+    for h in range(H):
+        head(h)
+    items = [(h, c0) for h in range(H) for c0 in range(0, R, chunk)]
+    done = [0]
+
+    def one(item):
+        h, c0 = item
+        q, k, v = kv[h]
+        r = rows[h][c0:c0 + chunk]
+        o, lse = dense.attention_forward(q, k, v, causal, rows=r)
+        O[:, c0:c0 + len(r), h] = o[:, :, 0]
+        LSE[:, h, c0:c0 + len(r)] = lse[:, 0]
+        done[0] += 1
+        if done[0] % max(1, len(items) // 16) == 0:
+            say(f"oracle {done[0]}/{len(items)} row chunks")
+
+    with threadpool_limits(1), concurrent.futures.ThreadPoolExecutor(workers) as ex:
+        list(ex.map(one, items))
+    return O, LSE
+
+
+def gather_rows(O, LSE, rows):
+    Og = np.stack([O[:, r, h].double().numpy() for h, r in enumerate(rows)], axis=2)
+    Lg = np.stack([LSE[:, h, r].double().numpy() for h, r in enumerate(rows)], axis=1)
+    return Og, Lg
+
+
+def check(Og, Lg, Of, Lf, rel):
+    err = float(np.abs(Og - Of).max())
+    r = rel_l2(Og, Of)
+    lerr = float(np.abs(Lg - Lf).max())
+    say(f"max_abs={err:.3e} rel_l2={r:.3e} lse_abs={lerr:.3e}")
+    assert np.isfinite(Og).all() and np.isfinite(Lg).all()
+    assert err <= 1e-2 and r <= rel and lerr <= 1e-4
+
+
+def test_fp16_causal_L131072_budget_8GB():
+    need_gpu()
+    say("fp16 causal B=1 H=32 d=128 L=131072 budget 8GB")
+    B, L, H, d = 1, 131072, 32, 128
+    Q, K, V = synth.make_inputs(20819 + 3, B, L, H, d, "f16")
+    O, LSE, plan = run_forward(Q, K, V, True, budget=8 * GB)
+    say(f"depth={plan.depth} tasks={plan.num_tasks} modelled={plan.modelled_device_bytes / GB:.3f} GB")
+    assert plan.depth >= 2 and plan.modelled_device_bytes <= 8 * GB
+    rows = synth.sample_rows(20819 + 3, L, 2048, H)
+    Of, Lf = oracle_rows(Q, K, V, True, rows)
+    check(*gather_rows(O, LSE, rows), Of, Lf, 6e-4)
+    O0, L0, _ = run_forward(Q, K, V, True, depth=0)
+    r = rel_l2(O.numpy(), O0.numpy())
+    say(f"rel_l2 vs depth 0 = {r:.3e}")
+    assert r <= 1e-3
+
+
+def test_bf16_streamed_L1M_host_budget_4GB():
+    need_gpu()
+    say("bf16 streamed B=1 H=8 d=128 L=1048576 host-resident budget 4GB")
+    B, L, H, d = 1, 1 << 20, 8, 128
+    Q, K, V = synth.make_inputs(20819 + 5, B, L, H, d, "bf16", pin_memory=True)
+    cq.cqsa_set_timing(True)
+    try:
+        O, LSE, plan = run_forward(Q, K, V, False, budget=4 * GB, host=True)
+        st = cq.cqsa_last_stats()
+    finally:
+        cq.cqsa_set_timing(False)
+    say(f"depth={plan.depth} tasks={plan.num_tasks} modelled={plan.modelled_device_bytes / GB:.3f} GB "
+        f"workspace={st['workspace_bytes'] / GB:.3f} GB h2d={st['h2d_bytes'] / GB:.1f} GB "
+        f"d2h={st['d2h_bytes'] / GB:.1f} GB wall={st['ms_wall']:.0f} ms "
+        f"stage={st['ms_stage']:.0f} ms d2h={st['ms_d2h']:.0f} ms merge={st['ms_merge']:.0f} ms")
+    assert plan.depth >= 2 and plan.modelled_device_bytes <= 4 * GB
+    assert st["workspace_bytes"] <= plan.modelled_device_bytes
+    Ls = [plan.task(t)["L_local"] for t in range(plan.num_tasks)]
+    assert st["h2d_bytes"] == 3 * sum(Ls) * H * d * 2
+    assert st["d2h_bytes"] == sum(Ls) * H * (d + 2) * 4
+    rows = synth.sample_rows(20819 + 5, L, 4096, H)
+    Of, Lf = oracle_rows(Q, K, V, False, rows)
+    check(*gather_rows(O, LSE, rows), Of, Lf, 4e-3)
