@@ -78,10 +78,16 @@ __global__ void __launch_bounds__(256, (D == 128 ? 1 : 2)) attn_bwd_dq(const Bwd
   const uint32_t wor = wave_live ? a.blk_or[q0w / 64] : 0u;
   const uint32_t wand = wave_live ? a.blk_and[q0w / 64] : 0u;
   const int nkt = (L + BN - 1) / BN;
-  auto next_live = [&](int kt) -> int {
+  // next live tile and its summaries, read before the tile prefetch is issued
+  auto next_live = [&](int kt, uint32_t& kor_out, uint32_t& kand_out) -> int {
     for (; kt < nkt; ++kt) {
       if (causal && kt * BN > lastq_wg) return nkt;
-      if ((qand & a.blk_and[kt]) == 0u) return kt;
+      const uint32_t an = a.blk_and[kt];
+      if ((qand & an) == 0u) {
+        kand_out = an;
+        kor_out = a.blk_or[kt];
+        return kt;
+      }
     }
     return nkt;
   };
@@ -100,7 +106,7 @@ __global__ void __launch_bounds__(256, (D == 128 ? 1 : 2)) attn_bwd_dq(const Bwd
       vreg[p] = zv;
     }
   };
-  auto sstore = [&](int buf, int kt) {
+  auto sstore = [&](int buf, int kt, uint32_t kor_t) {
     char* kb = smem + buf * STAGE;
     char* vb = kb + KBYTES;
 #pragma unroll
@@ -109,7 +115,7 @@ __global__ void __launch_bounds__(256, (D == 128 ? 1 : 2)) attn_bwd_dq(const Bwd
       *(u32x4*)(kb + row * KP + ch * 16) = kreg[p];
       *(u32x4*)(vb + row * VP + ch * 16) = vreg[p];
     }
-    if ((qor & a.blk_or[kt]) != 0u && tid < BN) {
+    if ((qor & kor_t) != 0u && tid < BN) {
       const int key = kt * BN + tid;
       kbits_s[buf][tid] = key < L ? run_bits(runs_s, a.n_runs, key) : 0u;
     }
@@ -128,17 +134,18 @@ __global__ void __launch_bounds__(256, (D == 128 ? 1 : 2)) attn_bwd_dq(const Bwd
   const float lse2 = qvalid ? a.lse[si] * kLog2e : 0.f;
   const float Dq = qvalid ? a.D[si] : 0.f;
 
-  int kt = next_live(0);
+  uint32_t kor = 0u, kand = 0u;
+  int kt = next_live(0, kor, kand);
   if (kt < nkt) {
     gload(kt);
-    sstore(0, kt);
+    sstore(0, kt, kor);
   }
   int buf = 0;
   while (kt < nkt) {
-    const int kn = next_live(kt + 1);
+    uint32_t nor = 0u, nand = 0u;
+    const int kn = next_live(kt + 1, nor, nand);
     if (kn < nkt) gload(kn);
-    __syncthreads();
-    const uint32_t kor = a.blk_or[kt], kand = a.blk_and[kt];
+    lds_barrier();
     const int k0 = kt * BN, k1 = (k0 + BN - 1 < L ? k0 + BN - 1 : L - 1);
     const bool wfull = !wave_live || (wand & kand) != 0u || (causal && k0 > wq1);
     if (!wfull) {
@@ -193,9 +200,11 @@ __global__ void __launch_bounds__(256, (D == 128 ? 1 : 2)) attn_bwd_dq(const Bwd
         }
       }
     }
-    if (kn < nkt) sstore(buf ^ 1, kn);
+    if (kn < nkt) sstore(buf ^ 1, kn, nor);
     buf ^= 1;
     kt = kn;
+    kor = nor;
+    kand = nand;
   }
   if (!qvalid) return;
   float* dst = a.dq + (int64_t(b) * a.Lg + gq) * rs + int64_t(h) * D;

@@ -82,35 +82,40 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_mfma(const FwdArgs a) {
   const uint32_t wand = wave_live ? a.blk_and[q0w / 64] : 0u;
 
   const int nkt = (L + BN - 1) / BN;
-  auto full_wg = [&](int kt) -> bool {
-    if (causal && kt * BN > lastq_wg) return true;
-    return (qand & a.blk_and[kt]) != 0u;
-  };
-  auto next_live = [&](int kt) -> int {
-    while (kt < nkt) {
+  // Next tile at or after kt that is not fully masked for the strip, with its
+  // block summaries.  Called before the tile prefetch is issued, so waiting on
+  // these small loads never waits on the prefetch.
+  auto next_live = [&](int kt, uint32_t& kor_out, uint32_t& kand_out) -> int {
+    for (; kt < nkt; ++kt) {
       if (causal && kt * BN > lastq_wg) return nkt;
-      if (!full_wg(kt)) return kt;
-      ++kt;
+      const uint32_t an = a.blk_and[kt];
+      if ((qand & an) == 0u) {
+        kand_out = an;
+        kor_out = a.blk_or[kt];
+        return kt;
+      }
     }
     return nkt;
   };
 
+  // Tile loads through a per-tile buffer resource (SGPR base, fixed 32-bit
+  // per-thread offsets); rows past the task end read as zero.
   u32x4 kreg[PASSES], vreg[PASSES];
+  uint32_t goff[PASSES];
+#pragma unroll
+  for (int p = 0; p < PASSES; ++p)
+    goff[p] = uint32_t(((p * RPP + tid / CHUNKS) * rs + (tid % CHUNKS) * 8) * 2);
   auto gload = [&](int kt) {
+    const int64_t rows = int64_t(L) - int64_t(kt) * BN;
+    const __amdgpu_buffer_rsrc_t rk = row_rsrc(Kg + int64_t(kt) * BN * rs, rows, rs * 2, D * 2);
+    const __amdgpu_buffer_rsrc_t rv = row_rsrc(Vg + int64_t(kt) * BN * rs, rows, rs * 2, D * 2);
 #pragma unroll
     for (int p = 0; p < PASSES; ++p) {
-      const int row = p * RPP + tid / CHUNKS, ch = tid % CHUNKS;
-      const int key = kt * BN + row;
-      u32x4 zk = {0u, 0u, 0u, 0u}, zv = {0u, 0u, 0u, 0u};
-      if (key < L) {
-        zk = *(const u32x4*)(Kg + int64_t(key) * rs + ch * 8);
-        zv = *(const u32x4*)(Vg + int64_t(key) * rs + ch * 8);
-      }
-      kreg[p] = zk;
-      vreg[p] = zv;
+      kreg[p] = buf_load16(rk, goff[p]);
+      vreg[p] = buf_load16(rv, goff[p]);
     }
   };
-  auto sstore = [&](int buf, int kt) {
+  auto sstore = [&](int buf, int kt, uint32_t kor_t) {
     char* kb = smem + buf * STAGE;
     char* vb = kb + KBYTES;
 #pragma unroll
@@ -120,7 +125,7 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_mfma(const FwdArgs a) {
       *(u32x4*)(vb + row * VP + ch * 16) = vreg[p];
     }
     // group bits of the tile's keys, only when the CQS mask can bite here
-    if ((qor & a.blk_or[kt]) != 0u && tid < BN) {
+    if ((qor & kor_t) != 0u && tid < BN) {
       const int key = kt * BN + tid;
       kbits_s[buf][tid] = key < L ? run_bits(runs_s, a.n_runs, key) : 0u;
     }
@@ -136,19 +141,20 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_mfma(const FwdArgs a) {
   __syncthreads();  // runs_s visible
   const uint32_t qbits = qvalid ? run_bits(runs_s, a.n_runs, myq) : 0u;
 
-  int kt = next_live(0);
+  uint32_t kor = 0u, kand = 0u;
+  int kt = next_live(0, kor, kand);
   if (kt < nkt) {
     gload(kt);
-    sstore(0, kt);
+    sstore(0, kt, kor);
   }
   int buf = 0;
   while (kt < nkt) {
-    const int kn = next_live(kt + 1);
+    uint32_t nor = 0u, nand = 0u;
+    const int kn = next_live(kt + 1, nor, nand);
     if (kn < nkt) gload(kn);
-    __syncthreads();
+    lds_barrier();
 
     // ---- compute on tile kt (wave-uniform verdict) ----
-    const uint32_t kor = a.blk_or[kt], kand = a.blk_and[kt];
     const int k0 = kt * BN, k1 = (k0 + BN - 1 < L ? k0 + BN - 1 : L - 1);
     const bool wfull = !wave_live || (wand & kand) != 0u || (causal && k0 > wq1);
     if (!wfull) {
@@ -189,11 +195,14 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_mfma(const FwdArgs a) {
       const float msafe = mnew == -INFINITY ? 0.f : mnew;
       const float alpha = fast_exp2(m_run - msafe);
       m_run = mnew;
-      l_run *= alpha;
+      // integer maxima change rarely: rescale only when some lane's did
+      if (__builtin_amdgcn_ballot_w64(alpha != 1.f) != 0ull) {
+        l_run *= alpha;
 #pragma unroll
-      for (int db = 0; db < DB; ++db)
+        for (int db = 0; db < DB; ++db)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
+          for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
+      }
       float psum = 0.f;
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
@@ -222,9 +231,11 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_mfma(const FwdArgs a) {
       }
     }
     // ---- stage the next tile into the other buffer ----
-    if (kn < nkt) sstore(buf ^ 1, kn);
+    if (kn < nkt) sstore(buf ^ 1, kn, nor);
     buf ^= 1;
     kt = kn;
+    kor = nor;
+    kand = nand;
   }
 
   const float l_tot = l_run + swap_halves(l_run);

@@ -226,7 +226,7 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
   }
 
   // ---- ordering against the caller's stream and the previous call ----
-  while (C->sync_events.size() < size_t(4 * nslot + 2)) {
+  while (C->sync_events.size() < size_t(4 * nslot + 3)) {
     hipEvent_t e;
     CQSA_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
     C->sync_events.push_back(e);
@@ -235,6 +235,7 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
   hipEvent_t* ev_staged = &C->sync_events[2];
   hipEvent_t* ev_free = &C->sync_events[2 + nslot];
   hipEvent_t* ev_done = &C->sync_events[2 + 2 * nslot];
+  hipEvent_t ev_rec = C->sync_events[2 + 4 * nslot];  // last recompose issued
   if (C->ws_free_valid) CQSA_HIP(hipStreamWaitEvent(st, C->ws_free, 0));
   CQSA_HIP(hipEventRecord(ev_start, st));
   CQSA_HIP(hipStreamWaitEvent(C->copy, ev_start, 0));
@@ -291,6 +292,7 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
     }
     HostMerger merger;
     std::vector<int64_t> last_item(nslot, -1);
+    bool rec_issued = false;
     std::vector<bool> used(nslot, false);
     const hipMemcpyKind kind = in_dev ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice;
     for (int64_t t = 0; t < ntask; ++t) {
@@ -338,7 +340,11 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
         rec.spans[kStStage].push_back(sp);
       }
       CQSA_HIP(hipEventRecord(ev_staged[si], C->copy));
-      CQSA_HIP(hipStreamWaitEvent(st, ev_staged[si], 0));
+      // Consecutive tasks alternate between the caller's stream and a second
+      // compute stream, so a task's kernel fills the tail of the previous one
+      // (two tasks in flight, App. A.3).  Inner kernels write only their slot.
+      const hipStream_t ls = (t & 1) ? C->lane : st;
+      CQSA_HIP(hipStreamWaitEvent(ls, ev_staged[si], 0));
       // inner kernel
       FwdArgs a{};
       a.q = S.q; a.k = S.k; a.v = S.v;
@@ -350,15 +356,17 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
       a.acc = S.acc; a.m = S.m; a.l = S.l; a.out_rows = Li;
       if (rec.timing) {
         sp = {rec.make(), rec.make()};
-        CQSA_HIP(hipEventRecord(sp.first, st));
+        CQSA_HIP(hipEventRecord(sp.first, ls));
       }
-      CQSA_HIP(launch_fwd(o.dtype, int(d), kModeStats, a, st));
+      CQSA_HIP(launch_fwd(o.dtype, int(d), kModeStats, a, ls));
       rec.stats.inner_launches += 1;
       if (rec.timing) {
-        CQSA_HIP(hipEventRecord(sp.second, st));
+        CQSA_HIP(hipEventRecord(sp.second, ls));
         rec.spans[kStInner].push_back(sp);
       }
       if (acc_dev) {
+        // recomposes touch shared rows: each waits for the one before it
+        if (rec_issued) CQSA_HIP(hipStreamWaitEvent(ls, ev_rec, 0));
         MergeArgs mg{};
         mg.acc_i = S.acc; mg.m_i = S.m; mg.l_i = S.l;
         mg.acc = acc; mg.m = m; mg.l = l;
@@ -366,14 +374,16 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
         mg.Li = Li; mg.L = L; mg.B = int32_t(B); mg.H = int32_t(H); mg.d = int32_t(d);
         if (rec.timing) {
           sp = {rec.make(), rec.make()};
-          CQSA_HIP(hipEventRecord(sp.first, st));
+          CQSA_HIP(hipEventRecord(sp.first, ls));
         }
-        CQSA_HIP(launch_recompose(mg, st));
+        CQSA_HIP(launch_recompose(mg, ls));
         if (rec.timing) {
-          CQSA_HIP(hipEventRecord(sp.second, st));
+          CQSA_HIP(hipEventRecord(sp.second, ls));
           rec.spans[kStMerge].push_back(sp);
         }
-        CQSA_HIP(hipEventRecord(ev_free[si], st));
+        CQSA_HIP(hipEventRecord(ev_rec, ls));
+        rec_issued = true;
+        CQSA_HIP(hipEventRecord(ev_free[si], ls));
       } else {
         // hand the statistics to the host: D2H into pinned staging, then merge;
         // the staging of this slot must have been consumed by its last merge
@@ -383,7 +393,7 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
         float* h_acc = (float*)hp;
         float* h_m = (float*)(hp + align_up(uint64_t(B) * p->max_L_local * H * d * 4));
         float* h_l = (float*)((char*)h_m + align_up(uint64_t(B) * p->max_L_local * H * 4));
-        CQSA_HIP(hipEventRecord(ev_done[si], st));
+        CQSA_HIP(hipEventRecord(ev_done[si], ls));
         CQSA_HIP(hipStreamWaitEvent(C->d2h, ev_done[si], 0));
         if (rec.timing) {
           sp = {rec.make(), rec.make()};
@@ -412,6 +422,7 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
       used[si] = true;
     }
     if (acc_dev) {
+      if (rec_issued) CQSA_HIP(hipStreamWaitEvent(st, ev_rec, 0));
       std::pair<hipEvent_t, hipEvent_t> sp{nullptr, nullptr};
       if (rec.timing) {
         sp = {rec.make(), rec.make()};
@@ -425,6 +436,10 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
     } else {
       if (!merger.finish()) return fail(CQSA_ERR_HIP, "host merge: event wait failed");
       host_finalize(acc, m, l, B, L, H, d);
+      // the second compute stream's last kernel precedes its D2H, which the
+      // merges waited for; order the caller's stream after it all the same
+      CQSA_HIP(hipEventRecord(ev_done[0], C->d2h));
+      CQSA_HIP(hipStreamWaitEvent(st, ev_done[0], 0));
     }
   }
   if (rec.timing) CQSA_HIP(hipEventRecord(rec.wall1, st));

@@ -92,6 +92,32 @@ __device__ __forceinline__ float swap_halves(float v) {
   return __builtin_bit_cast(float, lane < 32 ? r[1] : r[0]);
 }
 
+// Raw buffer resource over `rows` rows of a [.., rows, H, d] tensor starting at
+// `base` (row pitch `pitch_elems` 16-bit elements, `d` elements per row).  The
+// range ends at the last element of row rows-1, so loads of later rows return
+// zero (buffer range check) and every address is an SGPR base plus a 32-bit
+// per-lane offset.  The last dword selects the raw (untyped) buffer format.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t row_rsrc(const void* base, int64_t rows,
+                                                           int64_t pitch_bytes, int64_t row_bytes) {
+  int64_t bytes = rows > 0 ? (rows - 1) * pitch_bytes + row_bytes : 0;
+  if (bytes > 0x7fffffff) bytes = 0x7fffffff;
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
+                                           0x00020000);
+}
+
+__device__ __forceinline__ u32x4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t voff) {
+  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, 0, 0));
+}
+
+// Work-group barrier that orders LDS only.  __syncthreads() also orders
+// global memory, which makes every wave wait for its in-flight global loads
+// (the next tile's prefetch) at the barrier.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 __device__ __forceinline__ int lane_id() {
   return (int)__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
 }

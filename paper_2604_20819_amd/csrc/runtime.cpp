@@ -32,6 +32,7 @@ DevCtx* device_ctx(cqsa_status* st) {
     c->device = dev;
     if ((e = hipStreamCreateWithFlags(&c->copy, hipStreamNonBlocking)) != hipSuccess ||
         (e = hipStreamCreateWithFlags(&c->d2h, hipStreamNonBlocking)) != hipSuccess ||
+        (e = hipStreamCreateWithFlags(&c->lane, hipStreamNonBlocking)) != hipSuccess ||
         (e = hipEventCreateWithFlags(&c->ws_free, hipEventDisableTiming)) != hipSuccess) {
       *st = hip_fail(e, "creating library streams");
       return nullptr;

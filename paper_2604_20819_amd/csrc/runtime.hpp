@@ -22,6 +22,7 @@ struct DevCtx {
   bool ready = false;
   hipStream_t copy = nullptr;   // staging copies (H2D or D2D)
   hipStream_t d2h = nullptr;    // statistics device -> host
+  hipStream_t lane = nullptr;   // second compute stream: odd tasks' inner kernels
   hipEvent_t ws_free = nullptr; // recorded after the last call's last use of the workspace
   bool ws_free_valid = false;
   void* ws = nullptr;           // cached device workspace (built-in allocator)
