@@ -14,8 +14,9 @@
 //
 // gfx950 layouts: the dQ kernel works on S^T (lane = query) like the forward
 // and reads K^T operands with ds_read_b64_tr_b16; the dK/dV kernel works on S
-// (lane = key), keeps the wave's K and V rows as register operands, and reads
-// dO^T and Q^T operands from row-major LDS tiles with the transpose read.
+// (lane = key), keeps the wave's K rows as register operands and the work
+// group's V rows in LDS, and reads dO^T and Q^T operands from row-major LDS
+// tiles with the transpose read.
 #include "hip_common.hpp"
 #include "kernels.hpp"
 
@@ -24,7 +25,7 @@ namespace cqsa {
 constexpr float kLog2e = 1.4426950408889634f;
 
 template <typename E, int D>
-__global__ void __launch_bounds__(256, (D == 128 ? 1 : 2)) attn_bwd_dq(const BwdArgs a) {
+__global__ void __launch_bounds__(256, 2) attn_bwd_dq(const BwdArgs a) {
   constexpr int BM = 128, BN = 64;
   constexpr int KP = D * 2 + 64;  // K tile: transpose reads and row reads
   constexpr int VP = D * 2 + 16;  // V tile: row reads
@@ -92,18 +93,20 @@ __global__ void __launch_bounds__(256, (D == 128 ? 1 : 2)) attn_bwd_dq(const Bwd
     return nkt;
   };
 
+  // tile loads through per-tile buffer resources; rows past the task read as zero
   u32x4 kreg[PASSES], vreg[PASSES];
+  uint32_t goff[PASSES];
+#pragma unroll
+  for (int p = 0; p < PASSES; ++p)
+    goff[p] = uint32_t(((p * RPP + tid / CHUNKS) * rs + (tid % CHUNKS) * 8) * 2);
   auto gload = [&](int kt) {
+    const int64_t rows = int64_t(L) - int64_t(kt) * BN;
+    const __amdgpu_buffer_rsrc_t rk = row_rsrc(Kg + int64_t(kt) * BN * rs, rows, rs * 2, D * 2);
+    const __amdgpu_buffer_rsrc_t rv = row_rsrc(Vg + int64_t(kt) * BN * rs, rows, rs * 2, D * 2);
 #pragma unroll
     for (int p = 0; p < PASSES; ++p) {
-      const int row = p * RPP + tid / CHUNKS, ch = tid % CHUNKS, key = kt * BN + row;
-      u32x4 zk = {0u, 0u, 0u, 0u}, zv = {0u, 0u, 0u, 0u};
-      if (key < L) {
-        zk = *(const u32x4*)(Kg + int64_t(key) * rs + ch * 8);
-        zv = *(const u32x4*)(Vg + int64_t(key) * rs + ch * 8);
-      }
-      kreg[p] = zk;
-      vreg[p] = zv;
+      kreg[p] = buf_load16(rk, goff[p]);
+      vreg[p] = buf_load16(rv, goff[p]);
     }
   };
   auto sstore = [&](int buf, int kt, uint32_t kor_t) {
@@ -153,28 +156,26 @@ __global__ void __launch_bounds__(256, (D == 128 ? 1 : 2)) attn_bwd_dq(const Bwd
       const bool use_bits = (qor & kor) != 0u;
       const char* Kb = smem + buf * STAGE;
       const char* Vb = Kb + KBYTES;
-      f32x16 s[2], dp[2];
+      // one 32-key block at a time: S^T, dP^T, dS^T, then its dQ^T products
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
+        f32x16 s, dp;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          s[kb][r] = 0.f;
-          dp[kb][r] = 0.f;
+          s[r] = 0.f;
+          dp[r] = 0.f;
         }
         const int row = 32 * kb + (lane & 31);
 #pragma unroll
         for (int ks = 0; ks < DK; ++ks) {
           const u32x4 ka = *(const u32x4*)(Kb + row * KP + (16 * ks + 8 * half) * 2);
-          s[kb] = mfma32<E>(bitcast_u4<vec8>(ka), qf[ks], s[kb]);
+          s = mfma32<E>(bitcast_u4<vec8>(ka), qf[ks], s);
           const u32x4 va = *(const u32x4*)(Vb + row * VP + (16 * ks + 8 * half) * 2);
-          dp[kb] = mfma32<E>(bitcast_u4<vec8>(va), of[ks], dp[kb]);
+          dp = mfma32<E>(bitcast_u4<vec8>(va), of[ks], dp);
         }
-      }
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          float p = fast_exp2(fmaf(s[kb][r], c, -lse2));
+          float p = fast_exp2(fmaf(s[r], c, -lse2));
           if (!wclear) {
             const int kl = 32 * kb + 8 * (r >> 2) + 4 * half + (r & 3);
             const int key = k0 + kl;
@@ -182,21 +183,21 @@ __global__ void __launch_bounds__(256, (D == 128 ? 1 : 2)) attn_bwd_dq(const Bwd
             if (use_bits) keep = keep && ((kbits_s[buf][kl] & qbits) == 0u);
             if (!keep) p = 0.f;
           }
-          s[kb][r] = p * (dp[kb][r] - Dq);  // dS^T
+          s[r] = p * (dp[r] - Dq);  // dS^T
         }
 #pragma unroll
-      for (int ks2 = 0; ks2 < 4; ++ks2) {
-        const int kb = ks2 >> 1, sub = ks2 & 1;
-        float pv[8];
+        for (int sub = 0; sub < 2; ++sub) {
+          float pv[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) pv[e] = s[kb][8 * sub + e];
-        const vec8 bs = pack8<E>(pv);
-        const int row = 32 * kb + 16 * sub + 4 * half + ((lane & 15) >> 2);
+          for (int e = 0; e < 8; ++e) pv[e] = s[8 * sub + e];
+          const vec8 bs = pack8<E>(pv);
+          const int trow = 32 * kb + 16 * sub + 4 * half + ((lane & 15) >> 2);
 #pragma unroll
-        for (int db = 0; db < DB; ++db) {
-          const int col = 32 * db + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
-          const char* p0 = Kb + row * KP + col * 2;
-          dq[db] = mfma32<E>(lds_tr_pair<E>(p0, p0 + 8 * KP), bs, dq[db]);
+          for (int db = 0; db < DB; ++db) {
+            const int col = 32 * db + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+            const char* p0 = Kb + trow * KP + col * 2;
+            dq[db] = mfma32<E>(lds_tr_pair<E>(p0, p0 + 8 * KP), bs, dq[db]);
+          }
         }
       }
     }
@@ -226,11 +227,13 @@ template <typename E, int D>
 __global__ void __launch_bounds__(256, (D == 128 ? 1 : 2)) attn_bwd_dkdv(const BwdArgs a) {
   constexpr int BK = 128, BQ = 64;
   constexpr int P2 = D * 2 + 64;  // Q and dO tiles: transpose reads and row reads
+  constexpr int VKP = D * 2 + 16; // the work group's V rows: 16-byte row reads
   constexpr int DK = D / 16, DB = D / 32, CHUNKS = D / 8, RPP = 256 / CHUNKS, PASSES = BQ / RPP;
   typedef typename E::vec8 vec8;
 
   __shared__ __attribute__((aligned(16))) char qs[BQ * P2];
   __shared__ __attribute__((aligned(16))) char os[BQ * P2];
+  __shared__ __attribute__((aligned(16))) char vs[BK * VKP];
   __shared__ __attribute__((aligned(16))) float lse_s[BQ];
   __shared__ __attribute__((aligned(16))) float d_s[BQ];
   __shared__ uint32_t qbits_s[BQ];
@@ -257,16 +260,22 @@ __global__ void __launch_bounds__(256, (D == 128 ? 1 : 2)) attn_bwd_dkdv(const B
   const int k0w = strip * BK + wave * 32;
   const int mykey = k0w + (lane & 31);
   const bool kvalid = mykey < L;
-  vec8 kf[DK], vf[DK];
+  vec8 kf[DK];
 #pragma unroll
   for (int ks = 0; ks < DK; ++ks) {
-    u32x4 u = {0u, 0u, 0u, 0u}, w = {0u, 0u, 0u, 0u};
-    if (kvalid) {
-      u = *(const u32x4*)(Kg + int64_t(mykey) * rs + ks * 16 + half * 8);
-      w = *(const u32x4*)(Vg + int64_t(mykey) * rs + ks * 16 + half * 8);
-    }
+    u32x4 u = {0u, 0u, 0u, 0u};
+    if (kvalid) u = *(const u32x4*)(Kg + int64_t(mykey) * rs + ks * 16 + half * 8);
     kf[ks] = bitcast_u4<vec8>(u);
-    vf[ks] = bitcast_u4<vec8>(w);
+  }
+  // the work group's V rows stay in LDS (register operands of dP = dO V^T)
+  {
+    const __amdgpu_buffer_rsrc_t rv =
+        row_rsrc(Vg + int64_t(strip) * BK * rs, int64_t(L) - int64_t(strip) * BK, rs * 2, D * 2);
+#pragma unroll
+    for (int p = 0; p < BK / RPP; ++p) {
+      const int row = p * RPP + tid / CHUNKS, ch = tid % CHUNKS;
+      *(u32x4*)(vs + row * VKP + ch * 16) = buf_load16(rv, uint32_t((row * rs + ch * 8) * 2));
+    }
   }
 
   const int lastk_wg = (strip * BK + BK < L ? strip * BK + BK : L) - 1;
@@ -302,16 +311,17 @@ __global__ void __launch_bounds__(256, (D == 128 ? 1 : 2)) attn_bwd_dkdv(const B
 
   for (int qt = next_live(causal ? first_key / BQ : 0); qt < nqt; qt = next_live(qt + 1)) {
     __syncthreads();  // every wave is done with the previous tile
+    {
+      const int64_t rows = int64_t(L) - int64_t(qt) * BQ;
+      const __amdgpu_buffer_rsrc_t rq = row_rsrc(Qg + int64_t(qt) * BQ * rs, rows, rs * 2, D * 2);
+      const __amdgpu_buffer_rsrc_t ro = row_rsrc(Og + int64_t(qt) * BQ * rs, rows, rs * 2, D * 2);
 #pragma unroll
-    for (int p = 0; p < PASSES; ++p) {
-      const int row = p * RPP + tid / CHUNKS, ch = tid % CHUNKS, q = qt * BQ + row;
-      u32x4 zq = {0u, 0u, 0u, 0u}, zo = {0u, 0u, 0u, 0u};
-      if (q < L) {
-        zq = *(const u32x4*)(Qg + int64_t(q) * rs + ch * 8);
-        zo = *(const u32x4*)(Og + int64_t(q) * rs + ch * 8);
+      for (int p = 0; p < PASSES; ++p) {
+        const int row = p * RPP + tid / CHUNKS, ch = tid % CHUNKS;
+        const uint32_t off = uint32_t((row * rs + ch * 8) * 2);
+        *(u32x4*)(qs + row * P2 + ch * 16) = buf_load16(rq, off);
+        *(u32x4*)(os + row * P2 + ch * 16) = buf_load16(ro, off);
       }
-      *(u32x4*)(qs + row * P2 + ch * 16) = zq;
-      *(u32x4*)(os + row * P2 + ch * 16) = zo;
     }
     const uint32_t qor = a.blk_or[qt], qand = a.blk_and[qt];
     if (tid < BQ) {
@@ -333,7 +343,7 @@ __global__ void __launch_bounds__(256, (D == 128 ? 1 : 2)) attn_bwd_dkdv(const B
     if (wfull) continue;
     const bool wclear = (wor & qor) == 0u && (!causal || q0 >= wk1);
     const bool use_bits = (kor & qor) != 0u;
-#pragma unroll
+#pragma unroll 1
     for (int qb = 0; qb < 2; ++qb) {
       f32x16 s, dp;
 #pragma unroll
@@ -347,34 +357,33 @@ __global__ void __launch_bounds__(256, (D == 128 ? 1 : 2)) attn_bwd_dkdv(const B
         const u32x4 qa = *(const u32x4*)(qs + row * P2 + (16 * ks + 8 * half) * 2);
         s = mfma32<E>(bitcast_u4<vec8>(qa), kf[ks], s);
         const u32x4 oa = *(const u32x4*)(os + row * P2 + (16 * ks + 8 * half) * 2);
-        dp = mfma32<E>(bitcast_u4<vec8>(oa), vf[ks], dp);
+        const u32x4 vb = *(const u32x4*)(vs + (wave * 32 + (lane & 31)) * VKP + (16 * ks + 8 * half) * 2);
+        dp = mfma32<E>(bitcast_u4<vec8>(oa), bitcast_u4<vec8>(vb), dp);
       }
-      float pr[16];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int ql = 32 * qb + 8 * i + 4 * half;
-        const f32x4 l4 = *(const f32x4*)(lse_s + ql);
-        const f32x4 d4 = *(const f32x4*)(d_s + ql);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int r = 4 * i + j;
-          float p = fast_exp2(fmaf(s[r], c, -l4[j]));
-          if (!wclear) {
-            const int q = q0 + ql + j;
-            bool keep = (!causal || mykey <= q);
-            if (use_bits) keep = keep && ((qbits_s[ql + j] & kbits) == 0u);
-            if (!keep) p = 0.f;
-          }
-          pr[r] = p;
-          s[r] = p * (dp[r] - d4[j]);  // dS
-        }
-      }
+      // 16 queries at a time: P and dS = P (dP - D), packed for dV and dK
 #pragma unroll
       for (int sub = 0; sub < 2; ++sub) {
-        const vec8 bp = pack8<E>(pr + 8 * sub);
-        float dsv[8];
+        float pv[8], dsv[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) dsv[e] = s[8 * sub + e];
+        for (int ii = 0; ii < 2; ++ii) {
+          const int ql = 32 * qb + 8 * (2 * sub + ii) + 4 * half;
+          const f32x4 l4 = *(const f32x4*)(lse_s + ql);
+          const f32x4 d4 = *(const f32x4*)(d_s + ql);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int r = 8 * sub + 4 * ii + j;
+            float p = fast_exp2(fmaf(s[r], c, -l4[j]));
+            if (!wclear) {
+              const int q = q0 + ql + j;
+              bool keep = (!causal || mykey <= q);
+              if (use_bits) keep = keep && ((qbits_s[ql + j] & kbits) == 0u);
+              if (!keep) p = 0.f;
+            }
+            pv[4 * ii + j] = p;
+            dsv[4 * ii + j] = p * (dp[r] - d4[j]);
+          }
+        }
+        const vec8 bp = pack8<E>(pv);
         const vec8 bs = pack8<E>(dsv);
         const int trow = 32 * qb + 16 * sub + 4 * half + ((lane & 15) >> 2);
 #pragma unroll

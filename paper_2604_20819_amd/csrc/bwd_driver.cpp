@@ -2,11 +2,13 @@
 // Eq. "globallse"), equal to Alg. 2.
 //
 // caller stream : D = rowsum(dO * O) over the full sequence, zero dQ/dK/dV;
-//                 per task wait "staged", run the key-parallel dK/dV kernel
-//                 and the query-parallel dQ kernel; both add their task rows
-//                 into the global fp32 gradients (tasks are ordered on this
-//                 stream and a task holds each token once), then free the slot;
-// copy stream   : gather each task's runs of Q, K, V, dO into slot t % S.
+//                 per task wait "staged", run the key-parallel dK/dV kernel,
+//                 which adds the task's rows into the global fp32 dK and dV;
+// second stream : per task the query-parallel dQ kernel, adding into dQ.
+//                 Each stream keeps the tasks in order and a task holds each
+//                 token once, so these read-modify-writes never race;
+// copy stream   : gather each task's runs of Q, K, V, dO into slot t % S once
+//                 both kernels of the slot's previous task are done.
 // Depth 0 reads the caller's tensors in place (the undecomposed backward).
 #include <algorithm>
 #include <cmath>
@@ -75,7 +77,7 @@ cqsa_status backward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa
   float* d_D = (float*)(base + tab_bytes);
   const uint64_t in_b = align_up(uint64_t(B) * p->max_L_local * H * d * elem);
 
-  while (C->sync_events.size() < size_t(4 * nslot + 2)) {
+  while (C->sync_events.size() < size_t(4 * nslot + 3)) {
     hipEvent_t e;
     CQSA_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
     C->sync_events.push_back(e);
@@ -83,7 +85,9 @@ cqsa_status backward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa
   hipEvent_t ev_start = C->sync_events[0];
   hipEvent_t ev_tab = C->sync_events[1];
   hipEvent_t* ev_staged = &C->sync_events[2];
-  hipEvent_t* ev_free = &C->sync_events[2 + nslot];
+  hipEvent_t* ev_free = &C->sync_events[2 + nslot];      // dK/dV kernel done with the slot
+  hipEvent_t* ev_free_q = &C->sync_events[2 + 2 * nslot]; // dQ kernel done with the slot
+  hipEvent_t ev_pre = C->sync_events[2 + 3 * nslot];      // preprocess and zero fill done
   if (C->ws_free_valid) CQSA_HIP(hipStreamWaitEvent(st, C->ws_free, 0));
   CQSA_HIP(hipEventRecord(ev_start, st));
   CQSA_HIP(hipStreamWaitEvent(C->copy, ev_start, 0));
@@ -106,6 +110,12 @@ cqsa_status backward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa
     rec.spans[kStFinal].push_back(sp);
   }
   CQSA_HIP(hipStreamWaitEvent(st, ev_tab, 0));
+  // dQ kernels run on the second compute stream (they write dQ only, the dK/dV
+  // kernels on the caller's stream write dK and dV only): a task's two kernels
+  // overlap, and each stream keeps its own tasks in order.
+  const hipStream_t qs = C->lane;
+  CQSA_HIP(hipEventRecord(ev_pre, st));
+  CQSA_HIP(hipStreamWaitEvent(qs, ev_pre, 0));
 
   std::vector<bool> used(nslot, false);
   for (int64_t t = 0; t < ntask; ++t) {
@@ -119,7 +129,10 @@ cqsa_status backward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa
     if (direct) {
       a.q = Q->data; a.k = K->data; a.v = V->data; a.dO = dO->data;
     } else {
-      if (used[si]) CQSA_HIP(hipStreamWaitEvent(C->copy, ev_free[si], 0));
+      if (used[si]) {
+        CQSA_HIP(hipStreamWaitEvent(C->copy, ev_free[si], 0));
+        CQSA_HIP(hipStreamWaitEvent(C->copy, ev_free_q[si], 0));
+      }
       StageArgs sa{};
       sa.src[0] = Q->data; sa.src[1] = K->data; sa.src[2] = V->data; sa.src[3] = dO->data;
       for (int x = 0; x < 4; ++x) sa.dst[x] = sb + x * in_b;
@@ -137,6 +150,7 @@ cqsa_status backward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa
       }
       CQSA_HIP(hipEventRecord(ev_staged[si], C->copy));
       CQSA_HIP(hipStreamWaitEvent(st, ev_staged[si], 0));
+      CQSA_HIP(hipStreamWaitEvent(qs, ev_staged[si], 0));
       a.q = sa.dst[0]; a.k = sa.dst[1]; a.v = sa.dst[2]; a.dO = sa.dst[3];
     }
     a.L = int32_t(Li); a.B = int32_t(B); a.H = int32_t(H); a.causal = p->g.causal;
@@ -146,20 +160,31 @@ cqsa_status backward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa
     a.blk_and = (const uint32_t*)(d_tab + to.blk_and);
     a.lse = LSE; a.D = d_D; a.Lg = L;
     a.dq = (float*)dQ->data; a.dk = (float*)dK->data; a.dv = (float*)dV->data;
+    std::pair<hipEvent_t, hipEvent_t> sk{nullptr, nullptr}, sq{nullptr, nullptr};
     if (rec.timing) {
-      sp = {rec.make(), rec.make()};
-      CQSA_HIP(hipEventRecord(sp.first, st));
+      sk = {rec.make(), rec.make()};
+      sq = {rec.make(), rec.make()};
+      CQSA_HIP(hipEventRecord(sk.first, st));
+      CQSA_HIP(hipEventRecord(sq.first, qs));
     }
     CQSA_HIP(launch_bwd_dkdv(o.dtype, int(d), a, st));
-    CQSA_HIP(launch_bwd_dq(o.dtype, int(d), a, st));
-    rec.stats.inner_launches += 1;
+    CQSA_HIP(launch_bwd_dq(o.dtype, int(d), a, qs));
+    rec.stats.inner_launches += 2;
     if (rec.timing) {
-      CQSA_HIP(hipEventRecord(sp.second, st));
-      rec.spans[kStInner].push_back(sp);
+      CQSA_HIP(hipEventRecord(sk.second, st));
+      CQSA_HIP(hipEventRecord(sq.second, qs));
+      rec.spans[kStInner].push_back(sk);
+      rec.spans[kStInner].push_back(sq);
     }
-    if (!direct) CQSA_HIP(hipEventRecord(ev_free[si], st));
+    if (!direct) {
+      CQSA_HIP(hipEventRecord(ev_free[si], st));
+      CQSA_HIP(hipEventRecord(ev_free_q[si], qs));
+    }
     used[si] = true;
   }
+  // join the dQ stream back into the caller's stream
+  CQSA_HIP(hipEventRecord(ev_pre, qs));
+  CQSA_HIP(hipStreamWaitEvent(st, ev_pre, 0));
   if (rec.timing) CQSA_HIP(hipEventRecord(rec.wall1, st));
   CQSA_HIP(hipEventRecord(C->ws_free, st));
   C->ws_free_valid = true;
