@@ -7,9 +7,19 @@ B=1, H=16, d=128, L=32768, non-causal, softmax scale 1/sqrt(d), CQS depth 1
 Q, K, V are i.i.d. N(0,1) from a fixed seed, cast to bf16.
 
 One step = one pass of the whole forward hot path: plan the call, stage every
-task's runs, run the inner kernel per task, recompose, finalize.  The bench
-also times the undecomposed call (depth 0, one kernel) for the runtime ratio,
-and the decomposed forward+backward when the backward is built.
+task's runs, run the inner kernel per task (the automatic launch grouping
+puts one 14043-token task in each launch here, alternating between two
+compute streams), merge, finalize.  The bench also times the undecomposed
+call (depth 0, one kernel) for the runtime ratio, the same forward with all
+seven tasks in one launch and one merge (each kernel then runs alone, which
+gives clean per-kernel rates), and the decomposed forward+backward.
+
+`roofline` is the inner forward kernel: algorithmic FLOPs per launch over the
+mean HIP-event duration of its launches in the headline run.  Consecutive
+launches overlap on the two streams, so a launch shares the GPU for most of
+its span; `kernels.inner_fwd` also gives the rate over the union of the
+launches' spans (`achieved_busy`), the measured concurrency, and the rates of
+the single-launch and undecomposed runs.
 
 Prints one JSON line.  Algorithmic FLOPs: forward 4*d*B*H*pairs with
 pairs = L^2 (non-causal); forward+backward 3.5x forward.
@@ -36,7 +46,46 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target CPU time of the oracle sample")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB MiB five times (calibrates "
+                         "the FETCH_SIZE / WRITE_SIZE counters) and exit")
     return ap.parse_args()
+
+
+# HBM traffic of one inner forward launch, from the committed counter summary;
+# reported only while the kernel sources still hash to what was profiled.
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "inner_fwd_bf16_L32768_H16_d128_traffic.txt")
+KERNEL_SOURCES = ("attn_fwd.hip", "hip_common.hpp", "records.hpp", "kernels.hpp")
+
+
+def kernel_source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2604_20819_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic():
+    try:
+        kv = dict(line.split(":", 1) for line in open(TRAFFIC_FILE) if ":" in line)
+    except OSError:
+        return None
+    if kv.get("kernel_sources_sha256", "").strip() != kernel_source_hash():
+        return None
+    return int(kv["traffic_bytes_per_launch"].strip())
+
+
+def copy_probe(mib):
+    import torch
+    n = mib * (1 << 20) // 4
+    x = torch.ones(n, dtype=torch.float32, device="cuda")
+    y = torch.empty_like(x)
+    for _ in range(5):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes_read": n * 4, "copy_probe_bytes_written": n * 4}))
 
 
 def fwd_flops(causal=False):
@@ -84,8 +133,15 @@ def cpu_baseline(Q, K, V, seconds):
                       f"x {H} heads against all {L} keys ({t_used:.1f} s)"}
 
 
+def task_rows(plan):
+    return [plan.task(t)["L_local"] for t in range(plan.num_tasks)]
+
+
 def main():
     args = parse()
+    if args.copy_probe:
+        copy_probe(args.copy_probe)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
               "(the decomposition shards across GPUs by design, but this build "
@@ -105,40 +161,86 @@ def main():
     O = torch.empty((B, L, H, D), dtype=torch.float32, device=dev)
     LSE = torch.empty((B, H, L), dtype=torch.float32, device=dev)
 
-    def plan_for(depth, backward=False):
+    def plan_for(depth, backward=False, tps=0):
         return cq.cqsa_plan(L, H, D, False, 0, cq.make_opts(B=B, dtype="bf16", depth=depth,
-                                                            with_backward=backward))
+                                                            with_backward=backward,
+                                                            tasks_per_slot=tps))
 
     cq.cqsa_set_timing(True)
 
-    def fwd_step(depth):
+    def fwd_step(depth, tps=0):
         def step():
-            plan = plan_for(depth)
+            plan = plan_for(depth, tps=tps)   # planning is part of the step
             cq.cqsa_forward(plan, q, k, v, O, LSE)
             return cq.cqsa_last_stats()
         return step
 
-    ms_dec, stats = time_steps(fwd_step(1), args.steps, args.warmup, torch)
-    ms_inner = sum(s["ms_inner"] for s in stats) / sum(s["inner_launches"] for s in stats)
-    ms_merge = sum(s["ms_merge"] for s in stats) / len(stats)
-    ms_stage = sum(s["ms_stage"] for s in stats) / len(stats)
-    ms_und, _ = time_steps(fwd_step(0), args.steps, args.warmup, torch)
+    def mean(stats, key):
+        return sum(s[key] for s in stats) / len(stats)
 
     flops = fwd_flops(False)
+    # headline: the decomposed forward with the automatic launch grouping
+    ms_dec, stats = time_steps(fwd_step(1), args.steps, args.warmup, torch)
+    launches = stats[-1]["inner_launches"]
+    ms_launch = mean(stats, "ms_inner") / launches
+    ms_busy = mean(stats, "ms_inner_busy")
+    # undecomposed call (depth 0): one launch of the same kernel, no merge
+    ms_und, st_und = time_steps(fwd_step(0), args.steps, args.warmup, torch)
+    # all seven tasks in one launch and one merge: every kernel runs alone
+    ms_one, st_one = time_steps(fwd_step(1, tps=7), args.steps, args.warmup, torch)
+
     tflops = flops / (ms_dec * 1e-3) / 1e12
-    per_launch = flops / 7.0            # the 7 tasks' kept pairs sum to L^2
-    achieved = per_launch / (ms_inner * 1e-3) / 1e12
+    # the seven tasks' kept pairs sum to L^2 (each pair once): flops per launch
+    per_launch = flops / launches
+    achieved = per_launch / (ms_launch * 1e-3) / 1e12
+
+    plan1 = plan_for(1)
+    rows = task_rows(plan1)
+    pair_b = 4 * D + 8                      # acc_i row + m_i + l_i (fp32)
+    merge_bytes = sum(rows) * B * H * pair_b + B * H * L * (4 * D + 4)   # one final merge
+    stage_bytes = 2 * st_one[-1]["d2d_bytes"]                          # read + write
+    kernels = {
+        "inner_fwd": {
+            "bound": "mfma", "unit": "TFLOP/s", "launches_per_step": launches,
+            "ms_per_launch": round(ms_launch, 4),
+            "achieved_per_launch": round(achieved, 2),
+            "concurrency": round(mean(stats, "ms_inner") / ms_busy, 3),
+            "achieved_busy": round(flops / (ms_busy * 1e-3) / 1e12, 2),
+            "single_launch_all_tasks": round(flops / (mean(st_one, "ms_inner") * 1e-3) / 1e12, 2),
+            "undecomposed_launch": round(flops / (mean(st_und, "ms_inner") * 1e-3) / 1e12, 2),
+        },
+        "stage": {"bound": "hbm", "unit": "GB/s", "bytes_per_step": stage_bytes,
+                  "achieved": round(stage_bytes / (mean(st_one, "ms_stage") * 1e-3) / 1e9, 1)},
+        "merge_final": {"bound": "hbm", "unit": "GB/s", "bytes_per_launch": merge_bytes,
+                        "ms_per_launch": round(mean(st_one, "ms_merge"), 4),
+                        "achieved": round(merge_bytes / (mean(st_one, "ms_merge") * 1e-3) / 1e9, 1)},
+    }
 
     fwd_bwd = None
     try:
         dQ, dK, dV = (torch.empty((B, L, H, D), dtype=torch.float32, device=dev) for _ in range(3))
+        bstats = []
 
         def fb_step():
             plan = plan_for(1, backward=True)
             cq.cqsa_forward(plan, q, k, v, O, LSE)
             cq.cqsa_backward(plan, q, k, v, O, LSE, do, dQ, dK, dV)
+            bstats.append(cq.cqsa_last_stats())
         ms_fb, _ = time_steps(fb_step, max(3, args.steps // 2), 1, torch)
+        bstats = bstats[1:]
         fwd_bwd = {"tflops": 3.5 * flops / (ms_fb * 1e-3) / 1e12, "ms_per_step": ms_fb}
+        pre_bytes = B * L * H * (2 * D + 4 * D) + B * H * L * 4     # dO, O in; D out
+        zero_bytes = 3 * B * L * H * D * 4
+        kernels["inner_bwd"] = {
+            "bound": "mfma", "unit": "TFLOP/s", "launches_per_step": bstats[-1]["inner_launches"],
+            "concurrency": round(mean(bstats, "ms_inner") / mean(bstats, "ms_inner_busy"), 3),
+            "achieved_busy": round(2.5 * flops / (mean(bstats, "ms_inner_busy") * 1e-3) / 1e12, 2)}
+        kernels["bwd_preprocess"] = {
+            "bound": "hbm", "unit": "GB/s", "bytes_per_launch": pre_bytes,
+            "achieved": round(pre_bytes / (mean(bstats, "ms_finalize") * 1e-3) / 1e9, 1)}
+        kernels["bwd_zero_fill"] = {
+            "bound": "hbm", "unit": "GB/s", "bytes_per_step": zero_bytes,
+            "achieved": round(zero_bytes / (mean(bstats, "ms_merge") * 1e-3) / 1e9, 1)}
     except cq.CqsaError as e:
         if e.status != -2:
             raise
@@ -163,11 +265,11 @@ def main():
         "runtime_ratio_vs_undecomposed": round(ms_dec / ms_und, 4),
         "undecomposed_ms": round(ms_und, 4),
         "undecomposed_tflops": round(flops / (ms_und * 1e-3) / 1e12, 2),
-        "stage_ms": {"inner_per_launch": round(ms_inner, 4), "recompose_per_step": round(ms_merge, 4),
-                     "staging_per_step": round(ms_stage, 4)},
+        "single_launch_ms": round(ms_one, 4),
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": BF16_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / BF16_PEAK_TFLOPS, 4),
-                     "traffic": None},
+                     "traffic": measured_traffic()},
+        "kernels": kernels,
     }
     if fwd_bwd is not None:
         line["fwd_bwd"] = {"tflops": round(fwd_bwd["tflops"], 2),

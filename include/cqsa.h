@@ -75,6 +75,11 @@ typedef struct {
   int32_t inputs_on_device;  /* 1: Q, K, V (and dO) are device-resident; 0: host-resident (1) */
   int32_t acc_on_device;     /* 1: accumulator/outputs on device; 0: on host, merged by host threads (1) */
   int32_t with_backward;     /* 1: the footprint must also fit cqsa_backward (0) */
+  int32_t tasks_per_slot;    /* forward tasks staged, launched and merged together, in [0, 32]:
+                                0 = automatic: enough tasks for 1024 inner-kernel work groups
+                                per launch (capped at 32 and at the task count, reduced until
+                                the budget fits; 1 when acc_on_device = 0); >= 1 forced;
+                                > 1 needs acc_on_device = 1 (0) */
 } cqsa_plan_opts;
 
 /* One contiguous run of a task's tokens: global tokens
@@ -118,10 +123,15 @@ typedef struct {
   double ms_wall;                   /* first enqueue to completion, device clock */
   double ms_stage;                  /* sum of staging copy spans */
   double ms_inner;                  /* sum of inner forward (or backward) kernel spans */
-  double ms_merge;                  /* sum of recompose (device) or host-merge spans */
-  double ms_finalize;               /* finalize (forward) or preprocess (backward) span */
+  double ms_merge;                  /* forward: sum of merge-launch spans (device; the last one
+                                       also finalises) or host-merge time; backward: zero-fill of
+                                       dQ, dK, dV (the scatter-adds are fused into the kernels) */
+  double ms_finalize;               /* forward: host finalisation time (acc on host);
+                                       backward: preprocess span (D = rowsum(dO * O)) */
   double ms_d2h;                    /* sum of statistics device-to-host spans */
   int64_t tiles_full, tiles_clear, tiles_mixed; /* 128x128 tile census of the plan */
+  int64_t merge_launches;           /* device merge launches (forward) */
+  double ms_inner_busy;             /* time at least one inner kernel ran (union of its spans) */
 } cqsa_run_stats;
 
 /* Fill `o` with the defaults listed in cqsa_plan_opts. */
@@ -144,6 +154,8 @@ cqsa_status cqsa_plan_get_task(const cqsa_plan_t* plan, int64_t t, cqsa_task* ou
 /* Modelled peak device bytes of a call under this plan: caller tensors that are
  * device-resident plus everything the library allocates. 0 if plan is NULL. */
 uint64_t cqsa_plan_modelled_device_bytes(const cqsa_plan_t* plan);
+/* Forward tasks per staging slot and launch group the plan chose; -1 if plan is NULL. */
+int32_t cqsa_plan_tasks_per_slot(const cqsa_plan_t* plan);
 /* Pooled 128x128 tile census over causal-retained tiles of every task (App. A.2). */
 cqsa_status cqsa_plan_tile_census(const cqsa_plan_t* plan, int64_t* full, int64_t* clear,
                                   int64_t* mixed);

@@ -40,7 +40,7 @@ class cqsa_plan_opts(ctypes.Structure):
                 ("depth", ctypes.c_int32), ("min_depth", ctypes.c_int32),
                 ("max_depth", ctypes.c_int32), ("n_slots", ctypes.c_int32),
                 ("inputs_on_device", ctypes.c_int32), ("acc_on_device", ctypes.c_int32),
-                ("with_backward", ctypes.c_int32)]
+                ("with_backward", ctypes.c_int32), ("tasks_per_slot", ctypes.c_int32)]
 
 
 class cqsa_run(ctypes.Structure):
@@ -65,7 +65,8 @@ class cqsa_run_stats(ctypes.Structure):
                 ("ms_inner", ctypes.c_double), ("ms_merge", ctypes.c_double),
                 ("ms_finalize", ctypes.c_double), ("ms_d2h", ctypes.c_double),
                 ("tiles_full", ctypes.c_int64), ("tiles_clear", ctypes.c_int64),
-                ("tiles_mixed", ctypes.c_int64)]
+                ("tiles_mixed", ctypes.c_int64), ("merge_launches", ctypes.c_int64),
+                ("ms_inner_busy", ctypes.c_double)]
 
 
 # Every symbol include/cqsa.h declares, with its ctypes signature.
@@ -78,6 +79,7 @@ _SIGS = {
     "cqsa_plan_num_tasks": (ctypes.c_int64, [ctypes.c_void_p]),
     "cqsa_plan_get_task": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.POINTER(cqsa_task)]),
     "cqsa_plan_modelled_device_bytes": (ctypes.c_uint64, [ctypes.c_void_p]),
+    "cqsa_plan_tasks_per_slot": (ctypes.c_int32, [ctypes.c_void_p]),
     "cqsa_plan_tile_census": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(ctypes.c_int64),
                                              ctypes.POINTER(ctypes.c_int64),
                                              ctypes.POINTER(ctypes.c_int64)]),
@@ -131,7 +133,8 @@ def cqsa_plan_opts_default():
 
 
 def make_opts(B=1, dtype="bf16", c=7, interest=(0, 1, 3), depth=-1, min_depth=1, max_depth=4,
-              n_slots=2, inputs_on_device=True, acc_on_device=True, with_backward=False):
+              n_slots=2, inputs_on_device=True, acc_on_device=True, with_backward=False,
+              tasks_per_slot=0):
     o = cqsa_plan_opts_default()
     o.B = B
     o.dtype = {"f32": CQSA_F32, "f16": CQSA_F16, "bf16": CQSA_BF16}[dtype]
@@ -143,6 +146,7 @@ def make_opts(B=1, dtype="bf16", c=7, interest=(0, 1, 3), depth=-1, min_depth=1,
     o.inputs_on_device = int(bool(inputs_on_device))
     o.acc_on_device = int(bool(acc_on_device))
     o.with_backward = int(bool(with_backward))
+    o.tasks_per_slot = int(tasks_per_slot)
     return o
 
 
@@ -170,6 +174,10 @@ class Plan:
     @property
     def modelled_device_bytes(self):
         return lib().cqsa_plan_modelled_device_bytes(self.handle)
+
+    @property
+    def tasks_per_slot(self):
+        return lib().cqsa_plan_tasks_per_slot(self.handle)
 
     def task(self, t):
         """Task t as a dict of plain Python values."""

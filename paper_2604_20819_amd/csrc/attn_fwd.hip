@@ -1,9 +1,10 @@
 // Inner forward kernels: masked flash-style attention over one CQS task.
 //
-// Each work group owns a 128-query strip of one (batch, head) and walks the
-// task's 64-key tiles with an online softmax, emitting the local statistics
-// (unnormalised acc, row max m, row sum l) that the max-shifted merge of
-// App. A.1 (Eq. "merge") recomposes across tasks.
+// One launch covers the tasks of a launch group.  Each work group owns a
+// 128-query strip of one (task, batch, head) and walks the task's 64-key
+// tiles with an online softmax, emitting the local statistics (unnormalised
+// acc, row max m, row sum l) that the max-shifted merge of App. A.1
+// (Eq. "merge") recomposes across tasks.
 //
 // Tile verdicts (App. A.2): from the 64-token block summaries a (strip, key
 // tile) pair is fully masked (AND(rows) & AND(cols) != 0, or causally empty),
@@ -41,18 +42,25 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_mfma(const FwdArgs a) {
   __shared__ uint32_t kbits_s[2][BN];
   __shared__ DevRun runs_s[kMaxRuns];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5;
-  const int L = a.L;
+  const int tid = threadIdx.x, lane = tid & 63, half = lane >> 5;
+  // uniform per wave, so per-wave loads and branches stay scalar
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  int64_t work = xcd_remap(blockIdx.x, gridDim.x);
+  const int tj = find_task(a.tasks, a.ntask, BM, int64_t(a.H) * a.B, work);
+  const DevTask tk = a.tasks[tj];
+  const int L = int(tk.L_local);
   const int64_t nstrips = (L + BM - 1) / BM;
-  const int64_t work = xcd_remap(blockIdx.x, nstrips * a.H * a.B);
   const int strip = int(work % nstrips);
   const int h = int((work / nstrips) % a.H);
   const int b = int(work / (nstrips * a.H));
+  const int n_runs = tk.n_runs;
+  const uint32_t* blk_or = (const uint32_t*)(a.tab + tk.or_off);
+  const uint32_t* blk_and = (const uint32_t*)(a.tab + tk.and_off);
 
-  for (int i = tid; i < a.n_runs; i += 256) runs_s[i] = ((const DevRun*)a.runs)[i];
+  for (int i = tid; i < n_runs; i += 256) runs_s[i] = ((const DevRun*)(a.tab + tk.runs_off))[i];
 
   const int64_t rs = int64_t(a.H) * D;  // elements between consecutive tokens
-  const int64_t base = (int64_t(b) * a.seq_rows + a.row0) * rs + int64_t(h) * D;
+  const int64_t base = int64_t(b) * L * rs + int64_t(h) * D + tj * a.in_stride;
   const uint16_t* Qg = (const uint16_t*)a.q + base;
   const uint16_t* Kg = (const uint16_t*)a.k + base;
   const uint16_t* Vg = (const uint16_t*)a.v + base;
@@ -74,26 +82,50 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_mfma(const FwdArgs a) {
   // block summaries of the strip and of this wave's queries
   const int lastq_wg = (strip * BM + BM < L ? strip * BM + BM : L) - 1;
   const int qb0 = strip * 2, qb1 = lastq_wg / 64;
-  const uint32_t qor = a.blk_or[qb0] | a.blk_or[qb1];
-  const uint32_t qand = a.blk_and[qb0] & a.blk_and[qb1];
+  const uint32_t qor = blk_or[qb0] | blk_or[qb1];
+  const uint32_t qand = blk_and[qb0] & blk_and[qb1];
   const bool wave_live = q0w < L;
   const int wq1 = wave_live ? (q0w + 31 < L ? q0w + 31 : L - 1) : 0;
-  const uint32_t wor = wave_live ? a.blk_or[q0w / 64] : 0u;
-  const uint32_t wand = wave_live ? a.blk_and[q0w / 64] : 0u;
+  const uint32_t wor = wave_live ? blk_or[q0w / 64] : 0u;
+  const uint32_t wand = wave_live ? blk_and[q0w / 64] : 0u;
 
   const int nkt = (L + BN - 1) / BN;
-  // Next tile at or after kt that is not fully masked for the strip, with its
-  // block summaries.  Called before the tile prefetch is issued, so waiting on
-  // these small loads never waits on the prefetch.
+  // Tile skipping (App. A.2): a key tile is live for the strip unless it is
+  // fully masked (AND of the strip's and the tile's group bits non-zero) or
+  // causally empty.  Each wave reads a window of 64 tiles' block summaries
+  // with one vector load (lane i holds tile k0 + i); a ballot then names the
+  // first live tile.  The main loop issues the window for the tile after the
+  // next one before its prefetch and consumes it after the compute, so these
+  // loads never stall a tile.
+  struct Window {
+    uint32_t an, on;  // this lane's tile summaries (AND, OR)
+  };
+  auto window = [&](int k0) {
+    const int k = k0 + lane;
+    Window w{0xFFFFFFFFu, 0u};
+    if (k < nkt) {
+      w.an = blk_and[k];
+      w.on = blk_or[k];
+    }
+    return w;
+  };
+  // First live tile in [k0, k0 + 64), or -1; its summaries in kor_out/kand_out.
+  auto pick = [&](int k0, const Window& w, uint32_t& kor_out, uint32_t& kand_out) -> int {
+    const int k = k0 + lane;
+    const bool ok = k < nkt && !(causal && k * BN > lastq_wg) && (qand & w.an) == 0u;
+    const uint64_t m = __builtin_amdgcn_ballot_w64(ok);
+    if (m == 0ull) return -1;
+    const int i = __builtin_ctzll(m);
+    kand_out = __builtin_amdgcn_readlane(w.an, i);
+    kor_out = __builtin_amdgcn_readlane(w.on, i);
+    return k0 + i;
+  };
+  // First live tile at or after kt (blocking; walks windows).
   auto next_live = [&](int kt, uint32_t& kor_out, uint32_t& kand_out) -> int {
-    for (; kt < nkt; ++kt) {
+    for (; kt < nkt; kt += 64) {
       if (causal && kt * BN > lastq_wg) return nkt;
-      const uint32_t an = a.blk_and[kt];
-      if ((qand & an) == 0u) {
-        kand_out = an;
-        kor_out = a.blk_or[kt];
-        return kt;
-      }
+      const int r = pick(kt, window(kt), kor_out, kand_out);
+      if (r >= 0) return r;
     }
     return nkt;
   };
@@ -127,7 +159,7 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_mfma(const FwdArgs a) {
     // group bits of the tile's keys, only when the CQS mask can bite here
     if ((qor & kor_t) != 0u && tid < BN) {
       const int key = kt * BN + tid;
-      kbits_s[buf][tid] = key < L ? run_bits(runs_s, a.n_runs, key) : 0u;
+      kbits_s[buf][tid] = key < L ? run_bits(runs_s, n_runs, key) : 0u;
     }
   };
 
@@ -139,18 +171,21 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_mfma(const FwdArgs a) {
   float m_run = -INFINITY, l_run = 0.f;
 
   __syncthreads();  // runs_s visible
-  const uint32_t qbits = qvalid ? run_bits(runs_s, a.n_runs, myq) : 0u;
+  const uint32_t qbits = qvalid ? run_bits(runs_s, n_runs, myq) : 0u;
 
-  uint32_t kor = 0u, kand = 0u;
+  uint32_t kor = 0u, kand = 0u, nor = 0u, nand = 0u;
   int kt = next_live(0, kor, kand);
   if (kt < nkt) {
     gload(kt);
     sstore(0, kt, kor);
   }
+  int kn = kt < nkt ? next_live(kt + 1, nor, nand) : nkt;
   int buf = 0;
   while (kt < nkt) {
-    uint32_t nor = 0u, nand = 0u;
-    const int kn = next_live(kt + 1, nor, nand);
+    // Summary window after kn, loaded now and used after this tile's
+    // compute; then the prefetch of tile kn.
+    const int kc = kn + 1;
+    const Window cw = window(kc);
     if (kn < nkt) gload(kn);
     lds_barrier();
 
@@ -231,17 +266,28 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_mfma(const FwdArgs a) {
       }
     }
     // ---- stage the next tile into the other buffer ----
-    if (kn < nkt) sstore(buf ^ 1, kn, nor);
+    int kc2 = nkt;
+    uint32_t or2 = 0u, and2 = 0u;
+    if (kn < nkt) {
+      sstore(buf ^ 1, kn, nor);
+      if (kc < nkt) {
+        kc2 = pick(kc, cw, or2, and2);
+        if (kc2 < 0) kc2 = next_live(kc + 64, or2, and2);
+      }
+    }
     buf ^= 1;
     kt = kn;
     kor = nor;
     kand = nand;
+    kn = kc2;
+    nor = or2;
+    nand = and2;
   }
 
   const float l_tot = l_run + swap_halves(l_run);
   if (!qvalid) return;
   if (MODE == kModeStats) {
-    float* accp = a.acc + (int64_t(b) * L + myq) * rs + int64_t(h) * D;
+    float* accp = a.acc + tj * a.acc_stride + (int64_t(b) * L + myq) * rs + int64_t(h) * D;
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
@@ -250,13 +296,13 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_mfma(const FwdArgs a) {
         *(f32x4*)(accp + 32 * db + 8 * i + 4 * half) = v;
       }
     if (half == 0) {
-      const int64_t si = (int64_t(b) * a.H + h) * L + myq;
+      const int64_t si = tj * a.st_stride + (int64_t(b) * a.H + h) * L + myq;
       a.m[si] = m_run;
       a.l[si] = l_tot;
     }
   } else {
     const float inv = 1.f / l_tot;
-    float* op = a.acc + (int64_t(b) * a.out_rows + myq) * rs + int64_t(h) * D;
+    float* op = a.acc + (int64_t(b) * L + myq) * rs + int64_t(h) * D;
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
@@ -266,7 +312,7 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_mfma(const FwdArgs a) {
         *(f32x4*)(op + 32 * db + 8 * i + 4 * half) = v;
       }
     if (half == 0) {
-      const int64_t si = (int64_t(b) * a.H + h) * a.out_rows + myq;
+      const int64_t si = (int64_t(b) * a.H + h) * L + myq;
       a.m[si] = (m_run + __log2f(l_tot)) * 0.69314718055994530942f;
     }
   }
@@ -282,15 +328,18 @@ __global__ void __launch_bounds__(256) attn_fwd_f32(const FwdArgs a) {
   __shared__ uint32_t kbits_s[BN];
   __shared__ DevRun runs_s[kMaxRuns];
   const int tid = threadIdx.x, sub = tid & 7, ql = tid >> 3;
-  const int L = a.L;
+  int64_t work = blockIdx.x;
+  const int tj = find_task(a.tasks, a.ntask, QPB, int64_t(a.H) * a.B, work);
+  const DevTask tk = a.tasks[tj];
+  const int L = int(tk.L_local);
   const int64_t nstrips = (L + QPB - 1) / QPB;
-  const int64_t work = blockIdx.x;
   const int strip = int(work % nstrips);
   const int h = int((work / nstrips) % a.H);
   const int b = int(work / (nstrips * a.H));
-  for (int i = tid; i < a.n_runs; i += 256) runs_s[i] = ((const DevRun*)a.runs)[i];
+  const int n_runs = tk.n_runs;
+  for (int i = tid; i < n_runs; i += 256) runs_s[i] = ((const DevRun*)(a.tab + tk.runs_off))[i];
   const int64_t rs = int64_t(a.H) * D;
-  const int64_t base = (int64_t(b) * a.seq_rows + a.row0) * rs + int64_t(h) * D;
+  const int64_t base = int64_t(b) * L * rs + int64_t(h) * D + tj * a.in_stride;
   const float* Qg = (const float*)a.q + base;
   const float* Kg = (const float*)a.k + base;
   const float* Vg = (const float*)a.v + base;
@@ -304,7 +353,7 @@ __global__ void __launch_bounds__(256) attn_fwd_f32(const FwdArgs a) {
     o[i] = 0.f;
   }
   __syncthreads();
-  const uint32_t qbits = qvalid ? run_bits(runs_s, a.n_runs, myq) : 0u;
+  const uint32_t qbits = qvalid ? run_bits(runs_s, n_runs, myq) : 0u;
   float m_run = -INFINITY, l_run = 0.f;
   const int nkt = (L + BN - 1) / BN;
   for (int kt = 0; kt < nkt; ++kt) {
@@ -316,7 +365,7 @@ __global__ void __launch_bounds__(256) attn_fwd_f32(const FwdArgs a) {
     }
     if (tid < BN) {
       const int key = kt * BN + tid;
-      kbits_s[tid] = key < L ? run_bits(runs_s, a.n_runs, key) : 0xFFFFFFFFu;
+      kbits_s[tid] = key < L ? run_bits(runs_s, n_runs, key) : 0xFFFFFFFFu;
     }
     __syncthreads();
     float s[BN];
@@ -351,30 +400,28 @@ __global__ void __launch_bounds__(256) attn_fwd_f32(const FwdArgs a) {
   }
   if (!qvalid) return;
   if (MODE == kModeStats) {
-    float* accp = a.acc + (int64_t(b) * L + myq) * rs + int64_t(h) * D + sub * SL;
+    float* accp = a.acc + tj * a.acc_stride + (int64_t(b) * L + myq) * rs + int64_t(h) * D + sub * SL;
 #pragma unroll
     for (int i = 0; i < SL; ++i) accp[i] = o[i];
     if (sub == 0) {
-      const int64_t si = (int64_t(b) * a.H + h) * L + myq;
+      const int64_t si = tj * a.st_stride + (int64_t(b) * a.H + h) * L + myq;
       a.m[si] = m_run;
       a.l[si] = l_run;
     }
   } else {
     const float inv = 1.f / l_run;
-    float* op = a.acc + (int64_t(b) * a.out_rows + myq) * rs + int64_t(h) * D + sub * SL;
+    float* op = a.acc + (int64_t(b) * L + myq) * rs + int64_t(h) * D + sub * SL;
 #pragma unroll
     for (int i = 0; i < SL; ++i) op[i] = o[i] * inv;
     if (sub == 0) {
-      const int64_t si = (int64_t(b) * a.H + h) * a.out_rows + myq;
+      const int64_t si = (int64_t(b) * a.H + h) * L + myq;
       a.m[si] = (m_run + log2f(l_run)) * 0.69314718055994530942f;
     }
   }
 }
 
 template <typename E, int D>
-static hipError_t launch_mfma(FwdMode mode, const FwdArgs& a, hipStream_t s) {
-  const int64_t n = ((a.L + 127) / 128) * int64_t(a.H) * a.B;
-  if (n == 0) return hipSuccess;
+static hipError_t launch_mfma(FwdMode mode, const FwdArgs& a, int64_t n, hipStream_t s) {
   if (mode == kModeStats)
     hipLaunchKernelGGL((attn_fwd_mfma<E, D, kModeStats>), dim3(unsigned(n)), dim3(256), 0, s, a);
   else
@@ -383,9 +430,7 @@ static hipError_t launch_mfma(FwdMode mode, const FwdArgs& a, hipStream_t s) {
 }
 
 template <int D>
-static hipError_t launch_f32(FwdMode mode, const FwdArgs& a, hipStream_t s) {
-  const int64_t n = ((a.L + 31) / 32) * int64_t(a.H) * a.B;
-  if (n == 0) return hipSuccess;
+static hipError_t launch_f32(FwdMode mode, const FwdArgs& a, int64_t n, hipStream_t s) {
   if (mode == kModeStats)
     hipLaunchKernelGGL((attn_fwd_f32<D, kModeStats>), dim3(unsigned(n)), dim3(256), 0, s, a);
   else
@@ -393,11 +438,17 @@ static hipError_t launch_f32(FwdMode mode, const FwdArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_fwd(cqsa_dtype dt, int d, FwdMode mode, const FwdArgs& a, hipStream_t s) {
-  if (a.n_runs > kMaxRuns) return hipErrorInvalidValue;
-  if (dt == CQSA_BF16) return d == 128 ? launch_mfma<BF16, 128>(mode, a, s) : launch_mfma<BF16, 64>(mode, a, s);
-  if (dt == CQSA_F16) return d == 128 ? launch_mfma<F16, 128>(mode, a, s) : launch_mfma<F16, 64>(mode, a, s);
-  return d == 128 ? launch_f32<128>(mode, a, s) : launch_f32<64>(mode, a, s);
+int fwd_rows_per_wg(cqsa_dtype dt) { return dt == CQSA_F32 ? 32 : 128; }
+
+hipError_t launch_fwd(cqsa_dtype dt, int d, FwdMode mode, const FwdArgs& a, int64_t wgs,
+                      hipStream_t s) {
+  if (wgs <= 0) return hipSuccess;
+  if (wgs > 0x7fffffff || a.ntask < 1) return hipErrorInvalidValue;
+  if (dt == CQSA_BF16)
+    return d == 128 ? launch_mfma<BF16, 128>(mode, a, wgs, s) : launch_mfma<BF16, 64>(mode, a, wgs, s);
+  if (dt == CQSA_F16)
+    return d == 128 ? launch_mfma<F16, 128>(mode, a, wgs, s) : launch_mfma<F16, 64>(mode, a, wgs, s);
+  return d == 128 ? launch_f32<128>(mode, a, wgs, s) : launch_f32<64>(mode, a, wgs, s);
 }
 
 }  // namespace cqsa

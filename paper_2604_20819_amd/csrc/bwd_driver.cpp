@@ -102,12 +102,19 @@ cqsa_status backward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa
     CQSA_HIP(hipEventRecord(sp.first, st));
   }
   CQSA_HIP(launch_bwd_preprocess(dO->data, (const float*)O->data, d_D, o.dtype, B, L, H, int(d), st));
+  if (rec.timing) {
+    CQSA_HIP(hipEventRecord(sp.second, st));
+    rec.spans[kStFinal].push_back(sp);
+    sp = {rec.make(), rec.make()};
+    CQSA_HIP(hipEventRecord(sp.first, st));
+  }
+  // the fused scatter-adds accumulate into zeroed gradients
   CQSA_HIP(launch_fill_zero((float*)dQ->data, B * L * H * d, st));
   CQSA_HIP(launch_fill_zero((float*)dK->data, B * L * H * d, st));
   CQSA_HIP(launch_fill_zero((float*)dV->data, B * L * H * d, st));
   if (rec.timing) {
     CQSA_HIP(hipEventRecord(sp.second, st));
-    rec.spans[kStFinal].push_back(sp);
+    rec.spans[kStMerge].push_back(sp);
   }
   CQSA_HIP(hipStreamWaitEvent(st, ev_tab, 0));
   // dQ kernels run on the second compute stream (they write dQ only, the dK/dV

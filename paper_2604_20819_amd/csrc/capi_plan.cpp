@@ -36,6 +36,7 @@ void cqsa_plan_opts_default(cqsa_plan_opts* o) {
   o->inputs_on_device = 1;
   o->acc_on_device = 1;
   o->with_backward = 0;
+  o->tasks_per_slot = 0;
 }
 
 cqsa_status cqsa_plan(int64_t L, int32_t H, int32_t d, int32_t causal,
@@ -61,23 +62,50 @@ cqsa_status cqsa_plan(int64_t L, int32_t H, int32_t d, int32_t causal,
     auto fits = [&](const Footprint& f) {
       return device_budget_bytes == 0 || f.peak <= device_budget_bytes;
     };
-    if (o.depth >= 0) {
-      p->depth = o.depth;
-      p->tasks = build_tasks(L, o, o.depth);
-      p->fp = footprint(g, o, o.depth, p->tasks);
-    } else {
-      bool found = false;
-      for (int32_t dep = o.min_depth; dep <= o.max_depth; ++dep) {
-        std::vector<Task> tasks = build_tasks(L, o, dep);
-        Footprint f = footprint(g, o, dep, tasks);
-        if (fits(f)) {
+    // Plans `tasks` at `dep` with the largest group size that fits the budget
+    // (or the forced one); returns whether the result fits.
+    auto plan_depth = [&](int32_t dep, std::vector<Task>&& tasks) {
+      const int64_t ntask = int64_t(tasks.size());
+      int32_t g_hi = 1;
+      if (o.tasks_per_slot > 0) {
+        g_hi = int32_t(std::min<int64_t>(o.tasks_per_slot, std::max<int64_t>(1, ntask)));
+      } else if (o.acc_on_device) {
+        // enough tasks per launch for kLaunchWgs work groups (two waves of
+        // the GPU's resident work groups); large tasks launch one by one
+        int64_t Lmax = 1;
+        for (const Task& t : tasks) Lmax = std::max(Lmax, t.L_local);
+        const int64_t rows = o.dtype == CQSA_F32 ? 32 : 128;
+        const int64_t wgs = std::max<int64_t>(1, (Lmax + rows - 1) / rows * o.B * H);
+        g_hi = int32_t(std::min<int64_t>({(kLaunchWgs + wgs - 1) / wgs, int64_t(kMaxContrib),
+                                          std::max<int64_t>(1, ntask)}));
+      }
+      const SegmentCover sc = segment_cover(L, tasks);
+      bool ok = false;
+      for (int32_t gs = std::max(1, g_hi); gs >= 1; --gs) {
+        std::vector<Group> groups = make_groups(ntask, gs);
+        std::vector<uint8_t> image;
+        std::vector<TableOffsets> offs;
+        pack_image(tasks, sc, H, &groups, &image, &offs);
+        Footprint f = footprint(g, o, dep, tasks, gs, image.size());
+        ok = fits(f);
+        if (ok || gs == 1 || o.tasks_per_slot > 0) {
           p->depth = dep;
-          p->tasks = std::move(tasks);
           p->fp = f;
-          found = true;
+          p->groups = std::move(groups);
+          p->packed = std::move(image);
+          p->table_off = std::move(offs);
           break;
         }
       }
+      p->tasks = std::move(tasks);
+      return ok;
+    };
+    if (o.depth >= 0) {
+      plan_depth(o.depth, build_tasks(L, o, o.depth));
+    } else {
+      bool found = false;
+      for (int32_t dep = o.min_depth; dep <= o.max_depth && !found; ++dep)
+        found = plan_depth(dep, build_tasks(L, o, dep));
       if (!found) {
         delete p;
         return fail(CQSA_ERR_BUDGET,
@@ -90,11 +118,10 @@ cqsa_status cqsa_plan(int64_t L, int32_t H, int32_t d, int32_t causal,
       p->max_L_local = std::max(p->max_L_local, t.L_local);
       max_runs = std::max(max_runs, t.runs.size());
     }
-    if (max_runs > 128) {
+    if (max_runs > size_t(kMaxRuns)) {
       delete p;
       return fail(CQSA_ERR_UNSUPPORTED, "cqsa_plan: a task has more than 128 runs (depth too large)");
     }
-    pack_tables(p->tasks, &p->packed, &p->table_off);
     *out = p;
     return CQSA_OK;
   } catch (const std::bad_alloc&) {
@@ -127,6 +154,8 @@ cqsa_status cqsa_plan_get_task(const cqsa_plan_t* p, int64_t t, cqsa_task* out) 
 }
 
 uint64_t cqsa_plan_modelled_device_bytes(const cqsa_plan_t* p) { return p ? p->fp.peak : 0; }
+
+int32_t cqsa_plan_tasks_per_slot(const cqsa_plan_t* p) { return p ? p->fp.group_size : -1; }
 
 cqsa_status cqsa_plan_tile_census(const cqsa_plan_t* p, int64_t* full, int64_t* clear,
                                   int64_t* mixed) {

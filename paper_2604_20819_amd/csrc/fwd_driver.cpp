@@ -1,17 +1,22 @@
 // cqsa_forward: the task streamer of the decomposed forward.
 //
-// Per task (Alg. 1, computed with the max-shifted merge of App. A.1):
-//   copy stream   : gather the task's runs of Q, K, V into staging slot t % S
-//                   (H2D from host inputs or D2D), then signal "staged";
-//   caller stream : wait "staged", run the inner forward kernel (local
-//                   statistics), then either recompose into the device
-//                   accumulator (acc on device) or hand the statistics to the
-//                   D2H stream and a host merge thread (acc on host);
+// The plan cuts the task list into launch groups of `group_size` consecutive
+// tasks (Alg. 1, computed with the max-shifted merge of App. A.1).  Per group:
+//   copy stream    : gather every task's runs of Q, K, V into its sub-slot of
+//                    staging slot k % S (H2D from host inputs or D2D), then
+//                    signal "staged";
+//   compute stream : wait "staged", run ONE inner-kernel launch over all the
+//                    group's tasks (local statistics per task); groups
+//                    alternate between the caller's stream and a second
+//                    compute stream so that consecutive launches overlap;
+//   aux stream     : device accumulator -- one gather-merge launch folds the
+//                    group's statistics into the running (acc, m, l), and the
+//                    last group's merge writes O and LSE; host accumulator --
+//                    D2H of the statistics, merged by a host thread;
 //   the slot is freed by an event once its last reader is done.
-// With S >= 2 slots the gather of task t+1 overlaps the compute of task t
-// (App. A.3: transfers overlap compute, at most two tasks in flight).
-// Depth 0 on device-resident tensors is the undecomposed call: one kernel that
-// writes O and LSE directly.
+// With S >= 2 slots the gather of group k+1 overlaps the compute of group k
+// (App. A.3: transfers overlap compute).  Depth 0 on device-resident tensors
+// is the undecomposed call: one kernel that writes O and LSE directly.
 #include <algorithm>
 #include <cmath>
 #include <condition_variable>
@@ -180,7 +185,7 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
   const bool in_dev = o.inputs_on_device, acc_dev = o.acc_on_device;
   const int depth = p->depth;
   const int64_t ntask = int64_t(p->tasks.size());
-  const bool direct = depth == 0 && in_dev && acc_dev;
+  const bool direct = direct_forward(o, depth);
 
   CallRecord& rec = call_record();
   rec.reset();
@@ -194,220 +199,207 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
   }
 
   // ---- workspace layout ----
+  // [plan image][running l][slot 0]...[slot S-1]; a slot holds group_size
+  // task sub-slots {Q, K, V, acc, m, l}, each sized for the longest task.
+  const int64_t ngroup = int64_t(p->groups.size());
+  const int64_t gsz = p->fp.group_size;
   const uint64_t tab_bytes = align_up(p->packed.size());
-  const uint64_t gl_bytes = (acc_dev && !direct) ? align_up(uint64_t(B) * H * L * 4) : 0;
-  const uint64_t slot_bytes = direct ? 0 : fwd_slot_bytes(p->g, o, p->max_L_local, true, true);
-  const int64_t nslot = std::min<int64_t>(o.n_slots, std::max<int64_t>(1, ntask));
-  const uint64_t total = tab_bytes + gl_bytes + uint64_t(nslot) * slot_bytes;
+  const uint64_t gl_bytes =
+      (acc_dev && !direct && ngroup > 1) ? align_up(uint64_t(B) * H * L * 4) : 0;
+  const uint64_t sub_bytes = direct ? 0 : fwd_slot_bytes(p->g, o, p->max_L_local, true, true);
+  std::vector<int64_t> slot_tasks;
+  if (!direct) slot_tasks = fwd_slot_tasks(ntask, int32_t(gsz), o.n_slots);
+  const int64_t nslot = int64_t(slot_tasks.size());
+  std::vector<uint64_t> slot_off(nslot + 1, 0);
+  for (int64_t i = 0; i < nslot; ++i) slot_off[i + 1] = slot_off[i] + uint64_t(slot_tasks[i]) * sub_bytes;
+  const uint64_t total = tab_bytes + gl_bytes + slot_off[nslot];
   Workspace ws;
   if ((s = acquire_workspace(C, total, &ws)) != CQSA_OK) return s;
   rec.stats.workspace_bytes = total;
   char* base = (char*)ws.ptr;
   char* d_tab = base;
-  float* d_gl = (float*)(base + tab_bytes);
-  struct Slot {
-    char *q, *k, *v;
-    float *acc, *m, *l;
-  };
-  std::vector<Slot> slots(nslot);
-  {
-    const uint64_t rows = uint64_t(B) * p->max_L_local * H;
-    const uint64_t in_b = align_up(rows * d * elem), acc_b = align_up(rows * d * 4),
-                   st_b = align_up(rows * 4);
-    for (int64_t i = 0; i < nslot; ++i) {
-      char* sb = base + tab_bytes + gl_bytes + uint64_t(i) * slot_bytes;
-      slots[i].q = sb;
-      slots[i].k = sb + in_b;
-      slots[i].v = sb + 2 * in_b;
-      slots[i].acc = (float*)(sb + 3 * in_b);
-      slots[i].m = (float*)(sb + 3 * in_b + acc_b);
-      slots[i].l = (float*)(sb + 3 * in_b + acc_b + st_b);
-    }
-  }
+  float* d_gl = gl_bytes ? (float*)(base + tab_bytes) : nullptr;
+  const uint64_t in_b = align_up(uint64_t(B) * p->max_L_local * H * d * elem);
+  const uint64_t acc_b = align_up(uint64_t(B) * p->max_L_local * H * d * 4);
+  const uint64_t st_b = align_up(uint64_t(B) * p->max_L_local * H * 4);
+  auto slot_base = [&](int64_t si) { return base + tab_bytes + gl_bytes + slot_off[si]; };
+  const DevTask* d_tasks = (const DevTask*)d_tab;
+  const int rows_wg = fwd_rows_per_wg(o.dtype);
 
   // ---- ordering against the caller's stream and the previous call ----
-  while (C->sync_events.size() < size_t(4 * nslot + 3)) {
+  while (C->sync_events.size() < size_t(4 * std::max<int64_t>(nslot, 1) + 3)) {
     hipEvent_t e;
     CQSA_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
     C->sync_events.push_back(e);
   }
   hipEvent_t ev_start = C->sync_events[0];
+  hipEvent_t ev_tail = C->sync_events[1];
   hipEvent_t* ev_staged = &C->sync_events[2];
   hipEvent_t* ev_free = &C->sync_events[2 + nslot];
-  hipEvent_t* ev_done = &C->sync_events[2 + 2 * nslot];
-  hipEvent_t ev_rec = C->sync_events[2 + 4 * nslot];  // last recompose issued
+  hipEvent_t* ev_inner = &C->sync_events[2 + 2 * nslot];
   if (C->ws_free_valid) CQSA_HIP(hipStreamWaitEvent(st, C->ws_free, 0));
   CQSA_HIP(hipEventRecord(ev_start, st));
   CQSA_HIP(hipStreamWaitEvent(C->copy, ev_start, 0));
   CQSA_HIP(hipMemcpyAsync(d_tab, p->packed.data(), p->packed.size(), hipMemcpyHostToDevice,
                           C->copy));
 
+  auto span_begin = [&](hipStream_t sm) -> std::pair<hipEvent_t, hipEvent_t> {
+    std::pair<hipEvent_t, hipEvent_t> sp{nullptr, nullptr};
+    if (rec.timing) {
+      sp = {rec.make(), rec.make()};
+      if (hipEventRecord(sp.first, sm) != hipSuccess) sp = {nullptr, nullptr};
+    }
+    return sp;
+  };
+  auto span_end = [&](std::pair<hipEvent_t, hipEvent_t> sp, hipStream_t sm, Stage k) {
+    if (sp.first && hipEventRecord(sp.second, sm) == hipSuccess) rec.spans[k].push_back(sp);
+  };
+
   float* Od = (float*)O->data;
   if (direct) {
     CQSA_HIP(hipEventRecord(ev_staged[0], C->copy));
     CQSA_HIP(hipStreamWaitEvent(st, ev_staged[0], 0));
-    const Task& t = p->tasks[0];
-    const TableOffsets& to = p->table_off[0];
     FwdArgs a{};
     a.q = Q->data; a.k = K->data; a.v = V->data;
-    a.seq_rows = L; a.row0 = 0; a.L = int32_t(t.L_local); a.B = int32_t(B); a.H = int32_t(H);
-    a.causal = p->g.causal; a.scale_log2 = scale_log2;
-    a.runs = d_tab + to.runs; a.n_runs = int32_t(t.runs.size());
-    a.blk_or = (const uint32_t*)(d_tab + to.blk_or);
-    a.blk_and = (const uint32_t*)(d_tab + to.blk_and);
-    a.acc = Od; a.m = LSE; a.l = nullptr; a.out_rows = L;
-    std::pair<hipEvent_t, hipEvent_t> sp{nullptr, nullptr};
-    if (rec.timing) {
-      sp = {rec.make(), rec.make()};
-      CQSA_HIP(hipEventRecord(sp.first, st));
-    }
-    CQSA_HIP(launch_fwd(o.dtype, int(d), kModeFinal, a, st));
-    if (rec.timing) {
-      CQSA_HIP(hipEventRecord(sp.second, st));
-      rec.spans[kStInner].push_back(sp);
-    }
+    a.acc = Od; a.m = LSE; a.l = nullptr;
+    a.tab = d_tab; a.tasks = d_tasks; a.ntask = 1;
+    a.B = int32_t(B); a.H = int32_t(H); a.causal = p->g.causal; a.scale_log2 = scale_log2;
+    const int64_t wgs = ((L + rows_wg - 1) / rows_wg) * B * H;
+    auto sp = span_begin(st);
+    CQSA_HIP(launch_fwd(o.dtype, int(d), kModeFinal, a, wgs, st));
+    span_end(sp, st, kStInner);
     rec.stats.inner_launches = 1;
   } else {
-    // accumulator: the O buffer holds acc, the LSE buffer holds m (log2)
+    // running global state: acc in the O buffer, m (log2) in the LSE buffer,
+    // l in the workspace (device) or on the host
     float* acc = Od;
     float* m = LSE;
     float* l = d_gl;
     std::vector<float> l_host;
     char* pin = nullptr;
     uint64_t pin_slot = 0;
-    if (acc_dev) {
-      CQSA_HIP(launch_acc_init(acc, m, l, B * L * H * d, B * H * L, st));
-    } else {
+    if (!acc_dev) {
       l_host.assign(size_t(B * H * L), 0.f);
       l = l_host.data();
       parallel_rows(B * L, [&](int64_t lo, int64_t hi) {
         std::fill(acc + lo * H * d, acc + hi * H * d, 0.f);
       });
       std::fill(m, m + B * H * L, -INFINITY);
-      const uint64_t rows = uint64_t(B) * p->max_L_local * H;
-      pin_slot = align_up(rows * d * 4) + 2 * align_up(rows * 4);
+      pin_slot = acc_b + 2 * st_b;
       void* pv = nullptr;
       if ((s = acquire_pinned(C, size_t(pin_slot * nslot), &pv)) != CQSA_OK) return s;
       pin = (char*)pv;
     }
     HostMerger merger;
     std::vector<int64_t> last_item(nslot, -1);
-    bool rec_issued = false;
     std::vector<bool> used(nslot, false);
     const hipMemcpyKind kind = in_dev ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice;
-    for (int64_t t = 0; t < ntask; ++t) {
-      const Task& task = p->tasks[t];
-      const int64_t Li = task.L_local;
-      if (Li == 0) continue;
-      const int64_t si = t % nslot;
-      Slot& S = slots[si];
-      const TableOffsets& to = p->table_off[t];
+    const char* srcs[3] = {(const char*)Q->data, (const char*)K->data, (const char*)V->data};
+    for (int64_t k = 0; k < ngroup; ++k) {
+      const Group& G = p->groups[k];
+      const int64_t si = k % nslot;
+      char* sb = slot_base(si);
       if (used[si]) CQSA_HIP(hipStreamWaitEvent(C->copy, ev_free[si], 0));
-      // gather
-      std::pair<hipEvent_t, hipEvent_t> sp{nullptr, nullptr};
-      if (rec.timing) {
-        sp = {rec.make(), rec.make()};
-        CQSA_HIP(hipEventRecord(sp.first, C->copy));
-      }
-      const char* srcs[3] = {(const char*)Q->data, (const char*)K->data, (const char*)V->data};
-      char* dsts[3] = {S.q, S.k, S.v};
-      if (in_dev) {
-        // device inputs: one gather kernel over the runs of all three tensors
-        StageArgs sa{};
-        for (int x = 0; x < 3; ++x) {
-          sa.src[x] = srcs[x];
-          sa.dst[x] = dsts[x];
+      // gather every task of the group into its sub-slot
+      int64_t wgs = 0;
+      for (int64_t j = 0; j < G.count; ++j) {
+        const int64_t t = G.task0 + j;
+        const Task& task = p->tasks[t];
+        const int64_t Li = task.L_local;
+        wgs += ((Li + rows_wg - 1) / rows_wg) * B * H;
+        if (Li == 0) continue;
+        char* sub = sb + uint64_t(j) * sub_bytes;
+        char* dsts[3] = {sub, sub + in_b, sub + 2 * in_b};
+        auto sp = span_begin(C->copy);
+        if (in_dev) {
+          // device inputs: one gather kernel over the runs of all three tensors
+          StageArgs sa{};
+          for (int x = 0; x < 3; ++x) {
+            sa.src[x] = srcs[x];
+            sa.dst[x] = dsts[x];
+          }
+          sa.n_tensors = 3; sa.row_bytes = int64_t(row_bytes); sa.Li = Li; sa.Lg = L;
+          sa.B = int32_t(B); sa.runs = d_tab + p->table_off[t].runs;
+          sa.n_runs = int32_t(task.runs.size());
+          CQSA_HIP(launch_stage(sa, C->copy));
+        } else {
+          // host inputs: one asynchronous H2D copy per run and batch element
+          for (int x = 0; x < 3; ++x)
+            for (const Run& r : task.runs)
+              for (int64_t b = 0; b < B; ++b)
+                CQSA_HIP(hipMemcpyAsync(dsts[x] + (b * Li + r.local_start) * row_bytes,
+                                        srcs[x] + (b * L + r.global_start) * row_bytes,
+                                        r.length * row_bytes, kind, C->copy));
         }
-        sa.n_tensors = 3; sa.row_bytes = int64_t(row_bytes); sa.Li = Li; sa.Lg = L;
-        sa.B = int32_t(B); sa.runs = d_tab + to.runs; sa.n_runs = int32_t(task.runs.size());
-        CQSA_HIP(launch_stage(sa, C->copy));
-      } else {
-        // host inputs: one asynchronous H2D copy per run and batch element
-        for (int x = 0; x < 3; ++x)
-          for (const Run& r : task.runs)
-            for (int64_t b = 0; b < B; ++b)
-              CQSA_HIP(hipMemcpyAsync(dsts[x] + (b * Li + r.local_start) * row_bytes,
-                                      srcs[x] + (b * L + r.global_start) * row_bytes,
-                                      r.length * row_bytes, kind, C->copy));
-      }
-      const uint64_t moved = uint64_t(3) * B * Li * row_bytes;
-      if (in_dev)
-        rec.stats.d2d_bytes += moved;
-      else
-        rec.stats.h2d_bytes += moved;
-      if (rec.timing) {
-        CQSA_HIP(hipEventRecord(sp.second, C->copy));
-        rec.spans[kStStage].push_back(sp);
+        span_end(sp, C->copy, kStStage);
+        const uint64_t moved = uint64_t(3) * B * Li * row_bytes;
+        if (in_dev)
+          rec.stats.d2d_bytes += moved;
+        else
+          rec.stats.h2d_bytes += moved;
       }
       CQSA_HIP(hipEventRecord(ev_staged[si], C->copy));
-      // Consecutive tasks alternate between the caller's stream and a second
-      // compute stream, so a task's kernel fills the tail of the previous one
-      // (two tasks in flight, App. A.3).  Inner kernels write only their slot.
-      const hipStream_t ls = (t & 1) ? C->lane : st;
+      // Consecutive groups alternate between the caller's stream and a second
+      // compute stream, so a group's launch fills the tail of the previous
+      // one (App. A.3: at most two slots in flight).  Inner kernels write
+      // only their slot.
+      const hipStream_t ls = (k & 1) ? C->lane : st;
       CQSA_HIP(hipStreamWaitEvent(ls, ev_staged[si], 0));
-      // inner kernel
       FwdArgs a{};
-      a.q = S.q; a.k = S.k; a.v = S.v;
-      a.seq_rows = Li; a.row0 = 0; a.L = int32_t(Li); a.B = int32_t(B); a.H = int32_t(H);
-      a.causal = p->g.causal; a.scale_log2 = scale_log2;
-      a.runs = d_tab + to.runs; a.n_runs = int32_t(task.runs.size());
-      a.blk_or = (const uint32_t*)(d_tab + to.blk_or);
-      a.blk_and = (const uint32_t*)(d_tab + to.blk_and);
-      a.acc = S.acc; a.m = S.m; a.l = S.l; a.out_rows = Li;
-      if (rec.timing) {
-        sp = {rec.make(), rec.make()};
-        CQSA_HIP(hipEventRecord(sp.first, ls));
+      a.q = sb; a.k = sb + in_b; a.v = sb + 2 * in_b;
+      a.in_stride = int64_t(sub_bytes / elem);
+      a.acc = (float*)(sb + 3 * in_b);
+      a.m = (float*)(sb + 3 * in_b + acc_b);
+      a.l = (float*)(sb + 3 * in_b + acc_b + st_b);
+      a.acc_stride = a.st_stride = int64_t(sub_bytes / 4);
+      a.tab = d_tab; a.tasks = d_tasks + G.task0; a.ntask = int32_t(G.count);
+      a.B = int32_t(B); a.H = int32_t(H); a.causal = p->g.causal; a.scale_log2 = scale_log2;
+      {
+        auto sp = span_begin(ls);
+        CQSA_HIP(launch_fwd(o.dtype, int(d), kModeStats, a, wgs, ls));
+        span_end(sp, ls, kStInner);
       }
-      CQSA_HIP(launch_fwd(o.dtype, int(d), kModeStats, a, ls));
       rec.stats.inner_launches += 1;
-      if (rec.timing) {
-        CQSA_HIP(hipEventRecord(sp.second, ls));
-        rec.spans[kStInner].push_back(sp);
-      }
+      CQSA_HIP(hipEventRecord(ev_inner[si], ls));
       if (acc_dev) {
-        // recomposes touch shared rows: each waits for the one before it
-        if (rec_issued) CQSA_HIP(hipStreamWaitEvent(ls, ev_rec, 0));
-        MergeArgs mg{};
-        mg.acc_i = S.acc; mg.m_i = S.m; mg.l_i = S.l;
-        mg.acc = acc; mg.m = m; mg.l = l;
-        mg.runs = d_tab + to.runs; mg.n_runs = int32_t(task.runs.size());
-        mg.Li = Li; mg.L = L; mg.B = int32_t(B); mg.H = int32_t(H); mg.d = int32_t(d);
-        if (rec.timing) {
-          sp = {rec.make(), rec.make()};
-          CQSA_HIP(hipEventRecord(sp.first, ls));
+        // merge on the auxiliary stream: combines run in group order there,
+        // and the next group's inner kernel overlaps this one's combine
+        CQSA_HIP(hipStreamWaitEvent(C->aux, ev_inner[si], 0));
+        CombineArgs cb{};
+        cb.segs = (const DevSeg*)(d_tab + G.seg_off); cb.n_seg = G.n_seg;
+        cb.contribs = (const DevContrib*)(d_tab + G.contrib_off);
+        cb.tasks = d_tasks + G.task0;
+        cb.acc_i = a.acc; cb.m_i = a.m; cb.l_i = a.l;
+        cb.acc_stride = a.acc_stride; cb.st_stride = a.st_stride;
+        cb.acc = acc; cb.m = m; cb.l = l; cb.L = L;
+        cb.B = int32_t(B); cb.H = int32_t(H); cb.d = int32_t(d); cb.final = G.final ? 1 : 0;
+        if (G.blocks > 0) {
+          auto sp = span_begin(C->aux);
+          CQSA_HIP(launch_combine(cb, G.blocks, C->aux));
+          span_end(sp, C->aux, kStMerge);
+          rec.stats.merge_launches += 1;
         }
-        CQSA_HIP(launch_recompose(mg, ls));
-        if (rec.timing) {
-          CQSA_HIP(hipEventRecord(sp.second, ls));
-          rec.spans[kStMerge].push_back(sp);
-        }
-        CQSA_HIP(hipEventRecord(ev_rec, ls));
-        rec_issued = true;
-        CQSA_HIP(hipEventRecord(ev_free[si], ls));
+        CQSA_HIP(hipEventRecord(ev_free[si], C->aux));
       } else {
         // hand the statistics to the host: D2H into pinned staging, then merge;
         // the staging of this slot must have been consumed by its last merge
+        // (groups hold one task when the accumulator is on the host)
         if (!merger.wait_done(last_item[si])) return fail(CQSA_ERR_HIP, "host merge failed");
+        const int64_t t = G.task0;
+        const int64_t Li = p->tasks[t].L_local;
         char* hp = pin + uint64_t(si) * pin_slot;
         const uint64_t rows = uint64_t(B) * Li * H;
         float* h_acc = (float*)hp;
-        float* h_m = (float*)(hp + align_up(uint64_t(B) * p->max_L_local * H * d * 4));
-        float* h_l = (float*)((char*)h_m + align_up(uint64_t(B) * p->max_L_local * H * 4));
-        CQSA_HIP(hipEventRecord(ev_done[si], ls));
-        CQSA_HIP(hipStreamWaitEvent(C->d2h, ev_done[si], 0));
-        if (rec.timing) {
-          sp = {rec.make(), rec.make()};
-          CQSA_HIP(hipEventRecord(sp.first, C->d2h));
-        }
-        CQSA_HIP(hipMemcpyAsync(h_acc, S.acc, rows * d * 4, hipMemcpyDeviceToHost, C->d2h));
-        CQSA_HIP(hipMemcpyAsync(h_m, S.m, rows * 4, hipMemcpyDeviceToHost, C->d2h));
-        CQSA_HIP(hipMemcpyAsync(h_l, S.l, rows * 4, hipMemcpyDeviceToHost, C->d2h));
+        float* h_m = (float*)(hp + acc_b);
+        float* h_l = (float*)(hp + acc_b + st_b);
+        CQSA_HIP(hipStreamWaitEvent(C->aux, ev_inner[si], 0));
+        auto sp = span_begin(C->aux);
+        CQSA_HIP(hipMemcpyAsync(h_acc, a.acc, rows * d * 4, hipMemcpyDeviceToHost, C->aux));
+        CQSA_HIP(hipMemcpyAsync(h_m, a.m, rows * 4, hipMemcpyDeviceToHost, C->aux));
+        CQSA_HIP(hipMemcpyAsync(h_l, a.l, rows * 4, hipMemcpyDeviceToHost, C->aux));
+        span_end(sp, C->aux, kStD2H);
         rec.stats.d2h_bytes += rows * (d + 2) * 4;
-        if (rec.timing) {
-          CQSA_HIP(hipEventRecord(sp.second, C->d2h));
-          rec.spans[kStD2H].push_back(sp);
-        }
-        CQSA_HIP(hipEventRecord(ev_free[si], C->d2h));
+        CQSA_HIP(hipEventRecord(ev_free[si], C->aux));
         const hipEvent_t wait_ev = ev_free[si];
         const Task* tp = &p->tasks[t];
         last_item[si] = merger.push([=, &rec]() -> bool {
@@ -421,26 +413,16 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
       }
       used[si] = true;
     }
-    if (acc_dev) {
-      if (rec_issued) CQSA_HIP(hipStreamWaitEvent(st, ev_rec, 0));
-      std::pair<hipEvent_t, hipEvent_t> sp{nullptr, nullptr};
-      if (rec.timing) {
-        sp = {rec.make(), rec.make()};
-        CQSA_HIP(hipEventRecord(sp.first, st));
-      }
-      CQSA_HIP(launch_finalize(acc, m, l, B, L, H, int(d), st));
-      if (rec.timing) {
-        CQSA_HIP(hipEventRecord(sp.second, st));
-        rec.spans[kStFinal].push_back(sp);
-      }
-    } else {
+    if (!acc_dev) {
       if (!merger.finish()) return fail(CQSA_ERR_HIP, "host merge: event wait failed");
+      auto t0 = std::chrono::steady_clock::now();
       host_finalize(acc, m, l, B, L, H, d);
-      // the second compute stream's last kernel precedes its D2H, which the
-      // merges waited for; order the caller's stream after it all the same
-      CQSA_HIP(hipEventRecord(ev_done[0], C->d2h));
-      CQSA_HIP(hipStreamWaitEvent(st, ev_done[0], 0));
+      auto t1 = std::chrono::steady_clock::now();
+      rec.host_final_ms += std::chrono::duration<double, std::milli>(t1 - t0).count();
     }
+    // every inner kernel precedes its merge or D2H on the auxiliary stream
+    CQSA_HIP(hipEventRecord(ev_tail, C->aux));
+    CQSA_HIP(hipStreamWaitEvent(st, ev_tail, 0));
   }
   if (rec.timing) CQSA_HIP(hipEventRecord(rec.wall1, st));
   CQSA_HIP(hipEventRecord(C->ws_free, st));

@@ -13,6 +13,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "records.hpp"
+
 namespace cqsa {
 
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
@@ -122,15 +124,6 @@ __device__ __forceinline__ int lane_id() {
   return (int)__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
 }
 
-// One maximal run of a task on the device (see plan.hpp).
-struct DevRun {
-  int64_t local_start;
-  int64_t global_start;
-  int64_t length;
-  uint32_t bits;
-  uint32_t pad;
-};
-
 // Group bits and global index of a task-local token (runs sorted by local start).
 __device__ __forceinline__ uint32_t run_bits(const DevRun* runs, int n, int64_t local) {
   for (int i = 0; i < n; ++i)
@@ -142,6 +135,20 @@ __device__ __forceinline__ int64_t run_global(const DevRun* runs, int n, int64_t
     if (local < runs[i].local_start + runs[i].length)
       return runs[i].global_start + (local - runs[i].local_start);
   return 0;
+}
+
+// Task of a work item in a launch over several tasks, whose work items are
+// laid out task after task (ceil(L_j / rows) * per_row items for task j).
+// Returns j and leaves the item's index within task j in `w`.
+__device__ __forceinline__ int find_task(const DevTask* tasks, int ntask, int rows,
+                                         int64_t per_row, int64_t& w) {
+  int j = 0;
+  for (; j < ntask - 1; ++j) {
+    const int64_t n = ((tasks[j].L_local + rows - 1) / rows) * per_row;
+    if (w < n) break;
+    w -= n;
+  }
+  return j;
 }
 
 // Work-group id remapped so that consecutive work items land on the same XCD

@@ -5,10 +5,9 @@
 #include <stdint.h>
 
 #include "cqsa.h"
+#include "records.hpp"
 
 namespace cqsa {
-
-constexpr int kMaxRuns = 128;  // runs per task the kernels accept (l**depth bound)
 
 // Epilogue of the inner forward kernel.
 enum FwdMode : int {
@@ -16,38 +15,46 @@ enum FwdMode : int {
   kModeFinal = 1,  // single task covering all tokens: write O = acc/l and LSE
 };
 
+// One launch of the inner forward kernel over `ntask` tasks (a launch group).
+// Task j's rows are [B, L_j, H, d] at q/k/v + j * in_stride elements and its
+// statistics are acc_j [B, L_j, H, d] at acc + j * acc_stride, m_j and l_j
+// [B, H, L_j] at m/l + j * st_stride.  In final mode the single task spans all
+// L tokens: q/k/v are the caller's tensors, acc is O and m is LSE.
 struct FwdArgs {
-  const void* q;        // [B, seq_rows, H, d] input rows (staged slot or caller tensor)
+  const void* q;
   const void* k;
   const void* v;
-  int64_t seq_rows;     // rows per batch element in q/k/v
-  int64_t row0;         // first row of the task in q/k/v
-  int32_t L;            // task length
+  int64_t in_stride;
+  float* acc;
+  float* m;             // log2 domain (stats) or natural-log LSE (final)
+  float* l;             // stats only
+  int64_t acc_stride, st_stride;
+  const char* tab;      // packed plan image (DevTask offsets are relative to it)
+  const DevTask* tasks; // the launch's tasks
+  int32_t ntask;
   int32_t B, H;
   int32_t causal;
   float scale_log2;     // softmax scale * log2(e)
-  const void* runs;     // DevRun[n_runs], task-local
-  int32_t n_runs;
-  const uint32_t* blk_or;   // per 64-token block
-  const uint32_t* blk_and;
-  float* acc;           // stats: [B, L, H, d]; final: O [B, out_rows, H, d]
-  float* m;             // stats: [B, H, L] (log2 domain); final: LSE [B, H, out_rows]
-  float* l;             // stats: [B, H, L]; final: unused
-  int64_t out_rows;
 };
 
-// Recompose one task's statistics into the global accumulator (device).
-struct MergeArgs {
-  const float* acc_i;   // [B, Li, H, d]
-  const float* m_i;     // [B, H, Li] log2 domain
-  const float* l_i;     // [B, H, Li]
-  float* acc;           // [B, L, H, d]  (the O buffer)
-  float* m;             // [B, H, L]     (the LSE buffer, log2 domain until finalize)
-  float* l;             // [B, H, L]
-  const void* runs;     // DevRun[n_runs]
-  int32_t n_runs;
-  int64_t Li, L;
+// Gather-merge of one launch group's task statistics into the global
+// accumulator (App. A.1, Eq. "merge"), fused with the finalisation
+// O = acc / l, LSE = m + log l when the group is the last one.
+struct CombineArgs {
+  const DevSeg* segs;        // the group's segments, ascending blk0
+  int32_t n_seg;
+  const DevContrib* contribs;
+  const DevTask* tasks;      // the group's tasks (for L_j)
+  const float* acc_i;        // task j's statistics at + j * acc_stride / st_stride
+  const float* m_i;
+  const float* l_i;
+  int64_t acc_stride, st_stride;
+  float* acc;                // [B, L, H, d] running acc, or O when final
+  float* m;                  // [B, H, L] running max (log2), or LSE when final
+  float* l;                  // [B, H, L] running sum
+  int64_t L;
   int32_t B, H, d;
+  int32_t final;
 };
 
 // Inner backward kernels over one staged task (App. A.1, Eq. "globallse").
@@ -86,17 +93,19 @@ struct StageArgs {
   int32_t n_runs;
 };
 
-hipError_t launch_fwd(cqsa_dtype dt, int d, FwdMode mode, const FwdArgs& a, hipStream_t s);
-hipError_t launch_acc_init(float* acc, float* m, float* l, int64_t n_acc, int64_t n_stat,
-                           hipStream_t s);
-hipError_t launch_recompose(const MergeArgs& a, hipStream_t s);
+// `wgs` = total work groups: sum over the tasks of ceil(L_j / 128) * B * H
+// (ceil(L_j / 32) * B * H for fp32 inputs).
+hipError_t launch_fwd(cqsa_dtype dt, int d, FwdMode mode, const FwdArgs& a, int64_t wgs,
+                      hipStream_t s);
+int fwd_rows_per_wg(cqsa_dtype dt);
+// `blocks` = combine work groups per batch element (the group's last segment's
+// blk0 plus its block count).
+hipError_t launch_combine(const CombineArgs& a, int64_t blocks, hipStream_t s);
 hipError_t launch_stage(const StageArgs& a, hipStream_t s);
 hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t s);
 hipError_t launch_bwd_preprocess(const void* dO, const float* O, float* D, cqsa_dtype dt,
                                  int64_t B, int64_t L, int64_t H, int d, hipStream_t s);
 hipError_t launch_bwd_dkdv(cqsa_dtype dt, int d, const BwdArgs& a, hipStream_t s);
 hipError_t launch_bwd_dq(cqsa_dtype dt, int d, const BwdArgs& a, hipStream_t s);
-hipError_t launch_finalize(float* acc, float* m, const float* l, int64_t B, int64_t L, int64_t H,
-                           int d, hipStream_t s);
 
 }  // namespace cqsa

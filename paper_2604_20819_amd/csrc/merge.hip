@@ -1,132 +1,139 @@
-// Recomposition kernels (App. A.1): initialise the global accumulator, merge
-// one task's (acc_i, l_i, m_i) into it with the max-shifted rule of Eq.
-// "merge", and finalise O = acc / l, LSE = m + log l.
+// Recomposition (App. A.1): the max-shifted merge of Eq. "merge" of a launch
+// group's task statistics (acc_i, m_i, l_i) into the global accumulator, fused
+// with the finalisation O = acc / l, LSE = m + log l after the last group.
 //
-// Statistics are kept in the log2 domain with integer-valued maxima (the
-// inner kernels round running maxima up to integers), so both rescale factors
-// e^{m-m'} and e^{m_i-m'} are exact powers of two.  A task row with no kept
-// key carries m_i = -inf and is skipped as a null contribution.
+// Gather form: every work group owns kCombinePairs consecutive (token, head)
+// pairs of one elementary segment and one batch element.  A segment lies
+// inside one run of each task that holds it, so each contribution is a
+// contiguous slab of the task's statistics; the work group reads every
+// contribution (and the running global state when an earlier group touched
+// these tokens), merges in registers and writes each output once.  Work
+// groups own disjoint tokens, so the merge needs no atomics and no ordering
+// between tasks of the group.
 //
-// All passes are HBM-bound and walk rows of d contiguous floats with 16-byte
-// accesses; each work group owns (batch, head, 32 consecutive local rows) and
-// resolves local -> global rows through the task's runs.
-#include <algorithm>
-
+// Statistics are in the log2 domain with integer-valued maxima (the inner
+// kernels round running maxima up to integers), so every factor
+// 2^(m_i - m') is an exact power of two.  A task row with no kept key carries
+// m_i = -inf and l_i = 0: a null contribution with factor 0.
 #include "hip_common.hpp"
 #include "kernels.hpp"
 
 namespace cqsa {
 
-__global__ void __launch_bounds__(256) acc_init_kernel(float* acc, float* m, float* l,
-                                                       int64_t n_acc4, int64_t n_stat) {
-  const int64_t stride = int64_t(gridDim.x) * blockDim.x;
-  for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n_acc4; i += stride)
-    ((f32x4*)acc)[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n_stat; i += stride) {
-    m[i] = -INFINITY;
-    l[i] = 0.f;
-  }
-}
-
 template <int D>
-__global__ void __launch_bounds__(256) recompose_kernel(const MergeArgs a) {
-  constexpr int ROWS = 32, TPR = 8, FPT = D / TPR;  // threads per row, floats per thread
-  __shared__ DevRun runs_s[kMaxRuns];
+__global__ void __launch_bounds__(256) combine_kernel(const CombineArgs a) {
+  constexpr int P = kCombinePairs;
+  constexpr int F4 = D / 4;            // float4 per (token, head)
+  constexpr int NF = P * F4 / 256;     // float4 per thread
+  static_assert(P * F4 % 256 == 0, "combine tiling");
+  __shared__ float fac_s[kMaxContrib + 1][P];
+  __shared__ float inv_s[P];
+
   const int tid = threadIdx.x;
-  for (int i = tid; i < a.n_runs; i += 256) runs_s[i] = ((const DevRun*)a.runs)[i];
-  __syncthreads();
-  const int64_t nchunk = (a.Li + ROWS - 1) / ROWS;
-  const int64_t w = blockIdx.x;
-  const int64_t chunk = w % nchunk;
-  const int h = int((w / nchunk) % a.H);
-  const int b = int(w / (nchunk * a.H));
-  const int64_t r = chunk * ROWS + tid / TPR;
-  if (r >= a.Li) return;
-  int64_t g = -1;
-  for (int i = 0; i < a.n_runs; ++i)
-    if (r < runs_s[i].local_start + runs_s[i].length) {
-      g = runs_s[i].global_start + (r - runs_s[i].local_start);
-      break;
+  const int b = blockIdx.y;
+  const int64_t blk = blockIdx.x;
+  // segment of this work group: the last one with blk0 <= blk
+  int lo = 0, hi = a.n_seg - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (a.segs[mid].blk0 <= blk) lo = mid; else hi = mid - 1;
+  }
+  const DevSeg sg = a.segs[lo];
+  const int H = a.H;
+  const int64_t pair0 = (blk - sg.blk0) * P;        // first pair within the segment
+  const int64_t npair64 = sg.len * H - pair0;
+  const int npair = npair64 < P ? int(npair64) : P;
+  const int nc = sg.n_c < kMaxContrib ? sg.n_c : kMaxContrib;  // the planner caps n_c
+  const bool glob = sg.has_global != 0;
+
+  // merge factors of each pair (one thread per pair)
+  if (tid < npair) {
+    const int64_t pr = pair0 + tid;
+    const int64_t r = pr / H;
+    const int h = int(pr % H);
+    const int64_t gi = (int64_t(b) * H + h) * a.L + sg.g0 + r;
+    float mg = -INFINITY, lg = 0.f;
+    if (glob) {
+      mg = a.m[gi];
+      lg = a.l[gi];
     }
-  if (g < 0) return;
-  const int64_t si = (int64_t(b) * a.H + h) * a.Li + r;
-  const int64_t gi = (int64_t(b) * a.H + h) * a.L + g;
-  const float mi = a.m_i[si];
-  if (mi == -INFINITY) return;  // null contribution
-  const float mo = a.m[gi];
-  const float mn = fmaxf(mo, mi);
-  const float fo = mo == -INFINITY ? 0.f : fast_exp2(mo - mn);
-  const float fi = fast_exp2(mi - mn);
-  const int64_t rs = int64_t(a.H) * D;
-  const float* src = a.acc_i + (int64_t(b) * a.Li + r) * rs + int64_t(h) * D + (tid % TPR) * FPT;
-  float* dst = a.acc + (int64_t(b) * a.L + g) * rs + int64_t(h) * D + (tid % TPR) * FPT;
+    float mx = mg;
+    for (int k = 0; k < nc; ++k) {
+      const DevContrib c = a.contribs[sg.c_off + k];
+      const int64_t Lj = a.tasks[c.j].L_local;
+      const float mk = a.m_i[c.j * a.st_stride + (int64_t(b) * H + h) * Lj + c.local_start + r];
+      mx = fmaxf(mx, mk);
+    }
+    const float fg = mg == -INFINITY ? 0.f : fast_exp2(mg - mx);
+    float lsum = lg * fg;
+    fac_s[0][tid] = fg;
+    for (int k = 0; k < nc; ++k) {
+      const DevContrib c = a.contribs[sg.c_off + k];
+      const int64_t Lj = a.tasks[c.j].L_local;
+      const int64_t si = c.j * a.st_stride + (int64_t(b) * H + h) * Lj + c.local_start + r;
+      const float mk = a.m_i[si];
+      const float f = mk == -INFINITY ? 0.f : fast_exp2(mk - mx);
+      lsum += a.l_i[si] * f;
+      fac_s[k + 1][tid] = f;
+    }
+    if (a.final) {
+      inv_s[tid] = 1.f / lsum;
+      a.m[gi] = (mx + __log2f(lsum)) * 0.69314718055994530942f;
+    } else {
+      inv_s[tid] = 1.f;
+      a.m[gi] = mx;
+      a.l[gi] = lsum;
+    }
+  }
+  __syncthreads();
+
+  // stream the (token, head) rows: contiguous in the global tensor and in
+  // every contribution, 16 bytes per thread per pass
+  const int64_t row_g = (int64_t(b) * a.L + sg.g0) * H;  // pair index of token g0, head 0
+  f32x4 acc[NF];
 #pragma unroll
-  for (int i = 0; i < FPT; i += 4) {
-    const f32x4 x = *(const f32x4*)(src + i);
-    f32x4 y = *(const f32x4*)(dst + i);
-    y = y * fo + x * fi;
-    *(f32x4*)(dst + i) = y;
+  for (int i = 0; i < NF; ++i) {
+    const int f = tid + 256 * i, p = f / F4;
+    acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (glob && p < npair) {
+      const f32x4 x = *(const f32x4*)(a.acc + (row_g + pair0 + p) * D + (f % F4) * 4);
+      acc[i] = x * fac_s[0][p];
+    }
   }
-  if (tid % TPR == 0) {
-    a.l[gi] = a.l[gi] * fo + a.l_i[si] * fi;
-    a.m[gi] = mn;
-  }
-}
-
-template <int D>
-__global__ void __launch_bounds__(256) finalize_kernel(float* acc, float* m, const float* l,
-                                                       int64_t B, int64_t L, int64_t H) {
-  constexpr int ROWS = 32, TPR = 8, FPT = D / TPR;
-  const int tid = threadIdx.x;
-  const int64_t nchunk = (L + ROWS - 1) / ROWS;
-  const int64_t w = blockIdx.x;
-  const int64_t chunk = w % nchunk;
-  const int64_t h = (w / nchunk) % H;
-  const int64_t b = w / (nchunk * H);
-  const int64_t r = chunk * ROWS + tid / TPR;
-  if (r >= L) return;
-  const int64_t si = (b * H + h) * L + r;
-  const float ll = l[si];
-  const float inv = 1.f / ll;
-  float* p = acc + (b * L + r) * H * D + h * D + (tid % TPR) * FPT;
+  for (int k = 0; k < nc; ++k) {
+    const DevContrib c = a.contribs[sg.c_off + k];
+    const int64_t Lj = a.tasks[c.j].L_local;
+    const float* src = a.acc_i + c.j * a.acc_stride +
+                       ((int64_t(b) * Lj + c.local_start) * H + pair0) * D;
+    f32x4 x[NF];
 #pragma unroll
-  for (int i = 0; i < FPT; i += 4) {
-    f32x4 y = *(f32x4*)(p + i);
-    *(f32x4*)(p + i) = y * inv;
+    for (int i = 0; i < NF; ++i) {
+      const int f = tid + 256 * i, p = f / F4;
+      x[i] = p < npair ? *(const f32x4*)(src + int64_t(p) * D + (f % F4) * 4)
+                       : f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+    for (int i = 0; i < NF; ++i) {
+      const int p = (tid + 256 * i) / F4;
+      if (p < npair) acc[i] += x[i] * fac_s[k + 1][p];
+    }
   }
-  if (tid % TPR == 0) m[si] = (m[si] + __log2f(ll)) * 0.69314718055994530942f;
+#pragma unroll
+  for (int i = 0; i < NF; ++i) {
+    const int f = tid + 256 * i, p = f / F4;
+    if (p < npair)
+      *(f32x4*)(a.acc + (row_g + pair0 + p) * D + (f % F4) * 4) = acc[i] * inv_s[p];
+  }
 }
 
-hipError_t launch_acc_init(float* acc, float* m, float* l, int64_t n_acc, int64_t n_stat,
-                           hipStream_t s) {
-  const int64_t n4 = n_acc / 4;
-  int64_t blocks = (std::max(n4, n_stat) + 255) / 256;
-  if (blocks > 65536) blocks = 65536;
-  if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL(acc_init_kernel, dim3(unsigned(blocks)), dim3(256), 0, s, acc, m, l, n4,
-                     n_stat);
-  return hipGetLastError();
-}
-
-hipError_t launch_recompose(const MergeArgs& a, hipStream_t s) {
-  if (a.n_runs > kMaxRuns) return hipErrorInvalidValue;
-  const int64_t n = ((a.Li + 31) / 32) * int64_t(a.H) * a.B;
-  if (n == 0) return hipSuccess;
+hipError_t launch_combine(const CombineArgs& a, int64_t blocks, hipStream_t s) {
+  if (blocks <= 0 || a.B <= 0) return hipSuccess;
+  if (a.n_seg < 1 || blocks > 0x7fffffff || a.B > 65535) return hipErrorInvalidValue;
+  const dim3 grid(unsigned(blocks), unsigned(a.B));
   if (a.d == 128)
-    hipLaunchKernelGGL(recompose_kernel<128>, dim3(unsigned(n)), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(combine_kernel<128>, grid, dim3(256), 0, s, a);
   else
-    hipLaunchKernelGGL(recompose_kernel<64>, dim3(unsigned(n)), dim3(256), 0, s, a);
-  return hipGetLastError();
-}
-
-hipError_t launch_finalize(float* acc, float* m, const float* l, int64_t B, int64_t L, int64_t H,
-                           int d, hipStream_t s) {
-  const int64_t n = ((L + 31) / 32) * H * B;
-  if (n == 0) return hipSuccess;
-  if (d == 128)
-    hipLaunchKernelGGL(finalize_kernel<128>, dim3(unsigned(n)), dim3(256), 0, s, acc, m, l, B, L, H);
-  else
-    hipLaunchKernelGGL(finalize_kernel<64>, dim3(unsigned(n)), dim3(256), 0, s, acc, m, l, B, L, H);
+    hipLaunchKernelGGL(combine_kernel<64>, grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

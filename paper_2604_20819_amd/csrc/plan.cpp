@@ -86,6 +86,10 @@ cqsa_status validate_plan_args(int64_t L, int32_t H, int32_t d, const cqsa_plan_
     return bad(CQSA_ERR_INVALID_ARG, "inputs_on_device must be 0 or 1");
   if (o.acc_on_device != 0 && o.acc_on_device != 1)
     return bad(CQSA_ERR_INVALID_ARG, "acc_on_device must be 0 or 1");
+  if (o.tasks_per_slot < 0 || o.tasks_per_slot > kMaxContrib)
+    return bad(CQSA_ERR_INVALID_ARG, "tasks_per_slot must be in [0, 32]");
+  if (o.tasks_per_slot > 1 && !o.acc_on_device)
+    return bad(CQSA_ERR_UNSUPPORTED, "tasks_per_slot > 1 needs the accumulator on the device");
   if (o.with_backward && (!o.inputs_on_device || !o.acc_on_device))
     return bad(CQSA_ERR_UNSUPPORTED, "the backward supports device-resident tensors only");
   if (o.with_backward && o.dtype == CQSA_F32)
@@ -196,61 +200,150 @@ uint64_t bwd_slot_bytes(const Geometry& g, const cqsa_plan_opts& o, int64_t Lmax
   return staged ? 4 * align_up(rows * g.d * dtype_size(o.dtype)) : 0;
 }
 
-// Per task on the device: runs (32 bytes each) and two 32-bit words per block.
-uint64_t table_bytes(const std::vector<Task>& tasks) {
-  uint64_t s = 0;
-  for (const Task& t : tasks)
-    s += align_up(t.runs.size() * 32) + 2 * align_up(t.blk_or.size() * 4);
-  return s;
+bool direct_forward(const cqsa_plan_opts& o, int32_t depth) {
+  return depth == 0 && o.inputs_on_device && o.acc_on_device;
 }
 
-void pack_tables(const std::vector<Task>& tasks, std::vector<uint8_t>* image,
-                 std::vector<TableOffsets>* offs) {
-  image->assign(table_bytes(tasks), 0);
-  offs->clear();
-  uint64_t at = 0;
-  for (const Task& t : tasks) {
-    TableOffsets o;
-    o.runs = at;
-    for (size_t i = 0; i < t.runs.size(); ++i) {
-      int64_t rec[4] = {t.runs[i].local_start, t.runs[i].global_start, t.runs[i].length,
-                        int64_t(t.runs[i].bits)};
-      std::memcpy(image->data() + at + 32 * i, rec, 32);
+SegmentCover segment_cover(int64_t L, const std::vector<Task>& tasks) {
+  SegmentCover sc;
+  sc.bounds.push_back(0);
+  sc.bounds.push_back(L);
+  for (const Task& t : tasks)
+    for (const Run& r : t.runs) {
+      sc.bounds.push_back(r.global_start);
+      sc.bounds.push_back(r.global_start + r.length);
     }
-    at += align_up(t.runs.size() * 32);
-    o.blk_or = at;
-    std::memcpy(image->data() + at, t.blk_or.data(), t.blk_or.size() * 4);
-    at += align_up(t.blk_or.size() * 4);
-    o.blk_and = at;
-    std::memcpy(image->data() + at, t.blk_and.data(), t.blk_and.size() * 4);
-    at += align_up(t.blk_and.size() * 4);
+  std::sort(sc.bounds.begin(), sc.bounds.end());
+  sc.bounds.erase(std::unique(sc.bounds.begin(), sc.bounds.end()), sc.bounds.end());
+  sc.cover.assign(sc.bounds.size() - 1, {});
+  for (size_t t = 0; t < tasks.size(); ++t)
+    for (const Run& r : tasks[t].runs) {
+      size_t s = size_t(std::lower_bound(sc.bounds.begin(), sc.bounds.end(), r.global_start) -
+                        sc.bounds.begin());
+      for (; s + 1 < sc.bounds.size() && sc.bounds[s] < r.global_start + r.length; ++s)
+        sc.cover[s].push_back({int32_t(t), r.local_start + (sc.bounds[s] - r.global_start)});
+    }
+  return sc;
+}
+
+std::vector<int64_t> fwd_slot_tasks(int64_t ntask, int32_t group_size, int32_t n_slots) {
+  const int64_t g = std::max<int64_t>(1, group_size);
+  const int64_t ngroup = std::max<int64_t>(1, (ntask + g - 1) / g);
+  const int64_t ns = std::min<int64_t>(std::max(1, n_slots), ngroup);
+  std::vector<int64_t> cap(ns, 0);
+  for (int64_t k = 0; k < ngroup; ++k)
+    cap[k % ns] = std::max(cap[k % ns], std::min(g, std::max<int64_t>(0, ntask - k * g)));
+  for (int64_t& c : cap) c = std::max<int64_t>(1, c);
+  return cap;
+}
+
+int64_t fwd_subslots(int64_t ntask, int32_t group_size, int32_t n_slots) {
+  int64_t n = 0;
+  for (int64_t c : fwd_slot_tasks(ntask, group_size, n_slots)) n += c;
+  return n;
+}
+
+std::vector<Group> make_groups(int64_t ntask, int32_t group_size) {
+  std::vector<Group> gs;
+  const int64_t g = std::max<int64_t>(1, group_size);
+  for (int64_t t0 = 0; t0 < std::max<int64_t>(1, ntask); t0 += g) {
+    Group gr;
+    gr.task0 = t0;
+    gr.count = std::min<int64_t>(g, ntask - t0);
+    gs.push_back(gr);
+  }
+  gs.back().final = true;
+  return gs;
+}
+
+void pack_image(const std::vector<Task>& tasks, const SegmentCover& sc, int32_t H,
+                std::vector<Group>* groups, std::vector<uint8_t>* image,
+                std::vector<TableOffsets>* offs) {
+  std::vector<uint8_t>& im = *image;
+  im.clear();
+  offs->clear();
+  auto reserve = [&](uint64_t bytes) {
+    const uint64_t at = im.size();
+    im.resize(align_up(at + bytes), 0);
+    return at;
+  };
+  const uint64_t hdr = reserve(tasks.size() * sizeof(DevTask));
+  for (size_t t = 0; t < tasks.size(); ++t) {
+    const Task& k = tasks[t];
+    TableOffsets o;
+    o.runs = reserve(k.runs.size() * sizeof(DevRun));
+    for (size_t i = 0; i < k.runs.size(); ++i) {
+      DevRun r{k.runs[i].local_start, k.runs[i].global_start, k.runs[i].length, k.runs[i].bits, 0u};
+      std::memcpy(im.data() + o.runs + i * sizeof(DevRun), &r, sizeof(r));
+    }
+    o.blk_or = reserve(k.blk_or.size() * 4);
+    std::memcpy(im.data() + o.blk_or, k.blk_or.data(), k.blk_or.size() * 4);
+    o.blk_and = reserve(k.blk_and.size() * 4);
+    std::memcpy(im.data() + o.blk_and, k.blk_and.data(), k.blk_and.size() * 4);
+    DevTask d{k.L_local, int64_t(o.runs), int64_t(o.blk_or), int64_t(o.blk_and),
+              int32_t(k.runs.size()), {0, 0, 0}};
+    std::memcpy(im.data() + hdr + t * sizeof(DevTask), &d, sizeof(d));
     offs->push_back(o);
+  }
+  const size_t nseg = sc.cover.size();
+  for (Group& g : *groups) {
+    const int32_t t0 = int32_t(g.task0), t1 = int32_t(g.task0 + g.count);
+    std::vector<DevSeg> segs;
+    std::vector<DevContrib> cons;
+    int64_t blk = 0;
+    for (size_t s = 0; s < nseg; ++s) {
+      const auto& cv = sc.cover[s];
+      const int32_t c_off = int32_t(cons.size());
+      bool earlier = false;
+      for (const auto& e : cv) {
+        if (e.first < t0) earlier = true;
+        if (e.first >= t0 && e.first < t1) cons.push_back(DevContrib{e.second, e.first - t0, 0});
+      }
+      const int32_t n_c = int32_t(cons.size()) - c_off;
+      if (n_c == 0 && !g.final) continue;
+      const int64_t len = sc.bounds[s + 1] - sc.bounds[s];
+      segs.push_back(DevSeg{sc.bounds[s], len, blk, c_off, n_c, earlier ? 1 : 0, 0});
+      blk += (len * H + kCombinePairs - 1) / kCombinePairs;
+    }
+    g.n_seg = int32_t(segs.size());
+    g.blocks = blk;
+    g.seg_off = reserve(segs.size() * sizeof(DevSeg));
+    if (!segs.empty()) std::memcpy(im.data() + g.seg_off, segs.data(), segs.size() * sizeof(DevSeg));
+    g.contrib_off = reserve(cons.size() * sizeof(DevContrib));
+    if (!cons.empty())
+      std::memcpy(im.data() + g.contrib_off, cons.data(), cons.size() * sizeof(DevContrib));
   }
 }
 
 Footprint footprint(const Geometry& g, const cqsa_plan_opts& o, int32_t depth,
-                    const std::vector<Task>& tasks) {
+                    const std::vector<Task>& tasks, int32_t group_size, uint64_t image_bytes) {
   Footprint f;
   int64_t Lmax = 0;
   for (const Task& t : tasks) Lmax = std::max(Lmax, t.L_local);
+  const int64_t ntask = int64_t(tasks.size());
+  f.group_size = std::max<int32_t>(1, group_size);
+  f.groups = (ntask + f.group_size - 1) / f.group_size;
   const uint64_t tok = uint64_t(o.B) * uint64_t(g.L) * uint64_t(g.H);
   const uint64_t in_bytes = align_up(tok * g.d * dtype_size(o.dtype));
   const uint64_t f32_full = align_up(tok * g.d * 4);
   const uint64_t stat_full = align_up(tok * 4);
+  const bool direct = direct_forward(o, depth);
   f.resident_fwd = (o.inputs_on_device ? 3 * in_bytes : 0) +
                    (o.acc_on_device ? f32_full + stat_full : 0);
   f.resident_bwd = 4 * in_bytes + f32_full + stat_full + 3 * f32_full;
-  const bool staged_fwd = depth > 0 || !o.inputs_on_device;
-  const bool stats_fwd = depth > 0 || !o.acc_on_device;
-  f.slot_fwd = fwd_slot_bytes(g, o, Lmax, staged_fwd, stats_fwd);
+  // slot i holds as many task sub-slots (each sized for the longest task) as
+  // the largest group that uses it (groups k with k % n_slots == i)
+  f.slot_fwd = direct ? 0 : fwd_slot_bytes(g, o, Lmax, true, true);
   f.slot_bwd = bwd_slot_bytes(g, o, Lmax, depth > 0);
-  f.global_fwd = (o.acc_on_device && depth > 0) ? stat_full : 0;   // global row sums l
-  f.global_bwd = stat_full;                                         // D = rowsum(dO * O)
-  f.tables = table_bytes(tasks);
-  const uint64_t slots = uint64_t(std::min<int64_t>(o.n_slots, int64_t(tasks.size())));
-  uint64_t peak_fwd = f.resident_fwd + slots * f.slot_fwd + f.global_fwd + f.tables;
+  // running row sums l, needed while more than one group merges on device
+  f.global_fwd = (o.acc_on_device && !direct && f.groups > 1) ? stat_full : 0;
+  f.global_bwd = stat_full;  // D = rowsum(dO * O)
+  f.tables = align_up(image_bytes);
+  const uint64_t subslots_fwd = uint64_t(fwd_subslots(ntask, f.group_size, o.n_slots));
+  const uint64_t slots_bwd = uint64_t(std::min<int64_t>(o.n_slots, ntask));
+  uint64_t peak_fwd = f.resident_fwd + subslots_fwd * f.slot_fwd + f.global_fwd + f.tables;
   uint64_t peak_bwd = o.with_backward
-                          ? f.resident_bwd + slots * f.slot_bwd + f.global_bwd + f.tables
+                          ? f.resident_bwd + slots_bwd * f.slot_bwd + f.global_bwd + f.tables
                           : 0;
   f.peak = std::max(peak_fwd, peak_bwd);
   return f;

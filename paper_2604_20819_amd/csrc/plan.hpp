@@ -8,11 +8,15 @@
 #include <vector>
 
 #include "cqsa.h"
+#include "records.hpp"
 
 namespace cqsa {
 
 constexpr int kBlock = 64;   // tokens per block summary (App. A.2)
 constexpr int kTile = 128;   // census tile edge (App. A.2)
+// Work groups one forward launch should offer: two waves of the MI355X's
+// resident inner-kernel work groups (256 CUs x 2).
+constexpr int64_t kLaunchWgs = 1024;
 
 // One maximal run of a task: local tokens [local_start, local_start+length)
 // are global tokens [global_start, global_start+length), all with `bits`.
@@ -39,16 +43,36 @@ struct TableOffsets {
   uint64_t blk_and = 0; // uint32[n_blocks]
 };
 
+// A launch group: tasks [task0, task0 + count) are staged into one slot,
+// run by one inner-kernel launch and merged by one combine launch.
+struct Group {
+  int64_t task0 = 0, count = 0;
+  uint64_t seg_off = 0;      // DevSeg[n_seg] in the packed image
+  uint64_t contrib_off = 0;  // DevContrib[..] in the packed image
+  int32_t n_seg = 0;
+  int64_t blocks = 0;        // combine work groups per batch element
+  bool final = false;        // last group: the combine writes O and LSE
+};
+
+// Elementary global segments: the cuts of every task's runs.  cover[s] lists
+// (task, local token of the segment's first token) in ascending task order.
+struct SegmentCover {
+  std::vector<int64_t> bounds;  // segment s is [bounds[s], bounds[s + 1])
+  std::vector<std::vector<std::pair<int32_t, int64_t>>> cover;
+};
+
 // Everything the runtime allocates for one call, in bytes.
 struct Footprint {
   uint64_t resident_fwd = 0;   // caller tensors on device during the forward
   uint64_t resident_bwd = 0;   // caller tensors on device during the backward
-  uint64_t slot_fwd = 0;       // one forward staging slot (inputs + task statistics)
+  uint64_t slot_fwd = 0;       // one forward task sub-slot (staged inputs + statistics)
   uint64_t slot_bwd = 0;       // one backward staging slot (inputs)
   uint64_t global_fwd = 0;     // forward device workspace independent of slots
   uint64_t global_bwd = 0;     // backward device workspace independent of slots
-  uint64_t tables = 0;         // packed per-task tables
+  uint64_t tables = 0;         // packed plan image (task and merge tables)
   uint64_t peak = 0;           // modelled peak device bytes
+  int32_t group_size = 1;      // tasks per forward staging slot
+  int64_t groups = 1;          // forward launch groups
 };
 
 struct Geometry {
@@ -66,9 +90,11 @@ struct cqsa_plan_s {
   int64_t max_L_local;
   std::vector<cqsa::Task> tasks;
   cqsa::Footprint fp;
-  // packed per-task tables, uploaded to the device by every call
+  // packed plan image, uploaded to the device by every call: DevTask[ntask]
+  // at offset 0, then every task's tables, then every group's merge tables
   std::vector<uint8_t> packed;
   std::vector<cqsa::TableOffsets> table_off;
+  std::vector<cqsa::Group> groups;
   // lazily computed census
   mutable std::once_flag census_once;
   mutable int64_t census[3] = {0, 0, 0};
@@ -85,9 +111,23 @@ cqsa_status validate_plan_args(int64_t L, int32_t H, int32_t d, const cqsa_plan_
 // Builds the c**depth tasks of BuildSubseq with ascending chunk order.
 std::vector<Task> build_tasks(int64_t L, const cqsa_plan_opts& o, int32_t depth);
 
-// Footprint of running `tasks` under `o` (mirrors the runtime's allocations).
+// Footprint of running `tasks` under `o` with `group_size` tasks per forward
+// slot and a plan image of `image_bytes` (mirrors the runtime's allocations).
 Footprint footprint(const Geometry& g, const cqsa_plan_opts& o, int32_t depth,
-                    const std::vector<Task>& tasks);
+                    const std::vector<Task>& tasks, int32_t group_size, uint64_t image_bytes);
+
+// True when the forward writes O directly from one undecomposed launch.
+bool direct_forward(const cqsa_plan_opts& o, int32_t depth);
+
+SegmentCover segment_cover(int64_t L, const std::vector<Task>& tasks);
+
+// Task sub-slots of each forward staging slot: slot i serves the groups
+// k with k % S == i (S = min(n_slots, groups)) and holds the largest of them.
+std::vector<int64_t> fwd_slot_tasks(int64_t ntask, int32_t group_size, int32_t n_slots);
+int64_t fwd_subslots(int64_t ntask, int32_t group_size, int32_t n_slots);
+
+// Consecutive groups of `group_size` tasks (the last one may be shorter).
+std::vector<Group> make_groups(int64_t ntask, int32_t group_size);
 
 void tile_census(const std::vector<Task>& tasks, int64_t out[3]);
 
@@ -97,11 +137,12 @@ bool is_perfect_difference_set(const int32_t* I, int32_t l, int32_t c);
 uint64_t fwd_slot_bytes(const Geometry& g, const cqsa_plan_opts& o, int64_t Lmax, bool staged,
                         bool stats);
 uint64_t bwd_slot_bytes(const Geometry& g, const cqsa_plan_opts& o, int64_t Lmax, bool staged);
-uint64_t table_bytes(const std::vector<Task>& tasks);
-// Packs every task's runs and block summaries into one image (layout of
-// table_bytes; the DevRun record is 32 bytes).
-void pack_tables(const std::vector<Task>& tasks, std::vector<uint8_t>* image,
-                 std::vector<TableOffsets>* offs);
+// Packs the plan image: the DevTask records, every task's runs and block
+// summaries, and every group's segments and contributions (filling the
+// groups' offsets and combine block counts for H heads).
+void pack_image(const std::vector<Task>& tasks, const SegmentCover& sc, int32_t H,
+                std::vector<Group>* groups, std::vector<uint8_t>* image,
+                std::vector<TableOffsets>* offs);
 
 inline uint64_t align_up(uint64_t x, uint64_t a = 256) { return (x + a - 1) / a * a; }
 

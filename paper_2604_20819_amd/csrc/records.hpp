@@ -1,0 +1,62 @@
+// Records of the packed plan image that the kernels read (internal).
+//
+// The planner writes them on the host and every call uploads the image once;
+// the layouts are plain C++ so host and device code share one definition.
+#pragma once
+
+#include <stdint.h>
+
+namespace cqsa {
+
+constexpr int kMaxRuns = 128;      // runs per task the kernels accept (l**depth bound)
+constexpr int kMaxContrib = 32;    // tasks of one launch group that may share a token
+constexpr int kCombinePairs = 64;  // (token, head) pairs per combine work group
+
+// One maximal run of a task: local tokens [local_start, local_start + length)
+// are global tokens [global_start, global_start + length), all with `bits`.
+struct DevRun {
+  int64_t local_start;
+  int64_t global_start;
+  int64_t length;
+  uint32_t bits;
+  uint32_t pad;
+};
+
+// One task: its length and where its tables sit in the image (byte offsets).
+struct DevTask {
+  int64_t L_local;
+  int64_t runs_off;   // DevRun[n_runs]
+  int64_t or_off;     // uint32[ceil(L_local / 64)] block OR of the group bits
+  int64_t and_off;    // uint32[ceil(L_local / 64)] block AND of the group bits
+  int32_t n_runs;
+  int32_t pad[3];
+};
+
+// Elementary global segment of a launch group's merge: tokens
+// [g0, g0 + len) lie inside one run of every task that holds them.  The
+// segment's contributions are DevContrib[c_off .. c_off + n_c); has_global
+// says whether tasks of earlier groups already merged into these tokens.
+// Combine work groups blk0 .. blk0 + ceil(len * H / kCombinePairs) - 1 own it.
+struct DevSeg {
+  int64_t g0;
+  int64_t len;
+  int64_t blk0;
+  int32_t c_off;
+  int32_t n_c;
+  int32_t has_global;
+  int32_t pad;
+};
+
+// Token g0 of a segment is local token `local_start` of the group's task j.
+struct DevContrib {
+  int64_t local_start;
+  int32_t j;
+  int32_t pad;
+};
+
+static_assert(sizeof(DevRun) == 32, "DevRun layout");
+static_assert(sizeof(DevTask) == 48, "DevTask layout");
+static_assert(sizeof(DevSeg) == 40, "DevSeg layout");
+static_assert(sizeof(DevContrib) == 16, "DevContrib layout");
+
+}  // namespace cqsa

@@ -3,6 +3,7 @@
 // that are not planning or compute.
 #include "runtime.hpp"
 
+#include <algorithm>
 #include <cmath>
 #include <cstring>
 
@@ -31,7 +32,7 @@ DevCtx* device_ctx(cqsa_status* st) {
   if (!c->ready) {
     c->device = dev;
     if ((e = hipStreamCreateWithFlags(&c->copy, hipStreamNonBlocking)) != hipSuccess ||
-        (e = hipStreamCreateWithFlags(&c->d2h, hipStreamNonBlocking)) != hipSuccess ||
+        (e = hipStreamCreateWithFlags(&c->aux, hipStreamNonBlocking)) != hipSuccess ||
         (e = hipStreamCreateWithFlags(&c->lane, hipStreamNonBlocking)) != hipSuccess ||
         (e = hipEventCreateWithFlags(&c->ws_free, hipEventDisableTiming)) != hipSuccess) {
       *st = hip_fail(e, "creating library streams");
@@ -116,6 +117,7 @@ void CallRecord::reset() {
   for (auto& v : spans) v.clear();
   wall0 = wall1 = nullptr;
   host_merge_ms = 0.0;
+  host_final_ms = 0.0;
   std::memset(&stats, 0, sizeof(stats));
   timing = t_timing;
 }
@@ -189,6 +191,26 @@ cqsa_status cqsa_last_stats(cqsa_run_stats* out) {
       *dst[k] = acc;
     }
     s.ms_merge += r.host_merge_ms;
+    s.ms_finalize += r.host_final_ms;
+    // union of the inner-kernel spans on the device clock
+    std::vector<std::pair<double, double>> iv;
+    for (auto& pr : r.spans[kStInner]) {
+      const double a = span(r.wall0, pr.first), b = span(r.wall0, pr.second);
+      iv.push_back({a, b});
+    }
+    std::sort(iv.begin(), iv.end());
+    double busy = 0.0, cs = 0.0, ce = -1.0;
+    for (auto& x : iv) {
+      if (x.first > ce) {
+        if (ce > cs) busy += ce - cs;
+        cs = x.first;
+        ce = x.second;
+      } else if (x.second > ce) {
+        ce = x.second;
+      }
+    }
+    if (ce > cs) busy += ce - cs;
+    s.ms_inner_busy = busy;
   }
   *out = s;
   return CQSA_OK;

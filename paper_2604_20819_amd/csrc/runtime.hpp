@@ -21,8 +21,8 @@ struct DevCtx {
   int device = -1;
   bool ready = false;
   hipStream_t copy = nullptr;   // staging copies (H2D or D2D)
-  hipStream_t d2h = nullptr;    // statistics device -> host
-  hipStream_t lane = nullptr;   // second compute stream: odd tasks' inner kernels
+  hipStream_t aux = nullptr;    // forward merges, or statistics device -> host
+  hipStream_t lane = nullptr;   // second compute stream (odd groups, backward dQ)
   hipEvent_t ws_free = nullptr; // recorded after the last call's last use of the workspace
   bool ws_free_valid = false;
   void* ws = nullptr;           // cached device workspace (built-in allocator)
@@ -54,6 +54,7 @@ struct CallRecord {
   std::vector<std::pair<hipEvent_t, hipEvent_t>> spans[kStCount];
   hipEvent_t wall0 = nullptr, wall1 = nullptr;
   double host_merge_ms = 0.0;
+  double host_final_ms = 0.0;
   cqsa_run_stats stats{};
   void reset();
   hipEvent_t make();                                    // timing event owned by the record

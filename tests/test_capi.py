@@ -107,20 +107,83 @@ def test_workload_depths(L, H, d, causal, budget, kw, want):
             assert q.modelled_device_bytes > budget
 
 
-def test_footprint_model_closed_form():
+def _image_bytes(p, g):
+    """Plan image size from the layout the planner documents: DevTask records,
+    per-task runs and block summaries, per-group segments and contributions."""
+    al = lambda x: (x + 255) // 256 * 256
+    tasks = [p.task(t) for t in range(p.num_tasks)]
+    size = al(len(tasks) * 48)
+    for tk in tasks:
+        size += al(len(tk["runs"]) * 32) + 2 * al(len(tk["block_or"]) * 4)
+    bounds = sorted({0, p.L} | {r[0] for tk in tasks for r in tk["runs"]}
+                    | {r[0] + r[1] for tk in tasks for r in tk["runs"]})
+    segs = list(zip(bounds[:-1], bounds[1:]))
+    holders = [[t for t, tk in enumerate(tasks)
+                if any(r[0] <= s0 < r[0] + r[1] for r in tk["runs"])] for s0, _ in segs]
+    for t0 in range(0, len(tasks), g):
+        final = t0 + g >= len(tasks)
+        n_seg = n_con = 0
+        for hs in holders:
+            k = sum(1 for t in hs if t0 <= t < t0 + g)
+            if k or final:
+                n_seg += 1
+                n_con += k
+        size += al(n_seg * 40) + al(n_con * 16)
+    return size
+
+
+@pytest.mark.parametrize("tps,want_g,subslots", [(0, 1, 2), (1, 1, 2), (7, 7, 7), (3, 3, 6),
+                                                  (4, 4, 7)])
+def test_footprint_model_closed_form(tps, want_g, subslots):
     """Footprint of the bf16 L=32768 H=16 d=128 depth-1 plan, recomputed here
-    from the workspace layout the header documents."""
+    from the workspace layout the header documents: with g tasks per slot and
+    two slots, slot i holds the largest group k = i (mod 2)."""
     L, H, d, B = 32768, 16, 128, 1
-    p = cq.cqsa_plan(L, H, d, False, 0, cq.make_opts(depth=1))
+    p = cq.cqsa_plan(L, H, d, False, 0, cq.make_opts(depth=1, tasks_per_slot=tps))
+    assert p.tasks_per_slot == want_g
     al = lambda x: (x + 255) // 256 * 256
     Lmax = max(p.task(t)["L_local"] for t in range(p.num_tasks))
     rows = B * Lmax * H
-    slot = 3 * al(rows * d * 2) + al(rows * d * 4) + 2 * al(rows * 4)
+    sub = 3 * al(rows * d * 2) + al(rows * d * 4) + 2 * al(rows * 4)
     resident = 3 * al(B * L * H * d * 2) + al(B * L * H * d * 4) + al(B * L * H * 4)
-    tables = sum(al(len(p.task(t)["runs"]) * 32) + 2 * al(len(p.task(t)["block_or"]) * 4)
-                 for t in range(p.num_tasks))
-    want = resident + 2 * slot + al(B * H * L * 4) + tables
+    groups = -(-7 // want_g)
+    running_l = al(B * H * L * 4) if groups > 1 else 0
+    want = resident + subslots * sub + running_l + al(_image_bytes(p, want_g))
     assert p.modelled_device_bytes == want
+
+
+def test_group_size_rules():
+    """Automatic tasks per slot: enough tasks for 1024 work groups per launch
+    (128-query strips x B x H per task), capped at 32 and at the task count;
+    one with a host accumulator; reduced until a capped budget fits."""
+    # L=4096, depth 2: 49 tasks of <= 84 tokens, 1 strip x 4 heads each
+    p = cq.cqsa_plan(4096, 4, 64, False, 0, cq.make_opts(depth=2))
+    assert p.tasks_per_slot == 32
+    # depth 1: 7 tasks of <= 586 tokens, 5 strips x 4 heads = 20 work groups each
+    p = cq.cqsa_plan(4096, 4, 64, False, 0, cq.make_opts(depth=1))
+    assert p.tasks_per_slot == 7
+    # 14043-token tasks x 16 heads: 110 x 16 = 1760 work groups, one per launch
+    p = cq.cqsa_plan(32768, 16, 128, False, 0, cq.make_opts(depth=1))
+    assert p.tasks_per_slot == 1
+    # 4682-token tasks x 16 heads: 37 x 16 = 592 -> two per launch
+    p = cq.cqsa_plan(32768, 16, 128, False, 0, cq.make_opts(depth=2))
+    assert p.tasks_per_slot == 2
+    # fp32 uses 32-query strips: 7 tasks of <= 147 tokens, 5 x 1 work groups
+    p = cq.cqsa_plan(1024, 1, 64, False, 0, cq.make_opts(dtype="f32", depth=1))
+    assert p.tasks_per_slot == 7
+    p = cq.cqsa_plan(4096, 4, 64, False, 0, cq.make_opts(depth=1, acc_on_device=False))
+    assert p.tasks_per_slot == 1
+    big = cq.cqsa_plan(4096, 4, 64, False, 0, cq.make_opts(depth=1))
+    one = cq.cqsa_plan(4096, 4, 64, False, 0, cq.make_opts(depth=1, tasks_per_slot=1))
+    budget = (big.modelled_device_bytes + one.modelled_device_bytes) // 2
+    mid = cq.cqsa_plan(4096, 4, 64, False, budget, cq.make_opts(depth=1))
+    assert 1 <= mid.tasks_per_slot < big.tasks_per_slot
+    assert mid.modelled_device_bytes <= budget
+    with pytest.raises(cq.CqsaError):
+        cq.cqsa_plan(4096, 4, 64, False, 0, cq.make_opts(depth=1, tasks_per_slot=33))
+    with pytest.raises(cq.CqsaError):
+        cq.cqsa_plan(4096, 4, 64, False, 0, cq.make_opts(depth=1, tasks_per_slot=2,
+                                                         acc_on_device=False))
 
 
 def test_forward_argument_errors_without_device_work():
