@@ -46,6 +46,11 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target CPU time of the oracle sample")
+    ap.add_argument("--workload", default="headline",
+                    choices=["headline", "fp16_causal_L131072_8GB",
+                             "bf16_causal_B2_L65536_fwdbwd_16GB", "bf16_streamed_L1M_host_4GB"],
+                    help="headline (default) or one of the other seeded workloads: "
+                         "their rates, depths and runtime ratios, one JSON line each")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB five times (calibrates "
                          "the FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -133,6 +138,113 @@ def cpu_baseline(Q, K, V, seconds):
                       f"x {H} heads against all {L} keys ({t_used:.1f} s)"}
 
 
+GB = 10 ** 9
+
+
+def other_workload(name, args):
+    """Seeded workloads beyond the headline: one JSON line each with the
+    decomposed rate, the depth the budget forces, and the runtime ratio to the
+    undecomposed call where that fits (host-link rates for the streamed one)."""
+    import torch
+
+    import paper_2604_20819_amd as cq
+    from paper_2604_20819_amd import synth
+
+    spec = {
+        "fp16_causal_L131072_8GB": dict(B=1, L=131072, H=32, d=128, causal=True, dt="f16",
+                                        budget=8 * GB, seed=20819 + 3, host=False, bwd=False),
+        "bf16_causal_B2_L65536_fwdbwd_16GB": dict(B=2, L=65536, H=16, d=128, causal=True,
+                                                  dt="bf16", budget=16 * GB, seed=20819 + 4,
+                                                  host=False, bwd=True),
+        "bf16_streamed_L1M_host_4GB": dict(B=1, L=1 << 20, H=8, d=128, causal=False, dt="bf16",
+                                           budget=4 * GB, seed=20819 + 5, host=True, bwd=False),
+    }[name]
+    Bw, Lw, Hw, dw, causal = spec["B"], spec["L"], spec["H"], spec["d"], spec["causal"]
+    host = spec["host"]
+    print(f"[workload] {name}: generating inputs", file=sys.stderr, flush=True)
+    ins = synth.make_inputs(spec["seed"], Bw, Lw, Hw, dw, spec["dt"], with_dO=spec["bwd"],
+                            pin_memory=host)
+    if host:
+        q, k, v = ins[:3]
+        O = torch.empty((Bw, Lw, Hw, dw), dtype=torch.float32, pin_memory=True)
+        LSE = torch.empty((Bw, Hw, Lw), dtype=torch.float32, pin_memory=True)
+    else:
+        q, k, v = (x.cuda() for x in ins[:3])
+        O = torch.empty((Bw, Lw, Hw, dw), dtype=torch.float32, device="cuda")
+        LSE = torch.empty((Bw, Hw, Lw), dtype=torch.float32, device="cuda")
+    pairs = Lw * (Lw + 1) // 2 if causal else Lw * Lw
+    flops = 4.0 * dw * Bw * Hw * pairs
+
+    def plan_for(depth=-1, budget=spec["budget"], backward=spec["bwd"]):
+        return cq.cqsa_plan(Lw, Hw, dw, causal, budget,
+                            cq.make_opts(B=Bw, dtype=spec["dt"], depth=depth,
+                                         inputs_on_device=not host, acc_on_device=not host,
+                                         with_backward=backward))
+
+    cq.cqsa_set_timing(True)
+    steps = 2 if host else max(3, args.steps // 4)
+    warm = 1
+
+    def fwd(plan):
+        def step():
+            cq.cqsa_forward(plan, q, k, v, O, LSE)
+            return cq.cqsa_last_stats()
+        return step
+
+    plan = plan_for()
+    print(f"[workload] {name}: depth {plan.depth}, {plan.num_tasks} tasks, "
+          f"{plan.tasks_per_slot} per launch", file=sys.stderr, flush=True)
+    ms, st = time_steps(fwd(plan), steps, warm, torch)
+    s = st[-1]
+    line = {"workload": name, "B": Bw, "L": Lw, "H": Hw, "d": dw, "causal": causal,
+            "dtype": spec["dt"], "budget_bytes": spec["budget"], "depth": plan.depth,
+            "tasks": plan.num_tasks, "tasks_per_launch": plan.tasks_per_slot,
+            "modelled_device_bytes": plan.modelled_device_bytes,
+            "workspace_bytes": s["workspace_bytes"],
+            "fwd_ms": round(ms, 3), "fwd_tflops": round(flops / (ms * 1e-3) / 1e12, 2),
+            "inner_fwd_busy_tflops": round(flops / (s["ms_inner_busy"] * 1e-3) / 1e12, 2)}
+    if host:
+        h2d, d2h = s["h2d_bytes"], s["d2h_bytes"]
+        copy_ms = s["ms_stage"] + s["ms_d2h"]
+        comp_ms = s["ms_inner_busy"]
+        line.update({
+            "h2d_bytes": h2d, "d2h_bytes": d2h,
+            "h2d_GBps": round(h2d / (s["ms_stage"] * 1e-3) / 1e9, 2),
+            "d2h_GBps": round(d2h / (s["ms_d2h"] * 1e-3) / 1e9, 2),
+            "wall_ms": round(s["ms_wall"], 2), "compute_ms": round(comp_ms, 2),
+            "copy_ms": round(copy_ms, 2), "host_merge_ms": round(s["ms_merge"], 2),
+            "overlap": round(1 - (s["ms_wall"] - max(comp_ms, copy_ms)) / min(comp_ms, copy_ms), 3),
+            "undecomposed": "does not apply: inputs and outputs are host-resident"})
+    else:
+        und = plan_for(depth=0, budget=0, backward=False)
+        ms0, _ = time_steps(fwd(und), steps, warm, torch)
+        line.update({"undecomposed_fwd_ms": round(ms0, 3),
+                     "undecomposed_modelled_bytes": und.modelled_device_bytes,
+                     "fwd_runtime_ratio": round(ms / ms0, 4)})
+        if spec["bwd"]:
+            do = ins[3].cuda()
+            dQ, dK, dV = (torch.empty((Bw, Lw, Hw, dw), dtype=torch.float32, device="cuda")
+                          for _ in range(3))
+
+            def fb(pl):
+                def step():
+                    cq.cqsa_forward(pl, q, k, v, O, LSE)
+                    cq.cqsa_backward(pl, q, k, v, O, LSE, do, dQ, dK, dV)
+                    return cq.cqsa_last_stats()
+                return step
+            msb, stb = time_steps(fb(plan), steps, warm, torch)
+            und_b = plan_for(depth=0, budget=0, backward=True)
+            msb0, _ = time_steps(fb(und_b), steps, warm, torch)
+            line.update({"fwd_bwd_ms": round(msb, 3),
+                         "fwd_bwd_tflops": round(3.5 * flops / (msb * 1e-3) / 1e12, 2),
+                         "inner_bwd_busy_tflops": round(
+                             2.5 * flops / (stb[-1]["ms_inner_busy"] * 1e-3) / 1e12, 2),
+                         "undecomposed_fwd_bwd_ms": round(msb0, 3),
+                         "fwd_bwd_runtime_ratio": round(msb / msb0, 4)})
+    cq.cqsa_set_timing(False)
+    print(json.dumps(line), flush=True)
+
+
 def task_rows(plan):
     return [plan.task(t)["L_local"] for t in range(plan.num_tasks)]
 
@@ -141,6 +253,12 @@ def main():
     args = parse()
     if args.copy_probe:
         copy_probe(args.copy_probe)
+        return
+    if args.workload != "headline":
+        if args.gpus != 1:
+            print("bench.py runs on one GPU only", file=sys.stderr)
+            sys.exit(2)
+        other_workload(args.workload, args)
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
