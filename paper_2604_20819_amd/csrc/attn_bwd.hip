@@ -37,7 +37,9 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dq(const BwdArgs a) {
   __shared__ uint32_t kbits_s[2][BN];
   __shared__ DevRun runs_s[kMaxRuns];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5;
+  const int tid = threadIdx.x, lane = tid & 63, half = lane >> 5;
+  // uniform per wave, so per-wave loads and branches stay scalar
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int L = a.L;
   const int64_t nstrips = (L + BM - 1) / BM;
   const int64_t work = xcd_remap(blockIdx.x, nstrips * a.H * a.B);
@@ -79,16 +81,35 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dq(const BwdArgs a) {
   const uint32_t wor = wave_live ? a.blk_or[q0w / 64] : 0u;
   const uint32_t wand = wave_live ? a.blk_and[q0w / 64] : 0u;
   const int nkt = (L + BN - 1) / BN;
-  // next live tile and its summaries, read before the tile prefetch is issued
+  // Tile skipping as in the forward: a window of 64 tiles' summaries per
+  // vector load (lane i = tile k0 + i) and a ballot for the first live one.
+  struct Window {
+    uint32_t an, on;
+  };
+  auto window = [&](int k0) {
+    const int k = k0 + lane;
+    Window w{0xFFFFFFFFu, 0u};
+    if (k < nkt) {
+      w.an = a.blk_and[k];
+      w.on = a.blk_or[k];
+    }
+    return w;
+  };
+  auto pick = [&](int k0, const Window& w, uint32_t& kor_out, uint32_t& kand_out) -> int {
+    const int k = k0 + lane;
+    const bool ok = k < nkt && !(causal && k * BN > lastq_wg) && (qand & w.an) == 0u;
+    const uint64_t m = __builtin_amdgcn_ballot_w64(ok);
+    if (m == 0ull) return -1;
+    const int i = __builtin_ctzll(m);
+    kand_out = __builtin_amdgcn_readlane(w.an, i);
+    kor_out = __builtin_amdgcn_readlane(w.on, i);
+    return k0 + i;
+  };
   auto next_live = [&](int kt, uint32_t& kor_out, uint32_t& kand_out) -> int {
-    for (; kt < nkt; ++kt) {
+    for (; kt < nkt; kt += 64) {
       if (causal && kt * BN > lastq_wg) return nkt;
-      const uint32_t an = a.blk_and[kt];
-      if ((qand & an) == 0u) {
-        kand_out = an;
-        kor_out = a.blk_or[kt];
-        return kt;
-      }
+      const int r = pick(kt, window(kt), kor_out, kand_out);
+      if (r >= 0) return r;
     }
     return nkt;
   };
@@ -137,16 +158,18 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dq(const BwdArgs a) {
   const float lse2 = qvalid ? a.lse[si] * kLog2e : 0.f;
   const float Dq = qvalid ? a.D[si] : 0.f;
 
-  uint32_t kor = 0u, kand = 0u;
+  uint32_t kor = 0u, kand = 0u, nor = 0u, nand = 0u;
   int kt = next_live(0, kor, kand);
   if (kt < nkt) {
     gload(kt);
     sstore(0, kt, kor);
   }
+  int kn = kt < nkt ? next_live(kt + 1, nor, nand) : nkt;
   int buf = 0;
   while (kt < nkt) {
-    uint32_t nor = 0u, nand = 0u;
-    const int kn = next_live(kt + 1, nor, nand);
+    // summary window after kn (used after the compute), then the prefetch of kn
+    const int kc = kn + 1;
+    const Window cw = window(kc);
     if (kn < nkt) gload(kn);
     lds_barrier();
     const int k0 = kt * BN, k1 = (k0 + BN - 1 < L ? k0 + BN - 1 : L - 1);
@@ -201,11 +224,22 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dq(const BwdArgs a) {
         }
       }
     }
-    if (kn < nkt) sstore(buf ^ 1, kn, nor);
+    int kc2 = nkt;
+    uint32_t or2 = 0u, and2 = 0u;
+    if (kn < nkt) {
+      sstore(buf ^ 1, kn, nor);
+      if (kc < nkt) {
+        kc2 = pick(kc, cw, or2, and2);
+        if (kc2 < 0) kc2 = next_live(kc + 64, or2, and2);
+      }
+    }
     buf ^= 1;
     kt = kn;
     kor = nor;
     kand = nand;
+    kn = kc2;
+    nor = or2;
+    nand = and2;
   }
   if (!qvalid) return;
   float* dst = a.dq + (int64_t(b) * a.Lg + gq) * rs + int64_t(h) * D;
@@ -231,15 +265,18 @@ __global__ void __launch_bounds__(256, (D == 128 ? 1 : 2)) attn_bwd_dkdv(const B
   constexpr int DK = D / 16, DB = D / 32, CHUNKS = D / 8, RPP = 256 / CHUNKS, PASSES = BQ / RPP;
   typedef typename E::vec8 vec8;
 
-  __shared__ __attribute__((aligned(16))) char qs[BQ * P2];
-  __shared__ __attribute__((aligned(16))) char os[BQ * P2];
+  // double-buffered query tiles (Q, dO) with their per-query statistics
+  __shared__ __attribute__((aligned(16))) char qs[2][BQ * P2];
+  __shared__ __attribute__((aligned(16))) char os[2][BQ * P2];
   __shared__ __attribute__((aligned(16))) char vs[BK * VKP];
-  __shared__ __attribute__((aligned(16))) float lse_s[BQ];
-  __shared__ __attribute__((aligned(16))) float d_s[BQ];
-  __shared__ uint32_t qbits_s[BQ];
+  __shared__ __attribute__((aligned(16))) float lse_s[2][BQ];
+  __shared__ __attribute__((aligned(16))) float d_s[2][BQ];
+  __shared__ uint32_t qbits_s[2][BQ];
   __shared__ DevRun runs_s[kMaxRuns];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5;
+  const int tid = threadIdx.x, lane = tid & 63, half = lane >> 5;
+  // uniform per wave, so per-wave loads and branches stay scalar
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int L = a.L;
   const int64_t nstrips = (L + BK - 1) / BK;
   const int64_t work = xcd_remap(blockIdx.x, nstrips * a.H * a.B);
@@ -288,12 +325,86 @@ __global__ void __launch_bounds__(256, (D == 128 ? 1 : 2)) attn_bwd_dkdv(const B
   const uint32_t wand = wave_live ? a.blk_and[k0w / 64] : 0u;
   const int nqt = (L + BQ - 1) / BQ;
   const int first_key = strip * BK;
-  auto next_live = [&](int qt) -> int {
-    for (; qt < nqt; ++qt) {
-      if (causal && qt * BQ + BQ - 1 < first_key) continue;
-      if ((kand & a.blk_and[qt]) == 0u) return qt;
+  const int64_t stat_base = (int64_t(b) * a.H + h) * a.Lg;
+
+  // Query-tile skipping as in the forward (a tile is dead when fully masked
+  // or, causally, entirely before the strip's first key): a window of 64
+  // tiles' summaries per vector load and a ballot for the first live one.
+  struct Window {
+    uint32_t an, on;
+  };
+  auto window = [&](int t0) {
+    const int t = t0 + lane;
+    Window w{0xFFFFFFFFu, 0u};
+    if (t < nqt) {
+      w.an = a.blk_and[t];
+      w.on = a.blk_or[t];
+    }
+    return w;
+  };
+  auto pick = [&](int t0, const Window& w, uint32_t& qor_out, uint32_t& qand_out) -> int {
+    const int t = t0 + lane;
+    const bool ok = t < nqt && !(causal && t * BQ + BQ - 1 < first_key) && (kand & w.an) == 0u;
+    const uint64_t m = __builtin_amdgcn_ballot_w64(ok);
+    if (m == 0ull) return -1;
+    const int i = __builtin_ctzll(m);
+    qand_out = __builtin_amdgcn_readlane(w.an, i);
+    qor_out = __builtin_amdgcn_readlane(w.on, i);
+    return t0 + i;
+  };
+  auto next_live = [&](int t, uint32_t& qor_out, uint32_t& qand_out) -> int {
+    for (; t < nqt; t += 64) {
+      const int r = pick(t, window(t), qor_out, qand_out);
+      if (r >= 0) return r;
     }
     return nqt;
+  };
+
+  // Query-tile loads, prefetched into registers during the previous tile's
+  // compute: Q and dO rows through per-tile buffer resources (rows past the
+  // task read as zero) and, for the first BQ threads, the query's global LSE
+  // (log2 units), D and group bits (LSE = +inf past the task gives P = 0).
+  u32x4 qreg[PASSES], oreg[PASSES];
+  uint32_t goff[PASSES];
+#pragma unroll
+  for (int p = 0; p < PASSES; ++p)
+    goff[p] = uint32_t(((p * RPP + tid / CHUNKS) * rs + (tid % CHUNKS) * 8) * 2);
+  float lse_r = INFINITY, d_r = 0.f;
+  uint32_t qb_r = 0u;
+  auto gload = [&](int qt) {
+    const int64_t rows = int64_t(L) - int64_t(qt) * BQ;
+    const __amdgpu_buffer_rsrc_t rq = row_rsrc(Qg + int64_t(qt) * BQ * rs, rows, rs * 2, D * 2);
+    const __amdgpu_buffer_rsrc_t ro = row_rsrc(Og + int64_t(qt) * BQ * rs, rows, rs * 2, D * 2);
+#pragma unroll
+    for (int p = 0; p < PASSES; ++p) {
+      qreg[p] = buf_load16(rq, goff[p]);
+      oreg[p] = buf_load16(ro, goff[p]);
+    }
+    if (tid < BQ) {
+      const int q = qt * BQ + tid;
+      lse_r = INFINITY;
+      d_r = 0.f;
+      qb_r = 0u;
+      if (q < L) {
+        const int64_t g = run_global(runs_s, a.n_runs, q);
+        lse_r = a.lse[stat_base + g] * kLog2e;
+        d_r = a.D[stat_base + g];
+        qb_r = run_bits(runs_s, a.n_runs, q);
+      }
+    }
+  };
+  auto sstore = [&](int buf) {
+#pragma unroll
+    for (int p = 0; p < PASSES; ++p) {
+      const int row = p * RPP + tid / CHUNKS, ch = tid % CHUNKS;
+      *(u32x4*)(qs[buf] + row * P2 + ch * 16) = qreg[p];
+      *(u32x4*)(os[buf] + row * P2 + ch * 16) = oreg[p];
+    }
+    if (tid < BQ) {
+      lse_s[buf][tid] = lse_r;
+      d_s[buf][tid] = d_r;
+      qbits_s[buf][tid] = qb_r;
+    }
   };
 
   f32x16 dk[DB], dv[DB];
@@ -305,97 +416,100 @@ __global__ void __launch_bounds__(256, (D == 128 ? 1 : 2)) attn_bwd_dkdv(const B
       dv[db][r] = 0.f;
     }
 
-  __syncthreads();
+  __syncthreads();  // runs_s and the V rows visible
   const uint32_t kbits = kvalid ? run_bits(runs_s, a.n_runs, mykey) : 0u;
-  const int64_t stat_base = (int64_t(b) * a.H + h) * a.Lg;
 
-  for (int qt = next_live(causal ? first_key / BQ : 0); qt < nqt; qt = next_live(qt + 1)) {
-    __syncthreads();  // every wave is done with the previous tile
-    {
-      const int64_t rows = int64_t(L) - int64_t(qt) * BQ;
-      const __amdgpu_buffer_rsrc_t rq = row_rsrc(Qg + int64_t(qt) * BQ * rs, rows, rs * 2, D * 2);
-      const __amdgpu_buffer_rsrc_t ro = row_rsrc(Og + int64_t(qt) * BQ * rs, rows, rs * 2, D * 2);
-#pragma unroll
-      for (int p = 0; p < PASSES; ++p) {
-        const int row = p * RPP + tid / CHUNKS, ch = tid % CHUNKS;
-        const uint32_t off = uint32_t((row * rs + ch * 8) * 2);
-        *(u32x4*)(qs + row * P2 + ch * 16) = buf_load16(rq, off);
-        *(u32x4*)(os + row * P2 + ch * 16) = buf_load16(ro, off);
-      }
-    }
-    const uint32_t qor = a.blk_or[qt], qand = a.blk_and[qt];
-    if (tid < BQ) {
-      const int q = qt * BQ + tid;
-      if (q < L) {
-        const int64_t g = run_global(runs_s, a.n_runs, q);
-        lse_s[tid] = a.lse[stat_base + g] * kLog2e;
-        d_s[tid] = a.D[stat_base + g];
-        qbits_s[tid] = run_bits(runs_s, a.n_runs, q);
-      } else {
-        lse_s[tid] = INFINITY;  // P = 0 for rows past the task
-        d_s[tid] = 0.f;
-        qbits_s[tid] = 0u;
-      }
-    }
-    __syncthreads();
+  uint32_t qor = 0u, qand = 0u, nor = 0u, nand = 0u;
+  int qt = next_live(causal ? first_key / BQ : 0, qor, qand);
+  if (qt < nqt) {
+    gload(qt);
+    sstore(0);
+  }
+  int qn = qt < nqt ? next_live(qt + 1, nor, nand) : nqt;
+  int buf = 0;
+  while (qt < nqt) {
+    // summary window after qn (used after the compute), then the prefetch of qn
+    const int qc = qn + 1;
+    const Window cw = window(qc);
+    if (qn < nqt) gload(qn);
+    lds_barrier();
     const int q0 = qt * BQ;
     const bool wfull = !wave_live || (wand & qand) != 0u || (causal && q0 + BQ - 1 < k0w);
-    if (wfull) continue;
-    const bool wclear = (wor & qor) == 0u && (!causal || q0 >= wk1);
-    const bool use_bits = (kor & qor) != 0u;
+    if (!wfull) {
+      const bool wclear = (wor & qor) == 0u && (!causal || q0 >= wk1);
+      const bool use_bits = (kor & qor) != 0u;
+      const char* qsb = qs[buf];
+      const char* osb = os[buf];
 #pragma unroll 1
-    for (int qb = 0; qb < 2; ++qb) {
-      f32x16 s, dp;
+      for (int qb = 0; qb < 2; ++qb) {
+        f32x16 s, dp;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        s[r] = 0.f;
-        dp[r] = 0.f;
-      }
-      const int row = 32 * qb + (lane & 31);
-#pragma unroll
-      for (int ks = 0; ks < DK; ++ks) {
-        const u32x4 qa = *(const u32x4*)(qs + row * P2 + (16 * ks + 8 * half) * 2);
-        s = mfma32<E>(bitcast_u4<vec8>(qa), kf[ks], s);
-        const u32x4 oa = *(const u32x4*)(os + row * P2 + (16 * ks + 8 * half) * 2);
-        const u32x4 vb = *(const u32x4*)(vs + (wave * 32 + (lane & 31)) * VKP + (16 * ks + 8 * half) * 2);
-        dp = mfma32<E>(bitcast_u4<vec8>(oa), bitcast_u4<vec8>(vb), dp);
-      }
-      // 16 queries at a time: P and dS = P (dP - D), packed for dV and dK
-#pragma unroll
-      for (int sub = 0; sub < 2; ++sub) {
-        float pv[8], dsv[8];
-#pragma unroll
-        for (int ii = 0; ii < 2; ++ii) {
-          const int ql = 32 * qb + 8 * (2 * sub + ii) + 4 * half;
-          const f32x4 l4 = *(const f32x4*)(lse_s + ql);
-          const f32x4 d4 = *(const f32x4*)(d_s + ql);
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int r = 8 * sub + 4 * ii + j;
-            float p = fast_exp2(fmaf(s[r], c, -l4[j]));
-            if (!wclear) {
-              const int q = q0 + ql + j;
-              bool keep = (!causal || mykey <= q);
-              if (use_bits) keep = keep && ((qbits_s[ql + j] & kbits) == 0u);
-              if (!keep) p = 0.f;
-            }
-            pv[4 * ii + j] = p;
-            dsv[4 * ii + j] = p * (dp[r] - d4[j]);
-          }
+        for (int r = 0; r < 16; ++r) {
+          s[r] = 0.f;
+          dp[r] = 0.f;
         }
-        const vec8 bp = pack8<E>(pv);
-        const vec8 bs = pack8<E>(dsv);
-        const int trow = 32 * qb + 16 * sub + 4 * half + ((lane & 15) >> 2);
+        const int row = 32 * qb + (lane & 31);
 #pragma unroll
-        for (int db = 0; db < DB; ++db) {
-          const int col = 32 * db + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
-          const char* po = os + trow * P2 + col * 2;
-          dv[db] = mfma32<E>(lds_tr_pair<E>(po, po + 8 * P2), bp, dv[db]);
-          const char* pq = qs + trow * P2 + col * 2;
-          dk[db] = mfma32<E>(lds_tr_pair<E>(pq, pq + 8 * P2), bs, dk[db]);
+        for (int ks = 0; ks < DK; ++ks) {
+          const u32x4 qa = *(const u32x4*)(qsb + row * P2 + (16 * ks + 8 * half) * 2);
+          s = mfma32<E>(bitcast_u4<vec8>(qa), kf[ks], s);
+          const u32x4 oa = *(const u32x4*)(osb + row * P2 + (16 * ks + 8 * half) * 2);
+          const u32x4 vb = *(const u32x4*)(vs + (wave * 32 + (lane & 31)) * VKP + (16 * ks + 8 * half) * 2);
+          dp = mfma32<E>(bitcast_u4<vec8>(oa), bitcast_u4<vec8>(vb), dp);
+        }
+        // 16 queries at a time: P and dS = P (dP - D), packed for dV and dK
+#pragma unroll
+        for (int sub = 0; sub < 2; ++sub) {
+          float pv[8], dsv[8];
+#pragma unroll
+          for (int ii = 0; ii < 2; ++ii) {
+            const int ql = 32 * qb + 8 * (2 * sub + ii) + 4 * half;
+            const f32x4 l4 = *(const f32x4*)(&lse_s[buf][ql]);
+            const f32x4 d4 = *(const f32x4*)(&d_s[buf][ql]);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const int r = 8 * sub + 4 * ii + j;
+              float p = fast_exp2(fmaf(s[r], c, -l4[j]));
+              if (!wclear) {
+                const int q = q0 + ql + j;
+                bool keep = (!causal || mykey <= q);
+                if (use_bits) keep = keep && ((qbits_s[buf][ql + j] & kbits) == 0u);
+                if (!keep) p = 0.f;
+              }
+              pv[4 * ii + j] = p;
+              dsv[4 * ii + j] = p * (dp[r] - d4[j]);
+            }
+          }
+          const vec8 bp = pack8<E>(pv);
+          const vec8 bs = pack8<E>(dsv);
+          const int trow = 32 * qb + 16 * sub + 4 * half + ((lane & 15) >> 2);
+#pragma unroll
+          for (int db = 0; db < DB; ++db) {
+            const int col = 32 * db + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+            const char* po = osb + trow * P2 + col * 2;
+            dv[db] = mfma32<E>(lds_tr_pair<E>(po, po + 8 * P2), bp, dv[db]);
+            const char* pq = qsb + trow * P2 + col * 2;
+            dk[db] = mfma32<E>(lds_tr_pair<E>(pq, pq + 8 * P2), bs, dk[db]);
+          }
         }
       }
     }
+    int qc2 = nqt;
+    uint32_t or2 = 0u, and2 = 0u;
+    if (qn < nqt) {
+      sstore(buf ^ 1);
+      if (qc < nqt) {
+        qc2 = pick(qc, cw, or2, and2);
+        if (qc2 < 0) qc2 = next_live(qc + 64, or2, and2);
+      }
+    }
+    buf ^= 1;
+    qt = qn;
+    qor = nor;
+    qand = nand;
+    qn = qc2;
+    nor = or2;
+    nand = and2;
   }
   if (!kvalid) return;
   const int64_t gk = run_global(runs_s, a.n_runs, mykey);
