@@ -75,6 +75,13 @@ def test_null_rows_exist_and_are_skipped():
     null = ~np.isfinite(m[0, 0])
     assert null.sum() == 10 and (task["tokens"][null] < 10).all()
     assert (ell[0, 0, null] == 0).all() and (acc[0, null] == 0).all()
+    # merged first, those null rows meet an empty accumulator; the null
+    # contribution must leave it empty and the result still equal dense
+    tasks = planner.build_tasks(N, 7, 1, (0, 1, 3))
+    O, LSE = decomposed.merged_forward(Q, K, V, tasks, True, order=[4, 0, 1, 2, 3, 5, 6])
+    Od, LSEd = dense.attention_forward(Q, K, V, True)
+    np.testing.assert_allclose(O, Od, rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(LSE, LSEd, rtol=1e-12, atol=1e-13)
 
 
 def test_overflow_numden_fp32_vs_max_shift():
