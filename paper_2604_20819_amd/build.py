@@ -62,6 +62,16 @@ def build(verbose=False):
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
+    # A kernel whose host-side instantiation the compiler dropped links as an
+    # undefined launch stub; refuse such a library instead of shipping it.
+    nm = shutil.which("nm")
+    if nm:
+        syms = subprocess.run([nm, "-D", tmp], capture_output=True, text=True).stdout
+        missing = [ln.split()[-1] for ln in syms.splitlines()
+                   if " U " in ln and "__device_stub__" in ln]
+        if missing:
+            os.remove(tmp)
+            raise RuntimeError("kernel launch stubs missing from the library: " + ", ".join(missing))
     os.replace(tmp, OUT)
     return OUT
 

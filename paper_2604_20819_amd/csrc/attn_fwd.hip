@@ -16,10 +16,12 @@
 // gfx950 design: S^T = K Q^T on v_mfma_f32_32x32x16 so each lane owns one
 // query column and its row statistics stay in-lane (one permlane32 swap per
 // tile); P^T feeds O^T = V^T P^T directly from registers, and V^T operands come
-// from row-major LDS through ds_read_b64_tr_b16.  Running maxima are rounded
-// up to integers in the log2 domain, so every rescale is an exact power of two
-// and 16-bit P is rounded identically whichever task, or the undecomposed
-// call, produced it.
+// from row-major LDS through ds_read_b64_tr_b16.  K/V tiles are double
+// buffered in LDS and filled by direct buffer-to-LDS loads issued right after
+// each tile barrier, so they cost no registers and no LDS store instructions.
+// Running maxima are rounded up to integers in the log2 domain, so every
+// rescale is an exact power of two and 16-bit P is rounded identically
+// whichever task, or the undecomposed call, produced it.
 #include "hip_common.hpp"
 #include "kernels.hpp"
 
@@ -28,17 +30,21 @@ namespace cqsa {
 template <typename E, int D, int MODE>
 __global__ void __launch_bounds__(256, 2) attn_fwd_mfma(const FwdArgs a) {
   constexpr int BM = 128, BN = 64;
-  constexpr int KP = D * 2 + 16;  // K row pitch (bytes): conflict-free 16-byte reads
-  constexpr int VP = D * 2 + 64;  // V row pitch (bytes): conflict-free transpose reads
-  constexpr int KBYTES = BN * KP, VBYTES = BN * VP, STAGE = KBYTES + VBYTES;
+  // K and V tiles: unpadded rows of 2D bytes; 16-byte chunk ch of row r sits
+  // in slot ch ^ swz(r), which keeps the K row reads and the V transpose
+  // reads free of bank conflicts.  Tiles arrive by direct global-to-LDS
+  // loads: one wave instruction fills 1 KB, lane i its i-th 16 bytes.
+  constexpr int RB = D * 2;              // row bytes
+  constexpr int KBYTES = BN * RB, VBYTES = BN * RB, STAGE = KBYTES + VBYTES;
   constexpr int DK = D / 16;             // k-steps of S^T = K Q^T
   constexpr int DB = D / 32;             // 32-wide d blocks of O^T
   constexpr int CHUNKS = D / 8;          // 16-byte chunks per row
-  constexpr int RPP = 256 / CHUNKS;      // rows per load pass
-  constexpr int PASSES = BN / RPP;
+  constexpr int RPI = 64 / CHUNKS;       // rows per 1 KB load instruction
+  constexpr int NDMA = BN / RPI / 4;     // load instructions per wave per tensor
   typedef typename E::vec8 vec8;
+  auto swz = [](int r) { return 2 * (r & 3) + ((r >> 2) & 1); };
 
-  __shared__ __attribute__((aligned(16))) char smem[2 * STAGE];
+  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
   __shared__ uint32_t kbits_s[2][BN];
   __shared__ DevRun runs_s[kMaxRuns];
 
@@ -130,32 +136,31 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_mfma(const FwdArgs a) {
     return nkt;
   };
 
-  // Tile loads through a per-tile buffer resource (SGPR base, fixed 32-bit
-  // per-thread offsets); rows past the task end read as zero.
-  u32x4 kreg[PASSES], vreg[PASSES];
-  uint32_t goff[PASSES];
+  // Tile loads: per-tile buffer resources (SGPR base, fixed per-lane 32-bit
+  // offsets; rows past the task end read as zero) feeding LDS directly.
+  // Instruction j of wave w fills rows RPI*(NDMA*w + j) ...; lane i carries
+  // slot i % CHUNKS of its row, i.e. global chunk (i % CHUNKS) ^ swz(row).
+  uint32_t goff[NDMA];
 #pragma unroll
-  for (int p = 0; p < PASSES; ++p)
-    goff[p] = uint32_t(((p * RPP + tid / CHUNKS) * rs + (tid % CHUNKS) * 8) * 2);
-  auto gload = [&](int kt) {
+  for (int j = 0; j < NDMA; ++j) {
+    const int row = RPI * (NDMA * wave + j) + lane / CHUNKS;
+    const int ch = (lane % CHUNKS) ^ swz(row);
+    goff[j] = uint32_t((row * rs + ch * 8) * 2);
+  }
+  auto gload = [&](int buf, int kt) {
     const int64_t rows = int64_t(L) - int64_t(kt) * BN;
     const __amdgpu_buffer_rsrc_t rk = row_rsrc(Kg + int64_t(kt) * BN * rs, rows, rs * 2, D * 2);
     const __amdgpu_buffer_rsrc_t rv = row_rsrc(Vg + int64_t(kt) * BN * rs, rows, rs * 2, D * 2);
-#pragma unroll
-    for (int p = 0; p < PASSES; ++p) {
-      kreg[p] = buf_load16(rk, goff[p]);
-      vreg[p] = buf_load16(rv, goff[p]);
-    }
-  };
-  auto sstore = [&](int buf, int kt, uint32_t kor_t) {
     char* kb = smem + buf * STAGE;
     char* vb = kb + KBYTES;
 #pragma unroll
-    for (int p = 0; p < PASSES; ++p) {
-      const int row = p * RPP + tid / CHUNKS, ch = tid % CHUNKS;
-      *(u32x4*)(kb + row * KP + ch * 16) = kreg[p];
-      *(u32x4*)(vb + row * VP + ch * 16) = vreg[p];
+    for (int j = 0; j < NDMA; ++j) {
+      const int off = (NDMA * wave + j) * 1024;
+      buf_load16_lds(rk, kb + off, goff[j]);
+      buf_load16_lds(rv, vb + off, goff[j]);
     }
+  };
+  auto sstore = [&](int buf, int kt, uint32_t kor_t) {
     // group bits of the tile's keys, only when the CQS mask can bite here
     if ((qor & kor_t) != 0u && tid < BN) {
       const int key = kt * BN + tid;
@@ -176,18 +181,21 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_mfma(const FwdArgs a) {
   uint32_t kor = 0u, kand = 0u, nor = 0u, nand = 0u;
   int kt = next_live(0, kor, kand);
   if (kt < nkt) {
-    gload(kt);
+    gload(0, kt);
     sstore(0, kt, kor);
   }
   int kn = kt < nkt ? next_live(kt + 1, nor, nand) : nkt;
   int buf = 0;
   while (kt < nkt) {
-    // Summary window after kn, loaded now and used after this tile's
-    // compute; then the prefetch of tile kn.
+    // this wave's tile loads have landed; after the barrier every wave's
+    // have, and every wave is done with the other buffer
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+    lds_barrier();
+    // summary window after kn (used after this tile's compute), then the
+    // loads of tile kn into the other buffer
     const int kc = kn + 1;
     const Window cw = window(kc);
-    if (kn < nkt) gload(kn);
-    lds_barrier();
+    if (kn < nkt) gload(buf ^ 1, kn);
 
     // ---- compute on tile kt (wave-uniform verdict) ----
     const int k0 = kt * BN, k1 = (k0 + BN - 1 < L ? k0 + BN - 1 : L - 1);
@@ -204,7 +212,8 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_mfma(const FwdArgs a) {
         for (int r = 0; r < 16; ++r) s[kb][r] = 0.f;
 #pragma unroll
         for (int ks = 0; ks < DK; ++ks) {
-          const u32x4 ka = *(const u32x4*)(Kb + (32 * kb + (lane & 31)) * KP + (16 * ks + 8 * half) * 2);
+          const int kr = 32 * kb + (lane & 31);
+          const u32x4 ka = *(const u32x4*)(Kb + kr * RB + (((2 * ks + half) ^ swz(kr)) << 4));
           s[kb] = mfma32<E>(bitcast_u4<vec8>(ka), qf[ks], s[kb]);
         }
       }
@@ -259,13 +268,13 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_mfma(const FwdArgs a) {
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
           const int col = 32 * db + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
-          const char* p0 = Vb + row * VP + col * 2;
-          const vec8 va = lds_tr_pair<E>(p0, p0 + 8 * VP);
+          const char* p0 = Vb + row * RB + (((col >> 3) ^ swz(row)) << 4) + (col & 7) * 2;
+          const vec8 va = lds_tr_pair<E>(p0, p0 + 8 * RB);
           o[db] = mfma32<E>(va, pb, o[db]);
         }
       }
     }
-    // ---- stage the next tile into the other buffer ----
+    // ---- group bits of the next tile, next live tile ----
     int kc2 = nkt;
     uint32_t or2 = 0u, and2 = 0u;
     if (kn < nkt) {

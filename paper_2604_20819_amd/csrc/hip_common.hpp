@@ -111,6 +111,13 @@ __device__ __forceinline__ u32x4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t v
   return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, 0, 0));
 }
 
+// 16 bytes per lane from a buffer resource straight into LDS: lane i's bytes
+// land at lds + 16 i (the wave fills 1 KB); out-of-range reads give zeros.
+__device__ __forceinline__ void buf_load16_lds(__amdgpu_buffer_rsrc_t r, void* lds, uint32_t voff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16, voff, 0,
+                                           0, 0);
+}
+
 // Work-group barrier that orders LDS only.  __syncthreads() also orders
 // global memory, which makes every wave wait for its in-flight global loads
 // (the next tile's prefetch) at the barrier.
