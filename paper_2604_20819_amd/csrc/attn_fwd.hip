@@ -205,13 +205,17 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_mfma(const FwdArgs a) {
       const bool use_bits = (qor & kor) != 0u;
       const char* Kb = smem + buf * STAGE;
       const char* Vb = Kb + KBYTES;
+      // the two 32-key blocks' accumulation chains alternate, so consecutive
+      // products never depend on each other
       f32x16 s[2];
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
+      for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) s[kb][r] = 0.f;
 #pragma unroll
-        for (int ks = 0; ks < DK; ++ks) {
+      for (int ks = 0; ks < DK; ++ks) {
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
           const int kr = 32 * kb + (lane & 31);
           const u32x4 ka = *(const u32x4*)(Kb + kr * RB + (((2 * ks + half) ^ swz(kr)) << 4));
           s[kb] = mfma32<E>(bitcast_u4<vec8>(ka), qf[ks], s[kb]);
