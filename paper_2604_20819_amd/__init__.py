@@ -273,6 +273,46 @@ def cqsa_release_workspace():
     _check(lib().cqsa_release_workspace(), "cqsa_release_workspace")
 
 
+_ALLOC_FN = ctypes.CFUNCTYPE(ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p)
+_RELEASE_FN = ctypes.CFUNCTYPE(None, ctypes.c_void_p, ctypes.c_void_p)
+_hooks = None  # the installed callbacks, kept alive while the library may call them
+
+
+def cqsa_set_allocator(alloc=None, release=None):
+    """Route the library's device workspace through alloc(nbytes) -> int device
+    address (0 = failure) and release(address); None for both restores the
+    built-in cached workspace."""
+    global _hooks
+    if (alloc is None) != (release is None):
+        raise ValueError("give both functions or neither")
+    if alloc is None:
+        _check(lib().cqsa_set_allocator(None, None, None), "cqsa_set_allocator")
+        _hooks = None
+        return
+    a = _ALLOC_FN(lambda n, ctx: alloc(int(n)) or None)
+    r = _RELEASE_FN(lambda ptr, ctx: release(int(ptr)))
+    _check(lib().cqsa_set_allocator(ctypes.cast(a, ctypes.c_void_p), ctypes.cast(r, ctypes.c_void_p),
+                                    None), "cqsa_set_allocator")
+    _hooks = (a, r)
+
+
+def use_torch_allocator(device=None):
+    """Serve the workspace from torch's caching allocator (on `device`)."""
+    torch = _torch()
+    held = {}
+
+    def alloc(n):
+        t = torch.empty((n,), dtype=torch.uint8, device=device or "cuda")
+        held[t.data_ptr()] = t
+        return t.data_ptr()
+
+    def release(ptr):
+        held.pop(ptr, None)
+
+    cqsa_set_allocator(alloc, release)
+    return held
+
+
 def forward(Q, K, V, causal, device_budget_bytes=0, depth=-1, scale=0.0, **opt_kw):
     """Plan and run a forward; returns (O, LSE, plan).  Outputs live where Q lives
     unless acc_on_device is given."""

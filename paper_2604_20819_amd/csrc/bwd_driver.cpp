@@ -28,6 +28,10 @@ cqsa_status backward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa
     return fail(CQSA_ERR_UNSUPPORTED, "cqsa_backward: device-resident plans only");
   if (o.dtype == CQSA_F32)
     return fail(CQSA_ERR_UNSUPPORTED, "cqsa_backward: fp16 and bf16 inputs only");
+  if (!o.with_backward && p->budget != 0)
+    return fail(CQSA_ERR_INVALID_ARG,
+                "cqsa_backward: the plan's budget was fitted without the backward "
+                "(plan with with_backward = 1)");
   cqsa_status s;
   const cqsa_mem dev = CQSA_MEM_DEVICE;
   if ((s = check_tensor(Q, "Q", p, o.dtype, dev)) != CQSA_OK) return s;

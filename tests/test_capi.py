@@ -2,6 +2,7 @@
 include/cqsa.h declares; planning through the ABI is bit-exact against the
 independent oracle planner; argument validation; the footprint model picks
 the depths the workload definitions call for."""
+import ctypes
 import os
 import re
 
@@ -201,3 +202,60 @@ def test_forward_argument_errors_without_device_work():
     with pytest.raises(cq.CqsaError) as e:
         cq.cqsa_forward(p, Q, Q, Q.half(), O, LSE)
     assert e.value.status == -1 and "dtype" in str(e.value)
+
+
+def _desc(dtype, where, B=1, L=64, H=1, d=64, data=0x1000):
+    """A tensor descriptor for argument checks that fail before device work
+    (the data pointer is never dereferenced)."""
+    code = {"f32": cq.CQSA_F32, "f16": cq.CQSA_F16, "bf16": cq.CQSA_BF16}[dtype]
+    return cq.cqsa_tensor(data, code, where, B, L, H, d)
+
+
+def _backward_status(plan, dt="bf16", where=None, lse=0x2000, lse_where=None, **over):
+    dev = cq.CQSA_MEM_DEVICE
+    where = dev if where is None else where
+    t = {n: _desc(dt, where) for n in ("Q", "K", "V", "dO")}
+    t.update({n: _desc("f32", where) for n in ("O", "dQ", "dK", "dV")})
+    t.update(over)
+    st = cq.lib().cqsa_backward(plan.handle, *(ctypes.byref(t[n]) for n in ("Q", "K", "V", "O")),
+                                ctypes.c_void_p(lse), dev if lse_where is None else lse_where,
+                                ctypes.byref(t["dO"]), ctypes.byref(t["dQ"]), ctypes.byref(t["dK"]),
+                                ctypes.byref(t["dV"]), ctypes.c_float(0.0), ctypes.c_void_p(0))
+    return st, cq.lib().cqsa_last_error().decode()
+
+
+def test_backward_argument_errors_without_device_work():
+    """Every argument error of cqsa_backward is reported before device work."""
+    ok = cq.cqsa_plan(64, 1, 64, False, 0, cq.make_opts(depth=1, with_backward=True))
+    # a capped budget fitted without the backward is refused (header contract)
+    capped = cq.cqsa_plan(64, 1, 64, False, 10 ** 9, cq.make_opts(depth=1))
+    st, msg = _backward_status(capped)
+    assert st == -1 and "with_backward" in msg
+    # host-resident plans and fp32 plans are not built for the backward
+    host = cq.cqsa_plan(64, 1, 64, False, 0, cq.make_opts(depth=1, inputs_on_device=False,
+                                                          acc_on_device=False))
+    assert _backward_status(host)[0] == -2
+    f32 = cq.cqsa_plan(64, 1, 64, False, 0, cq.make_opts(dtype="f32", depth=1))
+    assert _backward_status(f32, dt="f32")[0] == -2
+    # tensor residency, dtype and shape; LSE pointer and residency
+    st, msg = _backward_status(ok, dO=_desc("bf16", cq.CQSA_MEM_HOST))
+    assert st == -1 and "dO" in msg and "residency" in msg
+    st, msg = _backward_status(ok, dK=_desc("bf16", cq.CQSA_MEM_DEVICE))
+    assert st == -1 and "dK" in msg and "dtype" in msg
+    st, msg = _backward_status(ok, V=_desc("bf16", cq.CQSA_MEM_DEVICE, L=65))
+    assert st == -1 and "V" in msg and "shape" in msg
+    st, msg = _backward_status(ok, lse=0)
+    assert st == -1 and "LSE" in msg
+    st, msg = _backward_status(ok, lse_where=cq.CQSA_MEM_HOST)
+    assert st == -1 and "LSE" in msg
+    st, msg = _backward_status(ok, Q=_desc("bf16", cq.CQSA_MEM_DEVICE, data=0))
+    assert st == -1 and "Q.data" in msg
+
+
+def test_allocator_hook_arguments():
+    with pytest.raises(ValueError):
+        cq.cqsa_set_allocator(lambda n: 0, None)
+    # one C function without the other is refused by the library itself
+    st = cq.lib().cqsa_set_allocator(ctypes.c_void_p(0x10), None, None)
+    assert st == -1 and "both" in cq.lib().cqsa_last_error().decode()
+    cq.cqsa_set_allocator(None, None)   # restoring the built-in workspace is always fine
