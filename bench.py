@@ -201,6 +201,10 @@ def other_workload(name, args):
             "tasks": plan.num_tasks, "tasks_per_launch": plan.tasks_per_slot,
             "modelled_device_bytes": plan.modelled_device_bytes,
             "workspace_bytes": s["workspace_bytes"],
+            # what the call holds on the device: the library's workspace plus the
+            # caller's device-resident tensors (Q, K, V, O, LSE)
+            "device_bytes_in_use": s["workspace_bytes"] + (0 if host else sum(
+                t.numel() * t.element_size() for t in (q, k, v, O, LSE))),
             "fwd_ms": round(ms, 3), "fwd_tflops": round(flops / (ms * 1e-3) / 1e12, 2),
             "inner_fwd_busy_tflops": round(flops / (s["ms_inner_busy"] * 1e-3) / 1e12, 2)}
     if host:
@@ -297,6 +301,11 @@ def main():
         return sum(s[key] for s in stats) / len(stats)
 
     flops = fwd_flops(False)
+    # planning alone (host): part of every step below
+    t0 = time.perf_counter()
+    for _ in range(20):
+        plan_for(1)
+    plan_ms = (time.perf_counter() - t0) * 1e3 / 20
     # headline: the decomposed forward with the automatic launch grouping
     ms_dec, stats = time_steps(fwd_step(1), args.steps, args.warmup, torch)
     launches = stats[-1]["inner_launches"]
@@ -318,6 +327,7 @@ def main():
     merge_bytes = sum(rows) * B * H * pair_b + B * H * L * (4 * D + 4)   # one final merge
     stage_bytes = 2 * st_one[-1]["d2d_bytes"]                          # read + write
     kernels = {
+        "plan": {"bound": "host", "unit": "ms", "ms_per_call": round(plan_ms, 4)},
         "inner_fwd": {
             "bound": "mfma", "unit": "TFLOP/s", "launches_per_step": launches,
             "ms_per_launch": round(ms_launch, 4),

@@ -27,13 +27,18 @@ constexpr float kLog2e = 1.4426950408889634f;
 template <typename E, int D>
 __global__ void __launch_bounds__(256, 2) attn_bwd_dq(const BwdArgs a) {
   constexpr int BM = 128, BN = 64;
-  constexpr int KP = D * 2 + 64;  // K tile: transpose reads and row reads
-  constexpr int VP = D * 2 + 16;  // V tile: row reads
-  constexpr int KBYTES = BN * KP, VBYTES = BN * VP, STAGE = KBYTES + VBYTES;
-  constexpr int DK = D / 16, DB = D / 32, CHUNKS = D / 8, RPP = 256 / CHUNKS, PASSES = BN / RPP;
+  // K and V tiles: unpadded rows of 2D bytes with the forward's swizzle
+  // (chunk ch of row r in slot ch ^ swz(r)), free of bank conflicts for the
+  // K and V row reads and the K transpose reads; filled by direct
+  // buffer-to-LDS loads (lane i's 16 bytes at +16 i of a 1 KB block).
+  constexpr int RB = D * 2;
+  constexpr int KBYTES = BN * RB, VBYTES = BN * RB, STAGE = KBYTES + VBYTES;
+  constexpr int DK = D / 16, DB = D / 32, CHUNKS = D / 8;
+  constexpr int RPI = 64 / CHUNKS, NDMA = BN / RPI / 4;
   typedef typename E::vec8 vec8;
+  auto swz = [](int r) { return 2 * (r & 3) + ((r >> 2) & 1); };
 
-  __shared__ __attribute__((aligned(16))) char smem[2 * STAGE];
+  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
   __shared__ uint32_t kbits_s[2][BN];
   __shared__ DevRun runs_s[kMaxRuns];
 
@@ -114,31 +119,29 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dq(const BwdArgs a) {
     return nkt;
   };
 
-  // tile loads through per-tile buffer resources; rows past the task read as zero
-  u32x4 kreg[PASSES], vreg[PASSES];
-  uint32_t goff[PASSES];
+  // tile loads through per-tile buffer resources (rows past the task read as
+  // zero) straight into LDS; lane i of load j of wave w carries slot
+  // i % CHUNKS of row RPI * (NDMA * w + j) + i / CHUNKS
+  uint32_t goff[NDMA];
 #pragma unroll
-  for (int p = 0; p < PASSES; ++p)
-    goff[p] = uint32_t(((p * RPP + tid / CHUNKS) * rs + (tid % CHUNKS) * 8) * 2);
-  auto gload = [&](int kt) {
+  for (int j = 0; j < NDMA; ++j) {
+    const int row = RPI * (NDMA * wave + j) + lane / CHUNKS;
+    goff[j] = uint32_t((row * rs + ((lane % CHUNKS) ^ swz(row)) * 8) * 2);
+  }
+  auto gload = [&](int buf, int kt) {
     const int64_t rows = int64_t(L) - int64_t(kt) * BN;
     const __amdgpu_buffer_rsrc_t rk = row_rsrc(Kg + int64_t(kt) * BN * rs, rows, rs * 2, D * 2);
     const __amdgpu_buffer_rsrc_t rv = row_rsrc(Vg + int64_t(kt) * BN * rs, rows, rs * 2, D * 2);
-#pragma unroll
-    for (int p = 0; p < PASSES; ++p) {
-      kreg[p] = buf_load16(rk, goff[p]);
-      vreg[p] = buf_load16(rv, goff[p]);
-    }
-  };
-  auto sstore = [&](int buf, int kt, uint32_t kor_t) {
     char* kb = smem + buf * STAGE;
     char* vb = kb + KBYTES;
 #pragma unroll
-    for (int p = 0; p < PASSES; ++p) {
-      const int row = p * RPP + tid / CHUNKS, ch = tid % CHUNKS;
-      *(u32x4*)(kb + row * KP + ch * 16) = kreg[p];
-      *(u32x4*)(vb + row * VP + ch * 16) = vreg[p];
+    for (int j = 0; j < NDMA; ++j) {
+      const int off = (NDMA * wave + j) * 1024;
+      buf_load16_lds(rk, kb + off, goff[j]);
+      buf_load16_lds(rv, vb + off, goff[j]);
     }
+  };
+  auto sstore = [&](int buf, int kt, uint32_t kor_t) {
     if ((qor & kor_t) != 0u && tid < BN) {
       const int key = kt * BN + tid;
       kbits_s[buf][tid] = key < L ? run_bits(runs_s, a.n_runs, key) : 0u;
@@ -161,17 +164,20 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dq(const BwdArgs a) {
   uint32_t kor = 0u, kand = 0u, nor = 0u, nand = 0u;
   int kt = next_live(0, kor, kand);
   if (kt < nkt) {
-    gload(kt);
+    gload(0, kt);
     sstore(0, kt, kor);
   }
   int kn = kt < nkt ? next_live(kt + 1, nor, nand) : nkt;
   int buf = 0;
   while (kt < nkt) {
-    // summary window after kn (used after the compute), then the prefetch of kn
+    // this wave's tile loads have landed; after the barrier every wave's
+    // have, and every wave is done with the other buffer
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+    lds_barrier();
+    // summary window after kn (used after the compute), then the loads of kn
     const int kc = kn + 1;
     const Window cw = window(kc);
-    if (kn < nkt) gload(kn);
-    lds_barrier();
+    if (kn < nkt) gload(buf ^ 1, kn);
     const int k0 = kt * BN, k1 = (k0 + BN - 1 < L ? k0 + BN - 1 : L - 1);
     const bool wfull = !wave_live || (wand & kand) != 0u || (causal && k0 > wq1);
     if (!wfull) {
@@ -191,9 +197,10 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dq(const BwdArgs a) {
         const int row = 32 * kb + (lane & 31);
 #pragma unroll
         for (int ks = 0; ks < DK; ++ks) {
-          const u32x4 ka = *(const u32x4*)(Kb + row * KP + (16 * ks + 8 * half) * 2);
+          const int slot = ((2 * ks + half) ^ swz(row)) << 4;
+          const u32x4 ka = *(const u32x4*)(Kb + row * RB + slot);
           s = mfma32<E>(bitcast_u4<vec8>(ka), qf[ks], s);
-          const u32x4 va = *(const u32x4*)(Vb + row * VP + (16 * ks + 8 * half) * 2);
+          const u32x4 va = *(const u32x4*)(Vb + row * RB + slot);
           dp = mfma32<E>(bitcast_u4<vec8>(va), of[ks], dp);
         }
 #pragma unroll
@@ -218,8 +225,8 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dq(const BwdArgs a) {
 #pragma unroll
           for (int db = 0; db < DB; ++db) {
             const int col = 32 * db + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
-            const char* p0 = Kb + trow * KP + col * 2;
-            dq[db] = mfma32<E>(lds_tr_pair<E>(p0, p0 + 8 * KP), bs, dq[db]);
+            const char* p0 = Kb + trow * RB + (((col >> 3) ^ swz(trow)) << 4) + (col & 7) * 2;
+            dq[db] = mfma32<E>(lds_tr_pair<E>(p0, p0 + 8 * RB), bs, dq[db]);
           }
         }
       }
