@@ -267,15 +267,18 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dq(const BwdArgs a) {
 template <typename E, int D>
 __global__ void __launch_bounds__(256, (D == 128 ? 1 : 2)) attn_bwd_dkdv(const BwdArgs a) {
   constexpr int BK = 128, BQ = 64;
-  constexpr int P2 = D * 2 + 64;  // Q and dO tiles: transpose reads and row reads
-  constexpr int VKP = D * 2 + 16; // the work group's V rows: 16-byte row reads
-  constexpr int DK = D / 16, DB = D / 32, CHUNKS = D / 8, RPP = 256 / CHUNKS, PASSES = BQ / RPP;
+  // Q and dO tiles: unpadded rows of 2D bytes with the forward's swizzle
+  // (chunk ch of row r in slot ch ^ swz(r)), conflict-free for the row reads
+  // and the transpose reads; filled by direct buffer-to-LDS loads
+  constexpr int P2 = D * 2;
+  constexpr int DK = D / 16, DB = D / 32, CHUNKS = D / 8;
+  constexpr int RPI = 64 / CHUNKS, NDMA = BQ / RPI / 4;
   typedef typename E::vec8 vec8;
+  auto swz = [](int r) { return 2 * (r & 3) + ((r >> 2) & 1); };
 
   // double-buffered query tiles (Q, dO) with their per-query statistics
-  __shared__ __attribute__((aligned(16))) char qs[2][BQ * P2];
-  __shared__ __attribute__((aligned(16))) char os[2][BQ * P2];
-  __shared__ __attribute__((aligned(16))) char vs[BK * VKP];
+  __shared__ __attribute__((aligned(1024))) char qs[2][BQ * P2];
+  __shared__ __attribute__((aligned(1024))) char os[2][BQ * P2];
   __shared__ __attribute__((aligned(16))) float lse_s[2][BQ];
   __shared__ __attribute__((aligned(16))) float d_s[2][BQ];
   __shared__ uint32_t qbits_s[2][BQ];
@@ -304,22 +307,18 @@ __global__ void __launch_bounds__(256, (D == 128 ? 1 : 2)) attn_bwd_dkdv(const B
   const int k0w = strip * BK + wave * 32;
   const int mykey = k0w + (lane & 31);
   const bool kvalid = mykey < L;
-  vec8 kf[DK];
+  // the wave's K and V rows stay in registers (B operands of S = Q K^T and
+  // dP = dO V^T) for the whole strip
+  vec8 kf[DK], vf[DK];
 #pragma unroll
   for (int ks = 0; ks < DK; ++ks) {
-    u32x4 u = {0u, 0u, 0u, 0u};
-    if (kvalid) u = *(const u32x4*)(Kg + int64_t(mykey) * rs + ks * 16 + half * 8);
-    kf[ks] = bitcast_u4<vec8>(u);
-  }
-  // the work group's V rows stay in LDS (register operands of dP = dO V^T)
-  {
-    const __amdgpu_buffer_rsrc_t rv =
-        row_rsrc(Vg + int64_t(strip) * BK * rs, int64_t(L) - int64_t(strip) * BK, rs * 2, D * 2);
-#pragma unroll
-    for (int p = 0; p < BK / RPP; ++p) {
-      const int row = p * RPP + tid / CHUNKS, ch = tid % CHUNKS;
-      *(u32x4*)(vs + row * VKP + ch * 16) = buf_load16(rv, uint32_t((row * rs + ch * 8) * 2));
+    u32x4 u = {0u, 0u, 0u, 0u}, w = {0u, 0u, 0u, 0u};
+    if (kvalid) {
+      u = *(const u32x4*)(Kg + int64_t(mykey) * rs + ks * 16 + half * 8);
+      w = *(const u32x4*)(Vg + int64_t(mykey) * rs + ks * 16 + half * 8);
     }
+    kf[ks] = bitcast_u4<vec8>(u);
+    vf[ks] = bitcast_u4<vec8>(w);
   }
 
   const int lastk_wg = (strip * BK + BK < L ? strip * BK + BK : L) - 1;
@@ -367,25 +366,28 @@ __global__ void __launch_bounds__(256, (D == 128 ? 1 : 2)) attn_bwd_dkdv(const B
     return nqt;
   };
 
-  // Query-tile loads, prefetched into registers during the previous tile's
-  // compute: Q and dO rows through per-tile buffer resources (rows past the
-  // task read as zero) and, for the first BQ threads, the query's global LSE
-  // (log2 units), D and group bits (LSE = +inf past the task gives P = 0).
-  u32x4 qreg[PASSES], oreg[PASSES];
-  uint32_t goff[PASSES];
+  // Query-tile loads for the next tile, issued right after a tile barrier:
+  // Q and dO rows through per-tile buffer resources (rows past the task read
+  // as zero) straight into LDS, and, for the first BQ threads, the query's
+  // global LSE (log2 units), D and group bits into registers (LSE = +inf
+  // past the task gives P = 0), stored to LDS after the compute.
+  uint32_t goff[NDMA];
 #pragma unroll
-  for (int p = 0; p < PASSES; ++p)
-    goff[p] = uint32_t(((p * RPP + tid / CHUNKS) * rs + (tid % CHUNKS) * 8) * 2);
+  for (int j = 0; j < NDMA; ++j) {
+    const int row = RPI * (NDMA * wave + j) + lane / CHUNKS;
+    goff[j] = uint32_t((row * rs + ((lane % CHUNKS) ^ swz(row)) * 8) * 2);
+  }
   float lse_r = INFINITY, d_r = 0.f;
   uint32_t qb_r = 0u;
-  auto gload = [&](int qt) {
+  auto gload = [&](int buf, int qt) {
     const int64_t rows = int64_t(L) - int64_t(qt) * BQ;
     const __amdgpu_buffer_rsrc_t rq = row_rsrc(Qg + int64_t(qt) * BQ * rs, rows, rs * 2, D * 2);
     const __amdgpu_buffer_rsrc_t ro = row_rsrc(Og + int64_t(qt) * BQ * rs, rows, rs * 2, D * 2);
 #pragma unroll
-    for (int p = 0; p < PASSES; ++p) {
-      qreg[p] = buf_load16(rq, goff[p]);
-      oreg[p] = buf_load16(ro, goff[p]);
+    for (int j = 0; j < NDMA; ++j) {
+      const int off = (NDMA * wave + j) * 1024;
+      buf_load16_lds(rq, qs[buf] + off, goff[j]);
+      buf_load16_lds(ro, os[buf] + off, goff[j]);
     }
     if (tid < BQ) {
       const int q = qt * BQ + tid;
@@ -401,12 +403,6 @@ __global__ void __launch_bounds__(256, (D == 128 ? 1 : 2)) attn_bwd_dkdv(const B
     }
   };
   auto sstore = [&](int buf) {
-#pragma unroll
-    for (int p = 0; p < PASSES; ++p) {
-      const int row = p * RPP + tid / CHUNKS, ch = tid % CHUNKS;
-      *(u32x4*)(qs[buf] + row * P2 + ch * 16) = qreg[p];
-      *(u32x4*)(os[buf] + row * P2 + ch * 16) = oreg[p];
-    }
     if (tid < BQ) {
       lse_s[buf][tid] = lse_r;
       d_s[buf][tid] = d_r;
@@ -423,23 +419,26 @@ __global__ void __launch_bounds__(256, (D == 128 ? 1 : 2)) attn_bwd_dkdv(const B
       dv[db][r] = 0.f;
     }
 
-  __syncthreads();  // runs_s and the V rows visible
+  __syncthreads();  // runs_s visible
   const uint32_t kbits = kvalid ? run_bits(runs_s, a.n_runs, mykey) : 0u;
 
   uint32_t qor = 0u, qand = 0u, nor = 0u, nand = 0u;
   int qt = next_live(causal ? first_key / BQ : 0, qor, qand);
   if (qt < nqt) {
-    gload(qt);
+    gload(0, qt);
     sstore(0);
   }
   int qn = qt < nqt ? next_live(qt + 1, nor, nand) : nqt;
   int buf = 0;
   while (qt < nqt) {
-    // summary window after qn (used after the compute), then the prefetch of qn
+    // this wave's tile loads have landed; after the barrier every wave's
+    // have, and every wave is done with the other buffers
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+    lds_barrier();
+    // summary window after qn (used after the compute), then the loads of qn
     const int qc = qn + 1;
     const Window cw = window(qc);
-    if (qn < nqt) gload(qn);
-    lds_barrier();
+    if (qn < nqt) gload(buf ^ 1, qn);
     const int q0 = qt * BQ;
     const bool wfull = !wave_live || (wand & qand) != 0u || (causal && q0 + BQ - 1 < k0w);
     if (!wfull) {
@@ -458,11 +457,11 @@ __global__ void __launch_bounds__(256, (D == 128 ? 1 : 2)) attn_bwd_dkdv(const B
         const int row = 32 * qb + (lane & 31);
 #pragma unroll
         for (int ks = 0; ks < DK; ++ks) {
-          const u32x4 qa = *(const u32x4*)(qsb + row * P2 + (16 * ks + 8 * half) * 2);
+          const int slot = ((2 * ks + half) ^ swz(row)) << 4;
+          const u32x4 qa = *(const u32x4*)(qsb + row * P2 + slot);
           s = mfma32<E>(bitcast_u4<vec8>(qa), kf[ks], s);
-          const u32x4 oa = *(const u32x4*)(osb + row * P2 + (16 * ks + 8 * half) * 2);
-          const u32x4 vb = *(const u32x4*)(vs + (wave * 32 + (lane & 31)) * VKP + (16 * ks + 8 * half) * 2);
-          dp = mfma32<E>(bitcast_u4<vec8>(oa), bitcast_u4<vec8>(vb), dp);
+          const u32x4 oa = *(const u32x4*)(osb + row * P2 + slot);
+          dp = mfma32<E>(bitcast_u4<vec8>(oa), vf[ks], dp);
         }
         // 16 queries at a time: P and dS = P (dP - D), packed for dV and dK
 #pragma unroll
@@ -493,9 +492,10 @@ __global__ void __launch_bounds__(256, (D == 128 ? 1 : 2)) attn_bwd_dkdv(const B
 #pragma unroll
           for (int db = 0; db < DB; ++db) {
             const int col = 32 * db + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
-            const char* po = osb + trow * P2 + col * 2;
+            const int tcol = (((col >> 3) ^ swz(trow)) << 4) + (col & 7) * 2;
+            const char* po = osb + trow * P2 + tcol;
             dv[db] = mfma32<E>(lds_tr_pair<E>(po, po + 8 * P2), bp, dv[db]);
-            const char* pq = qsb + trow * P2 + col * 2;
+            const char* pq = qsb + trow * P2 + tcol;
             dk[db] = mfma32<E>(lds_tr_pair<E>(pq, pq + 8 * P2), bs, dk[db]);
           }
         }
