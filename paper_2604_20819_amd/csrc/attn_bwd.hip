@@ -265,8 +265,10 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dq(const BwdArgs a) {
 }
 
 template <typename E, int D>
-__global__ void __launch_bounds__(256, (D == 128 ? 1 : 2)) attn_bwd_dkdv(const BwdArgs a) {
-  constexpr int BK = 128, BQ = 64;
+__global__ void __launch_bounds__(256, 2) attn_bwd_dkdv(const BwdArgs a) {
+  // 32-query tiles (two per 64-token summary block) keep the registers and
+  // LDS within two work groups per CU
+  constexpr int BK = 128, BQ = 32;
   // Q and dO tiles: unpadded rows of 2D bytes with the forward's swizzle
   // (chunk ch of row r in slot ch ^ swz(r)), conflict-free for the row reads
   // and the transpose reads; filled by direct buffer-to-LDS loads
@@ -279,6 +281,7 @@ __global__ void __launch_bounds__(256, (D == 128 ? 1 : 2)) attn_bwd_dkdv(const B
   // double-buffered query tiles (Q, dO) with their per-query statistics
   __shared__ __attribute__((aligned(1024))) char qs[2][BQ * P2];
   __shared__ __attribute__((aligned(1024))) char os[2][BQ * P2];
+  __shared__ __attribute__((aligned(1024))) char vs[BK * P2];   // the strip's V rows, swizzled
   __shared__ __attribute__((aligned(16))) float lse_s[2][BQ];
   __shared__ __attribute__((aligned(16))) float d_s[2][BQ];
   __shared__ uint32_t qbits_s[2][BQ];
@@ -307,18 +310,25 @@ __global__ void __launch_bounds__(256, (D == 128 ? 1 : 2)) attn_bwd_dkdv(const B
   const int k0w = strip * BK + wave * 32;
   const int mykey = k0w + (lane & 31);
   const bool kvalid = mykey < L;
-  // the wave's K and V rows stay in registers (B operands of S = Q K^T and
-  // dP = dO V^T) for the whole strip
-  vec8 kf[DK], vf[DK];
+  // the wave's K rows stay in registers (B operands of S = Q K^T); the
+  // strip's V rows (B operands of dP = dO V^T) go to LDS once
+  vec8 kf[DK];
 #pragma unroll
   for (int ks = 0; ks < DK; ++ks) {
-    u32x4 u = {0u, 0u, 0u, 0u}, w = {0u, 0u, 0u, 0u};
-    if (kvalid) {
-      u = *(const u32x4*)(Kg + int64_t(mykey) * rs + ks * 16 + half * 8);
-      w = *(const u32x4*)(Vg + int64_t(mykey) * rs + ks * 16 + half * 8);
-    }
+    u32x4 u = {0u, 0u, 0u, 0u};
+    if (kvalid) u = *(const u32x4*)(Kg + int64_t(mykey) * rs + ks * 16 + half * 8);
     kf[ks] = bitcast_u4<vec8>(u);
-    vf[ks] = bitcast_u4<vec8>(w);
+  }
+  {
+    const __amdgpu_buffer_rsrc_t rv =
+        row_rsrc(Vg + int64_t(strip) * BK * rs, int64_t(L) - int64_t(strip) * BK, rs * 2, D * 2);
+    constexpr int NV = BK / RPI / 4;  // 1 KB loads per wave
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+      const int row = RPI * (NV * wave + j) + lane / CHUNKS;
+      buf_load16_lds(rv, vs + (NV * wave + j) * 1024,
+                     uint32_t((row * rs + ((lane % CHUNKS) ^ swz(row)) * 8) * 2));
+    }
   }
 
   const int lastk_wg = (strip * BK + BK < L ? strip * BK + BK : L) - 1;
@@ -343,8 +353,8 @@ __global__ void __launch_bounds__(256, (D == 128 ? 1 : 2)) attn_bwd_dkdv(const B
     const int t = t0 + lane;
     Window w{0xFFFFFFFFu, 0u};
     if (t < nqt) {
-      w.an = a.blk_and[t];
-      w.on = a.blk_or[t];
+      w.an = a.blk_and[t >> 1];
+      w.on = a.blk_or[t >> 1];
     }
     return w;
   };
@@ -447,7 +457,7 @@ __global__ void __launch_bounds__(256, (D == 128 ? 1 : 2)) attn_bwd_dkdv(const B
       const char* qsb = qs[buf];
       const char* osb = os[buf];
 #pragma unroll 1
-      for (int qb = 0; qb < 2; ++qb) {
+      for (int qb = 0; qb < BQ / 32; ++qb) {
         f32x16 s, dp;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
@@ -461,7 +471,9 @@ __global__ void __launch_bounds__(256, (D == 128 ? 1 : 2)) attn_bwd_dkdv(const B
           const u32x4 qa = *(const u32x4*)(qsb + row * P2 + slot);
           s = mfma32<E>(bitcast_u4<vec8>(qa), kf[ks], s);
           const u32x4 oa = *(const u32x4*)(osb + row * P2 + slot);
-          dp = mfma32<E>(bitcast_u4<vec8>(oa), vf[ks], dp);
+          const int vr = wave * 32 + (lane & 31);
+          const u32x4 vb = *(const u32x4*)(vs + vr * P2 + (((2 * ks + half) ^ swz(vr)) << 4));
+          dp = mfma32<E>(bitcast_u4<vec8>(oa), bitcast_u4<vec8>(vb), dp);
         }
         // 16 queries at a time: P and dS = P (dP - D), packed for dV and dK
 #pragma unroll
@@ -518,6 +530,7 @@ __global__ void __launch_bounds__(256, (D == 128 ? 1 : 2)) attn_bwd_dkdv(const B
     nor = or2;
     nand = and2;
   }
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // the V fill has landed even when no tile was live
   if (!kvalid) return;
   const int64_t gk = run_global(runs_s, a.n_runs, mykey);
   float* dkp = a.dk + (int64_t(b) * a.Lg + gk) * rs + int64_t(h) * D;
