@@ -39,7 +39,7 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dq(const BwdArgs a) {
   auto swz = [](int r) { return 2 * (r & 3) + ((r >> 2) & 1); };
 
   __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
-  __shared__ uint32_t kbits_s[2][BN];
+  __shared__ __attribute__((aligned(16))) uint32_t kbits_s[2][BN];
   __shared__ DevRun runs_s[kMaxRuns];
 
   const int tid = threadIdx.x, lane = tid & 63, half = lane >> 5;
@@ -203,16 +203,23 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dq(const BwdArgs a) {
           const u32x4 va = *(const u32x4*)(Vb + row * RB + slot);
           dp = mfma32<E>(bitcast_u4<vec8>(va), of[ks], dp);
         }
+        if (!wclear) {
+          // mixed tile: masked scores become -inf (so P = 0); the key bits
+          // arrive four keys per 16-byte LDS read and the test is a select
+          const uint32_t qmask = use_bits ? qbits : 0u;
+          u32x4 kbv[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) kbv[i] = *(const u32x4*)(&kbits_s[buf][32 * kb + 8 * i + 4 * half]);
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int key = k0 + 32 * kb + 8 * (r >> 2) + 4 * half + (r & 3);
+            const bool keep = (key < L) & (!causal | (key <= myq)) & ((kbv[r >> 2][r & 3] & qmask) == 0u);
+            s[r] = keep ? s[r] : -INFINITY;
+          }
+        }
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          float p = fast_exp2(fmaf(s[r], c, -lse2));
-          if (!wclear) {
-            const int kl = 32 * kb + 8 * (r >> 2) + 4 * half + (r & 3);
-            const int key = k0 + kl;
-            bool keep = key < L && (!causal || key <= myq);
-            if (use_bits) keep = keep && ((kbits_s[buf][kl] & qbits) == 0u);
-            if (!keep) p = 0.f;
-          }
+          const float p = fast_exp2(fmaf(s[r], c, -lse2));
           s[r] = p * (dp[r] - Dq);  // dS^T
         }
 #pragma unroll
@@ -284,7 +291,7 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dkdv(const BwdArgs a) {
   __shared__ __attribute__((aligned(1024))) char vs[BK * P2];   // the strip's V rows, swizzled
   __shared__ __attribute__((aligned(16))) float lse_s[2][BQ];
   __shared__ __attribute__((aligned(16))) float d_s[2][BQ];
-  __shared__ uint32_t qbits_s[2][BQ];
+  __shared__ __attribute__((aligned(16))) uint32_t qbits_s[2][BQ];
   __shared__ DevRun runs_s[kMaxRuns];
 
   const int tid = threadIdx.x, lane = tid & 63, half = lane >> 5;
@@ -454,6 +461,7 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dkdv(const BwdArgs a) {
     if (!wfull) {
       const bool wclear = (wor & qor) == 0u && (!causal || q0 >= wk1);
       const bool use_bits = (kor & qor) != 0u;
+      const uint32_t kmask = use_bits ? kbits : 0u;
       const char* qsb = qs[buf];
       const char* osb = os[buf];
 #pragma unroll 1
@@ -487,16 +495,20 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dkdv(const BwdArgs a) {
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
               const int r = 8 * sub + 4 * ii + j;
-              float p = fast_exp2(fmaf(s[r], c, -l4[j]));
-              if (!wclear) {
-                const int q = q0 + ql + j;
-                bool keep = (!causal || mykey <= q);
-                if (use_bits) keep = keep && ((qbits_s[buf][ql + j] & kbits) == 0u);
-                if (!keep) p = 0.f;
-              }
-              pv[4 * ii + j] = p;
-              dsv[4 * ii + j] = p * (dp[r] - d4[j]);
+              pv[4 * ii + j] = fast_exp2(fmaf(s[r], c, -l4[j]));
             }
+            if (!wclear) {
+              // mixed tile: the query bits of these four queries come in one
+              // 16-byte LDS read and the test is a select
+              const u32x4 qb4 = *(const u32x4*)(&qbits_s[buf][ql]);
+#pragma unroll
+              for (int j = 0; j < 4; ++j) {
+                const bool keep = (!causal | (mykey <= q0 + ql + j)) & ((qb4[j] & kmask) == 0u);
+                pv[4 * ii + j] = keep ? pv[4 * ii + j] : 0.f;
+              }
+            }
+#pragma unroll
+            for (int j = 0; j < 4; ++j) dsv[4 * ii + j] = pv[4 * ii + j] * (dp[8 * sub + 4 * ii + j] - d4[j]);
           }
           const vec8 bp = pack8<E>(pv);
           const vec8 bs = pack8<E>(dsv);

@@ -45,7 +45,7 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_mfma(const FwdArgs a) {
   auto swz = [](int r) { return 2 * (r & 3) + ((r >> 2) & 1); };
 
   __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
-  __shared__ uint32_t kbits_s[2][BN];
+  __shared__ __attribute__((aligned(16))) uint32_t kbits_s[2][BN];
   __shared__ DevRun runs_s[kMaxRuns];
 
   const int tid = threadIdx.x, lane = tid & 63, half = lane >> 5;
@@ -212,25 +212,53 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_mfma(const FwdArgs a) {
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) s[kb][r] = 0.f;
+      // K operands read two steps ahead of their products
+      auto kread = [&](int ks, int kb) {
+        const int kr = 32 * kb + (lane & 31);
+        return *(const u32x4*)(Kb + kr * RB + (((2 * ks + half) ^ swz(kr)) << 4));
+      };
+      u32x4 ka[3][2];
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        ka[0][kb] = kread(0, kb);
+        ka[1][kb] = kread(1, kb);
+      }
 #pragma unroll
       for (int ks = 0; ks < DK; ++ks) {
+        if (ks + 2 < DK) {
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-          const int kr = 32 * kb + (lane & 31);
-          const u32x4 ka = *(const u32x4*)(Kb + kr * RB + (((2 * ks + half) ^ swz(kr)) << 4));
-          s[kb] = mfma32<E>(bitcast_u4<vec8>(ka), qf[ks], s[kb]);
+          for (int kb = 0; kb < 2; ++kb) ka[(ks + 2) % 3][kb] = kread(ks + 2, kb);
         }
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) s[kb] = mfma32<E>(bitcast_u4<vec8>(ka[ks % 3][kb]), qf[ks], s[kb]);
+      }
+      // keep the reads two steps ahead of the products they feed
+      __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+      for (int ks = 0; ks < DK; ++ks) {
+        if (ks + 2 < DK) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
       }
       if (!wclear) {
+        // mixed tile: the group bits of this lane's 32 keys arrive four
+        // consecutive keys per 16-byte LDS read, all issued before any is
+        // used, and the per-element test is a select (no branch, no
+        // short-circuit); with use_bits false the bits drop out of the test
+        const uint32_t qmask = use_bits ? qbits : 0u;
+        u32x4 kbv[2][4];
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            kbv[kb][i] = *(const u32x4*)(&kbits_s[buf][32 * kb + 8 * i + 4 * half]);
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
-            const int kl = 32 * kb + 8 * (r >> 2) + 4 * half + (r & 3);
-            const int key = k0 + kl;
-            bool keep = key < L && (!causal || key <= myq);
-            if (use_bits) keep = keep && ((kbits_s[buf][kl] & qbits) == 0u);
-            if (!keep) s[kb][r] = -INFINITY;
+            const int key = k0 + 32 * kb + 8 * (r >> 2) + 4 * half + (r & 3);
+            const bool keep = (key < L) & (!causal | (key <= myq)) &
+                              ((kbv[kb][r >> 2][r & 3] & qmask) == 0u);
+            s[kb][r] = keep ? s[kb][r] : -INFINITY;
           }
       }
       float smax = -INFINITY;
