@@ -47,7 +47,7 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target CPU time of the oracle sample")
     ap.add_argument("--workload", default="headline",
-                    choices=["headline", "fp16_causal_L131072_8GB",
+                    choices=["headline", "fp16_causal_L131072_8GB", "fp16_causal_L131072_8GB_c21",
                              "bf16_causal_B2_L65536_fwdbwd_16GB", "bf16_streamed_L1M_host_4GB"],
                     help="headline (default) or one of the other seeded workloads: "
                          "their rates, depths and runtime ratios, one JSON line each")
@@ -153,6 +153,11 @@ def other_workload(name, args):
     spec = {
         "fp16_causal_L131072_8GB": dict(B=1, L=131072, H=32, d=128, causal=True, dt="f16",
                                         budget=8 * GB, seed=20819 + 3, host=False, bwd=False),
+        # the same call with the c=21 interest set (Table "interest_set"): one
+        # level of 21 tasks fits the budget where c=7 needs two levels (49 tasks)
+        "fp16_causal_L131072_8GB_c21": dict(B=1, L=131072, H=32, d=128, causal=True, dt="f16",
+                                            budget=8 * GB, seed=20819 + 3, host=False, bwd=False,
+                                            levels=[(21, (0, 1, 4, 14, 16))]),
         "bf16_causal_B2_L65536_fwdbwd_16GB": dict(B=2, L=65536, H=16, d=128, causal=True,
                                                   dt="bf16", budget=16 * GB, seed=20819 + 4,
                                                   host=False, bwd=True),
@@ -179,7 +184,7 @@ def other_workload(name, args):
         return cq.cqsa_plan(Lw, Hw, dw, causal, budget,
                             cq.make_opts(B=Bw, dtype=spec["dt"], depth=depth,
                                          inputs_on_device=not host, acc_on_device=not host,
-                                         with_backward=backward))
+                                         with_backward=backward, levels=spec.get("levels")))
 
     cq.cqsa_set_timing(True)
     steps = 2 if host else max(3, args.steps // 4)
@@ -198,7 +203,10 @@ def other_workload(name, args):
     s = st[-1]
     line = {"workload": name, "B": Bw, "L": Lw, "H": Hw, "d": dw, "causal": causal,
             "dtype": spec["dt"], "budget_bytes": spec["budget"], "depth": plan.depth,
+            "interest_sets": [c for c, _ in spec.get("levels", [(7, None)])],
             "tasks": plan.num_tasks, "tasks_per_launch": plan.tasks_per_slot,
+            "max_task_tokens": max(task_rows(plan)),
+            "staged_tokens": sum(task_rows(plan)),
             "modelled_device_bytes": plan.modelled_device_bytes,
             "workspace_bytes": s["workspace_bytes"],
             # what the call holds on the device: the library's workspace plus the

@@ -60,6 +60,15 @@ typedef struct {
 } cqsa_tensor;
 
 #define CQSA_MAX_INTEREST 16
+#define CQSA_MAX_LEVEL_SETS 4
+
+/* One level's interest set: a perfect (c, l, 1) cyclic difference set with
+ * c = l(l-1)+1 and interest[0] = 0 (App. C, Table "interest_set"). */
+typedef struct {
+  int32_t c;
+  int32_t l;
+  int32_t interest[CQSA_MAX_INTEREST];
+} cqsa_interest_set;
 
 /* Planning options.  cqsa_plan_opts_default() fills the defaults noted here. */
 typedef struct {
@@ -80,6 +89,12 @@ typedef struct {
                                 per launch (capped at 32 and at the task count, reduced until
                                 the budget fits; 1 when acc_on_device = 0); >= 1 forced;
                                 > 1 needs acc_on_device = 1 (0) */
+  int32_t n_level_sets;      /* 0: every level uses (c, l, interest).  n in [1, 4]: level t
+                                (1-based) uses level_sets[min(t, n) - 1], so the last set repeats
+                                below level n, and (c, l, interest) are ignored.  Section 3.3
+                                allows a different valid set at each depth, for finer control of
+                                the task length (0) */
+  cqsa_interest_set level_sets[CQSA_MAX_LEVEL_SETS];
 } cqsa_plan_opts;
 
 /* One contiguous run of a task's tokens: global tokens
@@ -92,8 +107,10 @@ typedef struct {
 
 /* Read-only view of one task (Alg. 3 entry).  Pointers stay valid until the
  * plan is destroyed.  Local token order equals global order (App. A.3).
- * Group bit numbering: at level t (1-based) the chunk (q_t + interest[j]) mod c,
- * j = 1..l-1, carries bit (t-1)*(l-1) + (j-1); the owner chunk q_t carries none.
+ * Group bit numbering: at level t (1-based) with set (c_t, l_t, I_t), the chunk
+ * (q_t + I_t[j]) mod c_t, j = 1..l_t-1, carries bit s_t + (j-1), where s_t is
+ * the sum of (l_u - 1) over the levels u < t ((t-1)*(l-1) when every level
+ * uses the same set); the owner chunk q_t carries none.
  * A local pair (q, k) is kept iff (bits[q] & bits[k]) == 0 (App. A.2), and, when
  * causal, global(k) <= global(q). */
 typedef struct {
@@ -139,7 +156,8 @@ void cqsa_plan_opts_default(cqsa_plan_opts* o);
 
 /* Plan a call on L tokens, H heads, head dim d (Section 3.4; Alg. 3).
  * device_budget_bytes = 0 means uncapped.  opts = NULL uses the defaults.
- * Validates (c, l, interest) as a perfect difference set (App. C).  With an
+ * Validates every level's (c, l, interest) as a perfect difference set
+ * (App. C); at most 32 group bits and 2^20 tasks in total.  With an
  * automatic depth, returns the smallest depth in [min_depth, max_depth] whose
  * modelled device footprint fits the budget, else CQSA_ERR_BUDGET; a forced
  * depth is planned even if it does not fit (the footprint is still reported).

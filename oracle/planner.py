@@ -32,6 +32,11 @@ Readings where the paper is silent or inconsistent
    j = 1..l-1, gets bit (t-1)*(l-1) + (j-1).  Alg. 3's Unique only merges
    groups with identical token sets, which cannot change the mask.
 4. Causal attention keeps a pair iff the key's global index <= the query's.
+5. Section 3.3 allows a different valid interest set at each depth.  With
+   level t using (c_t, I_t), the quorum tuple ranges over c_1 x ... x c_itr
+   (lexicographic), level t re-chunks into c_t chunks, and its non-owner
+   chunks take bits s_t + (j-1), where s_t is the sum of (l_u - 1) over the
+   levels u above t (reading 3 is the case of equal levels).
 """
 import itertools
 
@@ -77,7 +82,7 @@ def balanced_chunk_layout(L, c):
 
 
 def build_tasks(N, c, itr, I):
-    """BuildSubseq (Alg. 3) with readings 1-3.
+    """BuildSubseq (Alg. 3) with readings 1-3: every level uses (c, I).
 
     Returns a list (lexicographic quorum order) of dicts with
       quorum  : tuple (q_1, ..., q_itr)
@@ -86,12 +91,19 @@ def build_tasks(N, c, itr, I):
       bits    : uint32 array, OR of (1 << bit_index) over groups holding the token
     itr = 0 gives the single undecomposed task.
     """
-    l = len(I)
+    return build_tasks_levels(N, [(c, tuple(I))] * itr)
+
+
+def build_tasks_levels(N, levels):
+    """BuildSubseq (Alg. 3) with a set per level (reading 5): levels[t] is
+    (c_t, I_t) for level t + 1.  Same output as build_tasks."""
     tasks = []
-    for quorum in itertools.product(range(c), repeat=itr):
+    offsets = np.cumsum([0] + [len(I) - 1 for _, I in levels])
+    for quorum in itertools.product(*[range(c) for c, _ in levels]):
         tokens = np.arange(N, dtype=np.int64)
-        history = []          # per level: (owner, chunk list, labels over current tokens)
+        history = []          # per level: (owner, labels over current tokens)
         for t, q in enumerate(quorum):
+            c, I = levels[t]
             L = len(tokens)
             starts, ends = balanced_chunk_layout(L, c)
             labels = np.zeros(L, dtype=np.int64)
@@ -99,17 +111,18 @@ def build_tasks(N, c, itr, I):
                 labels[starts[u]:ends[u]] = u
             chunks = sorted(((q + o) % c) for o in I)           # reading 2
             gather = np.concatenate([np.arange(starts[u], ends[u]) for u in chunks])
-            history = [(own, ch, lab[gather]) for (own, ch, lab) in history]
-            history.append((q, chunks, labels[gather]))
+            history = [(own, lab[gather]) for (own, lab) in history]
+            history.append((q, labels[gather]))
             tokens = tokens[gather]
         groups = []
-        for t, (owner, chunks, labels) in enumerate(history):
+        for t, (owner, labels) in enumerate(history):
+            c, I = levels[t]
             for j, o in enumerate(I):
                 if j == 0:
                     continue
                 chunk = (owner + o) % c
                 member = labels == chunk
-                groups.append(((t * (l - 1)) + (j - 1), member))
+                groups.append((int(offsets[t]) + (j - 1), member))
         bits = np.zeros(len(tokens), dtype=np.uint32)
         for bit, member in groups:
             bits[member] |= np.uint32(1 << bit)

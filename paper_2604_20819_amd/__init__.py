@@ -34,13 +34,18 @@ class cqsa_tensor(ctypes.Structure):
                 ("d", ctypes.c_int64)]
 
 
+class cqsa_interest_set(ctypes.Structure):
+    _fields_ = [("c", ctypes.c_int32), ("l", ctypes.c_int32), ("interest", ctypes.c_int32 * 16)]
+
+
 class cqsa_plan_opts(ctypes.Structure):
     _fields_ = [("B", ctypes.c_int32), ("dtype", ctypes.c_int), ("c", ctypes.c_int32),
                 ("l", ctypes.c_int32), ("interest", ctypes.c_int32 * 16),
                 ("depth", ctypes.c_int32), ("min_depth", ctypes.c_int32),
                 ("max_depth", ctypes.c_int32), ("n_slots", ctypes.c_int32),
                 ("inputs_on_device", ctypes.c_int32), ("acc_on_device", ctypes.c_int32),
-                ("with_backward", ctypes.c_int32), ("tasks_per_slot", ctypes.c_int32)]
+                ("with_backward", ctypes.c_int32), ("tasks_per_slot", ctypes.c_int32),
+                ("n_level_sets", ctypes.c_int32), ("level_sets", cqsa_interest_set * 4)]
 
 
 class cqsa_run(ctypes.Structure):
@@ -134,7 +139,8 @@ def cqsa_plan_opts_default():
 
 def make_opts(B=1, dtype="bf16", c=7, interest=(0, 1, 3), depth=-1, min_depth=1, max_depth=4,
               n_slots=2, inputs_on_device=True, acc_on_device=True, with_backward=False,
-              tasks_per_slot=0):
+              tasks_per_slot=0, levels=None):
+    """levels: optional list of (c, interest) per depth (the last repeats below)."""
     o = cqsa_plan_opts_default()
     o.B = B
     o.dtype = {"f32": CQSA_F32, "f16": CQSA_F16, "bf16": CQSA_BF16}[dtype]
@@ -147,6 +153,15 @@ def make_opts(B=1, dtype="bf16", c=7, interest=(0, 1, 3), depth=-1, min_depth=1,
     o.acc_on_device = int(bool(acc_on_device))
     o.with_backward = int(bool(with_backward))
     o.tasks_per_slot = int(tasks_per_slot)
+    if levels:
+        if len(levels) > 4:
+            raise ValueError("at most 4 level sets")
+        o.n_level_sets = len(levels)
+        for k, (lc, li) in enumerate(levels):
+            o.level_sets[k].c = lc
+            o.level_sets[k].l = len(li)
+            for i in range(16):
+                o.level_sets[k].interest[i] = li[i] if i < len(li) else 0
     return o
 
 

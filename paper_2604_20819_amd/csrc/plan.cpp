@@ -9,8 +9,10 @@
 //  * BalancedChunkLayout(L, c) gives the first L mod c chunks one extra token.
 //  * A task's chunks are gathered in ascending chunk order, so local order is
 //    global order and causal masking composes by conjunction (App. A.3).
-//  * At level t (0-based here) the chunk (q + I[j]) mod c, j >= 1, carries bit
-//    t*(l-1) + (j-1); the owner chunk q (offset I[0] = 0) carries none.
+//  * At level t (0-based here) with set (c_t, l_t, I_t) the chunk
+//    (q + I_t[j]) mod c_t, j >= 1, carries bit s_t + (j-1), s_t being the sum
+//    of (l_u - 1) over the levels above; the owner chunk q (offset I_t[0] = 0)
+//    carries none.  Section 3.3 lets each depth use its own valid set.
 #include <algorithm>
 #include <cstring>
 #include <string>
@@ -52,6 +54,22 @@ static int64_t ipow(int64_t b, int32_t e) {
   return r;
 }
 
+LevelSet level_set(const cqsa_plan_opts& o, int32_t level) {
+  if (o.n_level_sets <= 0) return LevelSet{o.c, o.l, o.interest};
+  const cqsa_interest_set& s = o.level_sets[std::min(level, o.n_level_sets - 1)];
+  return LevelSet{s.c, s.l, s.interest};
+}
+
+static std::string check_set(int32_t c, int32_t l, const int32_t* I) {
+  if (l < 1 || l > CQSA_MAX_INTEREST) return "l must be in [1, 16]";
+  if (c != l * (l - 1) + 1) return "c must equal l(l-1)+1";
+  if (I[0] != 0) return "interest set must start with 0";
+  for (int32_t j = 0; j < l; ++j)
+    if (I[j] < 0 || I[j] >= c) return "interest offsets must lie in [0, c)";
+  if (!is_perfect_difference_set(I, l, c)) return "interest set is not a perfect (c,l,1) difference set";
+  return "";
+}
+
 cqsa_status validate_plan_args(int64_t L, int32_t H, int32_t d, const cqsa_plan_opts& o,
                                std::string* err) {
   auto bad = [&](cqsa_status s, const std::string& m) {
@@ -65,22 +83,29 @@ cqsa_status validate_plan_args(int64_t L, int32_t H, int32_t d, const cqsa_plan_
   if (d != 64 && d != 128) return bad(CQSA_ERR_UNSUPPORTED, "head dim must be 64 or 128");
   if (o.B < 1) return bad(CQSA_ERR_INVALID_ARG, "B must be >= 1");
   if (dtype_size(o.dtype) == 0) return bad(CQSA_ERR_INVALID_ARG, "unknown dtype");
-  if (o.l < 1 || o.l > CQSA_MAX_INTEREST) return bad(CQSA_ERR_INVALID_ARG, "l must be in [1, 16]");
-  if (o.c != o.l * (o.l - 1) + 1) return bad(CQSA_ERR_INVALID_ARG, "c must equal l(l-1)+1");
-  if (o.interest[0] != 0) return bad(CQSA_ERR_INVALID_ARG, "interest set must start with 0");
-  for (int32_t j = 0; j < o.l; ++j)
-    if (o.interest[j] < 0 || o.interest[j] >= o.c)
-      return bad(CQSA_ERR_INVALID_ARG, "interest offsets must lie in [0, c)");
-  if (!is_perfect_difference_set(o.interest, o.l, o.c))
-    return bad(CQSA_ERR_INVALID_ARG, "interest set is not a perfect (c,l,1) difference set");
+  if (o.n_level_sets < 0 || o.n_level_sets > CQSA_MAX_LEVEL_SETS)
+    return bad(CQSA_ERR_INVALID_ARG, "n_level_sets must be in [0, 4]");
+  if (o.n_level_sets == 0) {
+    const std::string e = check_set(o.c, o.l, o.interest);
+    if (!e.empty()) return bad(CQSA_ERR_INVALID_ARG, e);
+  }
+  for (int32_t i = 0; i < o.n_level_sets; ++i) {
+    const cqsa_interest_set& ls = o.level_sets[i];
+    const std::string e = check_set(ls.c, ls.l, ls.interest);
+    if (!e.empty()) return bad(CQSA_ERR_INVALID_ARG, "level set " + std::to_string(i) + ": " + e);
+  }
   if (o.depth < -1) return bad(CQSA_ERR_INVALID_ARG, "depth must be -1 (auto) or >= 0");
   if (o.min_depth < 0 || o.max_depth < o.min_depth)
     return bad(CQSA_ERR_INVALID_ARG, "need 0 <= min_depth <= max_depth");
-  int32_t top = o.depth >= 0 ? o.depth : o.max_depth;
-  if (int64_t(top) * (o.l - 1) > 32)
-    return bad(CQSA_ERR_UNSUPPORTED, "depth*(l-1) group bits exceed 32");
-  if (ipow(o.c, top) > (int64_t(1) << 20))
-    return bad(CQSA_ERR_UNSUPPORTED, "more than 2^20 tasks");
+  const int32_t top = o.depth >= 0 ? o.depth : o.max_depth;
+  int64_t bits = 0, ntask = 1;
+  for (int32_t t = 0; t < top; ++t) {
+    const LevelSet ls = level_set(o, t);
+    bits += ls.l - 1;
+    ntask = std::min<int64_t>(ntask * ls.c, int64_t(1) << 40);
+  }
+  if (bits > 32) return bad(CQSA_ERR_UNSUPPORTED, "the levels' group bits exceed 32");
+  if (ntask > (int64_t(1) << 20)) return bad(CQSA_ERR_UNSUPPORTED, "more than 2^20 tasks");
   if (o.n_slots < 1) return bad(CQSA_ERR_INVALID_ARG, "n_slots must be >= 1");
   if (o.inputs_on_device != 0 && o.inputs_on_device != 1)
     return bad(CQSA_ERR_INVALID_ARG, "inputs_on_device must be 0 or 1");
@@ -139,7 +164,7 @@ static void finish_task(Task& t) {
 }
 
 static void descend(const std::vector<Run>& cur, int64_t Lcur, int32_t level, int32_t depth,
-                    const cqsa_plan_opts& o, std::vector<int32_t>& quorum,
+                    uint32_t bit0, const cqsa_plan_opts& o, std::vector<int32_t>& quorum,
                     std::vector<Task>& out) {
   if (level == depth) {
     Task t;
@@ -150,17 +175,18 @@ static void descend(const std::vector<Run>& cur, int64_t Lcur, int32_t level, in
     out.push_back(std::move(t));
     return;
   }
-  const int64_t base = Lcur / o.c, extra = Lcur % o.c;
+  const LevelSet ls = level_set(o, level);
+  const int64_t base = Lcur / ls.c, extra = Lcur % ls.c;
   auto chunk_start = [&](int64_t u) { return u * base + std::min<int64_t>(u, extra); };
   struct Pick {
     int32_t chunk;
     uint32_t bit;
   };
-  for (int32_t q = 0; q < o.c; ++q) {
+  for (int32_t q = 0; q < ls.c; ++q) {
     std::vector<Pick> picks;
-    for (int32_t j = 0; j < o.l; ++j) {
-      int32_t chunk = (q + o.interest[j]) % o.c;
-      uint32_t bit = j == 0 ? 0u : (1u << (level * (o.l - 1) + (j - 1)));
+    for (int32_t j = 0; j < ls.l; ++j) {
+      int32_t chunk = (q + ls.interest[j]) % ls.c;
+      uint32_t bit = j == 0 ? 0u : (1u << (bit0 + uint32_t(j - 1)));
       picks.push_back({chunk, bit});
     }
     std::sort(picks.begin(), picks.end(),
@@ -173,7 +199,7 @@ static void descend(const std::vector<Run>& cur, int64_t Lcur, int32_t level, in
       at += b - a;
     }
     quorum.push_back(q);
-    descend(next, at, level + 1, depth, o, quorum, out);
+    descend(next, at, level + 1, depth, bit0 + uint32_t(ls.l - 1), o, quorum, out);
     quorum.pop_back();
   }
 }
@@ -182,7 +208,7 @@ std::vector<Task> build_tasks(int64_t L, const cqsa_plan_opts& o, int32_t depth)
   std::vector<Task> out;
   std::vector<Run> root{Run{0, 0, L, 0u}};
   std::vector<int32_t> quorum;
-  descend(root, L, 0, depth, o, quorum, out);
+  descend(root, L, 0, depth, 0u, o, quorum, out);
   return out;
 }
 

@@ -109,6 +109,13 @@ cqsa_status validate_plan_args(int64_t L, int32_t H, int32_t d, const cqsa_plan_
                                std::string* err);
 
 // Builds the c**depth tasks of BuildSubseq with ascending chunk order.
+// Interest set of level `level` (0-based): (c, l, interest), or the opts'
+// per-level set (the last one repeating below the given levels).
+struct LevelSet {
+  int32_t c, l;
+  const int32_t* interest;
+};
+LevelSet level_set(const cqsa_plan_opts& o, int32_t level);
 std::vector<Task> build_tasks(int64_t L, const cqsa_plan_opts& o, int32_t depth);
 
 // Footprint of running `tasks` under `o` with `group_size` tasks per forward

@@ -46,6 +46,76 @@ def test_planner_matches_oracle(N, itr, c):
         assert got["block_or"] == bor.tolist() and got["block_and"] == band.tolist()
 
 
+@pytest.mark.parametrize("N,levels,depth", [
+    (500, [(7, (0, 1, 3)), (13, (0, 1, 3, 9))], 2),
+    (500, [(13, (0, 1, 3, 9)), (7, (0, 1, 3))], 2),
+    (3000, [(21, (0, 1, 4, 14, 16)), (3, (0, 1))], 2),
+    (700, [(3, (0, 1)), (7, (0, 1, 3))], 3),        # the last set repeats below
+    (65536, [(13, (0, 1, 3, 9))], 1),
+    (90, [(7, (0, 1, 3)), (13, (0, 1, 3, 9)), (3, (0, 1))], 3)])
+def test_planner_matches_oracle_with_level_sets(N, levels, depth):
+    """Section 3.3: a different valid interest set per depth.  Tasks, runs,
+    bits and block summaries equal the oracle planner's."""
+    p = cq.cqsa_plan(N, 1, 64, False, 0, cq.make_opts(depth=depth, levels=levels))
+    full = (levels + [levels[-1]] * depth)[:depth]
+    ref = oplan.build_tasks_levels(N, full)
+    assert p.depth == depth and p.num_tasks == len(ref)
+    for t, rt in enumerate(ref):
+        got = p.task(t)
+        assert got["quorum"] == tuple(rt["quorum"])
+        assert got["runs"] == oplan.runs(rt)
+        bor, band = oplan.block_summaries(rt["bits"])
+        assert got["block_or"] == bor.tolist() and got["block_and"] == band.tolist()
+
+
+@pytest.mark.parametrize("levels,depth,status,msg", [
+    ([(7, (0, 1, 3)), (13, (0, 1, 3, 4))], 2, -1, "level set 1"),
+    ([(7, (0, 1, 3)), (12, (0, 1, 3, 9))], 2, -1, "c must equal"),
+    ([(21, (0, 1, 4, 14, 16))], 9, -2, "group bits exceed 32"),
+    ([(13, (0, 1, 3, 9)), (7, (0, 1, 3))], 7, -2, "2^20 tasks")])
+def test_level_set_errors(levels, depth, status, msg):
+    with pytest.raises(cq.CqsaError) as e:
+        cq.cqsa_plan(1000, 1, 64, False, 0, cq.make_opts(depth=depth, levels=levels))
+    assert e.value.status == status and msg in str(e.value)
+    o = cq.make_opts()
+    o.n_level_sets = 5
+    with pytest.raises(cq.CqsaError) as e:
+        cq.cqsa_plan(1000, 1, 64, False, 0, o)
+    assert e.value.status == -1
+
+
+def test_struct_layouts_match_the_header(tmp_path):
+    """The binding's ctypes mirrors have the sizes and field offsets of the C
+    structs in include/cqsa.h (checked by compiling the header with gcc)."""
+    import shutil
+    import subprocess
+    if shutil.which("gcc") is None:
+        pytest.skip("gcc not available")
+    checks = {"cqsa_plan_opts": ["B", "interest", "tasks_per_slot", "n_level_sets", "level_sets"],
+              "cqsa_interest_set": ["c", "l", "interest"],
+              "cqsa_tensor": ["data", "B", "d"], "cqsa_task": ["quorum", "runs", "block_and"],
+              "cqsa_run": ["global_start", "bits"],
+              "cqsa_run_stats": ["num_tasks", "ms_wall", "tiles_mixed", "ms_inner_busy"]}
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "cqsa.h"', "int main(void) {"]
+    for st, fields in checks.items():
+        lines.append(f'  printf("{st} %zu\\n", sizeof({st}));')
+        for f in fields:
+            lines.append(f'  printf("{st}.{f} %zu\\n", offsetof({st}, {f}));')
+    lines.append("  return 0;\n}")
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "layout"
+    inc = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include")
+    subprocess.run(["gcc", "-std=c11", "-I", inc, str(src), "-o", str(exe)], check=True)
+    got = dict(l.split() for l in subprocess.run([str(exe)], check=True, capture_output=True,
+                                                 text=True).stdout.splitlines())
+    for st, fields in checks.items():
+        cls = getattr(cq, st)
+        assert int(got[st]) == ctypes.sizeof(cls), st
+        for f in fields:
+            assert int(got[f"{st}.{f}"]) == getattr(cls, f).offset, (st, f)
+
+
 @pytest.mark.parametrize("N,itr", [(65536, 1), (65536, 2), (20000, 3)])
 def test_census_matches_oracle(N, itr):
     p = cq.cqsa_plan(N, 1, 64, True, 0, cq.make_opts(depth=itr))

@@ -25,12 +25,12 @@ pytestmark = pytest.mark.gpu
 REL = {"bf16": 6e-3, "f16": 8e-4}
 
 
-def run_fwd_bwd(Q, K, V, dO, causal, depth=-1, budget=0, n_slots=2):
+def run_fwd_bwd(Q, K, V, dO, causal, depth=-1, budget=0, n_slots=2, levels=None):
     B, L, H, d = Q.shape
     dt = {torch.float16: "f16", torch.bfloat16: "bf16"}[Q.dtype]
     plan = cq.cqsa_plan(L, H, d, causal, budget,
                         cq.make_opts(B=B, dtype=dt, depth=depth, n_slots=n_slots,
-                                     with_backward=True))
+                                     with_backward=True, levels=levels))
     q, k, v, do = (x.cuda() for x in (Q, K, V, dO))
     O = torch.empty((B, L, H, d), dtype=torch.float32, device="cuda")
     LSE = torch.empty((B, H, L), dtype=torch.float32, device="cuda")
@@ -108,6 +108,26 @@ def test_decomposed_matches_undecomposed(dt, causal):
             r = rel_l2(got[i].numpy(), ref[i].numpy())
             say(f"{name}: {r:.3e}")
             assert r <= 1e-3
+
+
+@pytest.mark.parametrize("levels,depth", [([(13, (0, 1, 3, 9))], 1),
+                                          ([(7, (0, 1, 3)), (13, (0, 1, 3, 9))], 2),
+                                          ([(21, (0, 1, 4, 14, 16)), (3, (0, 1))], 2)],
+                         ids=["c13", "c7-c13", "c21-c3"])
+def test_other_interest_sets_and_mixed_levels(levels, depth):
+    """Section 3.3: any valid interest set, and a different one per depth;
+    gradients equal the undecomposed call's."""
+    need_gpu()
+    Q, K, V, dO = synth.make_inputs(321, 1, 2500, 2, 128, "bf16", with_dO=True)
+    ref = run_fwd_bwd(Q, K, V, dO, True, depth=0)
+    say(f"bwd interest sets {levels} depth {depth}")
+    got = run_fwd_bwd(Q, K, V, dO, True, depth=depth, levels=levels)
+    assert got[-1].num_tasks == int(np.prod([c for c, _ in levels[:depth]] +
+                                            [levels[-1][0]] * max(0, depth - len(levels))))
+    for name, i in (("dQ", 2), ("dK", 3), ("dV", 4)):
+        r = rel_l2(got[i].numpy(), ref[i].numpy())
+        say(f"{name}: {r:.3e}")
+        assert r <= 1e-3
 
 
 def test_bf16_B2_H16_L8192_causal_full_gradients():

@@ -16,6 +16,7 @@ import pytest
 import torch
 
 from oracle import dense
+from oracle import planner as oplan
 from paper_2604_20819_amd import synth
 from tests.gpu_util import need_gpu, rel_l2, run_forward, say
 
@@ -95,6 +96,37 @@ def test_decomposed_matches_undecomposed(dt, causal):
         say(f"depth {depth}: rel_l2 vs depth 0 = {r:.3e}")
         assert r <= 1e-3
         assert np.abs(L1.numpy() - L0.numpy()).max() <= 1e-5
+
+
+LEVEL_CASES = [([(13, (0, 1, 3, 9))], 1), ([(21, (0, 1, 4, 14, 16))], 1),
+               ([(13, (0, 1, 3, 9))], 2), ([(7, (0, 1, 3)), (13, (0, 1, 3, 9))], 2),
+               ([(13, (0, 1, 3, 9)), (7, (0, 1, 3))], 2),
+               ([(3, (0, 1)), (7, (0, 1, 3)), (3, (0, 1))], 3)]
+
+
+@pytest.mark.parametrize("levels,depth", LEVEL_CASES,
+                         ids=["c13", "c21", "c13x2", "c7-c13", "c13-c7", "c3-c7-c3"])
+@pytest.mark.parametrize("causal", [False, True])
+def test_other_interest_sets_and_mixed_levels(levels, depth, causal):
+    """Section 3.3: any valid interest set (App. C, Table "interest_set"), and
+    a different one per depth.  The plan's tasks are the oracle planner's; the
+    output matches the float64 oracle and the undecomposed call."""
+    need_gpu()
+    L = 3000
+    Q, K, V = synth.make_inputs(77 + depth, 1, L, 3, 128, "bf16")
+    say(f"interest sets {levels} depth {depth} causal={causal}")
+    O0, L0, _ = run_forward(Q, K, V, causal, depth=0)
+    O, LSE, plan = run_forward(Q, K, V, causal, depth=depth, levels=levels)
+    full = (levels + [levels[-1]] * depth)[:depth]
+    ref_tasks = oplan.build_tasks_levels(L, full)
+    assert plan.num_tasks == len(ref_tasks)
+    for t in (0, len(ref_tasks) // 2, len(ref_tasks) - 1):
+        assert plan.task(t)["runs"] == oplan.runs(ref_tasks[t])
+    _check_vs_oracle(O, LSE, Q, K, V, causal, "bf16")
+    r = rel_l2(O.numpy(), O0.numpy())
+    say(f"  rel_l2 vs depth 0 = {r:.3e}")
+    assert r <= 1e-3
+    assert np.abs(LSE.numpy() - L0.numpy()).max() <= 1e-5
 
 
 @pytest.mark.parametrize("causal", [False, True])

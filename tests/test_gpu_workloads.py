@@ -2,7 +2,8 @@
 
 * fp16 causal, B=1 H=32 d=128 L=131072, 8 GB device budget: the planner must
   recurse to depth >= 2; 2048 sampled query rows per head against float64, all
-  rows against the undecomposed kernel (which fits at this size).
+  rows against the undecomposed kernel (which fits at this size).  The same
+  call with the c = 21 interest set fits at depth 1 and is checked the same way.
 * streamed out-of-core, bf16 non-causal, B=1 H=8 d=128 L=1048576, inputs and
   outputs in pinned host memory, 4 GB device budget (the accumulator is merged
   on the host); 4096 sampled query rows per head against float64, and the
@@ -93,6 +94,17 @@ def test_fp16_causal_L131072_budget_8GB():
     r = rel_l2(O.numpy(), O0.numpy())
     say(f"rel_l2 vs depth 0 = {r:.3e}")
     assert r <= 1e-3
+    # Section 3.3 / Table "interest_set": with c = 21 (l = 5) one level of 21
+    # tasks fits the same budget where c = 7 needs two levels (49 tasks)
+    del O, LSE
+    O2, L2, plan2 = run_forward(Q, K, V, True, budget=8 * GB, levels=[(21, (0, 1, 4, 14, 16))])
+    say(f"c=21: depth={plan2.depth} tasks={plan2.num_tasks} "
+        f"modelled={plan2.modelled_device_bytes / GB:.3f} GB")
+    assert plan2.depth == 1 and plan2.num_tasks == 21 and plan2.modelled_device_bytes <= 8 * GB
+    check(*gather_rows(O2, L2, rows), Of, Lf, 6e-4)
+    r2 = rel_l2(O2.numpy(), O0.numpy())
+    say(f"c=21: rel_l2 vs depth 0 = {r2:.3e}")
+    assert r2 <= 1e-3
 
 
 def test_bf16_streamed_L1M_host_budget_4GB():

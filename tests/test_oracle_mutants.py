@@ -69,6 +69,10 @@ PLAN_PINS = [
     T_plan.test_each_chunk_in_l_tasks_and_tokens_ascending,
     T_plan.test_bits_per_level,
 ]
+MIXED_PINS = [
+    lambda: T_plan.test_mixed_levels_cover_every_pair_once(T_plan.MIXED_LEVELS[0], False),
+    T_plan.test_mixed_levels_bits_are_disjoint_per_level,
+]
 DEC_PINS = [
     lambda: T_dec.test_merged_forward_equals_dense(7, 23, 1, False),
     lambda: T_dec.test_merged_forward_equals_dense(7, 64, 2, True),
@@ -99,14 +103,17 @@ MUTANTS = [
     ("bwd: dV with P untransposed", dense, "attention_backward",
      "p.T @ do", "p @ do", BWD_PINS),
     # planner
-    ("plan: interest offsets subtracted", planner, "build_tasks",
+    ("plan: interest offsets subtracted", planner, "build_tasks_levels",
      "sorted(((q + o) % c) for o in I)", "sorted(((q - o) % c) for o in I)", PLAN_PINS),
-    ("plan: chunks in descending order", planner, "build_tasks",
+    ("plan: chunks in descending order", planner, "build_tasks_levels",
      "sorted(((q + o) % c) for o in I)", "sorted(((q + o) % c for o in I), reverse=True)",
      PLAN_PINS),
-    ("plan: levels share group bits", planner, "build_tasks",
-     "((t * (l - 1)) + (j - 1), member)", "((j - 1), member)", PLAN_PINS),
-    ("plan: owner chunk masked too", planner, "build_tasks",
+    ("plan: levels share group bits", planner, "build_tasks_levels",
+     "(int(offsets[t]) + (j - 1), member)", "((j - 1), member)", PLAN_PINS),
+    ("plan: every level masks with the first level's set", planner, "build_tasks_levels",
+     "            c, I = levels[t]\n            for j, o in enumerate(I):",
+     "            c, I = levels[0]\n            for j, o in enumerate(I):", MIXED_PINS),
+    ("plan: owner chunk masked too", planner, "build_tasks_levels",
      "if j == 0:\n                    continue", "pass", PLAN_PINS),
     ("plan: remainder to the last chunks", planner, "balanced_chunk_layout",
      "(1 if u < extra else 0)", "(1 if u >= c - extra else 0)", PLAN_PINS),
@@ -135,5 +142,5 @@ def test_pins_catch_planted_mistake(label, module, name, old, new, pins):
 
 def test_unmutated_oracle_passes_the_same_pins():
     """The harness itself: the same pin lists pass on the real oracle."""
-    for pins in (FWD_PINS, BWD_PINS, PLAN_PINS, DEC_PINS):
+    for pins in (FWD_PINS, BWD_PINS, PLAN_PINS, MIXED_PINS, DEC_PINS):
         assert not caught(pins)

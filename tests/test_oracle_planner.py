@@ -113,6 +113,45 @@ def test_exactly_once_coverage(c, causal):
             assert (counts == want).all(), (N, itr)
 
 
+# Section 3.3: a different valid interest set may be used at each depth.
+MIXED_LEVELS = [
+    [(7, (0, 1, 3)), (13, (0, 1, 3, 9))],
+    [(13, (0, 1, 3, 9)), (7, (0, 1, 3))],
+    [(3, (0, 1)), (7, (0, 1, 3)), (3, (0, 1))],
+    [(21, (0, 1, 4, 14, 16)), (3, (0, 1))],
+]
+
+
+@pytest.mark.parametrize("levels", MIXED_LEVELS, ids=lambda v: "-".join(str(c) for c, _ in v))
+@pytest.mark.parametrize("causal", [False, True])
+def test_mixed_levels_cover_every_pair_once(levels, causal):
+    """Brute force: with a set per level every kept pair is computed by exactly
+    one task, there are prod(c_t) tasks, and each token sits in prod(l_t)."""
+    ntask = int(np.prod([c for c, _ in levels]))
+    per_token = int(np.prod([len(I) for _, I in levels]))
+    for N in (ntask // 2 + 1, ntask, 2 * ntask + 5, 150):
+        tasks = planner.build_tasks_levels(N, levels)
+        assert len(tasks) == ntask
+        appear = np.zeros(N, dtype=np.int64)
+        for t in tasks:
+            assert (np.diff(t["tokens"]) > 0).all()
+            appear[t["tokens"]] += 1
+        assert (appear == per_token).all(), N
+        counts = planner.coverage_counts(tasks, N, causal)
+        want = np.tril(np.ones((N, N), dtype=np.int64)) if causal else np.ones((N, N), dtype=np.int64)
+        assert (counts == want).all(), N
+
+
+def test_mixed_levels_bits_are_disjoint_per_level():
+    """Level t's groups use bits [s_t, s_t + l_t - 1), disjoint across levels."""
+    levels = [(7, (0, 1, 3)), (13, (0, 1, 3, 9))]
+    for task in planner.build_tasks_levels(200, levels):
+        assert {b for b, _ in task["groups"]} == set(range(2 + 3))
+        level2 = task["bits"] >> np.uint32(2)
+        assert (level2 < 8).all()
+        assert (np.bitwise_count(level2) <= 1).all() and (np.bitwise_count(task["bits"] & 3) <= 1).all()
+
+
 def test_each_chunk_in_l_tasks_and_tokens_ascending():
     for itr in (1, 2):
         tasks = planner.build_tasks(100, 7, itr, (0, 1, 3))
