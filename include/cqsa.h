@@ -82,7 +82,10 @@ typedef struct {
   int32_t max_depth;         /* last depth the automatic search tries (4) */
   int32_t n_slots;           /* staging slots in flight, >= 1 (2) */
   int32_t inputs_on_device;  /* 1: Q, K, V (and dO) are device-resident; 0: host-resident (1) */
-  int32_t acc_on_device;     /* 1: accumulator/outputs on device; 0: on host, merged by host threads (1) */
+  int32_t acc_on_device;     /* 1: accumulator/outputs on device; 0: on host, merged by host
+                                threads; -1: on the device when some depth in [min_depth,
+                                max_depth] fits the budget there, else on the host (forward
+                                plans only; query cqsa_plan_acc_on_device) (1) */
   int32_t with_backward;     /* 1: the footprint must also fit cqsa_backward (0) */
   int32_t tasks_per_slot;    /* forward tasks staged, launched and merged together, in [0, 32]:
                                 0 = automatic: enough tasks for 1024 inner-kernel work groups
@@ -149,6 +152,9 @@ typedef struct {
   int64_t tiles_full, tiles_clear, tiles_mixed; /* 128x128 tile census of the plan */
   int64_t merge_launches;           /* device merge launches (forward) */
   double ms_inner_busy;             /* time at least one inner kernel ran (union of its spans) */
+  int64_t guard_steps;              /* OOM guardrail fallbacks this call took (0: the plan ran) */
+  int64_t resident_tasks;           /* task working sets held at once (forward sub-slots or
+                                       backward staging slots; 0 for the undecomposed path) */
 } cqsa_run_stats;
 
 /* Fill `o` with the defaults listed in cqsa_plan_opts. */
@@ -174,6 +180,9 @@ cqsa_status cqsa_plan_get_task(const cqsa_plan_t* plan, int64_t t, cqsa_task* ou
 uint64_t cqsa_plan_modelled_device_bytes(const cqsa_plan_t* plan);
 /* Forward tasks per staging slot and launch group the plan chose; -1 if plan is NULL. */
 int32_t cqsa_plan_tasks_per_slot(const cqsa_plan_t* plan);
+/* Where the plan keeps the accumulator and outputs: 1 device, 0 host (the choice of an
+ * automatic acc_on_device = -1; App. A.3, residency); -1 if plan is NULL. */
+int32_t cqsa_plan_acc_on_device(const cqsa_plan_t* plan);
 /* Pooled 128x128 tile census over causal-retained tiles of every task (App. A.2). */
 cqsa_status cqsa_plan_tile_census(const cqsa_plan_t* plan, int64_t* full, int64_t* clear,
                                   int64_t* mixed);
@@ -185,7 +194,14 @@ void cqsa_plan_destroy(cqsa_plan_t* plan);                 /* NULL is a no-op */
  * LSE: fp32 [B, H, L] in `lse_where` memory (must equal O's residency).
  * scale <= 0 selects 1/sqrt(d) (Section 3.1).  Device-resident outputs are
  * written in stream order on hip_stream; host-resident outputs are complete
- * on return. */
+ * on return.
+ * OOM guardrail (Section 3.4): with an automatic depth, a workspace allocation
+ * failure (CQSA_ERR_DEVICE_OOM) is retried with fewer task working sets
+ * resident at once (halved tasks per launch group, then fewer staging
+ * slots), then one level deeper, up to max_depth; the configuration that
+ * succeeded is kept with the plan for later calls, and
+ * cqsa_run_stats.guard_steps counts the fallbacks.  A forced depth reports
+ * the failure.  Nothing is enqueued by an attempt that fails to allocate. */
 cqsa_status cqsa_forward(const cqsa_plan_t* plan, const cqsa_tensor* Q, const cqsa_tensor* K,
                          const cqsa_tensor* V, cqsa_tensor* O, float* LSE, cqsa_mem lse_where,
                          float scale, void* hip_stream);

@@ -71,7 +71,8 @@ class cqsa_run_stats(ctypes.Structure):
                 ("ms_finalize", ctypes.c_double), ("ms_d2h", ctypes.c_double),
                 ("tiles_full", ctypes.c_int64), ("tiles_clear", ctypes.c_int64),
                 ("tiles_mixed", ctypes.c_int64), ("merge_launches", ctypes.c_int64),
-                ("ms_inner_busy", ctypes.c_double)]
+                ("ms_inner_busy", ctypes.c_double), ("guard_steps", ctypes.c_int64),
+                ("resident_tasks", ctypes.c_int64)]
 
 
 # Every symbol include/cqsa.h declares, with its ctypes signature.
@@ -85,6 +86,7 @@ _SIGS = {
     "cqsa_plan_get_task": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.POINTER(cqsa_task)]),
     "cqsa_plan_modelled_device_bytes": (ctypes.c_uint64, [ctypes.c_void_p]),
     "cqsa_plan_tasks_per_slot": (ctypes.c_int32, [ctypes.c_void_p]),
+    "cqsa_plan_acc_on_device": (ctypes.c_int32, [ctypes.c_void_p]),
     "cqsa_plan_tile_census": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(ctypes.c_int64),
                                              ctypes.POINTER(ctypes.c_int64),
                                              ctypes.POINTER(ctypes.c_int64)]),
@@ -140,7 +142,8 @@ def cqsa_plan_opts_default():
 def make_opts(B=1, dtype="bf16", c=7, interest=(0, 1, 3), depth=-1, min_depth=1, max_depth=4,
               n_slots=2, inputs_on_device=True, acc_on_device=True, with_backward=False,
               tasks_per_slot=0, levels=None):
-    """levels: optional list of (c, interest) per depth (the last repeats below)."""
+    """levels: optional list of (c, interest) per depth (the last repeats below).
+    acc_on_device=None asks the planner to choose the accumulator residency."""
     o = cqsa_plan_opts_default()
     o.B = B
     o.dtype = {"f32": CQSA_F32, "f16": CQSA_F16, "bf16": CQSA_BF16}[dtype]
@@ -150,7 +153,7 @@ def make_opts(B=1, dtype="bf16", c=7, interest=(0, 1, 3), depth=-1, min_depth=1,
         o.interest[i] = interest[i] if i < len(interest) else 0
     o.depth, o.min_depth, o.max_depth, o.n_slots = depth, min_depth, max_depth, n_slots
     o.inputs_on_device = int(bool(inputs_on_device))
-    o.acc_on_device = int(bool(acc_on_device))
+    o.acc_on_device = -1 if acc_on_device is None else int(bool(acc_on_device))
     o.with_backward = int(bool(with_backward))
     o.tasks_per_slot = int(tasks_per_slot)
     if levels:
@@ -193,6 +196,10 @@ class Plan:
     @property
     def tasks_per_slot(self):
         return lib().cqsa_plan_tasks_per_slot(self.handle)
+
+    @property
+    def acc_on_device(self):
+        return lib().cqsa_plan_acc_on_device(self.handle)
 
     def task(self, t):
         """Task t as a dict of plain Python values."""

@@ -23,7 +23,7 @@ COMMON = [
     "-I", INCLUDE, "-I", CSRC, "-Wall", "-Wno-unused-function",
 ]
 SOURCES = [
-    "plan.cpp", "capi_plan.cpp", "runtime.cpp", "fwd_driver.cpp", "bwd_driver.cpp",
+    "plan.cpp", "capi_plan.cpp", "runtime.cpp", "fwd_driver.cpp", "bwd_driver.cpp", "guard.cpp",
     "attn_fwd.hip", "merge.hip", "attn_bwd.hip", "stage.hip",
 ]
 

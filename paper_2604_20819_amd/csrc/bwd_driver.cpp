@@ -13,6 +13,7 @@
 #include <algorithm>
 #include <cmath>
 
+#include "guard.hpp"
 #include "kernels.hpp"
 #include "runtime.hpp"
 
@@ -76,6 +77,7 @@ cqsa_status backward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa
   Workspace ws;
   if ((s = acquire_workspace(C, total, &ws)) != CQSA_OK) return s;
   rec.stats.workspace_bytes = total;
+  rec.stats.resident_tasks = direct ? 0 : nslot;
   char* base = (char*)ws.ptr;
   char* d_tab = base;
   float* d_D = (float*)(base + tab_bytes);
@@ -212,8 +214,10 @@ extern "C" cqsa_status cqsa_backward(const cqsa_plan_t* plan, const cqsa_tensor*
                                      cqsa_tensor* dV, float scale, void* hip_stream) {
   cqsa::clear_error();
   try {
-    return cqsa::backward_impl(plan, Q, K, V, O, LSE, lse_where, dO, dQ, dK, dV, scale,
+    return cqsa::run_guarded(plan, true, [&](const cqsa_plan_t* q) {
+      return cqsa::backward_impl(q, Q, K, V, O, LSE, lse_where, dO, dQ, dK, dV, scale,
                                (hipStream_t)hip_stream);
+    });
   } catch (const std::exception& e) {
     return cqsa::fail(CQSA_ERR_INTERNAL, std::string("cqsa_backward: ") + e.what());
   } catch (...) {

@@ -100,17 +100,25 @@ cqsa_status cqsa_plan(int64_t L, int32_t H, int32_t d, int32_t causal,
       p->tasks = std::move(tasks);
       return ok;
     };
-    if (o.depth >= 0) {
-      plan_depth(o.depth, build_tasks(L, o, o.depth));
-    } else {
-      bool found = false;
-      for (int32_t dep = o.min_depth; dep <= o.max_depth && !found; ++dep)
-        found = plan_depth(dep, build_tasks(L, o, dep));
-      if (!found) {
-        delete p;
-        return fail(CQSA_ERR_BUDGET,
-                    "cqsa_plan: no depth in [min_depth, max_depth] fits the device budget");
+    // residency (App. A.3): an automatic acc_on_device keeps the accumulator
+    // on the device when some depth fits the budget there, else on the host
+    const bool auto_acc = o.acc_on_device < 0;
+    bool found = false;
+    for (int32_t acc = auto_acc ? 1 : o.acc_on_device; acc >= (auto_acc ? 0 : o.acc_on_device) && !found;
+         --acc) {
+      o.acc_on_device = acc;
+      p->opts.acc_on_device = acc;
+      if (o.depth >= 0) {
+        found = plan_depth(o.depth, build_tasks(L, o, o.depth)) || !auto_acc || acc == 0;
+      } else {
+        for (int32_t dep = o.min_depth; dep <= o.max_depth && !found; ++dep)
+          found = plan_depth(dep, build_tasks(L, o, dep));
       }
+    }
+    if (!found) {
+      delete p;
+      return fail(CQSA_ERR_BUDGET,
+                  "cqsa_plan: no depth in [min_depth, max_depth] fits the device budget");
     }
     p->max_L_local = 0;
     size_t max_runs = 0;
@@ -132,6 +140,8 @@ cqsa_status cqsa_plan(int64_t L, int32_t H, int32_t d, int32_t causal,
 }
 
 int32_t cqsa_plan_depth(const cqsa_plan_t* p) { return p ? p->depth : -1; }
+
+int32_t cqsa_plan_acc_on_device(const cqsa_plan_t* p) { return p ? p->opts.acc_on_device : -1; }
 
 int64_t cqsa_plan_num_tasks(const cqsa_plan_t* p) { return p ? int64_t(p->tasks.size()) : -1; }
 

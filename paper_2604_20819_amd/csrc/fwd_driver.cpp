@@ -24,6 +24,7 @@
 #include <functional>
 #include <thread>
 
+#include "guard.hpp"
 #include "kernels.hpp"
 #include "runtime.hpp"
 
@@ -216,6 +217,7 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
   Workspace ws;
   if ((s = acquire_workspace(C, total, &ws)) != CQSA_OK) return s;
   rec.stats.workspace_bytes = total;
+  rec.stats.resident_tasks = direct ? 0 : fwd_subslots(ntask, int32_t(gsz), o.n_slots);
   char* base = (char*)ws.ptr;
   char* d_tab = base;
   float* d_gl = gl_bytes ? (float*)(base + tab_bytes) : nullptr;
@@ -443,7 +445,9 @@ extern "C" cqsa_status cqsa_forward(const cqsa_plan_t* plan, const cqsa_tensor* 
                                     void* hip_stream) {
   cqsa::clear_error();
   try {
-    return cqsa::forward_impl(plan, Q, K, V, O, LSE, lse_where, scale, (hipStream_t)hip_stream);
+    return cqsa::run_guarded(plan, false, [&](const cqsa_plan_t* q) {
+      return cqsa::forward_impl(q, Q, K, V, O, LSE, lse_where, scale, (hipStream_t)hip_stream);
+    });
   } catch (const std::exception& e) {
     return cqsa::fail(CQSA_ERR_INTERNAL, std::string("cqsa_forward: ") + e.what());
   } catch (...) {

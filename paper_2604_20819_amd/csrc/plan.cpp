@@ -109,13 +109,13 @@ cqsa_status validate_plan_args(int64_t L, int32_t H, int32_t d, const cqsa_plan_
   if (o.n_slots < 1) return bad(CQSA_ERR_INVALID_ARG, "n_slots must be >= 1");
   if (o.inputs_on_device != 0 && o.inputs_on_device != 1)
     return bad(CQSA_ERR_INVALID_ARG, "inputs_on_device must be 0 or 1");
-  if (o.acc_on_device != 0 && o.acc_on_device != 1)
-    return bad(CQSA_ERR_INVALID_ARG, "acc_on_device must be 0 or 1");
+  if (o.acc_on_device < -1 || o.acc_on_device > 1)
+    return bad(CQSA_ERR_INVALID_ARG, "acc_on_device must be -1 (auto), 0 or 1");
   if (o.tasks_per_slot < 0 || o.tasks_per_slot > kMaxContrib)
     return bad(CQSA_ERR_INVALID_ARG, "tasks_per_slot must be in [0, 32]");
-  if (o.tasks_per_slot > 1 && !o.acc_on_device)
+  if (o.tasks_per_slot > 1 && o.acc_on_device != 1)
     return bad(CQSA_ERR_UNSUPPORTED, "tasks_per_slot > 1 needs the accumulator on the device");
-  if (o.with_backward && (!o.inputs_on_device || !o.acc_on_device))
+  if (o.with_backward && (!o.inputs_on_device || o.acc_on_device != 1))
     return bad(CQSA_ERR_UNSUPPORTED, "the backward supports device-resident tensors only");
   if (o.with_backward && o.dtype == CQSA_F32)
     return bad(CQSA_ERR_UNSUPPORTED, "the backward supports fp16 and bf16 inputs only");

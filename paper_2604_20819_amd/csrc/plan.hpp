@@ -3,6 +3,7 @@
 #pragma once
 
 #include <cstdint>
+#include <memory>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -98,6 +99,10 @@ struct cqsa_plan_s {
   // lazily computed census
   mutable std::once_flag census_once;
   mutable int64_t census[3] = {0, 0, 0};
+  // OOM guardrail (Sec. 3.4): the fallback plans that last succeeded after
+  // an allocation failure under an automatic depth, reused by later calls
+  mutable std::mutex guard_mu;
+  mutable std::unique_ptr<cqsa_plan_s> guard_fwd, guard_bwd;
 };
 
 namespace cqsa {

@@ -84,6 +84,25 @@ def test_level_set_errors(levels, depth, status, msg):
     assert e.value.status == -1
 
 
+def test_automatic_accumulator_residency():
+    """App. A.3: residency moves the accumulator off the device when no depth
+    fits the budget with it there.  The 1M-token bf16 call with host inputs
+    and a 4 GB budget cannot hold its 4.3 GB fp32 output on the device."""
+    GB = 10 ** 9
+    p = cq.cqsa_plan(32768, 16, 128, False, 0, cq.make_opts(acc_on_device=None))
+    assert p.acc_on_device == 1 and p.depth == 1
+    p = cq.cqsa_plan(1 << 20, 8, 128, False, 4 * GB,
+                     cq.make_opts(acc_on_device=None, inputs_on_device=False))
+    assert p.acc_on_device == 0 and p.depth == 2 and p.modelled_device_bytes <= 4 * GB
+    # a forced depth keeps the device when it fits there, else goes to the host
+    p = cq.cqsa_plan(1 << 20, 8, 128, False, 4 * GB,
+                     cq.make_opts(acc_on_device=None, inputs_on_device=False, depth=3))
+    assert p.acc_on_device == 0 and p.depth == 3
+    with pytest.raises(cq.CqsaError) as e:
+        cq.cqsa_plan(4096, 4, 128, False, 0, cq.make_opts(acc_on_device=None, with_backward=True))
+    assert e.value.status == -2
+
+
 def test_struct_layouts_match_the_header(tmp_path):
     """The binding's ctypes mirrors have the sizes and field offsets of the C
     structs in include/cqsa.h (checked by compiling the header with gcc)."""
@@ -95,7 +114,8 @@ def test_struct_layouts_match_the_header(tmp_path):
               "cqsa_interest_set": ["c", "l", "interest"],
               "cqsa_tensor": ["data", "B", "d"], "cqsa_task": ["quorum", "runs", "block_and"],
               "cqsa_run": ["global_start", "bits"],
-              "cqsa_run_stats": ["num_tasks", "ms_wall", "tiles_mixed", "ms_inner_busy"]}
+              "cqsa_run_stats": ["num_tasks", "ms_wall", "tiles_mixed", "ms_inner_busy",
+                                 "guard_steps", "resident_tasks"]}
     lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "cqsa.h"', "int main(void) {"]
     for st, fields in checks.items():
         lines.append(f'  printf("{st} %zu\\n", sizeof({st}));')
