@@ -27,18 +27,28 @@
 
 namespace cqsa {
 
+// LDS row of a K/V tile: d padded up to 64, 128 or 256 elements, so that a
+// row holds at least 8 swizzle slots and a 1 KB direct load covers whole rows.
+// The padding chunks are loaded (the neighbouring row's bytes, or zero past
+// the buffer range) and never read by a product.
+template <int D>
+constexpr int lds_row_elems() {
+  return D <= 64 ? 64 : (D <= 128 ? 128 : 256);
+}
+
 template <typename E, int D, int MODE>
-__global__ void __launch_bounds__(256, 2) attn_fwd_mfma(const FwdArgs a) {
+__global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_fwd_mfma(const FwdArgs a) {
   constexpr int BM = 128, BN = 64;
   // K and V tiles: unpadded rows of 2D bytes; 16-byte chunk ch of row r sits
   // in slot ch ^ swz(r), which keeps the K row reads and the V transpose
   // reads free of bank conflicts.  Tiles arrive by direct global-to-LDS
   // loads: one wave instruction fills 1 KB, lane i its i-th 16 bytes.
-  constexpr int RB = D * 2;              // row bytes
+  constexpr int DP = lds_row_elems<D>(); // LDS row elements (d padded)
+  constexpr int RB = DP * 2;             // LDS row bytes
   constexpr int KBYTES = BN * RB, VBYTES = BN * RB, STAGE = KBYTES + VBYTES;
   constexpr int DK = D / 16;             // k-steps of S^T = K Q^T
   constexpr int DB = D / 32;             // 32-wide d blocks of O^T
-  constexpr int CHUNKS = D / 8;          // 16-byte chunks per row
+  constexpr int CHUNKS = DP / 8;         // 16-byte chunks per LDS row
   constexpr int RPI = 64 / CHUNKS;       // rows per 1 KB load instruction
   constexpr int NDMA = BN / RPI / 4;     // load instructions per wave per tensor
   typedef typename E::vec8 vec8;
@@ -485,11 +495,23 @@ hipError_t launch_fwd(cqsa_dtype dt, int d, FwdMode mode, const FwdArgs& a, int6
                       hipStream_t s) {
   if (wgs <= 0) return hipSuccess;
   if (wgs > 0x7fffffff || a.ntask < 1) return hipErrorInvalidValue;
-  if (dt == CQSA_BF16)
-    return d == 128 ? launch_mfma<BF16, 128>(mode, a, wgs, s) : launch_mfma<BF16, 64>(mode, a, wgs, s);
-  if (dt == CQSA_F16)
-    return d == 128 ? launch_mfma<F16, 128>(mode, a, wgs, s) : launch_mfma<F16, 64>(mode, a, wgs, s);
-  return d == 128 ? launch_f32<128>(mode, a, wgs, s) : launch_f32<64>(mode, a, wgs, s);
+  switch (d) {
+#define CQSA_FWD_D(DD)                                                   \
+  case DD:                                                               \
+    if (dt == CQSA_BF16) return launch_mfma<BF16, DD>(mode, a, wgs, s);  \
+    if (dt == CQSA_F16) return launch_mfma<F16, DD>(mode, a, wgs, s);    \
+    return launch_f32<DD>(mode, a, wgs, s);
+    CQSA_FWD_D(32)
+    CQSA_FWD_D(64)
+    CQSA_FWD_D(96)
+    CQSA_FWD_D(128)
+    CQSA_FWD_D(160)
+    CQSA_FWD_D(192)
+    CQSA_FWD_D(224)
+    CQSA_FWD_D(256)
+#undef CQSA_FWD_D
+  }
+  return hipErrorInvalidValue;
 }
 
 }  // namespace cqsa

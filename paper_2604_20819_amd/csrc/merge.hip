@@ -130,10 +130,17 @@ hipError_t launch_combine(const CombineArgs& a, int64_t blocks, hipStream_t s) {
   if (blocks <= 0 || a.B <= 0) return hipSuccess;
   if (a.n_seg < 1 || blocks > 0x7fffffff || a.B > 65535) return hipErrorInvalidValue;
   const dim3 grid(unsigned(blocks), unsigned(a.B));
-  if (a.d == 128)
-    hipLaunchKernelGGL(combine_kernel<128>, grid, dim3(256), 0, s, a);
-  else
-    hipLaunchKernelGGL(combine_kernel<64>, grid, dim3(256), 0, s, a);
+  switch (a.d) {
+    case 32: hipLaunchKernelGGL(combine_kernel<32>, grid, dim3(256), 0, s, a); break;
+    case 64: hipLaunchKernelGGL(combine_kernel<64>, grid, dim3(256), 0, s, a); break;
+    case 96: hipLaunchKernelGGL(combine_kernel<96>, grid, dim3(256), 0, s, a); break;
+    case 128: hipLaunchKernelGGL(combine_kernel<128>, grid, dim3(256), 0, s, a); break;
+    case 160: hipLaunchKernelGGL(combine_kernel<160>, grid, dim3(256), 0, s, a); break;
+    case 192: hipLaunchKernelGGL(combine_kernel<192>, grid, dim3(256), 0, s, a); break;
+    case 224: hipLaunchKernelGGL(combine_kernel<224>, grid, dim3(256), 0, s, a); break;
+    case 256: hipLaunchKernelGGL(combine_kernel<256>, grid, dim3(256), 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 

@@ -80,7 +80,8 @@ cqsa_status validate_plan_args(int64_t L, int32_t H, int32_t d, const cqsa_plan_
   if (L > (int64_t(1) << 31) - 1) return bad(CQSA_ERR_UNSUPPORTED, "L must be < 2^31");
   if (H < 1) return bad(CQSA_ERR_INVALID_ARG, "H must be >= 1");
   if (d < 1) return bad(CQSA_ERR_INVALID_ARG, "d must be >= 1");
-  if (d != 64 && d != 128) return bad(CQSA_ERR_UNSUPPORTED, "head dim must be 64 or 128");
+  if (d % 32 != 0 || d > 256)
+    return bad(CQSA_ERR_UNSUPPORTED, "head dim must be one of 32, 64, ..., 256");
   if (o.B < 1) return bad(CQSA_ERR_INVALID_ARG, "B must be >= 1");
   if (dtype_size(o.dtype) == 0) return bad(CQSA_ERR_INVALID_ARG, "unknown dtype");
   if (o.n_level_sets < 0 || o.n_level_sets > CQSA_MAX_LEVEL_SETS)
@@ -119,6 +120,8 @@ cqsa_status validate_plan_args(int64_t L, int32_t H, int32_t d, const cqsa_plan_
     return bad(CQSA_ERR_UNSUPPORTED, "the backward supports device-resident tensors only");
   if (o.with_backward && o.dtype == CQSA_F32)
     return bad(CQSA_ERR_UNSUPPORTED, "the backward supports fp16 and bf16 inputs only");
+  if (o.with_backward && d != 64 && d != 128)
+    return bad(CQSA_ERR_UNSUPPORTED, "the backward supports head dims 64 and 128");
   return CQSA_OK;
 }
 

@@ -84,6 +84,21 @@ def test_level_set_errors(levels, depth, status, msg):
     assert e.value.status == -1
 
 
+@pytest.mark.parametrize("d", [32, 64, 96, 128, 160, 192, 224, 256])
+def test_forward_head_dims_accepted(d):
+    p = cq.cqsa_plan(1000, 2, d, False, 0, cq.make_opts(depth=1))
+    assert p.depth == 1 and p.num_tasks == 7
+
+
+@pytest.mark.parametrize("d,backward", [(48, False), (288, False), (0, False), (96, True),
+                                        (32, True), (256, True)])
+def test_head_dims_refused(d, backward):
+    """Forward: multiples of 32 up to 256; backward: 64 and 128 (Sec. 5)."""
+    with pytest.raises(cq.CqsaError) as e:
+        cq.cqsa_plan(1000, 2, d, False, 0, cq.make_opts(with_backward=backward))
+    assert e.value.status in (-1, -2)
+
+
 def test_automatic_accumulator_residency():
     """App. A.3: residency moves the accumulator off the device when no depth
     fits the budget with it there.  The 1M-token bf16 call with host inputs
@@ -161,7 +176,7 @@ def test_plan_rejects_bad_geometry():
         cq.cqsa_plan(0, 2, 64, False, 0)
     assert e.value.status == -1
     with pytest.raises(cq.CqsaError) as e:
-        cq.cqsa_plan(100, 2, 96, False, 0)
+        cq.cqsa_plan(100, 2, 80, False, 0)
     assert e.value.status == -2
     with pytest.raises(cq.CqsaError) as e:
         cq.cqsa_plan(100, 2, 64, False, 0, cq.make_opts(depth=9))

@@ -74,6 +74,32 @@ def test_small_grid_vs_oracle(dt, d, causal, L, depth):
     _check_vs_oracle(O, LSE, Q, K, V, causal, dt)
 
 
+HEAD_DIMS = [32, 96, 160, 192, 224, 256]
+
+
+@pytest.mark.parametrize("d", HEAD_DIMS)
+@pytest.mark.parametrize("dt", ["bf16", "f16", "f32"])
+def test_other_head_dims(d, dt):
+    """Sec. 5 (kernel coverage): the forward covers head dims 32 to 256.  Rows
+    of the K/V tiles are padded in LDS; the padding must never reach O.  A
+    ragged length, causal and non-causal, undecomposed and decomposed.
+
+    Max-abs bound: P is rounded to the input dtype before the P.V product
+    (reading 7), so each weight carries a relative error of at most the unit
+    roundoff u (2^-8 bf16, 2^-11 fp16) and a row of O at most u * max|V|.
+    Early causal rows average a few keys, where this bound is nearly reached;
+    with more elements per row (large d) it can exceed a flat 1e-2."""
+    need_gpu()
+    u = {"bf16": 2.0 ** -8, "f16": 2.0 ** -11}.get(dt)
+    for causal, L, depth in ((False, 700, 0), (True, 1150, 1), (False, 333, 2)):
+        say(f"head dim d={d} dt={dt} causal={causal} L={L} depth={depth}")
+        Q, K, V = synth.make_inputs(13 + d + L, 1, L, 3, d, dt)
+        O, LSE, plan = run_forward(Q, K, V, causal, depth=depth)
+        assert plan.depth == depth
+        atol = None if u is None else u * float(np.abs(synth.as_f64(V)).max()) + 1e-5
+        _check_vs_oracle(O, LSE, Q, K, V, causal, dt, atol=atol)
+
+
 @pytest.mark.parametrize("d,causal", [(64, True), (128, False)])
 def test_fp32_grid(d, causal):
     need_gpu()
