@@ -48,7 +48,8 @@ def parse():
                     help="target CPU time of the oracle sample")
     ap.add_argument("--workload", default="headline",
                     choices=["headline", "fp16_causal_L131072_8GB", "fp16_causal_L131072_8GB_c21",
-                             "bf16_causal_B2_L65536_fwdbwd_16GB", "bf16_streamed_L1M_host_4GB"],
+                             "bf16_causal_B2_L65536_fwdbwd_16GB", "bf16_streamed_L1M_host_4GB",
+                             "bf16_L32768_H16_head_dims"],
                     help="headline (default) or one of the other seeded workloads: "
                          "their rates, depths and runtime ratios, one JSON line each")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
@@ -257,6 +258,38 @@ def other_workload(name, args):
     print(json.dumps(line), flush=True)
 
 
+def headdim_sweep(args):
+    """Forward rate at every head dim the forward takes (32 .. 256): bf16,
+    B=1 H=16 L=32768 non-causal, CQS depth 1 and undecomposed; one JSON line."""
+    import torch
+
+    import paper_2604_20819_amd as cq
+    from paper_2604_20819_amd import synth
+
+    B, L, H = 1, 32768, 16
+    out = {"workload": "bf16_L32768_H16_head_dims", "B": B, "L": L, "H": H, "causal": False,
+           "dtype": "bf16", "per_d": []}
+    steps = max(3, args.steps // 4)
+    for d in (32, 64, 96, 128, 160, 192, 224, 256):
+        print(f"[workload] head dim {d}", file=sys.stderr, flush=True)
+        Q, K, V = synth.make_inputs(20819 + d, B, L, H, d, "bf16")
+        q, k, v = (x.cuda() for x in (Q, K, V))
+        O = torch.empty((B, L, H, d), dtype=torch.float32, device="cuda")
+        LSE = torch.empty((B, H, L), dtype=torch.float32, device="cuda")
+        flops = 4.0 * d * B * H * L * L
+        row = {"d": d}
+        for depth in (1, 0):
+            plan = cq.cqsa_plan(L, H, d, False, 0, cq.make_opts(B=B, dtype="bf16", depth=depth))
+            ms, _ = time_steps(lambda: cq.cqsa_forward(plan, q, k, v, O, LSE), steps, 1, torch)
+            row["depth1_tflops" if depth else "undecomposed_tflops"] = round(flops / (ms * 1e-3) / 1e12, 2)
+            row["depth1_ms" if depth else "undecomposed_ms"] = round(ms, 3)
+        row["fwd_runtime_ratio"] = round(row["depth1_ms"] / row["undecomposed_ms"], 4)
+        out["per_d"].append(row)
+        del q, k, v, O, LSE
+        torch.cuda.empty_cache()
+    print(json.dumps(out), flush=True)
+
+
 def task_rows(plan):
     return [plan.task(t)["L_local"] for t in range(plan.num_tasks)]
 
@@ -270,7 +303,10 @@ def main():
         if args.gpus != 1:
             print("bench.py runs on one GPU only", file=sys.stderr)
             sys.exit(2)
-        other_workload(args.workload, args)
+        if args.workload == "bf16_L32768_H16_head_dims":
+            headdim_sweep(args)
+        else:
+            other_workload(args.workload, args)
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
