@@ -259,8 +259,9 @@ def other_workload(name, args):
 
 
 def headdim_sweep(args):
-    """Forward rate at every head dim the forward takes (32 .. 256): bf16,
-    B=1 H=16 L=32768 non-causal, CQS depth 1 and undecomposed; one JSON line."""
+    """Forward and forward+backward rates at every head dim (32 .. 256):
+    bf16, B=1 H=16 L=32768 non-causal, CQS depth 1 and undecomposed; one JSON
+    line."""
     import torch
 
     import paper_2604_20819_amd as cq
@@ -272,20 +273,31 @@ def headdim_sweep(args):
     steps = max(3, args.steps // 4)
     for d in (32, 64, 96, 128, 160, 192, 224, 256):
         print(f"[workload] head dim {d}", file=sys.stderr, flush=True)
-        Q, K, V = synth.make_inputs(20819 + d, B, L, H, d, "bf16")
-        q, k, v = (x.cuda() for x in (Q, K, V))
+        Q, K, V, dO = synth.make_inputs(20819 + d, B, L, H, d, "bf16", with_dO=True)
+        q, k, v, do = (x.cuda() for x in (Q, K, V, dO))
         O = torch.empty((B, L, H, d), dtype=torch.float32, device="cuda")
         LSE = torch.empty((B, H, L), dtype=torch.float32, device="cuda")
+        dQ, dK, dV = (torch.empty((B, L, H, d), dtype=torch.float32, device="cuda") for _ in range(3))
         flops = 4.0 * d * B * H * L * L
         row = {"d": d}
         for depth in (1, 0):
-            plan = cq.cqsa_plan(L, H, d, False, 0, cq.make_opts(B=B, dtype="bf16", depth=depth))
+            plan = cq.cqsa_plan(L, H, d, False, 0,
+                                cq.make_opts(B=B, dtype="bf16", depth=depth, with_backward=True))
             ms, _ = time_steps(lambda: cq.cqsa_forward(plan, q, k, v, O, LSE), steps, 1, torch)
-            row["depth1_tflops" if depth else "undecomposed_tflops"] = round(flops / (ms * 1e-3) / 1e12, 2)
-            row["depth1_ms" if depth else "undecomposed_ms"] = round(ms, 3)
+            tag = "depth1" if depth else "undecomposed"
+            row[tag + "_tflops"] = round(flops / (ms * 1e-3) / 1e12, 2)
+            row[tag + "_ms"] = round(ms, 3)
+
+            def fb():
+                cq.cqsa_forward(plan, q, k, v, O, LSE)
+                cq.cqsa_backward(plan, q, k, v, O, LSE, do, dQ, dK, dV)
+            msb, _ = time_steps(fb, max(2, steps // 2), 1, torch)
+            row[tag + "_fwd_bwd_tflops"] = round(3.5 * flops / (msb * 1e-3) / 1e12, 2)
+            row[tag + "_fwd_bwd_ms"] = round(msb, 3)
         row["fwd_runtime_ratio"] = round(row["depth1_ms"] / row["undecomposed_ms"], 4)
+        row["fwd_bwd_runtime_ratio"] = round(row["depth1_fwd_bwd_ms"] / row["undecomposed_fwd_bwd_ms"], 4)
         out["per_d"].append(row)
-        del q, k, v, O, LSE
+        del q, k, v, do, O, LSE, dQ, dK, dV
         torch.cuda.empty_cache()
     print(json.dumps(out), flush=True)
 

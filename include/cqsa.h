@@ -19,10 +19,10 @@
  *   - Outputs O, dQ, dK, dV are fp32 and LSE is the natural-log log-sum-exp
  *     of the scaled scores (Section 4.1: statistics, merge and output are
  *     fp32; App. A.1: lse = m + log l).
- *   - Inputs are fp32, fp16 or bf16.  Head dimension d: the forward takes
- *     32, 64, 96, ..., 256 (the head dims the paper's forward covers, Sec. 5,
- *     kernel coverage);
- *     the backward takes 64 and 128, as the paper's does.
+ *   - Inputs are fp32, fp16 or bf16.  Head dimension d: 32, 64, 96, ..., 256
+ *     for the forward (the head dims the paper's forward covers, Sec. 5,
+ *     kernel coverage) and for the backward (the paper's backward stops at
+ *     64 and 128 and names the wider range as needed for production).
  *   - Calls on device-resident outputs are ordered on `hip_stream` (a
  *     hipStream_t; NULL = the null stream) and return without waiting;
  *     a call with any host-resident output blocks until it is complete.

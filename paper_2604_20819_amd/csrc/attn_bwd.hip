@@ -25,15 +25,16 @@ namespace cqsa {
 constexpr float kLog2e = 1.4426950408889634f;
 
 template <typename E, int D>
-__global__ void __launch_bounds__(256, 2) attn_bwd_dq(const BwdArgs a) {
+__global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_bwd_dq(const BwdArgs a) {
   constexpr int BM = 128, BN = 64;
-  // K and V tiles: unpadded rows of 2D bytes with the forward's swizzle
-  // (chunk ch of row r in slot ch ^ swz(r)), free of bank conflicts for the
-  // K and V row reads and the K transpose reads; filled by direct
-  // buffer-to-LDS loads (lane i's 16 bytes at +16 i of a 1 KB block).
-  constexpr int RB = D * 2;
+  // K and V tiles: rows of DP elements (d padded as in the forward) with the
+  // forward's swizzle (chunk ch of row r in slot ch ^ swz(r)), free of bank
+  // conflicts for the K and V row reads and the K transpose reads; filled by
+  // direct buffer-to-LDS loads (lane i's 16 bytes at +16 i of a 1 KB block).
+  constexpr int DP = lds_row_elems<D>();
+  constexpr int RB = DP * 2;
   constexpr int KBYTES = BN * RB, VBYTES = BN * RB, STAGE = KBYTES + VBYTES;
-  constexpr int DK = D / 16, DB = D / 32, CHUNKS = D / 8;
+  constexpr int DK = D / 16, DB = D / 32, CHUNKS = DP / 8;
   constexpr int RPI = 64 / CHUNKS, NDMA = BN / RPI / 4;
   typedef typename E::vec8 vec8;
   auto swz = [](int r) { return 2 * (r & 3) + ((r >> 2) & 1); };
@@ -272,15 +273,17 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dq(const BwdArgs a) {
 }
 
 template <typename E, int D>
-__global__ void __launch_bounds__(256, 2) attn_bwd_dkdv(const BwdArgs a) {
+__global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_bwd_dkdv(const BwdArgs a) {
   // 32-query tiles (two per 64-token summary block) keep the registers and
-  // LDS within two work groups per CU
+  // LDS within two work groups per CU (one above d = 128)
   constexpr int BK = 128, BQ = 32;
-  // Q and dO tiles: unpadded rows of 2D bytes with the forward's swizzle
-  // (chunk ch of row r in slot ch ^ swz(r)), conflict-free for the row reads
-  // and the transpose reads; filled by direct buffer-to-LDS loads
-  constexpr int P2 = D * 2;
-  constexpr int DK = D / 16, DB = D / 32, CHUNKS = D / 8;
+  // Q and dO tiles: rows of DP elements (d padded as in the forward) with
+  // the forward's swizzle (chunk ch of row r in slot ch ^ swz(r)),
+  // conflict-free for the row reads and the transpose reads; filled by
+  // direct buffer-to-LDS loads
+  constexpr int DP = lds_row_elems<D>();
+  constexpr int P2 = DP * 2;
+  constexpr int DK = D / 16, DB = D / 32, CHUNKS = DP / 8;
   constexpr int RPI = 64 / CHUNKS, NDMA = BQ / RPI / 4;
   typedef typename E::vec8 vec8;
   auto swz = [](int r) { return 2 * (r & 3) + ((r >> 2) & 1); };
@@ -579,18 +582,30 @@ static hipError_t launch_dkdv_t(const BwdArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+#define CQSA_BWD_SWITCH(LAUNCH)                                        \
+  switch (d) {                                                         \
+    case 32: return dt == CQSA_BF16 ? LAUNCH<BF16, 32>(a, s) : LAUNCH<F16, 32>(a, s);    \
+    case 64: return dt == CQSA_BF16 ? LAUNCH<BF16, 64>(a, s) : LAUNCH<F16, 64>(a, s);    \
+    case 96: return dt == CQSA_BF16 ? LAUNCH<BF16, 96>(a, s) : LAUNCH<F16, 96>(a, s);    \
+    case 128: return dt == CQSA_BF16 ? LAUNCH<BF16, 128>(a, s) : LAUNCH<F16, 128>(a, s); \
+    case 160: return dt == CQSA_BF16 ? LAUNCH<BF16, 160>(a, s) : LAUNCH<F16, 160>(a, s); \
+    case 192: return dt == CQSA_BF16 ? LAUNCH<BF16, 192>(a, s) : LAUNCH<F16, 192>(a, s); \
+    case 224: return dt == CQSA_BF16 ? LAUNCH<BF16, 224>(a, s) : LAUNCH<F16, 224>(a, s); \
+    case 256: return dt == CQSA_BF16 ? LAUNCH<BF16, 256>(a, s) : LAUNCH<F16, 256>(a, s); \
+  }                                                                    \
+  return hipErrorInvalidValue;
+
 hipError_t launch_bwd_dq(cqsa_dtype dt, int d, const BwdArgs& a, hipStream_t s) {
   if (a.n_runs > kMaxRuns) return hipErrorInvalidValue;
-  if (dt == CQSA_BF16) return d == 128 ? launch_dq_t<BF16, 128>(a, s) : launch_dq_t<BF16, 64>(a, s);
-  if (dt == CQSA_F16) return d == 128 ? launch_dq_t<F16, 128>(a, s) : launch_dq_t<F16, 64>(a, s);
-  return hipErrorInvalidValue;
+  if (dt != CQSA_BF16 && dt != CQSA_F16) return hipErrorInvalidValue;
+  CQSA_BWD_SWITCH(launch_dq_t)
 }
 
 hipError_t launch_bwd_dkdv(cqsa_dtype dt, int d, const BwdArgs& a, hipStream_t s) {
   if (a.n_runs > kMaxRuns) return hipErrorInvalidValue;
-  if (dt == CQSA_BF16) return d == 128 ? launch_dkdv_t<BF16, 128>(a, s) : launch_dkdv_t<BF16, 64>(a, s);
-  if (dt == CQSA_F16) return d == 128 ? launch_dkdv_t<F16, 128>(a, s) : launch_dkdv_t<F16, 64>(a, s);
-  return hipErrorInvalidValue;
+  if (dt != CQSA_BF16 && dt != CQSA_F16) return hipErrorInvalidValue;
+  CQSA_BWD_SWITCH(launch_dkdv_t)
 }
+#undef CQSA_BWD_SWITCH
 
 }  // namespace cqsa

@@ -27,15 +27,6 @@
 
 namespace cqsa {
 
-// LDS row of a K/V tile: d padded up to 64, 128 or 256 elements, so that a
-// row holds at least 8 swizzle slots and a 1 KB direct load covers whole rows.
-// The padding chunks are loaded (the neighbouring row's bytes, or zero past
-// the buffer range) and never read by a product.
-template <int D>
-constexpr int lds_row_elems() {
-  return D <= 64 ? 64 : (D <= 128 ? 128 : 256);
-}
-
 template <typename E, int D, int MODE>
 __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_fwd_mfma(const FwdArgs a) {
   constexpr int BM = 128, BN = 64;

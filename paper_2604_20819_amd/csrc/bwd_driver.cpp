@@ -29,8 +29,8 @@ cqsa_status backward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa
     return fail(CQSA_ERR_UNSUPPORTED, "cqsa_backward: device-resident plans only");
   if (o.dtype == CQSA_F32)
     return fail(CQSA_ERR_UNSUPPORTED, "cqsa_backward: fp16 and bf16 inputs only");
-  if (p->g.d != 64 && p->g.d != 128)
-    return fail(CQSA_ERR_UNSUPPORTED, "cqsa_backward: head dims 64 and 128 only");
+  if (p->g.d % 32 != 0 || p->g.d > 256)
+    return fail(CQSA_ERR_UNSUPPORTED, "cqsa_backward: head dims 32, 64, ..., 256 only");
   if (!o.with_backward && p->budget != 0)
     return fail(CQSA_ERR_INVALID_ARG,
                 "cqsa_backward: the plan's budget was fitted without the backward "

@@ -84,6 +84,15 @@ __device__ __forceinline__ typename E::vec8 lds_tr_pair(const char* p0, const ch
   return __builtin_bit_cast(typename E::vec8, u);
 }
 
+// LDS row of a K/V tile: d padded up to 64, 128 or 256 elements, so that a
+// row holds at least 8 swizzle slots and a 1 KB direct load covers whole rows.
+// The padding chunks are loaded (the neighbouring row's bytes, or zero past
+// the buffer range) and never read by a product.
+template <int D>
+constexpr int lds_row_elems() {
+  return D <= 64 ? 64 : (D <= 128 ? 128 : 256);
+}
+
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // Value held by lane l^32 (the other half of the wave).

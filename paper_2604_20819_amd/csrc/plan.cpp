@@ -120,8 +120,6 @@ cqsa_status validate_plan_args(int64_t L, int32_t H, int32_t d, const cqsa_plan_
     return bad(CQSA_ERR_UNSUPPORTED, "the backward supports device-resident tensors only");
   if (o.with_backward && o.dtype == CQSA_F32)
     return bad(CQSA_ERR_UNSUPPORTED, "the backward supports fp16 and bf16 inputs only");
-  if (o.with_backward && d != 64 && d != 128)
-    return bad(CQSA_ERR_UNSUPPORTED, "the backward supports head dims 64 and 128");
   return CQSA_OK;
 }
 

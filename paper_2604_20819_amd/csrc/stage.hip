@@ -75,22 +75,29 @@ hipError_t launch_bwd_preprocess(const void* dO, const float* O, float* D, cqsa_
   const int64_t rows = B * L * H;
   const unsigned blocks = unsigned((rows * 16 + 255) / 256);
   if (rows == 0) return hipSuccess;
-  if (dt == CQSA_BF16) {
-    if (d == 128)
-      hipLaunchKernelGGL((preprocess_kernel<__bf16, 128>), dim3(blocks), dim3(256), 0, s,
-                         (const __bf16*)dO, O, D, B, L, H);
-    else
-      hipLaunchKernelGGL((preprocess_kernel<__bf16, 64>), dim3(blocks), dim3(256), 0, s,
-                         (const __bf16*)dO, O, D, B, L, H);
-  } else if (dt == CQSA_F16) {
-    if (d == 128)
-      hipLaunchKernelGGL((preprocess_kernel<_Float16, 128>), dim3(blocks), dim3(256), 0, s,
-                         (const _Float16*)dO, O, D, B, L, H);
-    else
-      hipLaunchKernelGGL((preprocess_kernel<_Float16, 64>), dim3(blocks), dim3(256), 0, s,
-                         (const _Float16*)dO, O, D, B, L, H);
-  } else {
-    return hipErrorInvalidValue;
+  switch (d) {
+#define CQSA_PRE_D(DD)                                                                   \
+  case DD:                                                                               \
+    if (dt == CQSA_BF16)                                                                 \
+      hipLaunchKernelGGL((preprocess_kernel<__bf16, DD>), dim3(blocks), dim3(256), 0, s, \
+                         (const __bf16*)dO, O, D, B, L, H);                              \
+    else if (dt == CQSA_F16)                                                             \
+      hipLaunchKernelGGL((preprocess_kernel<_Float16, DD>), dim3(blocks), dim3(256), 0,  \
+                         s, (const _Float16*)dO, O, D, B, L, H);                         \
+    else                                                                                 \
+      return hipErrorInvalidValue;                                                       \
+    break;
+    CQSA_PRE_D(32)
+    CQSA_PRE_D(64)
+    CQSA_PRE_D(96)
+    CQSA_PRE_D(128)
+    CQSA_PRE_D(160)
+    CQSA_PRE_D(192)
+    CQSA_PRE_D(224)
+    CQSA_PRE_D(256)
+#undef CQSA_PRE_D
+    default:
+      return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }

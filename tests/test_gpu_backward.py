@@ -96,6 +96,26 @@ def test_small_grid_vs_oracle(dt, d, causal, L, depth):
     _check_grads((dQ, dK, dV), oracle_grads(Q, K, V, dO, causal), dt, atol_zero=bound)
 
 
+@pytest.mark.parametrize("d", [32, 96, 160, 192, 224, 256])
+@pytest.mark.parametrize("dt", ["bf16", "f16"])
+def test_other_head_dims(d, dt):
+    """Head dims beyond the paper's backward (64, 128; Sec. 5 names the wider
+    range as needed for production): full gradients against float64, and the
+    decomposed gradients against the undecomposed ones."""
+    need_gpu()
+    for causal, L, depth in ((True, 700, 1), (False, 1100, 2)):
+        say(f"bwd head dim d={d} dt={dt} causal={causal} L={L} depth={depth}")
+        Q, K, V, dO = synth.make_inputs(17 + L + d, 1, L, 2, d, dt, with_dO=True)
+        got = run_fwd_bwd(Q, K, V, dO, causal, depth=depth)
+        assert got[-1].depth == depth
+        _check_grads(got[2:5], oracle_grads(Q, K, V, dO, causal), dt)
+        ref = run_fwd_bwd(Q, K, V, dO, causal, depth=0)
+        for name, i in (("dQ", 2), ("dK", 3), ("dV", 4)):
+            r = rel_l2(got[i].numpy(), ref[i].numpy())
+            say(f"{name} vs depth 0: {r:.3e}")
+            assert r <= 1e-3
+
+
 @pytest.mark.parametrize("dt,causal", [("bf16", True), ("f16", False)])
 def test_decomposed_matches_undecomposed(dt, causal):
     need_gpu()
