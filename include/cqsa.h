@@ -26,8 +26,10 @@
  *   - Calls on device-resident outputs are ordered on `hip_stream` (a
  *     hipStream_t; NULL = the null stream) and return without waiting;
  *     a call with any host-resident output blocks until it is complete.
- *   - The library is thread-safe for distinct plans and streams; a plan is
- *     immutable after creation and may be shared.
+ *   - The library is thread-safe for distinct plans and streams; a plan's
+ *     decomposition is immutable after creation and the plan may be shared
+ *     across threads (the only state a call may change is the OOM
+ *     guardrail's cached fallback, which is guarded and reference-counted).
  */
 #ifndef CQSA_H
 #define CQSA_H

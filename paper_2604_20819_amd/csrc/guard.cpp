@@ -55,7 +55,7 @@ bool next_config(Config& c, bool backward, const cqsa_plan_opts& o) {
   return false;
 }
 
-std::unique_ptr<cqsa_plan_s> build(const cqsa_plan_t* p, const Config& c, std::string* err) {
+std::shared_ptr<const cqsa_plan_s> build(const cqsa_plan_t* p, const Config& c, std::string* err) {
   cqsa_plan_opts o = p->opts;
   o.depth = c.depth;
   o.tasks_per_slot = c.group;
@@ -67,7 +67,7 @@ std::unique_ptr<cqsa_plan_s> build(const cqsa_plan_t* p, const Config& c, std::s
     *err = last_error_cstr();
     return nullptr;
   }
-  return std::unique_ptr<cqsa_plan_s>(out);
+  return std::shared_ptr<const cqsa_plan_s>(out, [](const cqsa_plan_s* q) { delete q; });
 }
 
 }  // namespace
@@ -75,12 +75,12 @@ std::unique_ptr<cqsa_plan_s> build(const cqsa_plan_t* p, const Config& c, std::s
 cqsa_status run_guarded(const cqsa_plan_t* p, bool backward,
                         const std::function<cqsa_status(const cqsa_plan_t*)>& run) {
   if (!p) return run(p);
-  const cqsa_plan_t* start = p;
+  std::shared_ptr<const cqsa_plan_s> cached;  // keeps the fallback alive for this call
   {
     std::lock_guard<std::mutex> g(p->guard_mu);
-    const auto& cached = backward ? p->guard_bwd : p->guard_fwd;
-    if (cached) start = cached.get();
+    cached = backward ? p->guard_bwd : p->guard_fwd;
   }
+  const cqsa_plan_t* start = cached ? cached.get() : p;
   cqsa_status s = run(start);
   if (s != CQSA_ERR_DEVICE_OOM || p->opts.depth >= 0) {
     if (s == CQSA_OK) call_record().stats.guard_steps = 0;
@@ -92,7 +92,7 @@ cqsa_status run_guarded(const cqsa_plan_t* p, bool backward,
   while (next_config(c, backward, p->opts)) {
     ++steps;
     std::string err;
-    std::unique_ptr<cqsa_plan_s> fb = build(p, c, &err);
+    std::shared_ptr<const cqsa_plan_s> fb = build(p, c, &err);
     if (!fb) return fail(CQSA_ERR_INTERNAL, "OOM guardrail: re-planning failed: " + err);
     c = config_of(fb.get());
     clear_error();

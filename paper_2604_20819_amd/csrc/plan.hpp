@@ -100,9 +100,11 @@ struct cqsa_plan_s {
   mutable std::once_flag census_once;
   mutable int64_t census[3] = {0, 0, 0};
   // OOM guardrail (Sec. 3.4): the fallback plans that last succeeded after
-  // an allocation failure under an automatic depth, reused by later calls
+  // an allocation failure under an automatic depth, reused by later calls.
+  // Shared, so a call keeps its fallback alive while another call on the
+  // same plan replaces the cached one.
   mutable std::mutex guard_mu;
-  mutable std::unique_ptr<cqsa_plan_s> guard_fwd, guard_bwd;
+  mutable std::shared_ptr<const cqsa_plan_s> guard_fwd, guard_bwd;
 };
 
 namespace cqsa {
