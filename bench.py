@@ -181,11 +181,12 @@ def other_workload(name, args):
     pairs = Lw * (Lw + 1) // 2 if causal else Lw * Lw
     flops = 4.0 * dw * Bw * Hw * pairs
 
-    def plan_for(depth=-1, budget=spec["budget"], backward=spec["bwd"]):
+    def plan_for(depth=-1, budget=spec["budget"], backward=spec["bwd"], in_place=None):
         return cq.cqsa_plan(Lw, Hw, dw, causal, budget,
                             cq.make_opts(B=Bw, dtype=spec["dt"], depth=depth,
                                          inputs_on_device=not host, acc_on_device=not host,
-                                         with_backward=backward, levels=spec.get("levels")))
+                                         with_backward=backward, levels=spec.get("levels"),
+                                         read_in_place=in_place))
 
     cq.cqsa_set_timing(True)
     steps = 2 if host else max(3, args.steps // 4)
@@ -206,8 +207,9 @@ def other_workload(name, args):
             "dtype": spec["dt"], "budget_bytes": spec["budget"], "depth": plan.depth,
             "interest_sets": [c for c, _ in spec.get("levels", [(7, None)])],
             "tasks": plan.num_tasks, "tasks_per_launch": plan.tasks_per_slot,
+            "reads_in_place": plan.reads_in_place,
             "max_task_tokens": max(task_rows(plan)),
-            "staged_tokens": sum(task_rows(plan)),
+            "task_tokens": sum(task_rows(plan)),
             "modelled_device_bytes": plan.modelled_device_bytes,
             "workspace_bytes": s["workspace_bytes"],
             # what the call holds on the device: the library's workspace plus the
@@ -234,6 +236,14 @@ def other_workload(name, args):
         line.update({"undecomposed_fwd_ms": round(ms0, 3),
                      "undecomposed_modelled_bytes": und.modelled_device_bytes,
                      "fwd_runtime_ratio": round(ms / ms0, 4)})
+        # the same budget when every task's runs are gathered into staging
+        # slots first: the depth it forces and its rate
+        stp = plan_for(in_place=False)
+        ms_s, _ = time_steps(fwd(stp), steps, warm, torch)
+        line.update({"staged_depth": stp.depth, "staged_tasks": stp.num_tasks,
+                     "staged_modelled_device_bytes": stp.modelled_device_bytes,
+                     "staged_fwd_ms": round(ms_s, 3),
+                     "staged_fwd_tflops": round(flops / (ms_s * 1e-3) / 1e12, 2)})
         if spec["bwd"]:
             do = ins[3].cuda()
             dQ, dK, dV = (torch.empty((Bw, Lw, Hw, dw), dtype=torch.float32, device="cuda")
@@ -248,6 +258,8 @@ def other_workload(name, args):
             msb, stb = time_steps(fb(plan), steps, warm, torch)
             und_b = plan_for(depth=0, budget=0, backward=True)
             msb0, _ = time_steps(fb(und_b), steps, warm, torch)
+            msb_s, _ = time_steps(fb(stp), steps, warm, torch)
+            line.update({"staged_fwd_bwd_ms": round(msb_s, 3)})
             line.update({"fwd_bwd_ms": round(msb, 3),
                          "fwd_bwd_tflops": round(3.5 * flops / (msb * 1e-3) / 1e12, 2),
                          "inner_bwd_busy_tflops": round(
@@ -339,16 +351,17 @@ def main():
     O = torch.empty((B, L, H, D), dtype=torch.float32, device=dev)
     LSE = torch.empty((B, H, L), dtype=torch.float32, device=dev)
 
-    def plan_for(depth, backward=False, tps=0):
+    def plan_for(depth, backward=False, tps=0, in_place=None):
         return cq.cqsa_plan(L, H, D, False, 0, cq.make_opts(B=B, dtype="bf16", depth=depth,
                                                             with_backward=backward,
-                                                            tasks_per_slot=tps))
+                                                            tasks_per_slot=tps,
+                                                            read_in_place=in_place))
 
     cq.cqsa_set_timing(True)
 
-    def fwd_step(depth, tps=0):
+    def fwd_step(depth, tps=0, in_place=None):
         def step():
-            plan = plan_for(depth, tps=tps)   # planning is part of the step
+            plan = plan_for(depth, tps=tps, in_place=in_place)   # planning is part of the step
             cq.cqsa_forward(plan, q, k, v, O, LSE)
             return cq.cqsa_last_stats()
         return step
@@ -371,6 +384,11 @@ def main():
     ms_und, st_und = time_steps(fwd_step(0), args.steps, args.warmup, torch)
     # all seven tasks in one launch and one merge: every kernel runs alone
     ms_one, st_one = time_steps(fwd_step(1, tps=7), args.steps, args.warmup, torch)
+    # the same decomposition with every task's runs gathered into staging
+    # slots first (the kernels otherwise read the caller's tensors in place)
+    ms_staged, _ = time_steps(fwd_step(1, in_place=False), args.steps, args.warmup, torch)
+    ms_one_st, st_one_st = time_steps(fwd_step(1, tps=7, in_place=False), args.steps,
+                                      args.warmup, torch)
 
     tflops = flops / (ms_dec * 1e-3) / 1e12
     # the seven tasks' kept pairs sum to L^2 (each pair once): flops per launch
@@ -381,7 +399,7 @@ def main():
     rows = task_rows(plan1)
     pair_b = 4 * D + 8                      # acc_i row + m_i + l_i (fp32)
     merge_bytes = sum(rows) * B * H * pair_b + B * H * L * (4 * D + 4)   # one final merge
-    stage_bytes = 2 * st_one[-1]["d2d_bytes"]                          # read + write
+    stage_bytes = 2 * st_one_st[-1]["d2d_bytes"]                       # read + write
     kernels = {
         "plan": {"bound": "host", "unit": "ms", "ms_per_call": round(plan_ms, 4)},
         "inner_fwd": {
@@ -394,7 +412,8 @@ def main():
             "undecomposed_launch": round(flops / (mean(st_und, "ms_inner") * 1e-3) / 1e12, 2),
         },
         "stage": {"bound": "hbm", "unit": "GB/s", "bytes_per_step": stage_bytes,
-                  "achieved": round(stage_bytes / (mean(st_one, "ms_stage") * 1e-3) / 1e9, 1)},
+                  "note": "staged plans only (read_in_place = 0)",
+                  "achieved": round(stage_bytes / (mean(st_one_st, "ms_stage") * 1e-3) / 1e9, 1)},
         "merge_final": {"bound": "hbm", "unit": "GB/s", "bytes_per_launch": merge_bytes,
                         "ms_per_launch": round(mean(st_one, "ms_merge"), 4),
                         "achieved": round(merge_bytes / (mean(st_one, "ms_merge") * 1e-3) / 1e9, 1)},
@@ -444,12 +463,16 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": "bf16 exact attention forward, B=1 H=16 d=128 L=32768 "
-                               "non-causal, CQS depth 1 (c=7, I=(0,1,3)), device-resident",
+                               "non-causal, CQS depth 1 (c=7, I=(0,1,3)), device-resident, "
+                               "read in place",
                    "B": B, "H": H, "d": D, "L": L, "causal": False, "depth": 1},
         "runtime_ratio_vs_undecomposed": round(ms_dec / ms_und, 4),
         "undecomposed_ms": round(ms_und, 4),
         "undecomposed_tflops": round(flops / (ms_und * 1e-3) / 1e12, 2),
         "single_launch_ms": round(ms_one, 4),
+        "staged_ms": round(ms_staged, 4),
+        "staged_tflops": round(flops / (ms_staged * 1e-3) / 1e12, 2),
+        "staged_single_launch_ms": round(ms_one_st, 4),
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": BF16_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / BF16_PEAK_TFLOPS, 4),
                      "traffic": measured_traffic()},

@@ -103,6 +103,16 @@ typedef struct {
                                 allows a different valid set at each depth, for finer control of
                                 the task length (0) */
   cqsa_interest_set level_sets[CQSA_MAX_LEVEL_SETS];
+  int32_t read_in_place;     /* how the inner kernels reach a task's tokens (App. A.3 gathers
+                                them into contiguous buffers):
+                                1: read in place -- the kernels address the runs inside the
+                                caller's device tensors, so no per-task copy is made and no
+                                task inputs are held in the workspace; needs
+                                inputs_on_device = 1 and B-slices under 2 GiB
+                                (L * H * d * elem < 2^31 bytes);
+                                0: gather every task's runs into staging slots first;
+                                -1: automatic -- 1 when its conditions hold, else 0 (query
+                                cqsa_plan_reads_in_place) (-1) */
 } cqsa_plan_opts;
 
 /* One contiguous run of a task's tokens: global tokens
@@ -188,6 +198,10 @@ int32_t cqsa_plan_tasks_per_slot(const cqsa_plan_t* plan);
 /* Where the plan keeps the accumulator and outputs: 1 device, 0 host (the choice of an
  * automatic acc_on_device = -1; App. A.3, residency); -1 if plan is NULL. */
 int32_t cqsa_plan_acc_on_device(const cqsa_plan_t* plan);
+/* Whether the plan's kernels read the caller's tensors in place: 1 yes, 0 they gather
+ * each task's runs into staging slots (the choice of read_in_place = -1); -1 if plan is
+ * NULL. */
+int32_t cqsa_plan_reads_in_place(const cqsa_plan_t* plan);
 /* Pooled 128x128 tile census over causal-retained tiles of every task (App. A.2). */
 cqsa_status cqsa_plan_tile_census(const cqsa_plan_t* plan, int64_t* full, int64_t* clear,
                                   int64_t* mixed);

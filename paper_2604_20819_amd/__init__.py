@@ -45,7 +45,8 @@ class cqsa_plan_opts(ctypes.Structure):
                 ("max_depth", ctypes.c_int32), ("n_slots", ctypes.c_int32),
                 ("inputs_on_device", ctypes.c_int32), ("acc_on_device", ctypes.c_int32),
                 ("with_backward", ctypes.c_int32), ("tasks_per_slot", ctypes.c_int32),
-                ("n_level_sets", ctypes.c_int32), ("level_sets", cqsa_interest_set * 4)]
+                ("n_level_sets", ctypes.c_int32), ("level_sets", cqsa_interest_set * 4),
+                ("read_in_place", ctypes.c_int32)]
 
 
 class cqsa_run(ctypes.Structure):
@@ -87,6 +88,7 @@ _SIGS = {
     "cqsa_plan_modelled_device_bytes": (ctypes.c_uint64, [ctypes.c_void_p]),
     "cqsa_plan_tasks_per_slot": (ctypes.c_int32, [ctypes.c_void_p]),
     "cqsa_plan_acc_on_device": (ctypes.c_int32, [ctypes.c_void_p]),
+    "cqsa_plan_reads_in_place": (ctypes.c_int32, [ctypes.c_void_p]),
     "cqsa_plan_tile_census": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(ctypes.c_int64),
                                              ctypes.POINTER(ctypes.c_int64),
                                              ctypes.POINTER(ctypes.c_int64)]),
@@ -141,9 +143,11 @@ def cqsa_plan_opts_default():
 
 def make_opts(B=1, dtype="bf16", c=7, interest=(0, 1, 3), depth=-1, min_depth=1, max_depth=4,
               n_slots=2, inputs_on_device=True, acc_on_device=True, with_backward=False,
-              tasks_per_slot=0, levels=None):
+              tasks_per_slot=0, levels=None, read_in_place=None):
     """levels: optional list of (c, interest) per depth (the last repeats below).
-    acc_on_device=None asks the planner to choose the accumulator residency."""
+    acc_on_device=None asks the planner to choose the accumulator residency;
+    read_in_place=None lets it choose whether the kernels read the caller's
+    tensors in place (True) or gather each task's runs first (False)."""
     o = cqsa_plan_opts_default()
     o.B = B
     o.dtype = {"f32": CQSA_F32, "f16": CQSA_F16, "bf16": CQSA_BF16}[dtype]
@@ -156,6 +160,7 @@ def make_opts(B=1, dtype="bf16", c=7, interest=(0, 1, 3), depth=-1, min_depth=1,
     o.acc_on_device = -1 if acc_on_device is None else int(bool(acc_on_device))
     o.with_backward = int(bool(with_backward))
     o.tasks_per_slot = int(tasks_per_slot)
+    o.read_in_place = -1 if read_in_place is None else int(bool(read_in_place))
     if levels:
         if len(levels) > 4:
             raise ValueError("at most 4 level sets")
@@ -200,6 +205,10 @@ class Plan:
     @property
     def acc_on_device(self):
         return lib().cqsa_plan_acc_on_device(self.handle)
+
+    @property
+    def reads_in_place(self):
+        return lib().cqsa_plan_reads_in_place(self.handle)
 
     def task(self, t):
         """Task t as a dict of plain Python values."""

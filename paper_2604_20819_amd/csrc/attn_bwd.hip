@@ -52,10 +52,15 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
   const int strip = int(work % nstrips);
   const int h = int((work / nstrips) % a.H);
   const int b = int(work / (nstrips * a.H));
-  for (int i = tid; i < a.n_runs; i += 256) runs_s[i] = ((const DevRun*)a.runs)[i];
+  const DevRun* runs_g = (const DevRun*)a.runs;
+  const bool in_place = a.in_place != 0;
+  for (int i = tid; i < a.n_runs; i += 256) runs_s[i] = runs_g[i];
 
+  // token rows: consecutive when staged, the runs' global rows when the
+  // caller's tensors are read in place (as in the forward)
   const int64_t rs = int64_t(a.H) * D;
-  const int64_t base = int64_t(b) * L * rs + int64_t(h) * D;
+  const int64_t seq = in_place ? a.Lg : int64_t(L);
+  const int64_t base = int64_t(b) * seq * rs + int64_t(h) * D;
   const uint16_t* Qg = (const uint16_t*)a.q + base;
   const uint16_t* Kg = (const uint16_t*)a.k + base;
   const uint16_t* Vg = (const uint16_t*)a.v + base;
@@ -66,13 +71,20 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
   const int q0w = strip * BM + wave * 32;
   const int myq = q0w + (lane & 31);
   const bool qvalid = myq < L;
+  // the wave's 32 queries lie in one 64-token block, so the table lookup and
+  // its branch are wave-uniform
+  int64_t qrow = myq;
+  if (in_place && q0w < L) {
+    const int32_t br = a.rows[q0w >> 6];
+    qrow = br != kNoRow ? int64_t(br) + (myq & 63) : (qvalid ? run_global(runs_g, a.n_runs, myq) : 0);
+  }
   vec8 qf[DK], of[DK];
 #pragma unroll
   for (int ks = 0; ks < DK; ++ks) {
     u32x4 u = {0u, 0u, 0u, 0u}, w = {0u, 0u, 0u, 0u};
     if (qvalid) {
-      u = *(const u32x4*)(Qg + int64_t(myq) * rs + ks * 16 + half * 8);
-      w = *(const u32x4*)(Og + int64_t(myq) * rs + ks * 16 + half * 8);
+      u = *(const u32x4*)(Qg + qrow * rs + ks * 16 + half * 8);
+      w = *(const u32x4*)(Og + qrow * rs + ks * 16 + half * 8);
     }
     qf[ks] = bitcast_u4<vec8>(u);
     of[ks] = bitcast_u4<vec8>(w);
@@ -87,21 +99,25 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
   const uint32_t wor = wave_live ? a.blk_or[q0w / 64] : 0u;
   const uint32_t wand = wave_live ? a.blk_and[q0w / 64] : 0u;
   const int nkt = (L + BN - 1) / BN;
-  // Tile skipping as in the forward: a window of 64 tiles' summaries per
-  // vector load (lane i = tile k0 + i) and a ballot for the first live one.
+  // Tile skipping as in the forward: a window of 64 tiles' summaries (and
+  // first rows, kNoRow across a run boundary) per vector load (lane i = tile
+  // k0 + i) and a ballot for the first live one.
   struct Window {
     uint32_t an, on;
+    int32_t row;
   };
   auto window = [&](int k0) {
     const int k = k0 + lane;
-    Window w{0xFFFFFFFFu, 0u};
+    Window w{0xFFFFFFFFu, 0u, 0};
     if (k < nkt) {
       w.an = a.blk_and[k];
       w.on = a.blk_or[k];
+      w.row = in_place ? a.rows[k] : k * BN;
     }
     return w;
   };
-  auto pick = [&](int k0, const Window& w, uint32_t& kor_out, uint32_t& kand_out) -> int {
+  auto pick = [&](int k0, const Window& w, uint32_t& kor_out, uint32_t& kand_out,
+                  int32_t& row_out) -> int {
     const int k = k0 + lane;
     const bool ok = k < nkt && !(causal && k * BN > lastq_wg) && (qand & w.an) == 0u;
     const uint64_t m = __builtin_amdgcn_ballot_w64(ok);
@@ -109,12 +125,13 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
     const int i = __builtin_ctzll(m);
     kand_out = __builtin_amdgcn_readlane(w.an, i);
     kor_out = __builtin_amdgcn_readlane(w.on, i);
+    row_out = __builtin_amdgcn_readlane(w.row, i);
     return k0 + i;
   };
-  auto next_live = [&](int kt, uint32_t& kor_out, uint32_t& kand_out) -> int {
+  auto next_live = [&](int kt, uint32_t& kor_out, uint32_t& kand_out, int32_t& row_out) -> int {
     for (; kt < nkt; kt += 64) {
       if (causal && kt * BN > lastq_wg) return nkt;
-      const int r = pick(kt, window(kt), kor_out, kand_out);
+      const int r = pick(kt, window(kt), kor_out, kand_out, row_out);
       if (r >= 0) return r;
     }
     return nkt;
@@ -129,17 +146,39 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
     const int row = RPI * (NDMA * wave + j) + lane / CHUNKS;
     goff[j] = uint32_t((row * rs + ((lane % CHUNKS) ^ swz(row)) * 8) * 2);
   }
-  auto gload = [&](int buf, int kt) {
-    const int64_t rows = int64_t(L) - int64_t(kt) * BN;
-    const __amdgpu_buffer_rsrc_t rk = row_rsrc(Kg + int64_t(kt) * BN * rs, rows, rs * 2, D * 2);
-    const __amdgpu_buffer_rsrc_t rv = row_rsrc(Vg + int64_t(kt) * BN * rs, rows, rs * 2, D * 2);
+  auto gload = [&](int buf, int kt, int32_t trow) {
     char* kb = smem + buf * STAGE;
     char* vb = kb + KBYTES;
+    if (trow != kNoRow) {
+      // consecutive rows from trow
+      const int64_t rows = int64_t(L) - int64_t(kt) * BN;
+      const __amdgpu_buffer_rsrc_t rk = row_rsrc(Kg + int64_t(trow) * rs, rows, rs * 2, D * 2);
+      const __amdgpu_buffer_rsrc_t rv = row_rsrc(Vg + int64_t(trow) * rs, rows, rs * 2, D * 2);
 #pragma unroll
-    for (int j = 0; j < NDMA; ++j) {
-      const int off = (NDMA * wave + j) * 1024;
-      buf_load16_lds(rk, kb + off, goff[j]);
-      buf_load16_lds(rv, vb + off, goff[j]);
+      for (int j = 0; j < NDMA; ++j) {
+        const int off = (NDMA * wave + j) * 1024;
+        buf_load16_lds(rk, kb + off, goff[j]);
+        buf_load16_lds(rv, vb + off, goff[j]);
+      }
+    } else {
+      // across a run boundary: per-lane rows from the slice base
+      const __amdgpu_buffer_rsrc_t rk = row_rsrc(Kg, seq, rs * 2, D * 2);
+      const __amdgpu_buffer_rsrc_t rv = row_rsrc(Vg, seq, rs * 2, D * 2);
+      // the lane index behind an opaque copy keeps the per-lane row math in
+      // this rarely taken branch (not hoisted out of the tile loop)
+      int ln = lane;
+      asm volatile("" : "+v"(ln));
+#pragma unroll
+      for (int j = 0; j < NDMA; ++j) {
+        const int row = RPI * (NDMA * wave + j) + ln / CHUNKS;
+        const int key = kt * BN + row;
+        const int ch = (ln % CHUNKS) ^ swz(row);
+        const uint32_t vo =
+            key < L ? uint32_t((run_global(runs_s, a.n_runs, key) * rs + ch * 8) * 2) : kOobOffset;
+        const int off = (NDMA * wave + j) * 1024;
+        buf_load16_lds(rk, kb + off, vo);
+        buf_load16_lds(rv, vb + off, vo);
+      }
     }
   };
   auto sstore = [&](int buf, int kt, uint32_t kor_t) {
@@ -163,12 +202,13 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
   const float Dq = qvalid ? a.D[si] : 0.f;
 
   uint32_t kor = 0u, kand = 0u, nor = 0u, nand = 0u;
-  int kt = next_live(0, kor, kand);
+  int32_t krow = 0, nrow = 0;
+  int kt = next_live(0, kor, kand, krow);
   if (kt < nkt) {
-    gload(0, kt);
+    gload(0, kt, krow);
     sstore(0, kt, kor);
   }
-  int kn = kt < nkt ? next_live(kt + 1, nor, nand) : nkt;
+  int kn = kt < nkt ? next_live(kt + 1, nor, nand, nrow) : nkt;
   int buf = 0;
   while (kt < nkt) {
     // this wave's tile loads have landed; after the barrier every wave's
@@ -178,7 +218,7 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
     // summary window after kn (used after the compute), then the loads of kn
     const int kc = kn + 1;
     const Window cw = window(kc);
-    if (kn < nkt) gload(buf ^ 1, kn);
+    if (kn < nkt) gload(buf ^ 1, kn, nrow);
     const int k0 = kt * BN, k1 = (k0 + BN - 1 < L ? k0 + BN - 1 : L - 1);
     const bool wfull = !wave_live || (wand & kand) != 0u || (causal && k0 > wq1);
     if (!wfull) {
@@ -241,11 +281,12 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
     }
     int kc2 = nkt;
     uint32_t or2 = 0u, and2 = 0u;
+    int32_t row2 = 0;
     if (kn < nkt) {
       sstore(buf ^ 1, kn, nor);
       if (kc < nkt) {
-        kc2 = pick(kc, cw, or2, and2);
-        if (kc2 < 0) kc2 = next_live(kc + 64, or2, and2);
+        kc2 = pick(kc, cw, or2, and2, row2);
+        if (kc2 < 0) kc2 = next_live(kc + 64, or2, and2, row2);
       }
     }
     buf ^= 1;
@@ -255,6 +296,7 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
     kn = kc2;
     nor = or2;
     nand = and2;
+    nrow = row2;
   }
   if (!qvalid) return;
   float* dst = a.dq + (int64_t(b) * a.Lg + gq) * rs + int64_t(h) * D;
@@ -306,10 +348,15 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
   const int strip = int(work % nstrips);
   const int h = int((work / nstrips) % a.H);
   const int b = int(work / (nstrips * a.H));
-  for (int i = tid; i < a.n_runs; i += 256) runs_s[i] = ((const DevRun*)a.runs)[i];
+  const DevRun* runs_g = (const DevRun*)a.runs;
+  const bool in_place = a.in_place != 0;
+  for (int i = tid; i < a.n_runs; i += 256) runs_s[i] = runs_g[i];
 
+  // token rows: consecutive when staged, the runs' global rows when the
+  // caller's tensors are read in place
   const int64_t rs = int64_t(a.H) * D;
-  const int64_t base = int64_t(b) * L * rs + int64_t(h) * D;
+  const int64_t seq = in_place ? a.Lg : int64_t(L);
+  const int64_t base = int64_t(b) * seq * rs + int64_t(h) * D;
   const uint16_t* Qg = (const uint16_t*)a.q + base;
   const uint16_t* Kg = (const uint16_t*)a.k + base;
   const uint16_t* Vg = (const uint16_t*)a.v + base;
@@ -320,24 +367,48 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
   const int k0w = strip * BK + wave * 32;
   const int mykey = k0w + (lane & 31);
   const bool kvalid = mykey < L;
+  // the wave's 32 keys lie in one 64-token block, so the table lookup and
+  // its branch are wave-uniform
+  int64_t krow = mykey;
+  if (in_place && k0w < L) {
+    const int32_t br = a.rows[k0w >> 6];
+    krow = br != kNoRow ? int64_t(br) + (mykey & 63) : (kvalid ? run_global(runs_g, a.n_runs, mykey) : 0);
+  }
   // the wave's K rows stay in registers (B operands of S = Q K^T); the
   // strip's V rows (B operands of dP = dO V^T) go to LDS once
   vec8 kf[DK];
 #pragma unroll
   for (int ks = 0; ks < DK; ++ks) {
     u32x4 u = {0u, 0u, 0u, 0u};
-    if (kvalid) u = *(const u32x4*)(Kg + int64_t(mykey) * rs + ks * 16 + half * 8);
+    if (kvalid) u = *(const u32x4*)(Kg + krow * rs + ks * 16 + half * 8);
     kf[ks] = bitcast_u4<vec8>(u);
   }
   {
+    // the strip's rows are consecutive from vrow unless, read in place, one
+    // of its two blocks crosses a run boundary or they lie in different runs
+    const int vb0 = strip * 2, vb1 = ((strip * BK + BK < L ? strip * BK + BK : L) - 1) >> 6;
+    int32_t vrow = strip * BK;
+    if (in_place) {
+      const int32_t r0 = a.rows[vb0], r1 = a.rows[vb1];
+      vrow = (r0 != kNoRow && (vb1 == vb0 || r1 == r0 + 64)) ? r0 : kNoRow;
+    }
+    const int64_t vrows = int64_t(L) - int64_t(strip) * BK;
     const __amdgpu_buffer_rsrc_t rv =
-        row_rsrc(Vg + int64_t(strip) * BK * rs, int64_t(L) - int64_t(strip) * BK, rs * 2, D * 2);
+        vrow != kNoRow ? row_rsrc(Vg + int64_t(vrow) * rs, vrows, rs * 2, D * 2)
+                       : row_rsrc(Vg, seq, rs * 2, D * 2);
     constexpr int NV = BK / RPI / 4;  // 1 KB loads per wave
 #pragma unroll
     for (int j = 0; j < NV; ++j) {
       const int row = RPI * (NV * wave + j) + lane / CHUNKS;
-      buf_load16_lds(rv, vs + (NV * wave + j) * 1024,
-                     uint32_t((row * rs + ((lane % CHUNKS) ^ swz(row)) * 8) * 2));
+      const int ch = (lane % CHUNKS) ^ swz(row);
+      uint32_t vo = uint32_t((row * rs + ch * 8) * 2);
+      if (vrow == kNoRow) {
+        // per-lane rows from the slice base (the runs in global memory: the
+        // LDS copy is not visible yet); tokens past the task end read zero
+        const int key = strip * BK + row;
+        vo = key < L ? uint32_t((run_global(runs_g, a.n_runs, key) * rs + ch * 8) * 2) : kOobOffset;
+      }
+      buf_load16_lds(rv, vs + (NV * wave + j) * 1024, vo);
     }
   }
 
@@ -385,6 +456,13 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
     }
     return nqt;
   };
+  // First row of query tile t < nqt in the inputs, or kNoRow when its block
+  // crosses a run boundary (a scalar load, issued one tile ahead of its use).
+  auto tile_row = [&](int t) -> int32_t {
+    if (!in_place) return t * BQ;
+    const int32_t r = a.rows[t >> 1];
+    return r != kNoRow ? r + (t & 1) * BQ : kNoRow;
+  };
 
   // Query-tile loads for the next tile, issued right after a tile barrier:
   // Q and dO rows through per-tile buffer resources (rows past the task read
@@ -399,15 +477,37 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
   }
   float lse_r = INFINITY, d_r = 0.f;
   uint32_t qb_r = 0u;
-  auto gload = [&](int buf, int qt) {
-    const int64_t rows = int64_t(L) - int64_t(qt) * BQ;
-    const __amdgpu_buffer_rsrc_t rq = row_rsrc(Qg + int64_t(qt) * BQ * rs, rows, rs * 2, D * 2);
-    const __amdgpu_buffer_rsrc_t ro = row_rsrc(Og + int64_t(qt) * BQ * rs, rows, rs * 2, D * 2);
+  auto gload = [&](int buf, int qt, int32_t trow) {
+    if (trow != kNoRow) {
+      // consecutive rows from trow
+      const int64_t rows = int64_t(L) - int64_t(qt) * BQ;
+      const __amdgpu_buffer_rsrc_t rq = row_rsrc(Qg + int64_t(trow) * rs, rows, rs * 2, D * 2);
+      const __amdgpu_buffer_rsrc_t ro = row_rsrc(Og + int64_t(trow) * rs, rows, rs * 2, D * 2);
 #pragma unroll
-    for (int j = 0; j < NDMA; ++j) {
-      const int off = (NDMA * wave + j) * 1024;
-      buf_load16_lds(rq, qs[buf] + off, goff[j]);
-      buf_load16_lds(ro, os[buf] + off, goff[j]);
+      for (int j = 0; j < NDMA; ++j) {
+        const int off = (NDMA * wave + j) * 1024;
+        buf_load16_lds(rq, qs[buf] + off, goff[j]);
+        buf_load16_lds(ro, os[buf] + off, goff[j]);
+      }
+    } else {
+      // across a run boundary: per-lane rows from the slice base
+      const __amdgpu_buffer_rsrc_t rq = row_rsrc(Qg, seq, rs * 2, D * 2);
+      const __amdgpu_buffer_rsrc_t ro = row_rsrc(Og, seq, rs * 2, D * 2);
+      // the lane index behind an opaque copy keeps the per-lane row math in
+      // this rarely taken branch (not hoisted out of the tile loop)
+      int ln = lane;
+      asm volatile("" : "+v"(ln));
+#pragma unroll
+      for (int j = 0; j < NDMA; ++j) {
+        const int row = RPI * (NDMA * wave + j) + ln / CHUNKS;
+        const int q = qt * BQ + row;
+        const int ch = (ln % CHUNKS) ^ swz(row);
+        const uint32_t vo =
+            q < L ? uint32_t((run_global(runs_s, a.n_runs, q) * rs + ch * 8) * 2) : kOobOffset;
+        const int off = (NDMA * wave + j) * 1024;
+        buf_load16_lds(rq, qs[buf] + off, vo);
+        buf_load16_lds(ro, os[buf] + off, vo);
+      }
     }
     if (tid < BQ) {
       const int q = qt * BQ + tid;
@@ -445,10 +545,11 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
   uint32_t qor = 0u, qand = 0u, nor = 0u, nand = 0u;
   int qt = next_live(causal ? first_key / BQ : 0, qor, qand);
   if (qt < nqt) {
-    gload(0, qt);
+    gload(0, qt, tile_row(qt));
     sstore(0);
   }
   int qn = qt < nqt ? next_live(qt + 1, nor, nand) : nqt;
+  int32_t nrow = qn < nqt ? tile_row(qn) : 0;
   int buf = 0;
   while (qt < nqt) {
     // this wave's tile loads have landed; after the barrier every wave's
@@ -458,7 +559,7 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
     // summary window after qn (used after the compute), then the loads of qn
     const int qc = qn + 1;
     const Window cw = window(qc);
-    if (qn < nqt) gload(buf ^ 1, qn);
+    if (qn < nqt) gload(buf ^ 1, qn, nrow);
     const int q0 = qt * BQ;
     const bool wfull = !wave_live || (wand & qand) != 0u || (causal && q0 + BQ - 1 < k0w);
     if (!wfull) {
@@ -530,11 +631,13 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
     }
     int qc2 = nqt;
     uint32_t or2 = 0u, and2 = 0u;
+    int32_t row2 = 0;
     if (qn < nqt) {
       sstore(buf ^ 1);
       if (qc < nqt) {
         qc2 = pick(qc, cw, or2, and2);
         if (qc2 < 0) qc2 = next_live(qc + 64, or2, and2);
+        if (qc2 < nqt) row2 = tile_row(qc2);
       }
     }
     buf ^= 1;
@@ -544,6 +647,7 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
     qn = qc2;
     nor = or2;
     nand = and2;
+    nrow = row2;
   }
   __builtin_amdgcn_s_waitcnt(0x0F70);  // the V fill has landed even when no tile was live
   if (!kvalid) return;

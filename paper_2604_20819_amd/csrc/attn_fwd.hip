@@ -63,11 +63,18 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
   const int n_runs = tk.n_runs;
   const uint32_t* blk_or = (const uint32_t*)(a.tab + tk.or_off);
   const uint32_t* blk_and = (const uint32_t*)(a.tab + tk.and_off);
+  const int32_t* blk_row = (const int32_t*)(a.tab + tk.row_off);
+  const DevRun* runs_g = (const DevRun*)(a.tab + tk.runs_off);
+  const bool in_place = a.in_place != 0;
 
-  for (int i = tid; i < n_runs; i += 256) runs_s[i] = ((const DevRun*)(a.tab + tk.runs_off))[i];
+  for (int i = tid; i < n_runs; i += 256) runs_s[i] = runs_g[i];
 
+  // Staged inputs hold the task's tokens as consecutive rows; inputs read in
+  // place are the caller's tensors, where local token t sits at the global
+  // row its run gives (the block row table answers for whole blocks).
   const int64_t rs = int64_t(a.H) * D;  // elements between consecutive tokens
-  const int64_t base = int64_t(b) * L * rs + int64_t(h) * D + tj * a.in_stride;
+  const int64_t seq = in_place ? a.Lg : int64_t(L);  // rows per batch element
+  const int64_t base = int64_t(b) * seq * rs + int64_t(h) * D + tj * a.in_stride;
   const uint16_t* Qg = (const uint16_t*)a.q + base;
   const uint16_t* Kg = (const uint16_t*)a.k + base;
   const uint16_t* Vg = (const uint16_t*)a.v + base;
@@ -77,12 +84,19 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
   const int q0w = strip * BM + wave * 32;  // first query of this wave
   const int myq = q0w + (lane & 31);
   const bool qvalid = myq < L;
+  // the wave's 32 queries lie in one 64-token block, so the table lookup and
+  // its branch are wave-uniform
+  int64_t qrow = myq;
+  if (in_place && q0w < L) {
+    const int32_t br = blk_row[q0w >> 6];
+    qrow = br != kNoRow ? int64_t(br) + (myq & 63) : (qvalid ? run_global(runs_g, n_runs, myq) : 0);
+  }
 
   vec8 qf[DK];
 #pragma unroll
   for (int ks = 0; ks < DK; ++ks) {
     u32x4 u = {0u, 0u, 0u, 0u};
-    if (qvalid) u = *(const u32x4*)(Qg + int64_t(myq) * rs + ks * 16 + half * 8);
+    if (qvalid) u = *(const u32x4*)(Qg + qrow * rs + ks * 16 + half * 8);
     qf[ks] = bitcast_u4<vec8>(u);
   }
 
@@ -103,21 +117,26 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
   // with one vector load (lane i holds tile k0 + i); a ballot then names the
   // first live tile.  The main loop issues the window for the tile after the
   // next one before its prefetch and consumes it after the compute, so these
-  // loads never stall a tile.
+  // loads never stall a tile.  The window also carries each tile's first
+  // row in the inputs (kNoRow for a tile that crosses a run boundary).
   struct Window {
     uint32_t an, on;  // this lane's tile summaries (AND, OR)
+    int32_t row;
   };
   auto window = [&](int k0) {
     const int k = k0 + lane;
-    Window w{0xFFFFFFFFu, 0u};
+    Window w{0xFFFFFFFFu, 0u, 0};
     if (k < nkt) {
       w.an = blk_and[k];
       w.on = blk_or[k];
+      w.row = in_place ? blk_row[k] : k * BN;
     }
     return w;
   };
-  // First live tile in [k0, k0 + 64), or -1; its summaries in kor_out/kand_out.
-  auto pick = [&](int k0, const Window& w, uint32_t& kor_out, uint32_t& kand_out) -> int {
+  // First live tile in [k0, k0 + 64), or -1; its summaries in kor_out/kand_out
+  // and its first row in row_out.
+  auto pick = [&](int k0, const Window& w, uint32_t& kor_out, uint32_t& kand_out,
+                  int32_t& row_out) -> int {
     const int k = k0 + lane;
     const bool ok = k < nkt && !(causal && k * BN > lastq_wg) && (qand & w.an) == 0u;
     const uint64_t m = __builtin_amdgcn_ballot_w64(ok);
@@ -125,13 +144,14 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
     const int i = __builtin_ctzll(m);
     kand_out = __builtin_amdgcn_readlane(w.an, i);
     kor_out = __builtin_amdgcn_readlane(w.on, i);
+    row_out = __builtin_amdgcn_readlane(w.row, i);
     return k0 + i;
   };
   // First live tile at or after kt (blocking; walks windows).
-  auto next_live = [&](int kt, uint32_t& kor_out, uint32_t& kand_out) -> int {
+  auto next_live = [&](int kt, uint32_t& kor_out, uint32_t& kand_out, int32_t& row_out) -> int {
     for (; kt < nkt; kt += 64) {
       if (causal && kt * BN > lastq_wg) return nkt;
-      const int r = pick(kt, window(kt), kor_out, kand_out);
+      const int r = pick(kt, window(kt), kor_out, kand_out, row_out);
       if (r >= 0) return r;
     }
     return nkt;
@@ -148,17 +168,41 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
     const int ch = (lane % CHUNKS) ^ swz(row);
     goff[j] = uint32_t((row * rs + ch * 8) * 2);
   }
-  auto gload = [&](int buf, int kt) {
-    const int64_t rows = int64_t(L) - int64_t(kt) * BN;
-    const __amdgpu_buffer_rsrc_t rk = row_rsrc(Kg + int64_t(kt) * BN * rs, rows, rs * 2, D * 2);
-    const __amdgpu_buffer_rsrc_t rv = row_rsrc(Vg + int64_t(kt) * BN * rs, rows, rs * 2, D * 2);
+  auto gload = [&](int buf, int kt, int32_t trow) {
     char* kb = smem + buf * STAGE;
     char* vb = kb + KBYTES;
+    if (trow != kNoRow) {
+      // the tile's tokens are consecutive rows from trow
+      const int64_t rows = int64_t(L) - int64_t(kt) * BN;
+      const __amdgpu_buffer_rsrc_t rk = row_rsrc(Kg + int64_t(trow) * rs, rows, rs * 2, D * 2);
+      const __amdgpu_buffer_rsrc_t rv = row_rsrc(Vg + int64_t(trow) * rs, rows, rs * 2, D * 2);
 #pragma unroll
-    for (int j = 0; j < NDMA; ++j) {
-      const int off = (NDMA * wave + j) * 1024;
-      buf_load16_lds(rk, kb + off, goff[j]);
-      buf_load16_lds(rv, vb + off, goff[j]);
+      for (int j = 0; j < NDMA; ++j) {
+        const int off = (NDMA * wave + j) * 1024;
+        buf_load16_lds(rk, kb + off, goff[j]);
+        buf_load16_lds(rv, vb + off, goff[j]);
+      }
+    } else {
+      // a tile crossing a run boundary (inputs read in place): each lane
+      // addresses its token's row from the slice base; tokens past the task
+      // end read as zero
+      const __amdgpu_buffer_rsrc_t rk = row_rsrc(Kg, seq, rs * 2, D * 2);
+      const __amdgpu_buffer_rsrc_t rv = row_rsrc(Vg, seq, rs * 2, D * 2);
+      // the lane index behind an opaque copy keeps the per-lane row math in
+      // this rarely taken branch (not hoisted out of the tile loop)
+      int ln = lane;
+      asm volatile("" : "+v"(ln));
+#pragma unroll
+      for (int j = 0; j < NDMA; ++j) {
+        const int row = RPI * (NDMA * wave + j) + ln / CHUNKS;
+        const int key = kt * BN + row;
+        const int ch = (ln % CHUNKS) ^ swz(row);
+        const uint32_t vo =
+            key < L ? uint32_t((run_global(runs_s, n_runs, key) * rs + ch * 8) * 2) : kOobOffset;
+        const int off = (NDMA * wave + j) * 1024;
+        buf_load16_lds(rk, kb + off, vo);
+        buf_load16_lds(rv, vb + off, vo);
+      }
     }
   };
   auto sstore = [&](int buf, int kt, uint32_t kor_t) {
@@ -180,12 +224,13 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
   const uint32_t qbits = qvalid ? run_bits(runs_s, n_runs, myq) : 0u;
 
   uint32_t kor = 0u, kand = 0u, nor = 0u, nand = 0u;
-  int kt = next_live(0, kor, kand);
+  int32_t krow = 0, nrow = 0;
+  int kt = next_live(0, kor, kand, krow);
   if (kt < nkt) {
-    gload(0, kt);
+    gload(0, kt, krow);
     sstore(0, kt, kor);
   }
-  int kn = kt < nkt ? next_live(kt + 1, nor, nand) : nkt;
+  int kn = kt < nkt ? next_live(kt + 1, nor, nand, nrow) : nkt;
   int buf = 0;
   while (kt < nkt) {
     // this wave's tile loads have landed; after the barrier every wave's
@@ -196,7 +241,7 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
     // loads of tile kn into the other buffer
     const int kc = kn + 1;
     const Window cw = window(kc);
-    if (kn < nkt) gload(buf ^ 1, kn);
+    if (kn < nkt) gload(buf ^ 1, kn, nrow);
 
     // ---- compute on tile kt (wave-uniform verdict) ----
     const int k0 = kt * BN, k1 = (k0 + BN - 1 < L ? k0 + BN - 1 : L - 1);
@@ -310,11 +355,12 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
     // ---- group bits of the next tile, next live tile ----
     int kc2 = nkt;
     uint32_t or2 = 0u, and2 = 0u;
+    int32_t row2 = 0;
     if (kn < nkt) {
       sstore(buf ^ 1, kn, nor);
       if (kc < nkt) {
-        kc2 = pick(kc, cw, or2, and2);
-        if (kc2 < 0) kc2 = next_live(kc + 64, or2, and2);
+        kc2 = pick(kc, cw, or2, and2, row2);
+        if (kc2 < 0) kc2 = next_live(kc + 64, or2, and2, row2);
       }
     }
     buf ^= 1;
@@ -324,6 +370,7 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
     kn = kc2;
     nor = or2;
     nand = and2;
+    nrow = row2;
   }
 
   const float l_tot = l_run + swap_halves(l_run);
@@ -368,6 +415,7 @@ __global__ void __launch_bounds__(256) attn_fwd_f32(const FwdArgs a) {
   __shared__ float ks_[BN][D + 1];
   __shared__ float vs_[BN][D + 1];
   __shared__ uint32_t kbits_s[BN];
+  __shared__ int64_t krow_s[BN];
   __shared__ DevRun runs_s[kMaxRuns];
   const int tid = threadIdx.x, sub = tid & 7, ql = tid >> 3;
   int64_t work = blockIdx.x;
@@ -379,19 +427,26 @@ __global__ void __launch_bounds__(256) attn_fwd_f32(const FwdArgs a) {
   const int h = int((work / nstrips) % a.H);
   const int b = int(work / (nstrips * a.H));
   const int n_runs = tk.n_runs;
-  for (int i = tid; i < n_runs; i += 256) runs_s[i] = ((const DevRun*)(a.tab + tk.runs_off))[i];
+  const DevRun* runs_g = (const DevRun*)(a.tab + tk.runs_off);
+  const int32_t* blk_row = (const int32_t*)(a.tab + tk.row_off);
+  const bool in_place = a.in_place != 0;
+  for (int i = tid; i < n_runs; i += 256) runs_s[i] = runs_g[i];
+  // token rows as in the MFMA kernel: consecutive when staged, the runs'
+  // global rows when read in place
   const int64_t rs = int64_t(a.H) * D;
-  const int64_t base = int64_t(b) * L * rs + int64_t(h) * D + tj * a.in_stride;
+  const int64_t seq = in_place ? a.Lg : int64_t(L);
+  const int64_t base = int64_t(b) * seq * rs + int64_t(h) * D + tj * a.in_stride;
   const float* Qg = (const float*)a.q + base;
   const float* Kg = (const float*)a.k + base;
   const float* Vg = (const float*)a.v + base;
   const float c = a.scale_log2;
   const int myq = strip * QPB + ql;
   const bool qvalid = myq < L;
+  const int64_t qrow = !qvalid ? 0 : in_place ? in_place_row(blk_row, runs_g, n_runs, myq) : myq;
   float q[SL], o[SL];
 #pragma unroll
   for (int i = 0; i < SL; ++i) {
-    q[i] = qvalid ? Qg[int64_t(myq) * rs + sub * SL + i] : 0.f;
+    q[i] = qvalid ? Qg[qrow * rs + sub * SL + i] : 0.f;
     o[i] = 0.f;
   }
   __syncthreads();
@@ -400,14 +455,16 @@ __global__ void __launch_bounds__(256) attn_fwd_f32(const FwdArgs a) {
   const int nkt = (L + BN - 1) / BN;
   for (int kt = 0; kt < nkt; ++kt) {
     __syncthreads();
-    for (int i = tid; i < BN * D; i += 256) {
-      const int r = i / D, dd = i % D, key = kt * BN + r;
-      ks_[r][dd] = key < L ? Kg[int64_t(key) * rs + dd] : 0.f;
-      vs_[r][dd] = key < L ? Vg[int64_t(key) * rs + dd] : 0.f;
-    }
     if (tid < BN) {
       const int key = kt * BN + tid;
       kbits_s[tid] = key < L ? run_bits(runs_s, n_runs, key) : 0xFFFFFFFFu;
+      krow_s[tid] = key >= L ? 0 : in_place ? run_global(runs_s, n_runs, key) : key;
+    }
+    __syncthreads();
+    for (int i = tid; i < BN * D; i += 256) {
+      const int r = i / D, dd = i % D, key = kt * BN + r;
+      ks_[r][dd] = key < L ? Kg[krow_s[r] * rs + dd] : 0.f;
+      vs_[r][dd] = key < L ? Vg[krow_s[r] * rs + dd] : 0.f;
     }
     __syncthreads();
     float s[BN];

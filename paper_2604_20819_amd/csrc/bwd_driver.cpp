@@ -59,6 +59,9 @@ cqsa_status backward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa
   const int depth = p->depth;
   const int64_t ntask = int64_t(p->tasks.size());
   const bool direct = depth == 0;
+  // kernels address the runs inside the caller's tensors: nothing is staged
+  const bool in_place = !direct && o.read_in_place == 1;
+  const bool staged = !direct && !in_place;
 
   CallRecord& rec = call_record();
   rec.reset();
@@ -73,13 +76,13 @@ cqsa_status backward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa
 
   const uint64_t tab_bytes = align_up(p->packed.size());
   const uint64_t d_bytes = align_up(uint64_t(B) * H * L * 4);
-  const uint64_t slot_bytes = bwd_slot_bytes(p->g, o, p->max_L_local, !direct);
+  const uint64_t slot_bytes = bwd_slot_bytes(p->g, o, p->max_L_local, staged);
   const int64_t nslot = std::min<int64_t>(o.n_slots, std::max<int64_t>(1, ntask));
   const uint64_t total = tab_bytes + d_bytes + uint64_t(nslot) * slot_bytes;
   Workspace ws;
   if ((s = acquire_workspace(C, total, &ws)) != CQSA_OK) return s;
   rec.stats.workspace_bytes = total;
-  rec.stats.resident_tasks = direct ? 0 : nslot;
+  rec.stats.resident_tasks = staged ? nslot : 0;
   char* base = (char*)ws.ptr;
   char* d_tab = base;
   float* d_D = (float*)(base + tab_bytes);
@@ -141,8 +144,10 @@ cqsa_status backward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa
     const TableOffsets& to = p->table_off[t];
     char* sb = base + tab_bytes + d_bytes + uint64_t(si) * slot_bytes;
     BwdArgs a{};
-    if (direct) {
+    if (!staged) {
       a.q = Q->data; a.k = K->data; a.v = V->data; a.dO = dO->data;
+      a.in_place = in_place ? 1 : 0;
+      a.rows = (const int32_t*)(d_tab + to.rows);
     } else {
       if (used[si]) {
         CQSA_HIP(hipStreamWaitEvent(C->copy, ev_free[si], 0));
@@ -191,7 +196,7 @@ cqsa_status backward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa
       rec.spans[kStInner].push_back(sk);
       rec.spans[kStInner].push_back(sq);
     }
-    if (!direct) {
+    if (staged) {
       CQSA_HIP(hipEventRecord(ev_free[si], st));
       CQSA_HIP(hipEventRecord(ev_free_q[si], qs));
     }

@@ -37,6 +37,7 @@ void cqsa_plan_opts_default(cqsa_plan_opts* o) {
   o->acc_on_device = 1;
   o->with_backward = 0;
   o->tasks_per_slot = 0;
+  o->read_in_place = -1;
 }
 
 cqsa_status cqsa_plan(int64_t L, int32_t H, int32_t d, int32_t causal,
@@ -54,6 +55,9 @@ cqsa_status cqsa_plan(int64_t L, int32_t H, int32_t d, int32_t causal,
     std::string err;
     cqsa_status s = validate_plan_args(L, H, d, o, &err);
     if (s != CQSA_OK) return fail(s, "cqsa_plan: " + err);
+    // inputs read in place when every batch element's slice is addressable
+    // by a 32-bit byte offset (the kernels' buffer loads)
+    if (o.read_in_place < 0) o.read_in_place = (o.inputs_on_device && in_place_fits(L, H, d, o)) ? 1 : 0;
     Geometry g{L, H, d, causal ? 1 : 0};
     auto* p = new cqsa_plan_s();
     p->g = g;
@@ -142,6 +146,8 @@ cqsa_status cqsa_plan(int64_t L, int32_t H, int32_t d, int32_t causal,
 int32_t cqsa_plan_depth(const cqsa_plan_t* p) { return p ? p->depth : -1; }
 
 int32_t cqsa_plan_acc_on_device(const cqsa_plan_t* p) { return p ? p->opts.acc_on_device : -1; }
+
+int32_t cqsa_plan_reads_in_place(const cqsa_plan_t* p) { return p ? p->opts.read_in_place : -1; }
 
 int64_t cqsa_plan_num_tasks(const cqsa_plan_t* p) { return p ? int64_t(p->tasks.size()) : -1; }
 

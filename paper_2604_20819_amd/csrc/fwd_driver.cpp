@@ -187,6 +187,8 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
   const int depth = p->depth;
   const int64_t ntask = int64_t(p->tasks.size());
   const bool direct = direct_forward(o, depth);
+  // kernels address the runs inside the caller's tensors: nothing is staged
+  const bool in_place = o.read_in_place == 1;
 
   CallRecord& rec = call_record();
   rec.reset();
@@ -201,13 +203,14 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
 
   // ---- workspace layout ----
   // [plan image][running l][slot 0]...[slot S-1]; a slot holds group_size
-  // task sub-slots {Q, K, V, acc, m, l}, each sized for the longest task.
+  // task sub-slots {Q, K, V, acc, m, l} ({acc, m, l} when the inputs are
+  // read in place), each sized for the longest task.
   const int64_t ngroup = int64_t(p->groups.size());
   const int64_t gsz = p->fp.group_size;
   const uint64_t tab_bytes = align_up(p->packed.size());
   const uint64_t gl_bytes =
       (acc_dev && !direct && ngroup > 1) ? align_up(uint64_t(B) * H * L * 4) : 0;
-  const uint64_t sub_bytes = direct ? 0 : fwd_slot_bytes(p->g, o, p->max_L_local, true, true);
+  const uint64_t sub_bytes = direct ? 0 : fwd_slot_bytes(p->g, o, p->max_L_local, !in_place, true);
   std::vector<int64_t> slot_tasks;
   if (!direct) slot_tasks = fwd_slot_tasks(ntask, int32_t(gsz), o.n_slots);
   const int64_t nslot = int64_t(slot_tasks.size());
@@ -221,7 +224,7 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
   char* base = (char*)ws.ptr;
   char* d_tab = base;
   float* d_gl = gl_bytes ? (float*)(base + tab_bytes) : nullptr;
-  const uint64_t in_b = align_up(uint64_t(B) * p->max_L_local * H * d * elem);
+  const uint64_t in_b = in_place ? 0 : align_up(uint64_t(B) * p->max_L_local * H * d * elem);
   const uint64_t acc_b = align_up(uint64_t(B) * p->max_L_local * H * d * 4);
   const uint64_t st_b = align_up(uint64_t(B) * p->max_L_local * H * 4);
   auto slot_base = [&](int64_t si) { return base + tab_bytes + gl_bytes + slot_off[si]; };
@@ -309,7 +312,7 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
         const Task& task = p->tasks[t];
         const int64_t Li = task.L_local;
         wgs += ((Li + rows_wg - 1) / rows_wg) * B * H;
-        if (Li == 0) continue;
+        if (Li == 0 || in_place) continue;
         char* sub = sb + uint64_t(j) * sub_bytes;
         char* dsts[3] = {sub, sub + in_b, sub + 2 * in_b};
         auto sp = span_begin(C->copy);
@@ -348,8 +351,15 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
       const hipStream_t ls = (k & 1) ? C->lane : st;
       CQSA_HIP(hipStreamWaitEvent(ls, ev_staged[si], 0));
       FwdArgs a{};
-      a.q = sb; a.k = sb + in_b; a.v = sb + 2 * in_b;
-      a.in_stride = int64_t(sub_bytes / elem);
+      if (in_place) {
+        a.q = Q->data; a.k = K->data; a.v = V->data;
+        a.in_stride = 0;
+        a.in_place = 1;
+        a.Lg = L;
+      } else {
+        a.q = sb; a.k = sb + in_b; a.v = sb + 2 * in_b;
+        a.in_stride = int64_t(sub_bytes / elem);
+      }
       a.acc = (float*)(sb + 3 * in_b);
       a.m = (float*)(sb + 3 * in_b + acc_b);
       a.l = (float*)(sb + 3 * in_b + acc_b + st_b);

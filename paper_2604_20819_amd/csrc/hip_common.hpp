@@ -153,6 +153,18 @@ __device__ __forceinline__ int64_t run_global(const DevRun* runs, int n, int64_t
   return 0;
 }
 
+// Tensor row of local token r when the inputs are read in place: from the
+// block row table when r's 64-token block lies in one run, else from the runs.
+__device__ __forceinline__ int64_t in_place_row(const int32_t* rows, const DevRun* runs, int n,
+                                                int r) {
+  const int32_t g = rows[r >> 6];
+  return g != kNoRow ? int64_t(g) + (r & 63) : run_global(runs, n, r);
+}
+
+// Byte offset that every buffer load treats as out of range (resources span
+// under 2^31 bytes): such lanes read zero.
+constexpr uint32_t kOobOffset = 0x80000000u;
+
 // Task of a work item in a launch over several tasks, whose work items are
 // laid out task after task (ceil(L_j / rows) * per_row items for task j).
 // Returns j and leaves the item's index within task j in `w`.

@@ -16,10 +16,13 @@ enum FwdMode : int {
 };
 
 // One launch of the inner forward kernel over `ntask` tasks (a launch group).
-// Task j's rows are [B, L_j, H, d] at q/k/v + j * in_stride elements and its
-// statistics are acc_j [B, L_j, H, d] at acc + j * acc_stride, m_j and l_j
-// [B, H, L_j] at m/l + j * st_stride.  In final mode the single task spans all
-// L tokens: q/k/v are the caller's tensors, acc is O and m is LSE.
+// Staged inputs: task j's rows are [B, L_j, H, d] at q/k/v + j * in_stride
+// elements.  Inputs read in place (in_place = 1): q/k/v are the caller's
+// [B, Lg, H, d] tensors and task j's local token t is the global row its runs
+// give (block row table DevTask::row_off).  Task j's statistics are acc_j
+// [B, L_j, H, d] at acc + j * acc_stride, m_j and l_j [B, H, L_j] at
+// m/l + j * st_stride.  In final mode the single task spans all L tokens:
+// q/k/v are the caller's tensors, acc is O and m is LSE.
 struct FwdArgs {
   const void* q;
   const void* k;
@@ -35,6 +38,8 @@ struct FwdArgs {
   int32_t B, H;
   int32_t causal;
   float scale_log2;     // softmax scale * log2(e)
+  int32_t in_place;     // 1: q/k/v are the caller's tensors, rows by the runs
+  int64_t Lg;           // rows per batch element of q/k/v when in_place
 };
 
 // Gather-merge of one launch group's task statistics into the global
@@ -57,12 +62,14 @@ struct CombineArgs {
   int32_t final;
 };
 
-// Inner backward kernels over one staged task (App. A.1, Eq. "globallse").
+// Inner backward kernels over one task (App. A.1, Eq. "globallse").
 struct BwdArgs {
-  const void* q;        // [B, L, H, d] staged task rows (seq_rows = L)
-  const void* k;
-  const void* v;
+  const void* q;        // [B, L, H, d] staged task rows, or, when in_place, the
+  const void* k;        // caller's [B, Lg, H, d] tensors with local token t at
+  const void* v;        // the global row its runs give
   const void* dO;
+  int32_t in_place;
+  const int32_t* rows;  // block row table (records.hpp), used when in_place
   int32_t L;            // task length
   int32_t B, H;
   int32_t causal;

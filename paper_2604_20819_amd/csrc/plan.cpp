@@ -70,6 +70,10 @@ static std::string check_set(int32_t c, int32_t l, const int32_t* I) {
   return "";
 }
 
+bool in_place_fits(int64_t L, int32_t H, int32_t d, const cqsa_plan_opts& o) {
+  return uint64_t(L) * uint64_t(H) * uint64_t(d) * dtype_size(o.dtype) <= 0x7fffffffull;
+}
+
 cqsa_status validate_plan_args(int64_t L, int32_t H, int32_t d, const cqsa_plan_opts& o,
                                std::string* err) {
   auto bad = [&](cqsa_status s, const std::string& m) {
@@ -118,6 +122,12 @@ cqsa_status validate_plan_args(int64_t L, int32_t H, int32_t d, const cqsa_plan_
     return bad(CQSA_ERR_UNSUPPORTED, "tasks_per_slot > 1 needs the accumulator on the device");
   if (o.with_backward && (!o.inputs_on_device || o.acc_on_device != 1))
     return bad(CQSA_ERR_UNSUPPORTED, "the backward supports device-resident tensors only");
+  if (o.read_in_place < -1 || o.read_in_place > 1)
+    return bad(CQSA_ERR_INVALID_ARG, "read_in_place must be -1 (auto), 0 or 1");
+  if (o.read_in_place == 1 && !o.inputs_on_device)
+    return bad(CQSA_ERR_UNSUPPORTED, "read_in_place = 1 needs device-resident inputs");
+  if (o.read_in_place == 1 && !in_place_fits(L, H, d, o))
+    return bad(CQSA_ERR_UNSUPPORTED, "read_in_place = 1 needs L * H * d * elem < 2^31 bytes");
   if (o.with_backward && o.dtype == CQSA_F32)
     return bad(CQSA_ERR_UNSUPPORTED, "the backward supports fp16 and bf16 inputs only");
   return CQSA_OK;
@@ -307,8 +317,22 @@ void pack_image(const std::vector<Task>& tasks, const SegmentCover& sc, int32_t 
     std::memcpy(im.data() + o.blk_or, k.blk_or.data(), k.blk_or.size() * 4);
     o.blk_and = reserve(k.blk_and.size() * 4);
     std::memcpy(im.data() + o.blk_and, k.blk_and.data(), k.blk_and.size() * 4);
+    // block row table for kernels that read the caller's tensors in place
+    const size_t nb = k.blk_or.size();
+    o.rows = reserve(nb * 4);
+    size_t ri = 0;
+    for (size_t i = 0; i < nb; ++i) {
+      const int64_t t0 = int64_t(i) * kBlock;
+      const int64_t t1 = std::min<int64_t>(t0 + kBlock, k.L_local);  // one past the last
+      while (k.runs[ri].local_start + k.runs[ri].length <= t0) ++ri;
+      const Run& r = k.runs[ri];
+      const int32_t row = t1 <= r.local_start + r.length
+                              ? int32_t(r.global_start + (t0 - r.local_start))
+                              : kNoRow;
+      std::memcpy(im.data() + o.rows + i * 4, &row, 4);
+    }
     DevTask d{k.L_local, int64_t(o.runs), int64_t(o.blk_or), int64_t(o.blk_and),
-              int32_t(k.runs.size()), {0, 0, 0}};
+              int32_t(k.runs.size()), 0, int64_t(o.rows)};
     std::memcpy(im.data() + hdr + t * sizeof(DevTask), &d, sizeof(d));
     offs->push_back(o);
   }
@@ -360,8 +384,9 @@ Footprint footprint(const Geometry& g, const cqsa_plan_opts& o, int32_t depth,
   f.resident_bwd = 4 * in_bytes + f32_full + stat_full + 3 * f32_full;
   // slot i holds as many task sub-slots (each sized for the longest task) as
   // the largest group that uses it (groups k with k % n_slots == i)
-  f.slot_fwd = direct ? 0 : fwd_slot_bytes(g, o, Lmax, true, true);
-  f.slot_bwd = bwd_slot_bytes(g, o, Lmax, depth > 0);
+  const bool staged = o.read_in_place != 1;
+  f.slot_fwd = direct ? 0 : fwd_slot_bytes(g, o, Lmax, staged, true);
+  f.slot_bwd = bwd_slot_bytes(g, o, Lmax, depth > 0 && staged);
   // running row sums l, needed while more than one group merges on device
   f.global_fwd = (o.acc_on_device && !direct && f.groups > 1) ? stat_full : 0;
   f.global_bwd = stat_full;  // D = rowsum(dO * O)

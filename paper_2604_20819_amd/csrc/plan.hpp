@@ -42,6 +42,7 @@ struct TableOffsets {
   uint64_t runs = 0;    // DevRun[n_runs]: {local_start, global_start, length, bits, pad}
   uint64_t blk_or = 0;  // uint32[n_blocks]
   uint64_t blk_and = 0; // uint32[n_blocks]
+  uint64_t rows = 0;    // int32[n_blocks] block row table (records.hpp, kNoRow)
 };
 
 // A launch group: tasks [task0, task0 + count) are staged into one slot,
@@ -110,6 +111,10 @@ struct cqsa_plan_s {
 namespace cqsa {
 
 size_t dtype_size(cqsa_dtype t);
+
+// True when a [L, H, d] slice of the inputs spans under 2^31 bytes, so the
+// kernels can address the caller's tensors in place with 32-bit offsets.
+bool in_place_fits(int64_t L, int32_t H, int32_t d, const cqsa_plan_opts& o);
 
 // Validates options and geometry; returns CQSA_OK or sets the error text.
 cqsa_status validate_plan_args(int64_t L, int32_t H, int32_t d, const cqsa_plan_opts& o,

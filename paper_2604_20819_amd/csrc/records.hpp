@@ -29,8 +29,15 @@ struct DevTask {
   int64_t or_off;     // uint32[ceil(L_local / 64)] block OR of the group bits
   int64_t and_off;    // uint32[ceil(L_local / 64)] block AND of the group bits
   int32_t n_runs;
-  int32_t pad[3];
+  int32_t pad;
+  int64_t row_off;    // int32[ceil(L_local / 64)] block rows (see kNoRow)
 };
+
+// Block row table: entry i is the global row of local token 64 i when the
+// tokens of block i (up to the task end) lie in one run, so they are
+// consecutive rows of the caller's tensors; kNoRow when the block crosses a
+// run boundary.
+constexpr int32_t kNoRow = -1;
 
 // Elementary global segment of a launch group's merge: tokens
 // [g0, g0 + len) lie inside one run of every task that holds them.  The

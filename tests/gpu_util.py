@@ -20,14 +20,15 @@ def say(*a):
 
 
 def run_forward(Q, K, V, causal, depth=-1, budget=0, n_slots=2, host=False, scale=0.0,
-                tasks_per_slot=0, levels=None):
+                tasks_per_slot=0, levels=None, read_in_place=None):
     """Run cqsa_forward; Q, K, V are CPU tensors.  host=True keeps inputs and
     outputs in pinned host memory (streamed path).  Returns CPU (O, LSE, plan)."""
     B, L, H, d = Q.shape
     dt = {torch.float32: "f32", torch.float16: "f16", torch.bfloat16: "bf16"}[Q.dtype]
     opts = cq.make_opts(B=B, dtype=dt, depth=depth, n_slots=n_slots,
                         inputs_on_device=not host, acc_on_device=not host,
-                        tasks_per_slot=tasks_per_slot, levels=levels)
+                        tasks_per_slot=tasks_per_slot, levels=levels,
+                        read_in_place=read_in_place)
     plan = cq.cqsa_plan(L, H, d, causal, budget, opts)
     if host:
         q, k, v = (x.pin_memory() for x in (Q, K, V))

@@ -118,6 +118,42 @@ def test_automatic_accumulator_residency():
     assert e.value.status == -2
 
 
+def test_read_in_place_choice_and_errors():
+    """The kernels read the caller's tensors in place when they are on the
+    device and a batch element's [L, H, d] slice spans under 2^31 bytes (the
+    reach of a buffer load's 32-bit offset); otherwise runs are gathered."""
+    p = cq.cqsa_plan(32768, 16, 128, False, 0, cq.make_opts())
+    assert p.reads_in_place == 1
+    p = cq.cqsa_plan(32768, 16, 128, False, 0, cq.make_opts(read_in_place=False))
+    assert p.reads_in_place == 0
+    p = cq.cqsa_plan(32768, 16, 128, False, 0, cq.make_opts(inputs_on_device=False,
+                                                            acc_on_device=False))
+    assert p.reads_in_place == 0
+    # 2^20 x 8 x 128 x 2 bytes = 2^31: one byte past the reach
+    p = cq.cqsa_plan(1 << 20, 8, 128, False, 0, cq.make_opts(depth=2))
+    assert p.reads_in_place == 0
+    p = cq.cqsa_plan((1 << 20) - 1, 8, 128, False, 0, cq.make_opts(depth=2))
+    assert p.reads_in_place == 1
+    p = cq.cqsa_plan(1 << 19, 8, 128, False, 0, cq.make_opts(depth=2, dtype="f32"))
+    assert p.reads_in_place == 0
+    for kw, status in [(dict(read_in_place=True, inputs_on_device=False, acc_on_device=False), -2),
+                       (dict(read_in_place=True, depth=2), -2)]:
+        with pytest.raises(cq.CqsaError) as e:
+            cq.cqsa_plan(1 << 20, 8, 128, False, 0, cq.make_opts(**kw))
+        assert e.value.status == status and "read_in_place" in str(e.value)
+    o = cq.make_opts()
+    o.read_in_place = 2
+    with pytest.raises(cq.CqsaError) as e:
+        cq.cqsa_plan(4096, 4, 64, False, 0, o)
+    assert e.value.status == -1
+    # in place the backward holds no staging slots: the forward's sub-slots
+    # are the peak, and they shrink by the three staged inputs
+    kw = dict(B=2, with_backward=True, depth=1)
+    a = cq.cqsa_plan(65536, 16, 128, True, 0, cq.make_opts(**kw))
+    b = cq.cqsa_plan(65536, 16, 128, True, 0, cq.make_opts(read_in_place=False, **kw))
+    assert a.modelled_device_bytes < b.modelled_device_bytes
+
+
 def test_struct_layouts_match_the_header(tmp_path):
     """The binding's ctypes mirrors have the sizes and field offsets of the C
     structs in include/cqsa.h (checked by compiling the header with gcc)."""
@@ -190,11 +226,14 @@ def test_budget_too_small():
 
 
 GB = 10 ** 9
-# (L, H, d, causal, budget, opts, expected depth) for the five workloads
+# (L, H, d, causal, budget, opts, expected depth) for the five workloads; the
+# 8 GB fp16 causal call needs depth 2 when every task's inputs are staged and
+# fits at depth 1 when the kernels read the caller's tensors in place
 WORKLOADS = [
     (1024, 1, 64, False, 0, dict(dtype="f32", depth=1), 1),
     (32768, 16, 128, False, 0, dict(dtype="bf16", depth=1), 1),
-    (131072, 32, 128, True, 8 * GB, dict(dtype="f16"), 2),
+    (131072, 32, 128, True, 8 * GB, dict(dtype="f16", read_in_place=False), 2),
+    (131072, 32, 128, True, 8 * GB, dict(dtype="f16"), 1),
     (65536, 16, 128, True, 16 * GB, dict(B=2, dtype="bf16", with_backward=True), 1),
     (1048576, 8, 128, False, 4 * GB, dict(dtype="bf16", inputs_on_device=False,
                                           acc_on_device=False), 2),
@@ -215,12 +254,13 @@ def test_workload_depths(L, H, d, causal, budget, kw, want):
 
 def _image_bytes(p, g):
     """Plan image size from the layout the planner documents: DevTask records,
-    per-task runs and block summaries, per-group segments and contributions."""
+    per-task runs, block summaries (OR, AND) and block row table, per-group
+    segments and contributions."""
     al = lambda x: (x + 255) // 256 * 256
     tasks = [p.task(t) for t in range(p.num_tasks)]
     size = al(len(tasks) * 48)
     for tk in tasks:
-        size += al(len(tk["runs"]) * 32) + 2 * al(len(tk["block_or"]) * 4)
+        size += al(len(tk["runs"]) * 32) + 3 * al(len(tk["block_or"]) * 4)
     bounds = sorted({0, p.L} | {r[0] for tk in tasks for r in tk["runs"]}
                     | {r[0] + r[1] for tk in tasks for r in tk["runs"]})
     segs = list(zip(bounds[:-1], bounds[1:]))
@@ -238,19 +278,22 @@ def _image_bytes(p, g):
     return size
 
 
+@pytest.mark.parametrize("in_place", [True, False])
 @pytest.mark.parametrize("tps,want_g,subslots", [(0, 1, 2), (1, 1, 2), (7, 7, 7), (3, 3, 6),
                                                   (4, 4, 7)])
-def test_footprint_model_closed_form(tps, want_g, subslots):
+def test_footprint_model_closed_form(tps, want_g, subslots, in_place):
     """Footprint of the bf16 L=32768 H=16 d=128 depth-1 plan, recomputed here
     from the workspace layout the header documents: with g tasks per slot and
-    two slots, slot i holds the largest group k = i (mod 2)."""
+    two slots, slot i holds the largest group k = i (mod 2); a task sub-slot
+    holds the statistics, plus the staged Q, K, V unless they are read in place."""
     L, H, d, B = 32768, 16, 128, 1
-    p = cq.cqsa_plan(L, H, d, False, 0, cq.make_opts(depth=1, tasks_per_slot=tps))
-    assert p.tasks_per_slot == want_g
+    p = cq.cqsa_plan(L, H, d, False, 0, cq.make_opts(depth=1, tasks_per_slot=tps,
+                                                       read_in_place=in_place))
+    assert p.tasks_per_slot == want_g and p.reads_in_place == int(in_place)
     al = lambda x: (x + 255) // 256 * 256
     Lmax = max(p.task(t)["L_local"] for t in range(p.num_tasks))
     rows = B * Lmax * H
-    sub = 3 * al(rows * d * 2) + al(rows * d * 4) + 2 * al(rows * 4)
+    sub = (0 if in_place else 3 * al(rows * d * 2)) + al(rows * d * 4) + 2 * al(rows * 4)
     resident = 3 * al(B * L * H * d * 2) + al(B * L * H * d * 4) + al(B * L * H * 4)
     groups = -(-7 // want_g)
     running_l = al(B * H * L * 4) if groups > 1 else 0

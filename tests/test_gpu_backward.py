@@ -25,12 +25,14 @@ pytestmark = pytest.mark.gpu
 REL = {"bf16": 6e-3, "f16": 8e-4}
 
 
-def run_fwd_bwd(Q, K, V, dO, causal, depth=-1, budget=0, n_slots=2, levels=None):
+def run_fwd_bwd(Q, K, V, dO, causal, depth=-1, budget=0, n_slots=2, levels=None,
+                read_in_place=None):
     B, L, H, d = Q.shape
     dt = {torch.float16: "f16", torch.bfloat16: "bf16"}[Q.dtype]
     plan = cq.cqsa_plan(L, H, d, causal, budget,
                         cq.make_opts(B=B, dtype=dt, depth=depth, n_slots=n_slots,
-                                     with_backward=True, levels=levels))
+                                     with_backward=True, levels=levels,
+                                     read_in_place=read_in_place))
     q, k, v, do = (x.cuda() for x in (Q, K, V, dO))
     O = torch.empty((B, L, H, d), dtype=torch.float32, device="cuda")
     LSE = torch.empty((B, H, L), dtype=torch.float32, device="cuda")

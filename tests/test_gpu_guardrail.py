@@ -140,11 +140,14 @@ def test_forced_depth_reports_the_failure_and_exhaustion_is_reported():
 
 
 def test_backward_guardrail():
+    """The backward's resident task working sets are its staging slots, so
+    the plan gathers its inputs (read in place it holds none)."""
     need_gpu()
     L, H, d = 2500, 2, 128
     Q, K, V, dO = synth.make_inputs(44, 1, L, H, d, "bf16", with_dO=True)
     q, k, v, do = (x.cuda() for x in (Q, K, V, dO))
-    plan = cq.cqsa_plan(L, H, d, True, 0, cq.make_opts(dtype="bf16", with_backward=True))
+    plan = cq.cqsa_plan(L, H, d, True, 0, cq.make_opts(dtype="bf16", with_backward=True,
+                                                       read_in_place=False))
     O = torch.empty((1, L, H, d), dtype=torch.float32, device="cuda")
     LSE = torch.empty((1, H, L), dtype=torch.float32, device="cuda")
     cq.cqsa_forward(plan, q, k, v, O, LSE)
