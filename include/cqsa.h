@@ -93,10 +93,11 @@ typedef struct {
                                 plans only; query cqsa_plan_acc_on_device) (1) */
   int32_t with_backward;     /* 1: the footprint must also fit cqsa_backward (0) */
   int32_t tasks_per_slot;    /* forward tasks staged, launched and merged together, in [0, 32]:
-                                0 = automatic: enough tasks for 1024 inner-kernel work groups
-                                per launch (capped at 32 and at the task count, reduced until
-                                the budget fits; 1 when acc_on_device = 0); >= 1 forced;
-                                > 1 needs acc_on_device = 1 (0) */
+                                0 = automatic: with inputs read in place, every task up to 32
+                                per launch; with staged inputs, enough tasks for 1024
+                                inner-kernel work groups per launch (capped at 32 and at the
+                                task count); either reduced until the budget fits, and 1 when
+                                acc_on_device = 0; >= 1 forced; > 1 needs acc_on_device = 1 (0) */
   int32_t n_level_sets;      /* 0: every level uses (c, l, interest).  n in [1, 4]: level t
                                 (1-based) uses level_sets[min(t, n) - 1], so the last set repeats
                                 below level n, and (c, l, interest) are ignored.  Section 3.3

@@ -73,6 +73,11 @@ cqsa_status cqsa_plan(int64_t L, int32_t H, int32_t d, int32_t causal,
       int32_t g_hi = 1;
       if (o.tasks_per_slot > 0) {
         g_hi = int32_t(std::min<int64_t>(o.tasks_per_slot, std::max<int64_t>(1, ntask)));
+      } else if (o.acc_on_device && o.read_in_place == 1) {
+        // nothing is staged, so a group costs only its statistics: one
+        // launch over as many tasks as a merge accepts keeps every work
+        // group in one grid (no tails between launches, one merge)
+        g_hi = int32_t(std::min<int64_t>(kMaxContrib, std::max<int64_t>(1, ntask)));
       } else if (o.acc_on_device) {
         // enough tasks per launch for kLaunchWgs work groups (two waves of
         // the GPU's resident work groups); large tasks launch one by one

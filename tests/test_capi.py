@@ -278,9 +278,10 @@ def _image_bytes(p, g):
     return size
 
 
-@pytest.mark.parametrize("in_place", [True, False])
-@pytest.mark.parametrize("tps,want_g,subslots", [(0, 1, 2), (1, 1, 2), (7, 7, 7), (3, 3, 6),
-                                                  (4, 4, 7)])
+@pytest.mark.parametrize("in_place,tps,want_g,subslots",
+                         [(False, 0, 1, 2), (True, 0, 7, 7)]
+                         + [(ip, tps, g, n) for ip in (True, False)
+                            for tps, g, n in ((1, 1, 2), (7, 7, 7), (3, 3, 6), (4, 4, 7))])
 def test_footprint_model_closed_form(tps, want_g, subslots, in_place):
     """Footprint of the bf16 L=32768 H=16 d=128 depth-1 plan, recomputed here
     from the workspace layout the header documents: with g tasks per slot and
@@ -302,32 +303,40 @@ def test_footprint_model_closed_form(tps, want_g, subslots, in_place):
 
 
 def test_group_size_rules():
-    """Automatic tasks per slot: enough tasks for 1024 work groups per launch
-    (128-query strips x B x H per task), capped at 32 and at the task count;
-    one with a host accumulator; reduced until a capped budget fits."""
+    """Automatic tasks per slot.  Staged inputs: enough tasks for 1024 work
+    groups per launch (128-query strips x B x H per task), capped at 32 and at
+    the task count.  Inputs read in place: every task, up to 32.  One with a
+    host accumulator; reduced until a capped budget fits."""
+    st = dict(read_in_place=False)
     # L=4096, depth 2: 49 tasks of <= 84 tokens, 1 strip x 4 heads each
-    p = cq.cqsa_plan(4096, 4, 64, False, 0, cq.make_opts(depth=2))
+    p = cq.cqsa_plan(4096, 4, 64, False, 0, cq.make_opts(depth=2, **st))
     assert p.tasks_per_slot == 32
     # depth 1: 7 tasks of <= 586 tokens, 5 strips x 4 heads = 20 work groups each
-    p = cq.cqsa_plan(4096, 4, 64, False, 0, cq.make_opts(depth=1))
+    p = cq.cqsa_plan(4096, 4, 64, False, 0, cq.make_opts(depth=1, **st))
     assert p.tasks_per_slot == 7
     # 14043-token tasks x 16 heads: 110 x 16 = 1760 work groups, one per launch
-    p = cq.cqsa_plan(32768, 16, 128, False, 0, cq.make_opts(depth=1))
+    p = cq.cqsa_plan(32768, 16, 128, False, 0, cq.make_opts(depth=1, **st))
     assert p.tasks_per_slot == 1
     # 4682-token tasks x 16 heads: 37 x 16 = 592 -> two per launch
-    p = cq.cqsa_plan(32768, 16, 128, False, 0, cq.make_opts(depth=2))
+    p = cq.cqsa_plan(32768, 16, 128, False, 0, cq.make_opts(depth=2, **st))
     assert p.tasks_per_slot == 2
     # fp32 uses 32-query strips: 7 tasks of <= 147 tokens, 5 x 1 work groups
-    p = cq.cqsa_plan(1024, 1, 64, False, 0, cq.make_opts(dtype="f32", depth=1))
+    p = cq.cqsa_plan(1024, 1, 64, False, 0, cq.make_opts(dtype="f32", depth=1, **st))
     assert p.tasks_per_slot == 7
-    p = cq.cqsa_plan(4096, 4, 64, False, 0, cq.make_opts(depth=1, acc_on_device=False))
-    assert p.tasks_per_slot == 1
-    big = cq.cqsa_plan(4096, 4, 64, False, 0, cq.make_opts(depth=1))
-    one = cq.cqsa_plan(4096, 4, 64, False, 0, cq.make_opts(depth=1, tasks_per_slot=1))
-    budget = (big.modelled_device_bytes + one.modelled_device_bytes) // 2
-    mid = cq.cqsa_plan(4096, 4, 64, False, budget, cq.make_opts(depth=1))
-    assert 1 <= mid.tasks_per_slot < big.tasks_per_slot
-    assert mid.modelled_device_bytes <= budget
+    # read in place: all seven, 32 of 49
+    p = cq.cqsa_plan(32768, 16, 128, False, 0, cq.make_opts(depth=1))
+    assert p.reads_in_place == 1 and p.tasks_per_slot == 7
+    p = cq.cqsa_plan(32768, 16, 128, False, 0, cq.make_opts(depth=2))
+    assert p.tasks_per_slot == 32
+    for kw in ({}, st):
+        p = cq.cqsa_plan(4096, 4, 64, False, 0, cq.make_opts(depth=1, acc_on_device=False, **kw))
+        assert p.tasks_per_slot == 1
+        big = cq.cqsa_plan(4096, 4, 64, False, 0, cq.make_opts(depth=1, **kw))
+        one = cq.cqsa_plan(4096, 4, 64, False, 0, cq.make_opts(depth=1, tasks_per_slot=1, **kw))
+        budget = (big.modelled_device_bytes + one.modelled_device_bytes) // 2
+        mid = cq.cqsa_plan(4096, 4, 64, False, budget, cq.make_opts(depth=1, **kw))
+        assert 1 <= mid.tasks_per_slot < big.tasks_per_slot
+        assert mid.modelled_device_bytes <= budget
     with pytest.raises(cq.CqsaError):
         cq.cqsa_plan(4096, 4, 64, False, 0, cq.make_opts(depth=1, tasks_per_slot=33))
     with pytest.raises(cq.CqsaError):

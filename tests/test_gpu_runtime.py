@@ -103,15 +103,18 @@ def test_work_is_ordered_on_the_callers_stream():
     assert torch.equal(Oc.cpu(), O0) and torch.equal(Lc.cpu(), L0)
 
 
+@pytest.mark.parametrize("in_place", [True, False])
 @pytest.mark.parametrize("depth,tps", [(1, 0), (2, 0), (1, 3)])
-def test_call_statistics(depth, tps):
-    """Bytes staged, launch counts and workspace size follow the plan."""
+def test_call_statistics(depth, tps, in_place):
+    """Bytes staged (none when the inputs are read in place), launch counts
+    and workspace size follow the plan."""
     need_gpu()
     L, H, d = 3000, 2, 128
     Q, K, V = _inputs(L=L, H=H, d=d, seed=35)
     cq.cqsa_set_timing(True)
     try:
-        O, LSE, plan = run_forward(Q, K, V, True, depth=depth, tasks_per_slot=tps)
+        O, LSE, plan = run_forward(Q, K, V, True, depth=depth, tasks_per_slot=tps,
+                                   read_in_place=in_place)
         st = cq.cqsa_last_stats()
     finally:
         cq.cqsa_set_timing(False)
@@ -119,7 +122,8 @@ def test_call_statistics(depth, tps):
     g = plan.tasks_per_slot
     groups = -(-plan.num_tasks // g)
     assert st["depth"] == depth and st["num_tasks"] == plan.num_tasks
-    assert st["d2d_bytes"] == 3 * rows * H * d * 2
+    assert plan.reads_in_place == int(in_place)
+    assert st["d2d_bytes"] == (0 if in_place else 3 * rows * H * d * 2)
     assert st["h2d_bytes"] == 0 and st["d2h_bytes"] == 0
     assert st["inner_launches"] == groups and st["merge_launches"] == groups
     assert 0 < st["workspace_bytes"] <= plan.modelled_device_bytes

@@ -84,9 +84,10 @@ def test_fp16_causal_L131072_budget_8GB():
     say("fp16 causal B=1 H=32 d=128 L=131072 budget 8GB")
     B, L, H, d = 1, 131072, 32, 128
     Q, K, V = synth.make_inputs(20819 + 3, B, L, H, d, "f16")
-    O, LSE, plan = run_forward(Q, K, V, True, budget=8 * GB)
+    # staged inputs: the per-task gather needs a second level (49 tasks)
+    O, LSE, plan = run_forward(Q, K, V, True, budget=8 * GB, read_in_place=False)
     say(f"depth={plan.depth} tasks={plan.num_tasks} modelled={plan.modelled_device_bytes / GB:.3f} GB")
-    assert plan.depth >= 2 and plan.modelled_device_bytes <= 8 * GB
+    assert plan.depth == 2 and plan.modelled_device_bytes <= 8 * GB
     rows = synth.sample_rows(20819 + 3, L, 2048, H)
     Of, Lf = oracle_rows(Q, K, V, True, rows)
     check(*gather_rows(O, LSE, rows), Of, Lf, 6e-4)
@@ -94,10 +95,22 @@ def test_fp16_causal_L131072_budget_8GB():
     r = rel_l2(O.numpy(), O0.numpy())
     say(f"rel_l2 vs depth 0 = {r:.3e}")
     assert r <= 1e-3
-    # Section 3.3 / Table "interest_set": with c = 21 (l = 5) one level of 21
-    # tasks fits the same budget where c = 7 needs two levels (49 tasks)
     del O, LSE
-    O2, L2, plan2 = run_forward(Q, K, V, True, budget=8 * GB, levels=[(21, (0, 1, 4, 14, 16))])
+    # read in place: no staged inputs, so one level of 7 tasks fits
+    O1, L1, plan1 = run_forward(Q, K, V, True, budget=8 * GB)
+    say(f"in place: depth={plan1.depth} tasks={plan1.num_tasks} "
+        f"modelled={plan1.modelled_device_bytes / GB:.3f} GB")
+    assert plan1.reads_in_place == 1 and plan1.depth == 1 and plan1.num_tasks == 7
+    assert plan1.modelled_device_bytes <= 8 * GB
+    check(*gather_rows(O1, L1, rows), Of, Lf, 6e-4)
+    r1 = rel_l2(O1.numpy(), O0.numpy())
+    say(f"in place: rel_l2 vs depth 0 = {r1:.3e}")
+    assert r1 <= 1e-3
+    del O1, L1
+    # Section 3.3 / Table "interest_set": with staged inputs and c = 21
+    # (l = 5) one level of 21 tasks fits where c = 7 needs two levels
+    O2, L2, plan2 = run_forward(Q, K, V, True, budget=8 * GB, levels=[(21, (0, 1, 4, 14, 16))],
+                                read_in_place=False)
     say(f"c=21: depth={plan2.depth} tasks={plan2.num_tasks} "
         f"modelled={plan2.modelled_device_bytes / GB:.3f} GB")
     assert plan2.depth == 1 and plan2.num_tasks == 21 and plan2.modelled_device_bytes <= 8 * GB
