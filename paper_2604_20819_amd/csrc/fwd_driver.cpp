@@ -156,6 +156,46 @@ class HostMerger {
   bool stop_ = false, ok_ = true;
 };
 
+// One piece of a task's staging: local rows [dst, dst + length) of the task
+// come either from the host tensors at global row `src`, or, when the task
+// staged just before holds the same tokens, from its staged rows at its local
+// row `src` (device to device).
+struct StagePiece {
+  int64_t dst, src, length;
+  bool reuse;
+};
+
+// Splits `cur`'s runs against the runs of the previously staged task `prev`
+// (both ascending in global order): overlapping tokens are reused, the rest
+// comes from the host.  Consecutive tasks in quorum order share chunks (at
+// depth 1 with I = (0, 1, 3), task q + 1 holds chunk q + 1 of task q).
+std::vector<StagePiece> stage_pieces(const Task& cur, const Task* prev) {
+  std::vector<StagePiece> out;
+  size_t pi = 0;
+  for (const Run& r : cur.runs) {
+    int64_t g = r.global_start;
+    const int64_t end = r.global_start + r.length;
+    while (g < end) {
+      // first run of prev that ends after g
+      while (prev && pi < prev->runs.size() &&
+             prev->runs[pi].global_start + prev->runs[pi].length <= g)
+        ++pi;
+      const Run* pr = (prev && pi < prev->runs.size()) ? &prev->runs[pi] : nullptr;
+      const int64_t dst = r.local_start + (g - r.global_start);
+      if (pr && pr->global_start <= g) {
+        const int64_t e = std::min(end, pr->global_start + pr->length);
+        out.push_back({dst, pr->local_start + (g - pr->global_start), e - g, true});
+        g = e;
+      } else {
+        const int64_t e = pr ? std::min(end, pr->global_start) : end;
+        out.push_back({dst, g, e - g, false});
+        g = e;
+      }
+    }
+  }
+  return out;
+}
+
 }  // namespace
 
 cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_tensor* K,
@@ -300,6 +340,9 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
     std::vector<bool> used(nslot, false);
     const hipMemcpyKind kind = in_dev ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice;
     const char* srcs[3] = {(const char*)Q->data, (const char*)K->data, (const char*)V->data};
+    // the task staged last and where its rows sit (host inputs reuse them)
+    const Task* prev_task = nullptr;
+    const char* prev_sub = nullptr;
     for (int64_t k = 0; k < ngroup; ++k) {
       const Group& G = p->groups[k];
       const int64_t si = k % nslot;
@@ -327,21 +370,37 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
           sa.B = int32_t(B); sa.runs = d_tab + p->table_off[t].runs;
           sa.n_runs = int32_t(task.runs.size());
           CQSA_HIP(launch_stage(sa, C->copy));
+          rec.stats.d2d_bytes += uint64_t(3) * B * Li * row_bytes;
         } else {
-          // host inputs: one asynchronous H2D copy per run and batch element
-          for (int x = 0; x < 3; ++x)
-            for (const Run& r : task.runs)
-              for (int64_t b = 0; b < B; ++b)
-                CQSA_HIP(hipMemcpyAsync(dsts[x] + (b * Li + r.local_start) * row_bytes,
-                                        srcs[x] + (b * L + r.global_start) * row_bytes,
-                                        r.length * row_bytes, kind, C->copy));
+          // host inputs: tokens the previously staged task also holds are
+          // copied device to device from its staged rows, which stay intact
+          // until a later staging (this copy stream) overwrites them; the
+          // rest crosses the host link, one asynchronous copy per piece and
+          // batch element.  No reuse when both tasks use the same sub-slot.
+          const bool can_reuse = prev_task && prev_sub != sub;
+          const int64_t Lp = can_reuse ? prev_task->L_local : 0;
+          const uint64_t in_bp = in_b;  // sub-slot tensor stride, as for dsts
+          for (const StagePiece& pc : stage_pieces(task, can_reuse ? prev_task : nullptr)) {
+            for (int x = 0; x < 3; ++x)
+              for (int64_t b = 0; b < B; ++b) {
+                char* dst = dsts[x] + (b * Li + pc.dst) * row_bytes;
+                if (pc.reuse)
+                  CQSA_HIP(hipMemcpyAsync(dst, prev_sub + x * in_bp + (b * Lp + pc.src) * row_bytes,
+                                          pc.length * row_bytes, hipMemcpyDeviceToDevice, C->copy));
+                else
+                  CQSA_HIP(hipMemcpyAsync(dst, srcs[x] + (b * L + pc.src) * row_bytes,
+                                          pc.length * row_bytes, kind, C->copy));
+              }
+            const uint64_t moved = uint64_t(3) * B * pc.length * row_bytes;
+            if (pc.reuse)
+              rec.stats.d2d_bytes += moved;
+            else
+              rec.stats.h2d_bytes += moved;
+          }
+          prev_task = &task;
+          prev_sub = sub;
         }
         span_end(sp, C->copy, kStStage);
-        const uint64_t moved = uint64_t(3) * B * Li * row_bytes;
-        if (in_dev)
-          rec.stats.d2d_bytes += moved;
-        else
-          rec.stats.h2d_bytes += moved;
       }
       CQSA_HIP(hipEventRecord(ev_staged[si], C->copy));
       // Consecutive groups alternate between the caller's stream and a second
@@ -415,8 +474,8 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
         const hipEvent_t wait_ev = ev_free[si];
         const Task* tp = &p->tasks[t];
         last_item[si] = merger.push([=, &rec]() -> bool {
-          auto t0 = std::chrono::steady_clock::now();
           if (hipEventSynchronize(wait_ev) != hipSuccess) return false;
+          auto t0 = std::chrono::steady_clock::now();  // the merge alone, not the wait
           host_merge(*tp, h_acc, h_m, h_l, acc, m, l, B, L, H, d);
           auto t1 = std::chrono::steady_clock::now();
           rec.host_merge_ms += std::chrono::duration<double, std::milli>(t1 - t0).count();

@@ -43,6 +43,24 @@ def run_forward(Q, K, V, causal, depth=-1, budget=0, n_slots=2, host=False, scal
     return O.cpu(), LSE.cpu(), plan
 
 
+def reused_tokens(plan, reuse=True):
+    """Tokens each staged task shares with the task staged just before it
+    (interval intersection of the two tasks' global runs), summed over the
+    plan; these are copied on the device instead of over the host link."""
+    if not reuse:
+        return 0
+    total, prev = 0, None
+    for t in range(plan.num_tasks):
+        tk = plan.task(t)
+        if tk["L_local"] == 0:
+            continue
+        runs = [(g, g + n) for g, n, _ in tk["runs"]]
+        if prev is not None:
+            total += sum(max(0, min(b1, b2) - max(a1, a2)) for a1, b1 in prev for a2, b2 in runs)
+        prev = runs
+    return total
+
+
 def rel_l2(x, ref):
     x = np.asarray(x, dtype=np.float64); ref = np.asarray(ref, dtype=np.float64)
     return float(np.linalg.norm((x - ref).ravel()) / np.linalg.norm(ref.ravel()))
