@@ -49,7 +49,8 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
   const int L = a.L;
   const int64_t nstrips = (L + BM - 1) / BM;
   const int64_t work = xcd_remap(blockIdx.x, nstrips * a.H * a.B);
-  const int strip = int(work % nstrips);
+  // causal: the last query strips see the most keys, so they go first
+  const int strip = a.causal ? int(nstrips - 1 - work % nstrips) : int(work % nstrips);
   const int h = int((work / nstrips) % a.H);
   const int b = int(work / (nstrips * a.H));
   const DevRun* runs_g = (const DevRun*)a.runs;

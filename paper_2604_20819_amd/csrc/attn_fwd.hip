@@ -57,7 +57,8 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
   const DevTask tk = a.tasks[tj];
   const int L = int(tk.L_local);
   const int64_t nstrips = (L + BM - 1) / BM;
-  const int strip = int(work % nstrips);
+  // causal: the last strips see the most keys, so they go first
+  const int strip = a.causal ? int(nstrips - 1 - work % nstrips) : int(work % nstrips);
   const int h = int((work / nstrips) % a.H);
   const int b = int(work / (nstrips * a.H));
   const int n_runs = tk.n_runs;
