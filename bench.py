@@ -303,7 +303,7 @@ def headdim_sweep(args):
             def fb():
                 cq.cqsa_forward(plan, q, k, v, O, LSE)
                 cq.cqsa_backward(plan, q, k, v, O, LSE, do, dQ, dK, dV)
-            msb, _ = time_steps(fb, max(2, steps // 2), 1, torch)
+            msb, _ = time_steps(fb, max(3, steps // 2), 2, torch)
             row[tag + "_fwd_bwd_tflops"] = round(3.5 * flops / (msb * 1e-3) / 1e12, 2)
             row[tag + "_fwd_bwd_ms"] = round(msb, 3)
         row["fwd_runtime_ratio"] = round(row["depth1_ms"] / row["undecomposed_ms"], 4)
@@ -357,14 +357,24 @@ def main():
                                                             tasks_per_slot=tps,
                                                             read_in_place=in_place))
 
-    cq.cqsa_set_timing(True)
-
-    def fwd_step(depth, tps=0, in_place=None):
+    def fwd_step(depth, tps=0, in_place=None, stats=True):
         def step():
             plan = plan_for(depth, tps=tps, in_place=in_place)   # planning is part of the step
             cq.cqsa_forward(plan, q, k, v, O, LSE)
-            return cq.cqsa_last_stats()
+            return cq.cqsa_last_stats() if stats else None
         return step
+
+    # Each rate: steps enqueued back to back with per-stage timing off, so
+    # nothing synchronises inside the timed region; then the same steps again
+    # with HIP-event timing on (one synchronisation per step) for the
+    # per-kernel figures.
+    def rate_and_stats(depth, tps=0, in_place=None):
+        cq.cqsa_set_timing(False)
+        ms, _ = time_steps(fwd_step(depth, tps, in_place, stats=False), args.steps, args.warmup,
+                           torch)
+        cq.cqsa_set_timing(True)
+        _, st = time_steps(fwd_step(depth, tps, in_place), args.steps, args.warmup, torch)
+        return ms, st
 
     def mean(stats, key):
         return sum(s[key] for s in stats) / len(stats)
@@ -376,21 +386,19 @@ def main():
         plan_for(1)
     plan_ms = (time.perf_counter() - t0) * 1e3 / 20
     # headline: the decomposed forward with the automatic launch grouping
-    ms_dec, stats = time_steps(fwd_step(1), args.steps, args.warmup, torch)
+    ms_dec, stats = rate_and_stats(1)
     launches = stats[-1]["inner_launches"]
     ms_launch = mean(stats, "ms_inner") / launches
     ms_busy = mean(stats, "ms_inner_busy")
     # undecomposed call (depth 0): one launch of the same kernel, no merge
-    ms_und, st_und = time_steps(fwd_step(0), args.steps, args.warmup, torch)
+    ms_und, st_und = rate_and_stats(0)
     # one task per launch on two alternating streams, merges overlapping
-    ms_one, st_one = time_steps(fwd_step(1, tps=1), args.steps, args.warmup, torch)
+    ms_one, st_one = rate_and_stats(1, tps=1)
     # the same decomposition with every task's runs gathered into staging
     # slots first (the kernels otherwise read the caller's tensors in place),
     # under its own automatic grouping and in one launch
-    ms_staged, st_staged = time_steps(fwd_step(1, in_place=False), args.steps, args.warmup,
-                                      torch)
-    ms_one_st, st_one_st = time_steps(fwd_step(1, tps=7, in_place=False), args.steps,
-                                      args.warmup, torch)
+    ms_staged, st_staged = rate_and_stats(1, in_place=False)
+    ms_one_st, st_one_st = rate_and_stats(1, tps=7, in_place=False)
 
     tflops = flops / (ms_dec * 1e-3) / 1e12
     # the seven tasks' kept pairs sum to L^2 (each pair once): flops per launch
@@ -429,12 +437,18 @@ def main():
         dQ, dK, dV = (torch.empty((B, L, H, D), dtype=torch.float32, device=dev) for _ in range(3))
         bstats = []
 
-        def fb_step():
-            plan = plan_for(1, backward=True)
-            cq.cqsa_forward(plan, q, k, v, O, LSE)
-            cq.cqsa_backward(plan, q, k, v, O, LSE, do, dQ, dK, dV)
-            bstats.append(cq.cqsa_last_stats())
-        ms_fb, _ = time_steps(fb_step, max(3, args.steps // 2), 1, torch)
+        def fb_step(stats=True):
+            def step():
+                plan = plan_for(1, backward=True)
+                cq.cqsa_forward(plan, q, k, v, O, LSE)
+                cq.cqsa_backward(plan, q, k, v, O, LSE, do, dQ, dK, dV)
+                if stats:
+                    bstats.append(cq.cqsa_last_stats())
+            return step
+        cq.cqsa_set_timing(False)
+        ms_fb, _ = time_steps(fb_step(False), max(3, args.steps // 2), 1, torch)
+        cq.cqsa_set_timing(True)
+        time_steps(fb_step(), max(3, args.steps // 2), 1, torch)
         bstats = bstats[1:]
         fwd_bwd = {"tflops": 3.5 * flops / (ms_fb * 1e-3) / 1e12, "ms_per_step": ms_fb}
         pre_bytes = B * L * H * (2 * D + 4 * D) + B * H * L * 4     # dO, O in; D out

@@ -315,6 +315,12 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
     }
 }
 
+// Above d = 192 the dK/dV accumulators of a whole row (2 x d/32 blocks) and
+// the wave's K rows do not fit in registers: the columns of dK and dV are
+// then split over two work groups per key strip, each recomputing S and dP
+// over the full d and accumulating its half of the columns.
+template <int D> constexpr int dkdv_splits() { return D > 192 ? 2 : 1; }
+
 template <typename E, int D>
 __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_bwd_dkdv(const BwdArgs a) {
   // 32-query tiles (two per 64-token summary block) keep the registers and
@@ -328,6 +334,7 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
   constexpr int P2 = DP * 2;
   constexpr int DK = D / 16, DB = D / 32, CHUNKS = DP / 8;
   constexpr int RPI = 64 / CHUNKS, NDMA = BQ / RPI / 4;
+  constexpr int NSPLIT = dkdv_splits<D>(), DBO = (DB + NSPLIT - 1) / NSPLIT;
   typedef typename E::vec8 vec8;
   auto swz = [](int r) { return 2 * (r & 3) + ((r >> 2) & 1); };
 
@@ -345,7 +352,10 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int L = a.L;
   const int64_t nstrips = (L + BK - 1) / BK;
-  const int64_t work = xcd_remap(blockIdx.x, nstrips * a.H * a.B);
+  // the two column halves of a strip are consecutive work items (same XCD)
+  const int64_t item = xcd_remap(blockIdx.x, nstrips * a.H * a.B * NSPLIT);
+  const int64_t work = item / NSPLIT;
+  const int db0 = int(item % NSPLIT) * DBO;  // first 32-column block of dK, dV owned
   const int strip = int(work % nstrips);
   const int h = int((work / nstrips) % a.H);
   const int b = int(work / (nstrips * a.H));
@@ -427,20 +437,29 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
 
   // Query-tile skipping as in the forward (a tile is dead when fully masked
   // or, causally, entirely before the strip's first key): a window of 64
-  // tiles' summaries per vector load and a ballot for the first live one.
+  // tiles' summaries and first rows (kNoRow when the tile's block crosses a
+  // run boundary) per vector load and a ballot for the first live one.
   struct Window {
     uint32_t an, on;
+    int32_t row;
   };
   auto window = [&](int t0) {
     const int t = t0 + lane;
-    Window w{0xFFFFFFFFu, 0u};
+    Window w{0xFFFFFFFFu, 0u, 0};
     if (t < nqt) {
       w.an = a.blk_and[t >> 1];
       w.on = a.blk_or[t >> 1];
+      if (in_place) {
+        const int32_t r = a.rows[t >> 1];
+        w.row = r != kNoRow ? r + (t & 1) * BQ : kNoRow;
+      } else {
+        w.row = t * BQ;
+      }
     }
     return w;
   };
-  auto pick = [&](int t0, const Window& w, uint32_t& qor_out, uint32_t& qand_out) -> int {
+  auto pick = [&](int t0, const Window& w, uint32_t& qor_out, uint32_t& qand_out,
+                  int32_t& row_out) -> int {
     const int t = t0 + lane;
     const bool ok = t < nqt && !(causal && t * BQ + BQ - 1 < first_key) && (kand & w.an) == 0u;
     const uint64_t m = __builtin_amdgcn_ballot_w64(ok);
@@ -448,21 +467,15 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
     const int i = __builtin_ctzll(m);
     qand_out = __builtin_amdgcn_readlane(w.an, i);
     qor_out = __builtin_amdgcn_readlane(w.on, i);
+    row_out = __builtin_amdgcn_readlane(w.row, i);
     return t0 + i;
   };
-  auto next_live = [&](int t, uint32_t& qor_out, uint32_t& qand_out) -> int {
+  auto next_live = [&](int t, uint32_t& qor_out, uint32_t& qand_out, int32_t& row_out) -> int {
     for (; t < nqt; t += 64) {
-      const int r = pick(t, window(t), qor_out, qand_out);
+      const int r = pick(t, window(t), qor_out, qand_out, row_out);
       if (r >= 0) return r;
     }
     return nqt;
-  };
-  // First row of query tile t < nqt in the inputs, or kNoRow when its block
-  // crosses a run boundary (a scalar load, issued one tile ahead of its use).
-  auto tile_row = [&](int t) -> int32_t {
-    if (!in_place) return t * BQ;
-    const int32_t r = a.rows[t >> 1];
-    return r != kNoRow ? r + (t & 1) * BQ : kNoRow;
   };
 
   // Query-tile loads for the next tile, issued right after a tile barrier:
@@ -531,9 +544,9 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
     }
   };
 
-  f32x16 dk[DB], dv[DB];
+  f32x16 dk[DBO], dv[DBO];
 #pragma unroll
-  for (int db = 0; db < DB; ++db)
+  for (int db = 0; db < DBO; ++db)
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       dk[db][r] = 0.f;
@@ -544,13 +557,13 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
   const uint32_t kbits = kvalid ? run_bits(runs_s, a.n_runs, mykey) : 0u;
 
   uint32_t qor = 0u, qand = 0u, nor = 0u, nand = 0u;
-  int qt = next_live(causal ? first_key / BQ : 0, qor, qand);
+  int32_t qrow = 0, nrow = 0;
+  int qt = next_live(causal ? first_key / BQ : 0, qor, qand, qrow);
   if (qt < nqt) {
-    gload(0, qt, tile_row(qt));
+    gload(0, qt, qrow);
     sstore(0);
   }
-  int qn = qt < nqt ? next_live(qt + 1, nor, nand) : nqt;
-  int32_t nrow = qn < nqt ? tile_row(qn) : 0;
+  int qn = qt < nqt ? next_live(qt + 1, nor, nand, nrow) : nqt;
   int buf = 0;
   while (qt < nqt) {
     // this wave's tile loads have landed; after the barrier every wave's
@@ -619,8 +632,9 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
           const vec8 bs = pack8<E>(dsv);
           const int trow = 32 * qb + 16 * sub + 4 * half + ((lane & 15) >> 2);
 #pragma unroll
-          for (int db = 0; db < DB; ++db) {
-            const int col = 32 * db + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+          for (int db = 0; db < DBO; ++db) {
+            if (NSPLIT > 1 && db0 + db >= DB) break;  // the last half of an odd d/32
+            const int col = 32 * (db0 + db) + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
             const int tcol = (((col >> 3) ^ swz(trow)) << 4) + (col & 7) * 2;
             const char* po = osb + trow * P2 + tcol;
             dv[db] = mfma32<E>(lds_tr_pair<E>(po, po + 8 * P2), bp, dv[db]);
@@ -636,9 +650,8 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
     if (qn < nqt) {
       sstore(buf ^ 1);
       if (qc < nqt) {
-        qc2 = pick(qc, cw, or2, and2);
-        if (qc2 < 0) qc2 = next_live(qc + 64, or2, and2);
-        if (qc2 < nqt) row2 = tile_row(qc2);
+        qc2 = pick(qc, cw, or2, and2, row2);
+        if (qc2 < 0) qc2 = next_live(qc + 64, or2, and2, row2);
       }
     }
     buf ^= 1;
@@ -656,10 +669,11 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
   float* dkp = a.dk + (int64_t(b) * a.Lg + gk) * rs + int64_t(h) * D;
   float* dvp = a.dv + (int64_t(b) * a.Lg + gk) * rs + int64_t(h) * D;
 #pragma unroll
-  for (int db = 0; db < DB; ++db)
+  for (int db = 0; db < DBO; ++db) {
+    if (NSPLIT > 1 && db0 + db >= DB) break;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int off = 32 * db + 8 * i + 4 * half;
+      const int off = 32 * (db0 + db) + 8 * i + 4 * half;
       f32x4 x = *(f32x4*)(dkp + off), y = *(f32x4*)(dvp + off);
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
@@ -669,6 +683,7 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
       *(f32x4*)(dkp + off) = x;
       *(f32x4*)(dvp + off) = y;
     }
+  }
 }
 
 template <typename E, int D>
@@ -681,7 +696,7 @@ static hipError_t launch_dq_t(const BwdArgs& a, hipStream_t s) {
 
 template <typename E, int D>
 static hipError_t launch_dkdv_t(const BwdArgs& a, hipStream_t s) {
-  const int64_t n = ((a.L + 127) / 128) * int64_t(a.H) * a.B;
+  const int64_t n = ((a.L + 127) / 128) * int64_t(a.H) * a.B * dkdv_splits<D>();
   if (n == 0) return hipSuccess;
   hipLaunchKernelGGL((attn_bwd_dkdv<E, D>), dim3(unsigned(n)), dim3(256), 0, s, a);
   return hipGetLastError();

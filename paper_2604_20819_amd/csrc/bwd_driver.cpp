@@ -102,8 +102,7 @@ cqsa_status backward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa
   if (C->ws_free_valid) CQSA_HIP(hipStreamWaitEvent(st, C->ws_free, 0));
   CQSA_HIP(hipEventRecord(ev_start, st));
   CQSA_HIP(hipStreamWaitEvent(C->copy, ev_start, 0));
-  CQSA_HIP(hipMemcpyAsync(d_tab, p->packed.data(), p->packed.size(), hipMemcpyHostToDevice,
-                          C->copy));
+  if ((s = upload_image(C, p->packed, d_tab, C->copy)) != CQSA_OK) return s;
   CQSA_HIP(hipEventRecord(ev_tab, C->copy));
 
   // preprocess and zero-fill on the caller's stream

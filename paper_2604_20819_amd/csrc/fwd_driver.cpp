@@ -283,10 +283,19 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
   hipEvent_t* ev_free = &C->sync_events[2 + nslot];
   hipEvent_t* ev_inner = &C->sync_events[2 + 2 * nslot];
   if (C->ws_free_valid) CQSA_HIP(hipStreamWaitEvent(st, C->ws_free, 0));
-  CQSA_HIP(hipEventRecord(ev_start, st));
-  CQSA_HIP(hipStreamWaitEvent(C->copy, ev_start, 0));
-  CQSA_HIP(hipMemcpyAsync(d_tab, p->packed.data(), p->packed.size(), hipMemcpyHostToDevice,
-                          C->copy));
+  // With nothing to stage and a single launch group (the direct call, or
+  // inputs read in place with every task in one launch) the whole call runs
+  // on the caller's stream: each hop between streams costs the GPU an event
+  // round trip per call.  Otherwise the image and the staging copies go on
+  // the copy stream and merges on the auxiliary stream.
+  const bool one_stream = direct || (in_place && acc_dev && ngroup == 1);
+  const hipStream_t cs = one_stream ? st : C->copy;  // image and staging copies
+  const hipStream_t ms = one_stream ? st : C->aux;   // merges, statistics D2H
+  if (cs != st) {
+    CQSA_HIP(hipEventRecord(ev_start, st));
+    CQSA_HIP(hipStreamWaitEvent(cs, ev_start, 0));
+  }
+  if ((s = upload_image(C, p->packed, d_tab, cs)) != CQSA_OK) return s;
 
   auto span_begin = [&](hipStream_t sm) -> std::pair<hipEvent_t, hipEvent_t> {
     std::pair<hipEvent_t, hipEvent_t> sp{nullptr, nullptr};
@@ -302,8 +311,6 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
 
   float* Od = (float*)O->data;
   if (direct) {
-    CQSA_HIP(hipEventRecord(ev_staged[0], C->copy));
-    CQSA_HIP(hipStreamWaitEvent(st, ev_staged[0], 0));
     FwdArgs a{};
     a.q = Q->data; a.k = K->data; a.v = V->data;
     a.acc = Od; a.m = LSE; a.l = nullptr;
@@ -347,7 +354,7 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
       const Group& G = p->groups[k];
       const int64_t si = k % nslot;
       char* sb = slot_base(si);
-      if (used[si]) CQSA_HIP(hipStreamWaitEvent(C->copy, ev_free[si], 0));
+      if (used[si]) CQSA_HIP(hipStreamWaitEvent(cs, ev_free[si], 0));
       // gather every task of the group into its sub-slot
       int64_t wgs = 0;
       for (int64_t j = 0; j < G.count; ++j) {
@@ -358,7 +365,7 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
         if (Li == 0 || in_place) continue;
         char* sub = sb + uint64_t(j) * sub_bytes;
         char* dsts[3] = {sub, sub + in_b, sub + 2 * in_b};
-        auto sp = span_begin(C->copy);
+        auto sp = span_begin(cs);
         if (in_dev) {
           // device inputs: one gather kernel over the runs of all three tensors
           StageArgs sa{};
@@ -369,7 +376,7 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
           sa.n_tensors = 3; sa.row_bytes = int64_t(row_bytes); sa.Li = Li; sa.Lg = L;
           sa.B = int32_t(B); sa.runs = d_tab + p->table_off[t].runs;
           sa.n_runs = int32_t(task.runs.size());
-          CQSA_HIP(launch_stage(sa, C->copy));
+          CQSA_HIP(launch_stage(sa, cs));
           rec.stats.d2d_bytes += uint64_t(3) * B * Li * row_bytes;
         } else {
           // host inputs: tokens the previously staged task also holds are
@@ -386,10 +393,10 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
                 char* dst = dsts[x] + (b * Li + pc.dst) * row_bytes;
                 if (pc.reuse)
                   CQSA_HIP(hipMemcpyAsync(dst, prev_sub + x * in_bp + (b * Lp + pc.src) * row_bytes,
-                                          pc.length * row_bytes, hipMemcpyDeviceToDevice, C->copy));
+                                          pc.length * row_bytes, hipMemcpyDeviceToDevice, cs));
                 else
                   CQSA_HIP(hipMemcpyAsync(dst, srcs[x] + (b * L + pc.src) * row_bytes,
-                                          pc.length * row_bytes, kind, C->copy));
+                                          pc.length * row_bytes, kind, cs));
               }
             const uint64_t moved = uint64_t(3) * B * pc.length * row_bytes;
             if (pc.reuse)
@@ -400,15 +407,17 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
           prev_task = &task;
           prev_sub = sub;
         }
-        span_end(sp, C->copy, kStStage);
+        span_end(sp, cs, kStStage);
       }
-      CQSA_HIP(hipEventRecord(ev_staged[si], C->copy));
       // Consecutive groups alternate between the caller's stream and a second
       // compute stream, so a group's launch fills the tail of the previous
       // one (App. A.3: at most two slots in flight).  Inner kernels write
       // only their slot.
       const hipStream_t ls = (k & 1) ? C->lane : st;
-      CQSA_HIP(hipStreamWaitEvent(ls, ev_staged[si], 0));
+      if (ls != cs) {
+        CQSA_HIP(hipEventRecord(ev_staged[si], cs));
+        CQSA_HIP(hipStreamWaitEvent(ls, ev_staged[si], 0));
+      }
       FwdArgs a{};
       if (in_place) {
         a.q = Q->data; a.k = K->data; a.v = V->data;
@@ -435,7 +444,7 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
       if (acc_dev) {
         // merge on the auxiliary stream: combines run in group order there,
         // and the next group's inner kernel overlaps this one's combine
-        CQSA_HIP(hipStreamWaitEvent(C->aux, ev_inner[si], 0));
+        if (ms != ls) CQSA_HIP(hipStreamWaitEvent(ms, ev_inner[si], 0));
         CombineArgs cb{};
         cb.segs = (const DevSeg*)(d_tab + G.seg_off); cb.n_seg = G.n_seg;
         cb.contribs = (const DevContrib*)(d_tab + G.contrib_off);
@@ -445,12 +454,12 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
         cb.acc = acc; cb.m = m; cb.l = l; cb.L = L;
         cb.B = int32_t(B); cb.H = int32_t(H); cb.d = int32_t(d); cb.final = G.final ? 1 : 0;
         if (G.blocks > 0) {
-          auto sp = span_begin(C->aux);
-          CQSA_HIP(launch_combine(cb, G.blocks, C->aux));
-          span_end(sp, C->aux, kStMerge);
+          auto sp = span_begin(ms);
+          CQSA_HIP(launch_combine(cb, G.blocks, ms));
+          span_end(sp, ms, kStMerge);
           rec.stats.merge_launches += 1;
         }
-        CQSA_HIP(hipEventRecord(ev_free[si], C->aux));
+        CQSA_HIP(hipEventRecord(ev_free[si], ms));
       } else {
         // hand the statistics to the host: D2H into pinned staging, then merge;
         // the staging of this slot must have been consumed by its last merge
@@ -463,14 +472,14 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
         float* h_acc = (float*)hp;
         float* h_m = (float*)(hp + acc_b);
         float* h_l = (float*)(hp + acc_b + st_b);
-        CQSA_HIP(hipStreamWaitEvent(C->aux, ev_inner[si], 0));
-        auto sp = span_begin(C->aux);
-        CQSA_HIP(hipMemcpyAsync(h_acc, a.acc, rows * d * 4, hipMemcpyDeviceToHost, C->aux));
-        CQSA_HIP(hipMemcpyAsync(h_m, a.m, rows * 4, hipMemcpyDeviceToHost, C->aux));
-        CQSA_HIP(hipMemcpyAsync(h_l, a.l, rows * 4, hipMemcpyDeviceToHost, C->aux));
-        span_end(sp, C->aux, kStD2H);
+        CQSA_HIP(hipStreamWaitEvent(ms, ev_inner[si], 0));
+        auto sp = span_begin(ms);
+        CQSA_HIP(hipMemcpyAsync(h_acc, a.acc, rows * d * 4, hipMemcpyDeviceToHost, ms));
+        CQSA_HIP(hipMemcpyAsync(h_m, a.m, rows * 4, hipMemcpyDeviceToHost, ms));
+        CQSA_HIP(hipMemcpyAsync(h_l, a.l, rows * 4, hipMemcpyDeviceToHost, ms));
+        span_end(sp, ms, kStD2H);
         rec.stats.d2h_bytes += rows * (d + 2) * 4;
-        CQSA_HIP(hipEventRecord(ev_free[si], C->aux));
+        CQSA_HIP(hipEventRecord(ev_free[si], ms));
         const hipEvent_t wait_ev = ev_free[si];
         const Task* tp = &p->tasks[t];
         last_item[si] = merger.push([=, &rec]() -> bool {
@@ -492,8 +501,10 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
       rec.host_final_ms += std::chrono::duration<double, std::milli>(t1 - t0).count();
     }
     // every inner kernel precedes its merge or D2H on the auxiliary stream
-    CQSA_HIP(hipEventRecord(ev_tail, C->aux));
-    CQSA_HIP(hipStreamWaitEvent(st, ev_tail, 0));
+    if (ms != st) {
+      CQSA_HIP(hipEventRecord(ev_tail, ms));
+      CQSA_HIP(hipStreamWaitEvent(st, ev_tail, 0));
+    }
   }
   if (rec.timing) CQSA_HIP(hipEventRecord(rec.wall1, st));
   CQSA_HIP(hipEventRecord(C->ws_free, st));

@@ -111,6 +111,32 @@ cqsa_status acquire_pinned(DevCtx* c, size_t bytes, void** out) {
   return CQSA_OK;
 }
 
+cqsa_status upload_image(DevCtx* c, const std::vector<uint8_t>& image, void* dst, hipStream_t s) {
+  const size_t n = image.size();
+  if (n == 0) return CQSA_OK;
+  const int i = c->img_next;
+  c->img_next ^= 1;
+  if (c->img_valid[i]) CQSA_HIP(hipEventSynchronize(c->img_done[i]));
+  if (c->img_bytes[i] < n) {
+    if (c->img_pin[i]) (void)hipHostFree(c->img_pin[i]);
+    c->img_pin[i] = nullptr;
+    c->img_bytes[i] = 0;
+    const hipError_t e = hipHostMalloc(&c->img_pin[i], n, hipHostMallocDefault);
+    if (e != hipSuccess) {
+      c->img_pin[i] = nullptr;
+      (void)hipGetLastError();
+      return fail(CQSA_ERR_INTERNAL, "hipHostMalloc of the plan image staging failed");
+    }
+    c->img_bytes[i] = n;
+  }
+  if (!c->img_done[i]) CQSA_HIP(hipEventCreateWithFlags(&c->img_done[i], hipEventDisableTiming));
+  std::memcpy(c->img_pin[i], image.data(), n);
+  CQSA_HIP(hipMemcpyAsync(dst, c->img_pin[i], n, hipMemcpyHostToDevice, s));
+  CQSA_HIP(hipEventRecord(c->img_done[i], s));
+  c->img_valid[i] = true;
+  return CQSA_OK;
+}
+
 void CallRecord::reset() {
   for (hipEvent_t e : owned) (void)hipEventDestroy(e);
   owned.clear();
@@ -231,6 +257,12 @@ cqsa_status cqsa_release_workspace(void) {
   if (c->pin) (void)hipHostFree(c->pin);
   c->pin = nullptr;
   c->pin_bytes = 0;
+  for (int i = 0; i < 2; ++i) {
+    if (c->img_pin[i]) (void)hipHostFree(c->img_pin[i]);
+    c->img_pin[i] = nullptr;
+    c->img_bytes[i] = 0;
+    c->img_valid[i] = false;
+  }
   return CQSA_OK;
 }
 

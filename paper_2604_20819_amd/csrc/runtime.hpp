@@ -29,6 +29,12 @@ struct DevCtx {
   size_t ws_bytes = 0;
   void* pin = nullptr;          // cached pinned host staging for host accumulation
   size_t pin_bytes = 0;
+  // pinned host ring the plan images are uploaded from (see upload_image)
+  void* img_pin[2] = {nullptr, nullptr};
+  size_t img_bytes[2] = {0, 0};
+  hipEvent_t img_done[2] = {nullptr, nullptr};
+  bool img_valid[2] = {false, false};
+  int img_next = 0;
   std::vector<hipEvent_t> sync_events;  // reusable non-timing events
   std::mutex mu;
 };
@@ -45,6 +51,12 @@ struct Workspace {
 cqsa_status acquire_workspace(DevCtx* c, size_t bytes, Workspace* ws);
 void release_workspace(DevCtx* c, Workspace* ws, hipStream_t s);
 cqsa_status acquire_pinned(DevCtx* c, size_t bytes, void** out);
+// Enqueues the H2D copy of a plan image on stream s.  The bytes go through a
+// ring of two pinned host buffers: a copy from pageable memory would block
+// the host until the stream reached it (serialising consecutive calls), and
+// an asynchronous copy must not read a plan the caller may destroy as soon
+// as the call returns.  A buffer is refilled once its previous copy is done.
+cqsa_status upload_image(DevCtx* c, const std::vector<uint8_t>& image, void* dst, hipStream_t s);
 
 // Event pairs for the optional per-stage timing of the last call.
 enum Stage { kStStage = 0, kStInner, kStMerge, kStFinal, kStD2H, kStCount };
