@@ -315,11 +315,11 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
     }
 }
 
-// Above d = 192 the dK/dV accumulators of a whole row (2 x d/32 blocks) and
+// Above d = 160 the dK/dV accumulators of a whole row (2 x d/32 blocks) and
 // the wave's K rows do not fit in registers: the columns of dK and dV are
 // then split over two work groups per key strip, each recomputing S and dP
 // over the full d and accumulating its half of the columns.
-template <int D> constexpr int dkdv_splits() { return D > 192 ? 2 : 1; }
+template <int D> constexpr int dkdv_splits() { return D > 160 ? 2 : 1; }
 
 template <typename E, int D>
 __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_bwd_dkdv(const BwdArgs a) {
