@@ -49,8 +49,9 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
   const int L = a.L;
   const int64_t nstrips = (L + BM - 1) / BM;
   const int64_t work = xcd_remap(blockIdx.x, nstrips * a.H * a.B);
-  // causal: the last query strips see the most keys, so they go first
-  const int strip = a.causal ? int(nstrips - 1 - work % nstrips) : int(work % nstrips);
+  // strips in the task's launch order (most live key tiles first)
+  static_assert(BM == kStrip, "strip tables are built for kStrip-row strips");
+  const int strip = a.qorder[work % nstrips];
   const int h = int((work / nstrips) % a.H);
   const int b = int(work / (nstrips * a.H));
   const DevRun* runs_g = (const DevRun*)a.runs;
@@ -356,7 +357,9 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
   const int64_t item = xcd_remap(blockIdx.x, nstrips * a.H * a.B * NSPLIT);
   const int64_t work = item / NSPLIT;
   const int db0 = int(item % NSPLIT) * DBO;  // first 32-column block of dK, dV owned
-  const int strip = int(work % nstrips);
+  // key strips in the task's launch order (most live query tiles first)
+  static_assert(BK == kStrip, "strip tables are built for kStrip-row strips");
+  const int strip = a.korder[work % nstrips];
   const int h = int((work / nstrips) % a.H);
   const int b = int(work / (nstrips * a.H));
   const DevRun* runs_g = (const DevRun*)a.runs;

@@ -57,8 +57,9 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
   const DevTask tk = a.tasks[tj];
   const int L = int(tk.L_local);
   const int64_t nstrips = (L + BM - 1) / BM;
-  // causal: the last strips see the most keys, so they go first
-  const int strip = a.causal ? int(nstrips - 1 - work % nstrips) : int(work % nstrips);
+  // strips in the task's launch order (most live key tiles first)
+  static_assert(BM == kStrip, "strip tables are built for kStrip-row strips");
+  const int strip = ((const int32_t*)(a.tab + tk.qorder_off))[work % nstrips];
   const int h = int((work / nstrips) % a.H);
   const int b = int(work / (nstrips * a.H));
   const int n_runs = tk.n_runs;

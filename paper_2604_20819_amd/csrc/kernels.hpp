@@ -70,6 +70,8 @@ struct BwdArgs {
   const void* dO;
   int32_t in_place;
   const int32_t* rows;  // block row table (records.hpp), used when in_place
+  const int32_t* qorder; // query-strip launch order (records.hpp, DevTask::qorder_off)
+  const int32_t* korder; // key-strip launch order
   int32_t L;            // task length
   int32_t B, H;
   int32_t causal;

@@ -293,7 +293,74 @@ std::vector<Group> make_groups(int64_t ntask, int32_t group_size) {
   return gs;
 }
 
-void pack_image(const std::vector<Task>& tasks, const SegmentCover& sc, int32_t H,
+namespace {
+
+// Stable permutation of 0..n-1 by descending count.
+std::vector<int32_t> longest_first(const std::vector<int64_t>& count) {
+  std::vector<int32_t> ord(count.size());
+  for (size_t i = 0; i < ord.size(); ++i) ord[i] = int32_t(i);
+  std::stable_sort(ord.begin(), ord.end(),
+                   [&](int32_t a, int32_t b) { return count[size_t(a)] > count[size_t(b)]; });
+  return ord;
+}
+
+}  // namespace
+
+// Prefix counts of each distinct value of `vals` (a task's block ANDs take a
+// few values: the group-bit patterns of its runs and of blocks that straddle
+// runs).  count(i, p) = positions before p holding value v[i].
+struct ValuePrefix {
+  std::vector<uint32_t> v;
+  std::vector<std::vector<int32_t>> pre;
+  explicit ValuePrefix(const std::vector<uint32_t>& vals) {
+    for (uint32_t x : vals)
+      if (std::find(v.begin(), v.end(), x) == v.end()) v.push_back(x);
+    pre.assign(v.size(), std::vector<int32_t>(vals.size() + 1, 0));
+    for (size_t i = 0; i < v.size(); ++i)
+      for (size_t p = 0; p < vals.size(); ++p) pre[i][p + 1] = pre[i][p] + (vals[p] == v[i] ? 1 : 0);
+  }
+  // positions in [lo, hi) whose value shares no bit with m
+  int64_t disjoint(uint32_t m, int64_t lo, int64_t hi) const {
+    int64_t n = 0;
+    if (hi <= lo) return 0;
+    for (size_t i = 0; i < v.size(); ++i)
+      if ((v[i] & m) == 0u) n += pre[i][size_t(hi)] - pre[i][size_t(lo)];
+    return n;
+  }
+};
+
+std::vector<int32_t> query_strip_order(const Task& t, bool causal) {
+  const int64_t L = t.L_local, nb = int64_t(t.blk_and.size());
+  const int64_t ns = (L + kStrip - 1) / kStrip;
+  const ValuePrefix vp(t.blk_and);  // 64-key tile k is block k
+  std::vector<int64_t> live(size_t(ns), 0);
+  for (int64_t s = 0; s < ns; ++s) {
+    const int64_t last = std::min(L, (s + 1) * kStrip) - 1;
+    const uint32_t qand = t.blk_and[size_t(2 * s)] & t.blk_and[size_t(last / kBlock)];
+    live[size_t(s)] = vp.disjoint(qand, 0, causal ? last / kBlock + 1 : nb);
+  }
+  return longest_first(live);
+}
+
+std::vector<int32_t> key_strip_order(const Task& t, bool causal) {
+  const int64_t L = t.L_local, nq = (L + 31) / 32;
+  const int64_t ns = (L + kStrip - 1) / kStrip;
+  std::vector<uint32_t> tile_and(static_cast<size_t>(nq));  // 32-query tile q lies in block q / 2
+  for (int64_t q = 0; q < nq; ++q) tile_and[size_t(q)] = t.blk_and[size_t(q / 2)];
+  const ValuePrefix vp(tile_and);
+  std::vector<int64_t> live(size_t(ns), 0);
+  for (int64_t s = 0; s < ns; ++s) {
+    const int64_t first = s * kStrip, last = std::min(L, (s + 1) * kStrip) - 1;
+    const uint32_t kand = t.blk_and[size_t(2 * s)] & t.blk_and[size_t(last / kBlock)];
+    // causally, tile q is dead when its last query, 32 q + 31, precedes the
+    // strip's first key (a multiple of 32): the first live tile is first / 32
+    const int64_t q0 = causal ? first / 32 : 0;
+    live[size_t(s)] = vp.disjoint(kand, q0, nq);
+  }
+  return longest_first(live);
+}
+
+void pack_image(const std::vector<Task>& tasks, const SegmentCover& sc, int32_t H, bool causal,
                 std::vector<Group>* groups, std::vector<uint8_t>* image,
                 std::vector<TableOffsets>* offs) {
   std::vector<uint8_t>& im = *image;
@@ -331,8 +398,14 @@ void pack_image(const std::vector<Task>& tasks, const SegmentCover& sc, int32_t 
                               : kNoRow;
       std::memcpy(im.data() + o.rows + i * 4, &row, 4);
     }
-    DevTask d{k.L_local, int64_t(o.runs), int64_t(o.blk_or), int64_t(o.blk_and),
-              int32_t(k.runs.size()), 0, int64_t(o.rows)};
+    // strip launch orders, longest first
+    const std::vector<int32_t> qo = query_strip_order(k, causal), ko = key_strip_order(k, causal);
+    o.qorder = reserve(qo.size() * 4);
+    if (!qo.empty()) std::memcpy(im.data() + o.qorder, qo.data(), qo.size() * 4);
+    o.korder = reserve(ko.size() * 4);
+    if (!ko.empty()) std::memcpy(im.data() + o.korder, ko.data(), ko.size() * 4);
+    DevTask d{k.L_local, int64_t(o.runs), int64_t(o.blk_or), int64_t(o.blk_and), int64_t(o.rows),
+              int64_t(o.qorder), int64_t(o.korder), int32_t(k.runs.size()), 0};
     std::memcpy(im.data() + hdr + t * sizeof(DevTask), &d, sizeof(d));
     offs->push_back(o);
   }

@@ -43,6 +43,8 @@ struct TableOffsets {
   uint64_t blk_or = 0;  // uint32[n_blocks]
   uint64_t blk_and = 0; // uint32[n_blocks]
   uint64_t rows = 0;    // int32[n_blocks] block row table (records.hpp, kNoRow)
+  uint64_t qorder = 0;  // int32[n_strips] query strips, longest first
+  uint64_t korder = 0;  // int32[n_strips] key strips, longest first
 };
 
 // A launch group: tasks [task0, task0 + count) are staged into one slot,
@@ -159,9 +161,18 @@ uint64_t bwd_slot_bytes(const Geometry& g, const cqsa_plan_opts& o, int64_t Lmax
 // Packs the plan image: the DevTask records, every task's runs and block
 // summaries, and every group's segments and contributions (filling the
 // groups' offsets and combine block counts for H heads).
-void pack_image(const std::vector<Task>& tasks, const SegmentCover& sc, int32_t H,
+void pack_image(const std::vector<Task>& tasks, const SegmentCover& sc, int32_t H, bool causal,
                 std::vector<Group>* groups, std::vector<uint8_t>* image,
                 std::vector<TableOffsets>* offs);
+
+// Strip orders of one task for its kernels' launch order (longest first):
+// 128-query strips by the 64-key tiles live for them, and 128-key strips by
+// the 32-query tiles live for them, with the kernels' liveness rule (a tile is
+// skipped when the AND of the strip's block summaries and of the tile's
+// shares a bit, or when it lies causally past the strip).  Ties keep strip
+// order.
+std::vector<int32_t> query_strip_order(const Task& t, bool causal);
+std::vector<int32_t> key_strip_order(const Task& t, bool causal);
 
 inline uint64_t align_up(uint64_t x, uint64_t a = 256) { return (x + a - 1) / a * a; }
 

@@ -28,10 +28,18 @@ struct DevTask {
   int64_t runs_off;   // DevRun[n_runs]
   int64_t or_off;     // uint32[ceil(L_local / 64)] block OR of the group bits
   int64_t and_off;    // uint32[ceil(L_local / 64)] block AND of the group bits
+  int64_t row_off;    // int32[ceil(L_local / 64)] block rows (see kNoRow)
+  int64_t qorder_off; // int32[ceil(L_local / kStrip)] query strips, most live key tiles first
+  int64_t korder_off; // int32[ceil(L_local / kStrip)] key strips, most live query tiles first
   int32_t n_runs;
   int32_t pad;
-  int64_t row_off;    // int32[ceil(L_local / 64)] block rows (see kNoRow)
 };
+
+// Rows of the strips the MFMA kernels assign to a work group: 128 queries
+// (forward, dQ) or 128 keys (dK/dV).  Strips of a (task, b, h) run in the
+// order of the task's strip tables, longest first, so a launch ends with its
+// shortest strips.
+constexpr int kStrip = 128;
 
 // Block row table: entry i is the global row of local token 64 i when the
 // tokens of block i (up to the task end) lie in one run, so they are
@@ -62,7 +70,7 @@ struct DevContrib {
 };
 
 static_assert(sizeof(DevRun) == 32, "DevRun layout");
-static_assert(sizeof(DevTask) == 48, "DevTask layout");
+static_assert(sizeof(DevTask) == 64, "DevTask layout");
 static_assert(sizeof(DevSeg) == 40, "DevSeg layout");
 static_assert(sizeof(DevContrib) == 16, "DevContrib layout");
 
