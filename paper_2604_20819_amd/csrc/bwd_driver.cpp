@@ -8,7 +8,9 @@
 //                 Each stream keeps the tasks in order and a task holds each
 //                 token once, so these read-modify-writes never race;
 // copy stream   : gather each task's runs of Q, K, V, dO into slot t % S once
-//                 both kernels of the slot's previous task are done.
+//                 both kernels of the slot's previous task are done (staged
+//                 plans only: a plan that reads its inputs in place passes
+//                 the caller's tensors and the task's block row table).
 // Depth 0 reads the caller's tensors in place (the undecomposed backward).
 #include <algorithm>
 #include <cmath>

@@ -15,8 +15,13 @@
 //                    D2H of the statistics, merged by a host thread;
 //   the slot is freed by an event once its last reader is done.
 // With S >= 2 slots the gather of group k+1 overlaps the compute of group k
-// (App. A.3: transfers overlap compute).  Depth 0 on device-resident tensors
-// is the undecomposed call: one kernel that writes O and LSE directly.
+// (App. A.3: transfers overlap compute).  When the plan reads device-resident
+// inputs in place nothing is gathered: a slot holds statistics only, and
+// with a single launch group the image upload, the inner launch and the
+// merge all run on the caller's stream.  Host-resident inputs reuse the
+// tokens the previously staged task also holds (a device-to-device copy from
+// its staged rows).  Depth 0 on device-resident tensors is the undecomposed
+// call: one kernel that writes O and LSE directly.
 #include <algorithm>
 #include <cmath>
 #include <condition_variable>
