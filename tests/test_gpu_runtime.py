@@ -129,3 +129,43 @@ def test_call_statistics(depth, tps, in_place):
     assert 0 < st["workspace_bytes"] <= plan.modelled_device_bytes
     assert st["ms_wall"] > 0 and 0 < st["ms_inner_busy"] <= st["ms_inner"] + 1e-6
     assert np.isfinite(O.numpy()).all()
+
+
+def test_back_to_back_calls_on_plans_destroyed_at_once():
+    """Calls return before their GPU work runs.  Each call copies its plan's
+    task tables to the device from library-owned pinned memory, so a plan may
+    be destroyed as soon as the call returns: here eight forwards on fresh
+    plans of two shapes (staged and in place, one and several launch groups)
+    are issued back to back, each plan dropped at once, and every output must
+    equal the same call made in isolation."""
+    need_gpu()
+    import gc
+    L, H, d = 2500, 2, 64
+    Q, K, V = _inputs(L=L, H=H, d=d, seed=61)
+    q, k, v = (x.cuda() for x in (Q, K, V))
+    shapes = [dict(depth=1, read_in_place=True), dict(depth=2, read_in_place=False, tasks_per_slot=4),
+              dict(depth=2, read_in_place=True), dict(depth=1, read_in_place=False)]
+
+    def call(kw, O, LSE):
+        plan = cq.cqsa_plan(L, H, d, True, 0, cq.make_opts(**kw))
+        cq.cqsa_forward(plan, q, k, v, O, LSE)
+        del plan
+        gc.collect()
+
+    refs = []
+    for kw in shapes:
+        O = torch.empty((1, L, H, d), dtype=torch.float32, device="cuda")
+        LSE = torch.empty((1, H, L), dtype=torch.float32, device="cuda")
+        call(kw, O, LSE)
+        torch.cuda.synchronize()
+        refs.append((O.cpu(), LSE.cpu()))
+    say("eight back-to-back calls on plans destroyed at once")
+    outs = []
+    for i in range(8):
+        O = torch.empty((1, L, H, d), dtype=torch.float32, device="cuda")
+        LSE = torch.empty((1, H, L), dtype=torch.float32, device="cuda")
+        call(shapes[i % 4], O, LSE)
+        outs.append((O, LSE))
+    torch.cuda.synchronize()
+    for i, (O, LSE) in enumerate(outs):
+        assert torch.equal(O.cpu(), refs[i % 4][0]) and torch.equal(LSE.cpu(), refs[i % 4][1]), i
