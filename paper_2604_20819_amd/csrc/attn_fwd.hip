@@ -27,9 +27,18 @@
 
 namespace cqsa {
 
+// Waves per work group: 8 (256-query strips) for d = 96 ... 192, where two
+// waves per SIMD is the occupancy either way and the kernel fits the 256
+// registers per lane that leaves: the K/V tiles a work group loads serve
+// twice the queries, and d = 160, 192 (one work group per CU for LDS) still
+// run two waves per SIMD.  4 (128-query strips) for d = 32, 64, whose 4-wave
+// work groups fit three to a CU, and for d = 224, 256, which would spill.
+template <int D> constexpr int fwd_waves() { return (D >= 96 && D <= 192) ? 8 : 4; }
+
 template <typename E, int D, int MODE>
-__global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_fwd_mfma(const FwdArgs a) {
-  constexpr int BM = 128, BN = 64;
+__global__ void __launch_bounds__(64 * fwd_waves<D>(), (lds_row_elems<D>() > 128 ? 1 : 2)) attn_fwd_mfma(const FwdArgs a) {
+  constexpr int WAVES = fwd_waves<D>(), NT = 64 * WAVES;
+  constexpr int BM = 32 * WAVES, BN = 64;
   // K and V tiles: unpadded rows of 2D bytes; 16-byte chunk ch of row r sits
   // in slot ch ^ swz(r), which keeps the K row reads and the V transpose
   // reads free of bank conflicts.  Tiles arrive by direct global-to-LDS
@@ -41,7 +50,7 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
   constexpr int DB = D / 32;             // 32-wide d blocks of O^T
   constexpr int CHUNKS = DP / 8;         // 16-byte chunks per LDS row
   constexpr int RPI = 64 / CHUNKS;       // rows per 1 KB load instruction
-  constexpr int NDMA = BN / RPI / 4;     // load instructions per wave per tensor
+  constexpr int NDMA = BN / RPI / WAVES; // load instructions per wave per tensor
   typedef typename E::vec8 vec8;
   auto swz = [](int r) { return 2 * (r & 3) + ((r >> 2) & 1); };
 
@@ -58,7 +67,8 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
   const int L = int(tk.L_local);
   const int64_t nstrips = (L + BM - 1) / BM;
   // strips in the task's launch order (most live key tiles first)
-  static_assert(BM == kStrip, "strip tables are built for kStrip-row strips");
+  // strips in the task's launch order (most live key tiles first; the plan
+  // builds this table for BM-row strips, BM = fwd_rows_per_wg)
   const int strip = ((const int32_t*)(a.tab + tk.qorder_off))[work % nstrips];
   const int h = int((work / nstrips) % a.H);
   const int b = int(work / (nstrips * a.H));
@@ -69,7 +79,7 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
   const DevRun* runs_g = (const DevRun*)(a.tab + tk.runs_off);
   const bool in_place = a.in_place != 0;
 
-  for (int i = tid; i < n_runs; i += 256) runs_s[i] = runs_g[i];
+  for (int i = tid; i < n_runs; i += NT) runs_s[i] = runs_g[i];
 
   // Staged inputs hold the task's tokens as consecutive rows; inputs read in
   // place are the caller's tensors, where local token t sits at the global
@@ -104,9 +114,12 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
 
   // block summaries of the strip and of this wave's queries
   const int lastq_wg = (strip * BM + BM < L ? strip * BM + BM : L) - 1;
-  const int qb0 = strip * 2, qb1 = lastq_wg / 64;
-  const uint32_t qor = blk_or[qb0] | blk_or[qb1];
-  const uint32_t qand = blk_and[qb0] & blk_and[qb1];
+  const int qb0 = strip * (BM / 64), qb1 = lastq_wg / 64;
+  uint32_t qor = 0u, qand = 0xFFFFFFFFu;
+  for (int qb = qb0; qb <= qb1; ++qb) {
+    qor |= blk_or[qb];
+    qand &= blk_and[qb];
+  }
   const bool wave_live = q0w < L;
   const int wq1 = wave_live ? (q0w + 31 < L ? q0w + 31 : L - 1) : 0;
   const uint32_t wor = wave_live ? blk_or[q0w / 64] : 0u;
@@ -524,9 +537,9 @@ __global__ void __launch_bounds__(256) attn_fwd_f32(const FwdArgs a) {
 template <typename E, int D>
 static hipError_t launch_mfma(FwdMode mode, const FwdArgs& a, int64_t n, hipStream_t s) {
   if (mode == kModeStats)
-    hipLaunchKernelGGL((attn_fwd_mfma<E, D, kModeStats>), dim3(unsigned(n)), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((attn_fwd_mfma<E, D, kModeStats>), dim3(unsigned(n)), dim3(64 * fwd_waves<D>()), 0, s, a);
   else
-    hipLaunchKernelGGL((attn_fwd_mfma<E, D, kModeFinal>), dim3(unsigned(n)), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((attn_fwd_mfma<E, D, kModeFinal>), dim3(unsigned(n)), dim3(64 * fwd_waves<D>()), 0, s, a);
   return hipGetLastError();
 }
 
@@ -539,7 +552,24 @@ static hipError_t launch_f32(FwdMode mode, const FwdArgs& a, int64_t n, hipStrea
   return hipGetLastError();
 }
 
-int fwd_rows_per_wg(cqsa_dtype dt) { return dt == CQSA_F32 ? 32 : 128; }
+int fwd_rows_per_wg(cqsa_dtype dt, int d) {
+  if (dt == CQSA_F32) return 32;
+  switch (d) {
+#define CQSA_FWD_ROWS(DD) \
+  case DD:                \
+    return 32 * fwd_waves<DD>();
+    CQSA_FWD_ROWS(32)
+    CQSA_FWD_ROWS(64)
+    CQSA_FWD_ROWS(96)
+    CQSA_FWD_ROWS(128)
+    CQSA_FWD_ROWS(160)
+    CQSA_FWD_ROWS(192)
+    CQSA_FWD_ROWS(224)
+    CQSA_FWD_ROWS(256)
+#undef CQSA_FWD_ROWS
+  }
+  return 128;
+}
 
 hipError_t launch_fwd(cqsa_dtype dt, int d, FwdMode mode, const FwdArgs& a, int64_t wgs,
                       hipStream_t s) {

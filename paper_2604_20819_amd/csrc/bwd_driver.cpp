@@ -177,7 +177,7 @@ cqsa_status backward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa
     a.L = int32_t(Li); a.B = int32_t(B); a.H = int32_t(H); a.causal = p->g.causal;
     a.scale_log2 = sc * 1.4426950408889634f; a.scale = sc;
     a.runs = d_tab + to.runs; a.n_runs = int32_t(task.runs.size());
-    a.qorder = (const int32_t*)(d_tab + to.qorder);
+    a.qorder = (const int32_t*)(d_tab + to.dqorder);
     a.korder = (const int32_t*)(d_tab + to.korder);
     a.blk_or = (const uint32_t*)(d_tab + to.blk_or);
     a.blk_and = (const uint32_t*)(d_tab + to.blk_and);

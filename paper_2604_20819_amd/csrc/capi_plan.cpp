@@ -79,8 +79,9 @@ cqsa_status cqsa_plan(int64_t L, int32_t H, int32_t d, int32_t causal,
         // group in one grid (no tails between launches, one merge)
         g_hi = int32_t(std::min<int64_t>(kMaxContrib, std::max<int64_t>(1, ntask)));
       } else if (o.acc_on_device) {
-        // enough tasks per launch for kLaunchWgs work groups (two waves of
-        // the GPU's resident work groups); large tasks launch one by one
+        // enough tasks per launch for kLaunchWgs 128-query strips (two waves
+        // of the GPU's resident 4-wave work groups; an 8-wave work group
+        // counts as two); large tasks launch one by one
         int64_t Lmax = 1;
         for (const Task& t : tasks) Lmax = std::max(Lmax, t.L_local);
         const int64_t rows = o.dtype == CQSA_F32 ? 32 : 128;
@@ -94,7 +95,7 @@ cqsa_status cqsa_plan(int64_t L, int32_t H, int32_t d, int32_t causal,
         std::vector<Group> groups = make_groups(ntask, gs);
         std::vector<uint8_t> image;
         std::vector<TableOffsets> offs;
-        pack_image(tasks, sc, H, causal != 0, &groups, &image, &offs);
+        pack_image(tasks, sc, H, causal != 0, fwd_rows_per_wg(o.dtype, d), &groups, &image, &offs);
         Footprint f = footprint(g, o, dep, tasks, gs, image.size());
         ok = fits(f);
         if (ok || gs == 1 || o.tasks_per_slot > 0) {

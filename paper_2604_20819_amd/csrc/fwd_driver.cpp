@@ -274,7 +274,7 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
   const uint64_t st_b = align_up(uint64_t(B) * p->max_L_local * H * 4);
   auto slot_base = [&](int64_t si) { return base + tab_bytes + gl_bytes + slot_off[si]; };
   const DevTask* d_tasks = (const DevTask*)d_tab;
-  const int rows_wg = fwd_rows_per_wg(o.dtype);
+  const int rows_wg = fwd_rows_per_wg(o.dtype, int(d));
 
   // ---- ordering against the caller's stream and the previous call ----
   while (C->sync_events.size() < size_t(4 * std::max<int64_t>(nslot, 1) + 3)) {

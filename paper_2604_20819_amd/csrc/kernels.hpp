@@ -70,7 +70,7 @@ struct BwdArgs {
   const void* dO;
   int32_t in_place;
   const int32_t* rows;  // block row table (records.hpp), used when in_place
-  const int32_t* qorder; // query-strip launch order (records.hpp, DevTask::qorder_off)
+  const int32_t* qorder; // dQ query-strip launch order (records.hpp, DevTask::dqorder_off)
   const int32_t* korder; // key-strip launch order
   int32_t L;            // task length
   int32_t B, H;
@@ -102,11 +102,11 @@ struct StageArgs {
   int32_t n_runs;
 };
 
-// `wgs` = total work groups: sum over the tasks of ceil(L_j / 128) * B * H
-// (ceil(L_j / 32) * B * H for fp32 inputs).
+// `wgs` = total work groups: sum over the tasks of ceil(L_j / rows) * B * H with
+// rows = fwd_rows_per_wg(dtype, d).
 hipError_t launch_fwd(cqsa_dtype dt, int d, FwdMode mode, const FwdArgs& a, int64_t wgs,
                       hipStream_t s);
-int fwd_rows_per_wg(cqsa_dtype dt);
+int fwd_rows_per_wg(cqsa_dtype dt, int d);
 // `blocks` = combine work groups per batch element (the group's last segment's
 // blk0 plus its block count).
 hipError_t launch_combine(const CombineArgs& a, int64_t blocks, hipStream_t s);

@@ -329,14 +329,15 @@ struct ValuePrefix {
   }
 };
 
-std::vector<int32_t> query_strip_order(const Task& t, bool causal) {
+std::vector<int32_t> query_strip_order(const Task& t, bool causal, int32_t rows) {
   const int64_t L = t.L_local, nb = int64_t(t.blk_and.size());
-  const int64_t ns = (L + kStrip - 1) / kStrip;
+  const int64_t ns = (L + rows - 1) / rows;
   const ValuePrefix vp(t.blk_and);  // 64-key tile k is block k
   std::vector<int64_t> live(size_t(ns), 0);
   for (int64_t s = 0; s < ns; ++s) {
-    const int64_t last = std::min(L, (s + 1) * kStrip) - 1;
-    const uint32_t qand = t.blk_and[size_t(2 * s)] & t.blk_and[size_t(last / kBlock)];
+    const int64_t last = std::min(L, (s + 1) * rows) - 1;
+    uint32_t qand = 0xFFFFFFFFu;  // AND over the strip's blocks
+    for (int64_t b = s * rows / kBlock; b <= last / kBlock; ++b) qand &= t.blk_and[size_t(b)];
     live[size_t(s)] = vp.disjoint(qand, 0, causal ? last / kBlock + 1 : nb);
   }
   return longest_first(live);
@@ -361,7 +362,7 @@ std::vector<int32_t> key_strip_order(const Task& t, bool causal) {
 }
 
 void pack_image(const std::vector<Task>& tasks, const SegmentCover& sc, int32_t H, bool causal,
-                std::vector<Group>* groups, std::vector<uint8_t>* image,
+                int32_t fwd_rows, std::vector<Group>* groups, std::vector<uint8_t>* image,
                 std::vector<TableOffsets>* offs) {
   std::vector<uint8_t>& im = *image;
   im.clear();
@@ -398,14 +399,17 @@ void pack_image(const std::vector<Task>& tasks, const SegmentCover& sc, int32_t 
                               : kNoRow;
       std::memcpy(im.data() + o.rows + i * 4, &row, 4);
     }
-    // strip launch orders, longest first
-    const std::vector<int32_t> qo = query_strip_order(k, causal), ko = key_strip_order(k, causal);
-    o.qorder = reserve(qo.size() * 4);
-    if (!qo.empty()) std::memcpy(im.data() + o.qorder, qo.data(), qo.size() * 4);
-    o.korder = reserve(ko.size() * 4);
-    if (!ko.empty()) std::memcpy(im.data() + o.korder, ko.data(), ko.size() * 4);
+    // strip launch orders, longest first: the forward's strips, dQ's and dK/dV's
+    auto put = [&](const std::vector<int32_t>& v) {
+      const uint64_t at = reserve(v.size() * 4);
+      if (!v.empty()) std::memcpy(im.data() + at, v.data(), v.size() * 4);
+      return at;
+    };
+    o.qorder = put(query_strip_order(k, causal, fwd_rows));
+    o.dqorder = put(query_strip_order(k, causal, kStrip));
+    o.korder = put(key_strip_order(k, causal));
     DevTask d{k.L_local, int64_t(o.runs), int64_t(o.blk_or), int64_t(o.blk_and), int64_t(o.rows),
-              int64_t(o.qorder), int64_t(o.korder), int32_t(k.runs.size()), 0};
+              int64_t(o.qorder), int64_t(o.dqorder), int64_t(o.korder), int32_t(k.runs.size()), 0};
     std::memcpy(im.data() + hdr + t * sizeof(DevTask), &d, sizeof(d));
     offs->push_back(o);
   }

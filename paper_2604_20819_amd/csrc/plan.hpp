@@ -15,8 +15,8 @@ namespace cqsa {
 
 constexpr int kBlock = 64;   // tokens per block summary (App. A.2)
 constexpr int kTile = 128;   // census tile edge (App. A.2)
-// Work groups one forward launch should offer: two waves of the MI355X's
-// resident inner-kernel work groups (256 CUs x 2).
+// 128-query strips one forward launch should offer: two waves of the
+// MI355X's resident 4-wave inner-kernel work groups (256 CUs x 2).
 constexpr int64_t kLaunchWgs = 1024;
 
 // One maximal run of a task: local tokens [local_start, local_start+length)
@@ -43,7 +43,8 @@ struct TableOffsets {
   uint64_t blk_or = 0;  // uint32[n_blocks]
   uint64_t blk_and = 0; // uint32[n_blocks]
   uint64_t rows = 0;    // int32[n_blocks] block row table (records.hpp, kNoRow)
-  uint64_t qorder = 0;  // int32[n_strips] query strips, longest first
+  uint64_t qorder = 0;  // int32[n_strips] forward query strips, longest first
+  uint64_t dqorder = 0; // int32[n_strips] dQ query strips (kStrip rows), longest first
   uint64_t korder = 0;  // int32[n_strips] key strips, longest first
 };
 
@@ -161,17 +162,21 @@ uint64_t bwd_slot_bytes(const Geometry& g, const cqsa_plan_opts& o, int64_t Lmax
 // Packs the plan image: the DevTask records, every task's runs and block
 // summaries, and every group's segments and contributions (filling the
 // groups' offsets and combine block counts for H heads).
+// `fwd_rows` is the forward kernel's query-strip height (fwd_rows_per_wg).
 void pack_image(const std::vector<Task>& tasks, const SegmentCover& sc, int32_t H, bool causal,
-                std::vector<Group>* groups, std::vector<uint8_t>* image,
+                int32_t fwd_rows, std::vector<Group>* groups, std::vector<uint8_t>* image,
                 std::vector<TableOffsets>* offs);
 
+// Query rows per work group of the inner forward kernel (attn_fwd.hip).
+int fwd_rows_per_wg(cqsa_dtype dt, int d);
+
 // Strip orders of one task for its kernels' launch order (longest first):
-// 128-query strips by the 64-key tiles live for them, and 128-key strips by
-// the 32-query tiles live for them, with the kernels' liveness rule (a tile is
-// skipped when the AND of the strip's block summaries and of the tile's
-// shares a bit, or when it lies causally past the strip).  Ties keep strip
-// order.
-std::vector<int32_t> query_strip_order(const Task& t, bool causal);
+// query strips of `rows` rows (a multiple of 64) by the 64-key tiles live for
+// them, and 128-key strips by the 32-query tiles live for them, with the
+// kernels' liveness rule (a tile is skipped when the AND of the strip's block
+// summaries and of the tile's shares a bit, or when it lies causally past the
+// strip).  Ties keep strip order.
+std::vector<int32_t> query_strip_order(const Task& t, bool causal, int32_t rows);
 std::vector<int32_t> key_strip_order(const Task& t, bool causal);
 
 inline uint64_t align_up(uint64_t x, uint64_t a = 256) { return (x + a - 1) / a * a; }

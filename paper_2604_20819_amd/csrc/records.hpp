@@ -29,14 +29,16 @@ struct DevTask {
   int64_t or_off;     // uint32[ceil(L_local / 64)] block OR of the group bits
   int64_t and_off;    // uint32[ceil(L_local / 64)] block AND of the group bits
   int64_t row_off;    // int32[ceil(L_local / 64)] block rows (see kNoRow)
-  int64_t qorder_off; // int32[ceil(L_local / kStrip)] query strips, most live key tiles first
+  int64_t qorder_off; // int32[ceil(L_local / R)] forward query strips of R rows, R the
+                      // forward's strip height (fwd_rows_per_wg), most live key tiles first
+  int64_t dqorder_off;// int32[ceil(L_local / kStrip)] dQ query strips, most live key tiles first
   int64_t korder_off; // int32[ceil(L_local / kStrip)] key strips, most live query tiles first
   int32_t n_runs;
   int32_t pad;
 };
 
-// Rows of the strips the MFMA kernels assign to a work group: 128 queries
-// (forward, dQ) or 128 keys (dK/dV).  Strips of a (task, b, h) run in the
+// Rows of the strips the backward kernels assign to a work group: 128
+// queries (dQ) or 128 keys (dK/dV).  Strips of a (task, b, h) run in the
 // order of the task's strip tables, longest first, so a launch ends with its
 // shortest strips.
 constexpr int kStrip = 128;
@@ -70,7 +72,7 @@ struct DevContrib {
 };
 
 static_assert(sizeof(DevRun) == 32, "DevRun layout");
-static_assert(sizeof(DevTask) == 64, "DevTask layout");
+static_assert(sizeof(DevTask) == 72, "DevTask layout");
 static_assert(sizeof(DevSeg) == 40, "DevSeg layout");
 static_assert(sizeof(DevContrib) == 16, "DevContrib layout");
 

@@ -254,15 +254,16 @@ def test_workload_depths(L, H, d, causal, budget, kw, want):
 
 def _image_bytes(p, g):
     """Plan image size from the layout the planner documents: DevTask records
-    (64 bytes), per-task runs, block summaries (OR, AND), block row table and
-    the two strip orders (one int32 per 128-token strip), per-group segments
-    and contributions."""
+    (72 bytes), per-task runs, block summaries (OR, AND), block row table and
+    the three strip orders (one int32 per strip: the forward's 256-query
+    strips at bf16 d = 128, and the backward's 128-token strips), per-group
+    segments and contributions."""
     al = lambda x: (x + 255) // 256 * 256
     tasks = [p.task(t) for t in range(p.num_tasks)]
-    size = al(len(tasks) * 64)
+    size = al(len(tasks) * 72)
     for tk in tasks:
         size += al(len(tk["runs"]) * 32) + 3 * al(len(tk["block_or"]) * 4)
-        size += 2 * al(-(-tk["L_local"] // 128) * 4)
+        size += al(-(-tk["L_local"] // 256) * 4) + 2 * al(-(-tk["L_local"] // 128) * 4)
     bounds = sorted({0, p.L} | {r[0] for tk in tasks for r in tk["runs"]}
                     | {r[0] + r[1] for tk in tasks for r in tk["runs"]})
     segs = list(zip(bounds[:-1], bounds[1:]))
