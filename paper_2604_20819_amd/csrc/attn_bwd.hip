@@ -24,9 +24,16 @@ namespace cqsa {
 
 constexpr float kLog2e = 1.4426950408889634f;
 
+// Waves per dQ work group: 8 over a 256-query strip at d = 160, where the
+// padded LDS rows leave one work group per CU and 4 waves would run one wave
+// per SIMD (a 40 B spill costs less); 4 over a 128-query strip elsewhere (at
+// d = 96 and 128 8 waves gained nothing, at 192 and up they spill more).
+template <int D> constexpr int dq_waves() { return D == 160 ? 8 : 4; }
+
 template <typename E, int D>
-__global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_bwd_dq(const BwdArgs a) {
-  constexpr int BM = 128, BN = 64;
+__global__ void __launch_bounds__(64 * dq_waves<D>(), (lds_row_elems<D>() > 128 ? 1 : 2)) attn_bwd_dq(const BwdArgs a) {
+  constexpr int WAVES = dq_waves<D>(), NT = 64 * WAVES;
+  constexpr int BM = 32 * WAVES, BN = 64;
   // K and V tiles: rows of DP elements (d padded as in the forward) with the
   // forward's swizzle (chunk ch of row r in slot ch ^ swz(r)), free of bank
   // conflicts for the K and V row reads and the K transpose reads; filled by
@@ -35,7 +42,7 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
   constexpr int RB = DP * 2;
   constexpr int KBYTES = BN * RB, VBYTES = BN * RB, STAGE = KBYTES + VBYTES;
   constexpr int DK = D / 16, DB = D / 32, CHUNKS = DP / 8;
-  constexpr int RPI = 64 / CHUNKS, NDMA = BN / RPI / 4;
+  constexpr int RPI = 64 / CHUNKS, NDMA = BN / RPI / WAVES;
   typedef typename E::vec8 vec8;
   auto swz = [](int r) { return 2 * (r & 3) + ((r >> 2) & 1); };
 
@@ -49,14 +56,14 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
   const int L = a.L;
   const int64_t nstrips = (L + BM - 1) / BM;
   const int64_t work = xcd_remap(blockIdx.x, nstrips * a.H * a.B);
-  // strips in the task's launch order (most live key tiles first)
-  static_assert(BM == kStrip, "strip tables are built for kStrip-row strips");
+  // strips in the task's launch order (most live key tiles first; the plan
+  // builds this table for BM-row strips, BM = dq_rows_per_wg)
   const int strip = a.qorder[work % nstrips];
   const int h = int((work / nstrips) % a.H);
   const int b = int(work / (nstrips * a.H));
   const DevRun* runs_g = (const DevRun*)a.runs;
   const bool in_place = a.in_place != 0;
-  for (int i = tid; i < a.n_runs; i += 256) runs_s[i] = runs_g[i];
+  for (int i = tid; i < a.n_runs; i += NT) runs_s[i] = runs_g[i];
 
   // token rows: consecutive when staged, the runs' global rows when the
   // caller's tensors are read in place (as in the forward)
@@ -93,9 +100,12 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
   }
 
   const int lastq_wg = (strip * BM + BM < L ? strip * BM + BM : L) - 1;
-  const int qb0 = strip * 2, qb1 = lastq_wg / 64;
-  const uint32_t qor = a.blk_or[qb0] | a.blk_or[qb1];
-  const uint32_t qand = a.blk_and[qb0] & a.blk_and[qb1];
+  const int qb0 = strip * (BM / 64), qb1 = lastq_wg / 64;
+  uint32_t qor = 0u, qand = 0xFFFFFFFFu;
+  for (int qb = qb0; qb <= qb1; ++qb) {
+    qor |= a.blk_or[qb];
+    qand &= a.blk_and[qb];
+  }
   const bool wave_live = q0w < L;
   const int wq1 = wave_live ? (q0w + 31 < L ? q0w + 31 : L - 1) : 0;
   const uint32_t wor = wave_live ? a.blk_or[q0w / 64] : 0u;
@@ -691,9 +701,10 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
 
 template <typename E, int D>
 static hipError_t launch_dq_t(const BwdArgs& a, hipStream_t s) {
-  const int64_t n = ((a.L + 127) / 128) * int64_t(a.H) * a.B;
+  constexpr int rows = 32 * dq_waves<D>();
+  const int64_t n = ((a.L + rows - 1) / rows) * int64_t(a.H) * a.B;
   if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL((attn_bwd_dq<E, D>), dim3(unsigned(n)), dim3(256), 0, s, a);
+  hipLaunchKernelGGL((attn_bwd_dq<E, D>), dim3(unsigned(n)), dim3(64 * dq_waves<D>()), 0, s, a);
   return hipGetLastError();
 }
 
@@ -717,6 +728,24 @@ static hipError_t launch_dkdv_t(const BwdArgs& a, hipStream_t s) {
     case 256: return dt == CQSA_BF16 ? LAUNCH<BF16, 256>(a, s) : LAUNCH<F16, 256>(a, s); \
   }                                                                    \
   return hipErrorInvalidValue;
+
+int dq_rows_per_wg(int d) {
+  switch (d) {
+#define CQSA_DQ_ROWS(DD) \
+  case DD:               \
+    return 32 * dq_waves<DD>();
+    CQSA_DQ_ROWS(32)
+    CQSA_DQ_ROWS(64)
+    CQSA_DQ_ROWS(96)
+    CQSA_DQ_ROWS(128)
+    CQSA_DQ_ROWS(160)
+    CQSA_DQ_ROWS(192)
+    CQSA_DQ_ROWS(224)
+    CQSA_DQ_ROWS(256)
+#undef CQSA_DQ_ROWS
+  }
+  return 128;
+}
 
 hipError_t launch_bwd_dq(cqsa_dtype dt, int d, const BwdArgs& a, hipStream_t s) {
   if (a.n_runs > kMaxRuns) return hipErrorInvalidValue;

@@ -362,8 +362,8 @@ std::vector<int32_t> key_strip_order(const Task& t, bool causal) {
 }
 
 void pack_image(const std::vector<Task>& tasks, const SegmentCover& sc, int32_t H, bool causal,
-                int32_t fwd_rows, std::vector<Group>* groups, std::vector<uint8_t>* image,
-                std::vector<TableOffsets>* offs) {
+                int32_t fwd_rows, int32_t dq_rows, std::vector<Group>* groups,
+                std::vector<uint8_t>* image, std::vector<TableOffsets>* offs) {
   std::vector<uint8_t>& im = *image;
   im.clear();
   offs->clear();
@@ -406,7 +406,7 @@ void pack_image(const std::vector<Task>& tasks, const SegmentCover& sc, int32_t 
       return at;
     };
     o.qorder = put(query_strip_order(k, causal, fwd_rows));
-    o.dqorder = put(query_strip_order(k, causal, kStrip));
+    o.dqorder = put(query_strip_order(k, causal, dq_rows));
     o.korder = put(key_strip_order(k, causal));
     DevTask d{k.L_local, int64_t(o.runs), int64_t(o.blk_or), int64_t(o.blk_and), int64_t(o.rows),
               int64_t(o.qorder), int64_t(o.dqorder), int64_t(o.korder), int32_t(k.runs.size()), 0};

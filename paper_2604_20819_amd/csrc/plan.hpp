@@ -44,7 +44,7 @@ struct TableOffsets {
   uint64_t blk_and = 0; // uint32[n_blocks]
   uint64_t rows = 0;    // int32[n_blocks] block row table (records.hpp, kNoRow)
   uint64_t qorder = 0;  // int32[n_strips] forward query strips, longest first
-  uint64_t dqorder = 0; // int32[n_strips] dQ query strips (kStrip rows), longest first
+  uint64_t dqorder = 0; // int32[n_strips] dQ query strips, longest first
   uint64_t korder = 0;  // int32[n_strips] key strips, longest first
 };
 
@@ -162,13 +162,15 @@ uint64_t bwd_slot_bytes(const Geometry& g, const cqsa_plan_opts& o, int64_t Lmax
 // Packs the plan image: the DevTask records, every task's runs and block
 // summaries, and every group's segments and contributions (filling the
 // groups' offsets and combine block counts for H heads).
-// `fwd_rows` is the forward kernel's query-strip height (fwd_rows_per_wg).
+// `fwd_rows` and `dq_rows` are the forward and dQ kernels' query-strip
+// heights (fwd_rows_per_wg, dq_rows_per_wg).
 void pack_image(const std::vector<Task>& tasks, const SegmentCover& sc, int32_t H, bool causal,
-                int32_t fwd_rows, std::vector<Group>* groups, std::vector<uint8_t>* image,
-                std::vector<TableOffsets>* offs);
+                int32_t fwd_rows, int32_t dq_rows, std::vector<Group>* groups,
+                std::vector<uint8_t>* image, std::vector<TableOffsets>* offs);
 
-// Query rows per work group of the inner forward kernel (attn_fwd.hip).
+// Query rows per work group of the inner forward and dQ kernels.
 int fwd_rows_per_wg(cqsa_dtype dt, int d);
+int dq_rows_per_wg(int d);
 
 // Strip orders of one task for its kernels' launch order (longest first):
 // query strips of `rows` rows (a multiple of 64) by the 64-key tiles live for

@@ -31,7 +31,8 @@ struct DevTask {
   int64_t row_off;    // int32[ceil(L_local / 64)] block rows (see kNoRow)
   int64_t qorder_off; // int32[ceil(L_local / R)] forward query strips of R rows, R the
                       // forward's strip height (fwd_rows_per_wg), most live key tiles first
-  int64_t dqorder_off;// int32[ceil(L_local / kStrip)] dQ query strips, most live key tiles first
+  int64_t dqorder_off;// int32[ceil(L_local / R)] dQ query strips of R rows, R the dQ
+                      // kernel's strip height (dq_rows_per_wg), most live key tiles first
   int64_t korder_off; // int32[ceil(L_local / kStrip)] key strips, most live query tiles first
   int32_t n_runs;
   int32_t pad;
