@@ -328,12 +328,15 @@ __global__ void __launch_bounds__(64 * dq_waves<D>(), (lds_row_elems<D>() > 128 
 
 // Above d = 160 the dK/dV accumulators of a whole row (2 x d/32 blocks) and
 // the wave's K rows do not fit in registers: the columns of dK and dV are
-// then split over two work groups per key strip, each recomputing S and dP
-// over the full d and accumulating its half of the columns.
+// then split over two halves of an 8-wave work group (waves w and w + 4 own
+// the same 32 keys), each half recomputing S and dP over the full d and
+// accumulating its half of the columns; the halves share the work group's
+// Q/dO tiles and V rows, and the 8 waves give two per SIMD where the padded
+// LDS rows allow one work group per CU.
 template <int D> constexpr int dkdv_splits() { return D > 160 ? 2 : 1; }
 
 template <typename E, int D>
-__global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_bwd_dkdv(const BwdArgs a) {
+__global__ void __launch_bounds__(256 * dkdv_splits<D>(), (lds_row_elems<D>() > 128 ? 1 : 2)) attn_bwd_dkdv(const BwdArgs a) {
   // 32-query tiles (two per 64-token summary block) keep the registers and
   // LDS within two work groups per CU (one above d = 128)
   constexpr int BK = 128, BQ = 32;
@@ -344,8 +347,9 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
   constexpr int DP = lds_row_elems<D>();
   constexpr int P2 = DP * 2;
   constexpr int DK = D / 16, DB = D / 32, CHUNKS = DP / 8;
-  constexpr int RPI = 64 / CHUNKS, NDMA = BQ / RPI / 4;
   constexpr int NSPLIT = dkdv_splits<D>(), DBO = (DB + NSPLIT - 1) / NSPLIT;
+  constexpr int WAVES = 4 * NSPLIT, NT = 64 * WAVES;
+  constexpr int RPI = 64 / CHUNKS, NDMA = BQ / RPI / WAVES;
   typedef typename E::vec8 vec8;
   auto swz = [](int r) { return 2 * (r & 3) + ((r >> 2) & 1); };
 
@@ -363,10 +367,11 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int L = a.L;
   const int64_t nstrips = (L + BK - 1) / BK;
-  // the two column halves of a strip are consecutive work items (same XCD)
-  const int64_t item = xcd_remap(blockIdx.x, nstrips * a.H * a.B * NSPLIT);
-  const int64_t work = item / NSPLIT;
-  const int db0 = int(item % NSPLIT) * DBO;  // first 32-column block of dK, dV owned
+  const int64_t work = xcd_remap(blockIdx.x, nstrips * a.H * a.B);
+  // the wave's 32 keys are the kw-th of the strip; it owns dK, dV columns
+  // from 32-column block db0 (both fixed at 4 waves, no split)
+  const int kw = NSPLIT > 1 ? (wave & 3) : wave;
+  const int db0 = NSPLIT > 1 ? (wave >> 2) * DBO : 0;
   // key strips in the task's launch order (most live query tiles first)
   static_assert(BK == kStrip, "strip tables are built for kStrip-row strips");
   const int strip = a.korder[work % nstrips];
@@ -374,7 +379,7 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
   const int b = int(work / (nstrips * a.H));
   const DevRun* runs_g = (const DevRun*)a.runs;
   const bool in_place = a.in_place != 0;
-  for (int i = tid; i < a.n_runs; i += 256) runs_s[i] = runs_g[i];
+  for (int i = tid; i < a.n_runs; i += NT) runs_s[i] = runs_g[i];
 
   // token rows: consecutive when staged, the runs' global rows when the
   // caller's tensors are read in place
@@ -388,7 +393,7 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
   const float c = a.scale_log2;
   const bool causal = a.causal != 0;
 
-  const int k0w = strip * BK + wave * 32;
+  const int k0w = strip * BK + kw * 32;
   const int mykey = k0w + (lane & 31);
   const bool kvalid = mykey < L;
   // the wave's 32 keys lie in one 64-token block, so the table lookup and
@@ -420,7 +425,7 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
     const __amdgpu_buffer_rsrc_t rv =
         vrow != kNoRow ? row_rsrc(Vg + int64_t(vrow) * rs, vrows, rs * 2, D * 2)
                        : row_rsrc(Vg, seq, rs * 2, D * 2);
-    constexpr int NV = BK / RPI / 4;  // 1 KB loads per wave
+    constexpr int NV = BK / RPI / WAVES;  // 1 KB loads per wave
 #pragma unroll
     for (int j = 0; j < NV; ++j) {
       const int row = RPI * (NV * wave + j) + lane / CHUNKS;
@@ -610,7 +615,7 @@ __global__ void __launch_bounds__(256, (lds_row_elems<D>() > 128 ? 1 : 2)) attn_
           const u32x4 qa = *(const u32x4*)(qsb + row * P2 + slot);
           s = mfma32<E>(bitcast_u4<vec8>(qa), kf[ks], s);
           const u32x4 oa = *(const u32x4*)(osb + row * P2 + slot);
-          const int vr = wave * 32 + (lane & 31);
+          const int vr = kw * 32 + (lane & 31);
           const u32x4 vb = *(const u32x4*)(vs + vr * P2 + (((2 * ks + half) ^ swz(vr)) << 4));
           dp = mfma32<E>(bitcast_u4<vec8>(oa), bitcast_u4<vec8>(vb), dp);
         }
@@ -710,9 +715,9 @@ static hipError_t launch_dq_t(const BwdArgs& a, hipStream_t s) {
 
 template <typename E, int D>
 static hipError_t launch_dkdv_t(const BwdArgs& a, hipStream_t s) {
-  const int64_t n = ((a.L + 127) / 128) * int64_t(a.H) * a.B * dkdv_splits<D>();
+  const int64_t n = ((a.L + 127) / 128) * int64_t(a.H) * a.B;
   if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL((attn_bwd_dkdv<E, D>), dim3(unsigned(n)), dim3(256), 0, s, a);
+  hipLaunchKernelGGL((attn_bwd_dkdv<E, D>), dim3(unsigned(n)), dim3(256 * dkdv_splits<D>()), 0, s, a);
   return hipGetLastError();
 }
 
