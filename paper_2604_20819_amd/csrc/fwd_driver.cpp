@@ -59,7 +59,10 @@ void parallel_rows(int64_t n, F f) {
 }
 
 // Max-shifted merge of one task's statistics into the host accumulator
-// (Eq. "merge", log2 domain, null rows skipped).
+// (Eq. "merge", log2 domain, null rows skipped).  A row whose running max is
+// still -inf has had no contribution yet: the first one is written, not
+// blended, so the accumulator needs no zero fill beforehand (every token has
+// a kept key in some task, so every row is written before finalisation).
 void host_merge(const Task& task, const float* acc_i, const float* m_i, const float* l_i,
                 float* acc, float* m, float* l, int64_t B, int64_t L, int64_t H, int64_t d) {
   const int64_t Li = task.L_local;
@@ -77,11 +80,17 @@ void host_merge(const Task& task, const float* acc_i, const float* m_i, const fl
         const float mi = m_i[si];
         if (mi == -INFINITY) continue;
         const float mo = m[gi];
-        const float mn = std::max(mo, mi);
-        const float fo = mo == -INFINITY ? 0.f : std::exp2(mo - mn);
-        const float fi = std::exp2(mi - mn);
         const float* src = acc_i + ((b * Li + r) * H + h) * d;
         float* dst = acc + ((b * L + g) * H + h) * d;
+        if (mo == -INFINITY) {
+          for (int64_t k = 0; k < d; ++k) dst[k] = src[k];
+          l[gi] = l_i[si];
+          m[gi] = mi;
+          continue;
+        }
+        const float mn = std::max(mo, mi);
+        const float fo = std::exp2(mo - mn);
+        const float fi = std::exp2(mi - mn);
         for (int64_t k = 0; k < d; ++k) dst[k] = dst[k] * fo + src[k] * fi;
         l[gi] = l[gi] * fo + l_i[si] * fi;
         m[gi] = mn;
@@ -336,11 +345,10 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
     char* pin = nullptr;
     uint64_t pin_slot = 0;
     if (!acc_dev) {
+      // running max -inf marks rows not yet merged (host_merge writes their
+      // first contribution), so acc itself needs no fill
       l_host.assign(size_t(B * H * L), 0.f);
       l = l_host.data();
-      parallel_rows(B * L, [&](int64_t lo, int64_t hi) {
-        std::fill(acc + lo * H * d, acc + hi * H * d, 0.f);
-      });
       std::fill(m, m + B * H * L, -INFINITY);
       pin_slot = acc_b + 2 * st_b;
       void* pv = nullptr;
