@@ -367,7 +367,11 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
       const Group& G = p->groups[k];
       const int64_t si = k % nslot;
       char* sb = slot_base(si);
-      if (used[si]) CQSA_HIP(hipStreamWaitEvent(cs, ev_free[si], 0));
+      // The slot's staged inputs are free once its previous group's inner
+      // kernel is done; its statistics once their merge or D2H is done.
+      // Staging waits for the first only, so the H2D of this group overlaps
+      // the D2H of the slot's previous statistics.
+      if (used[si] && !in_place) CQSA_HIP(hipStreamWaitEvent(cs, ev_inner[si], 0));
       // gather every task of the group into its sub-slot
       int64_t wgs = 0;
       for (int64_t j = 0; j < G.count; ++j) {
@@ -431,6 +435,8 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
         CQSA_HIP(hipEventRecord(ev_staged[si], cs));
         CQSA_HIP(hipStreamWaitEvent(ls, ev_staged[si], 0));
       }
+      // the inner kernel overwrites the slot's statistics
+      if (used[si]) CQSA_HIP(hipStreamWaitEvent(ls, ev_free[si], 0));
       FwdArgs a{};
       if (in_place) {
         a.q = Q->data; a.k = K->data; a.v = V->data;
