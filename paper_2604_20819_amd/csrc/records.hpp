@@ -38,10 +38,9 @@ struct DevTask {
   int32_t pad;
 };
 
-// Rows of the strips the backward kernels assign to a work group: 128
-// queries (dQ) or 128 keys (dK/dV).  Strips of a (task, b, h) run in the
-// order of the task's strip tables, longest first, so a launch ends with its
-// shortest strips.
+// Keys of the strip a dK/dV work group owns.  Strips of a (task, b, h) run in
+// the order of the task's strip tables (forward, dQ, dK/dV), longest first,
+// so a launch ends with its shortest strips.
 constexpr int kStrip = 128;
 
 // Block row table: entry i is the global row of local token 64 i when the
