@@ -114,6 +114,11 @@ typedef struct {
                                 0: gather every task's runs into staging slots first;
                                 -1: automatic -- 1 when its conditions hold, else 0 (query
                                 cqsa_plan_reads_in_place) (-1) */
+  int32_t out16;             /* 1: cqsa_forward writes O in the input dtype (bf16 or fp16), each
+                                element the fp32 result rounded to nearest even; the fp32
+                                result is kept in the workspace, and the footprint counts it.
+                                Needs a 16-bit dtype, acc_on_device = 1 and with_backward = 0
+                                (the backward reads the fp32 O).  0: O is fp32 (0) */
 } cqsa_plan_opts;
 
 /* One contiguous run of a task's tokens: global tokens
@@ -210,7 +215,8 @@ void cqsa_plan_destroy(cqsa_plan_t* plan);                 /* NULL is a no-op */
 
 /* Decomposed forward (Alg. 1 computed with the max-shifted merge of App. A.1).
  * Q, K, V: inputs matching the plan (B, L, H, d, dtype, and residency
- * inputs_on_device).  O: fp32 [B, L, H, d], where = acc_on_device ? device : host.
+ * inputs_on_device).  O: fp32 [B, L, H, d] (the plan's 16-bit dtype when the plan
+ * has out16 = 1), where = acc_on_device ? device : host.
  * LSE: fp32 [B, H, L] in `lse_where` memory (must equal O's residency).
  * scale <= 0 selects 1/sqrt(d) (Section 3.1).  Device-resident outputs are
  * written in stream order on hip_stream; host-resident outputs are complete

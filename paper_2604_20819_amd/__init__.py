@@ -46,7 +46,8 @@ class cqsa_plan_opts(ctypes.Structure):
                 ("inputs_on_device", ctypes.c_int32), ("acc_on_device", ctypes.c_int32),
                 ("with_backward", ctypes.c_int32), ("tasks_per_slot", ctypes.c_int32),
                 ("n_level_sets", ctypes.c_int32), ("level_sets", cqsa_interest_set * 4),
-                ("read_in_place", ctypes.c_int32)]
+                ("read_in_place", ctypes.c_int32),
+                ("out16", ctypes.c_int32)]
 
 
 class cqsa_run(ctypes.Structure):
@@ -143,11 +144,12 @@ def cqsa_plan_opts_default():
 
 def make_opts(B=1, dtype="bf16", c=7, interest=(0, 1, 3), depth=-1, min_depth=1, max_depth=4,
               n_slots=2, inputs_on_device=True, acc_on_device=True, with_backward=False,
-              tasks_per_slot=0, levels=None, read_in_place=None):
+              tasks_per_slot=0, levels=None, read_in_place=None, out16=False):
     """levels: optional list of (c, interest) per depth (the last repeats below).
     acc_on_device=None asks the planner to choose the accumulator residency;
     read_in_place=None lets it choose whether the kernels read the caller's
-    tensors in place (True) or gather each task's runs first (False)."""
+    tensors in place (True) or gather each task's runs first (False).
+    out16=True makes cqsa_forward write O in the input dtype."""
     o = cqsa_plan_opts_default()
     o.B = B
     o.dtype = {"f32": CQSA_F32, "f16": CQSA_F16, "bf16": CQSA_BF16}[dtype]
@@ -161,6 +163,7 @@ def make_opts(B=1, dtype="bf16", c=7, interest=(0, 1, 3), depth=-1, min_depth=1,
     o.with_backward = int(bool(with_backward))
     o.tasks_per_slot = int(tasks_per_slot)
     o.read_in_place = -1 if read_in_place is None else int(bool(read_in_place))
+    o.out16 = int(bool(out16))
     if levels:
         if len(levels) > 4:
             raise ValueError("at most 4 level sets")
@@ -268,7 +271,8 @@ def _stream_of(*ts):
 
 
 def cqsa_forward(plan, Q, K, V, O, LSE, scale=0.0, stream=None):
-    """O (fp32 [B,L,H,d]) and LSE (fp32 [B,H,L]) are written in place."""
+    """O (fp32 [B,L,H,d], or the input dtype with out16) and LSE (fp32 [B,H,L]) are
+    written in place."""
     if not (LSE.is_contiguous() and LSE.dtype == _torch().float32):
         raise ValueError("LSE must be a contiguous float32 tensor")
     tq, tk, tv, to = (as_cqsa_tensor(x) for x in (Q, K, V, O))

@@ -38,6 +38,7 @@ void cqsa_plan_opts_default(cqsa_plan_opts* o) {
   o->with_backward = 0;
   o->tasks_per_slot = 0;
   o->read_in_place = -1;
+  o->out16 = 0;
 }
 
 cqsa_status cqsa_plan(int64_t L, int32_t H, int32_t d, int32_t causal,

@@ -223,7 +223,7 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
   if ((s = check_tensor(Q, "Q", p, o.dtype, in_where)) != CQSA_OK) return s;
   if ((s = check_tensor(K, "K", p, o.dtype, in_where)) != CQSA_OK) return s;
   if ((s = check_tensor(V, "V", p, o.dtype, in_where)) != CQSA_OK) return s;
-  if ((s = check_tensor(O, "O", p, CQSA_F32, acc_where)) != CQSA_OK) return s;
+  if ((s = check_tensor(O, "O", p, o.out16 ? o.dtype : CQSA_F32, acc_where)) != CQSA_OK) return s;
   if (!LSE) return fail(CQSA_ERR_INVALID_ARG, "LSE is NULL");
   if (lse_where != acc_where)
     return fail(CQSA_ERR_INVALID_ARG, "LSE residency must equal the output residency");
@@ -270,7 +270,9 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
   const int64_t nslot = int64_t(slot_tasks.size());
   std::vector<uint64_t> slot_off(nslot + 1, 0);
   for (int64_t i = 0; i < nslot; ++i) slot_off[i + 1] = slot_off[i] + uint64_t(slot_tasks[i]) * sub_bytes;
-  const uint64_t total = tab_bytes + gl_bytes + slot_off[nslot];
+  // fp32 result when O is 16-bit: [B, L, H, d] after the slots
+  const uint64_t o32_bytes = o.out16 ? align_up(uint64_t(B) * L * H * d * 4) : 0;
+  const uint64_t total = tab_bytes + gl_bytes + slot_off[nslot] + o32_bytes;
   Workspace ws;
   if ((s = acquire_workspace(C, total, &ws)) != CQSA_OK) return s;
   rec.stats.workspace_bytes = total;
@@ -323,7 +325,7 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
     if (sp.first && hipEventRecord(sp.second, sm) == hipSuccess) rec.spans[k].push_back(sp);
   };
 
-  float* Od = (float*)O->data;
+  float* Od = o.out16 ? (float*)(base + tab_bytes + gl_bytes + slot_off[nslot]) : (float*)O->data;
   if (direct) {
     FwdArgs a{};
     a.q = Q->data; a.k = K->data; a.v = V->data;
@@ -524,6 +526,12 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
       CQSA_HIP(hipEventRecord(ev_tail, ms));
       CQSA_HIP(hipStreamWaitEvent(st, ev_tail, 0));
     }
+  }
+  if (o.out16) {
+    // O in the input dtype, rounded from the finished fp32 result
+    auto sp = span_begin(st);
+    CQSA_HIP(launch_cast_out(Od, O->data, B * L * H * d, o.dtype, st));
+    span_end(sp, st, kStFinal);
   }
   if (rec.timing) CQSA_HIP(hipEventRecord(rec.wall1, st));
   CQSA_HIP(hipEventRecord(C->ws_free, st));

@@ -112,6 +112,8 @@ int fwd_rows_per_wg(cqsa_dtype dt, int d);
 hipError_t launch_combine(const CombineArgs& a, int64_t blocks, hipStream_t s);
 hipError_t launch_stage(const StageArgs& a, hipStream_t s);
 hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t s);
+// dst[i] = src[i] rounded to the 16-bit dtype `dt` (nearest even), i < n.
+hipError_t launch_cast_out(const float* src, void* dst, int64_t n, cqsa_dtype dt, hipStream_t s);
 hipError_t launch_bwd_preprocess(const void* dO, const float* O, float* D, cqsa_dtype dt,
                                  int64_t B, int64_t L, int64_t H, int d, hipStream_t s);
 hipError_t launch_bwd_dkdv(cqsa_dtype dt, int d, const BwdArgs& a, hipStream_t s);

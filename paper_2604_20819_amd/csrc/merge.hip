@@ -126,6 +126,42 @@ __global__ void __launch_bounds__(256) combine_kernel(const CombineArgs a) {
   }
 }
 
+// fp32 result rounded to a 16-bit output dtype (nearest even): 8 elements
+// per thread, one 32-byte read and one 16-byte write.
+template <typename T>
+__global__ void __launch_bounds__(256) cast_out_kernel(const float* __restrict__ src,
+                                                       T* __restrict__ dst, int64_t n) {
+  const int64_t i = (int64_t(blockIdx.x) * 256 + threadIdx.x) * 8;
+  if (i + 8 <= n) {
+    const f32x4 x0 = *(const f32x4*)(src + i), x1 = *(const f32x4*)(src + i + 4);
+    typedef __attribute__((__vector_size__(8 * sizeof(T)))) T t8;
+    t8 y;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      y[e] = (T)x0[e];
+      y[4 + e] = (T)x1[e];
+    }
+    *(t8*)(dst + i) = y;
+  } else {
+    for (int64_t k = i; k < n; ++k) dst[k] = (T)src[k];
+  }
+}
+
+hipError_t launch_cast_out(const float* src, void* dst, int64_t n, cqsa_dtype dt, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  const int64_t blocks = (n + 2047) / 2048;
+  if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+  if (dt == CQSA_BF16)
+    hipLaunchKernelGGL(cast_out_kernel<__bf16>, dim3(unsigned(blocks)), dim3(256), 0, s, src,
+                       (__bf16*)dst, n);
+  else if (dt == CQSA_F16)
+    hipLaunchKernelGGL(cast_out_kernel<_Float16>, dim3(unsigned(blocks)), dim3(256), 0, s, src,
+                       (_Float16*)dst, n);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
 hipError_t launch_combine(const CombineArgs& a, int64_t blocks, hipStream_t s) {
   if (blocks <= 0 || a.B <= 0) return hipSuccess;
   if (a.n_seg < 1 || blocks > 0x7fffffff || a.B > 65535) return hipErrorInvalidValue;

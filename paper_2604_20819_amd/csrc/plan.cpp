@@ -130,6 +130,13 @@ cqsa_status validate_plan_args(int64_t L, int32_t H, int32_t d, const cqsa_plan_
     return bad(CQSA_ERR_UNSUPPORTED, "read_in_place = 1 needs L * H * d * elem < 2^31 bytes");
   if (o.with_backward && o.dtype == CQSA_F32)
     return bad(CQSA_ERR_UNSUPPORTED, "the backward supports fp16 and bf16 inputs only");
+  if (o.out16 != 0 && o.out16 != 1) return bad(CQSA_ERR_INVALID_ARG, "out16 must be 0 or 1");
+  if (o.out16 && o.dtype == CQSA_F32)
+    return bad(CQSA_ERR_INVALID_ARG, "out16 = 1 needs fp16 or bf16 inputs");
+  if (o.out16 && o.acc_on_device != 1)
+    return bad(CQSA_ERR_UNSUPPORTED, "out16 = 1 needs acc_on_device = 1");
+  if (o.out16 && o.with_backward)
+    return bad(CQSA_ERR_UNSUPPORTED, "out16 = 1 is forward only: the backward reads the fp32 O");
   return CQSA_OK;
 }
 
@@ -456,8 +463,10 @@ Footprint footprint(const Geometry& g, const cqsa_plan_opts& o, int32_t depth,
   const uint64_t f32_full = align_up(tok * g.d * 4);
   const uint64_t stat_full = align_up(tok * 4);
   const bool direct = direct_forward(o, depth);
+  // caller's O and LSE; with out16 the caller's O is 16-bit and the fp32
+  // result sits in the workspace
   f.resident_fwd = (o.inputs_on_device ? 3 * in_bytes : 0) +
-                   (o.acc_on_device ? f32_full + stat_full : 0);
+                   (o.acc_on_device ? f32_full + stat_full + (o.out16 ? in_bytes : 0) : 0);
   f.resident_bwd = 4 * in_bytes + f32_full + stat_full + 3 * f32_full;
   // slot i holds as many task sub-slots (each sized for the longest task) as
   // the largest group that uses it (groups k with k % n_slots == i)

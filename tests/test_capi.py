@@ -8,6 +8,7 @@ import re
 
 import numpy as np
 import pytest
+import torch
 
 import paper_2604_20819_amd as cq
 from oracle import planner as oplan
@@ -419,3 +420,42 @@ def test_allocator_hook_arguments():
     st = cq.lib().cqsa_set_allocator(ctypes.c_void_p(0x10), None, None)
     assert st == -1 and "both" in cq.lib().cqsa_last_error().decode()
     cq.cqsa_set_allocator(None, None)   # restoring the built-in workspace is always fine
+
+
+def test_out16_footprint_and_errors():
+    """out16 = 1: cqsa_forward writes O in the input dtype and keeps the fp32
+    result in its workspace, so the modelled peak grows by exactly the 16-bit
+    O (the caller's O shrinks from fp32 to 16 bits, the workspace gains the
+    fp32 copy)."""
+    L, H, d = 32768, 16, 128
+    for dt in ("bf16", "f16"):
+        for depth in (0, 1, 2):
+            a = cq.cqsa_plan(L, H, d, True, 0, cq.make_opts(dtype=dt, depth=depth))
+            b = cq.cqsa_plan(L, H, d, True, 0, cq.make_opts(dtype=dt, depth=depth, out16=True))
+            assert b.modelled_device_bytes - a.modelled_device_bytes == L * H * d * 2
+    for kw, status in [(dict(dtype="f32", out16=True), -1),
+                       (dict(out16=True, acc_on_device=False, inputs_on_device=False), -2),
+                       (dict(out16=True, with_backward=True), -2)]:
+        with pytest.raises(cq.CqsaError) as e:
+            cq.cqsa_plan(4096, 4, 64, False, 0, cq.make_opts(**kw))
+        assert e.value.status == status and "out16" in str(e.value)
+    o = cq.make_opts()
+    o.out16 = 2
+    with pytest.raises(cq.CqsaError) as e:
+        cq.cqsa_plan(4096, 4, 64, False, 0, o)
+    assert e.value.status == -1
+
+
+def test_out16_output_dtype_checked_before_any_device_work():
+    """The O dtype must follow the plan: the input dtype with out16, fp32
+    without; a mismatch is an argument error raised before any device call
+    (host-resident inputs, so the tensors here never touch a GPU)."""
+    B, L, H, d = 1, 256, 2, 64
+    Q, K, V = (torch.zeros((B, L, H, d), dtype=torch.bfloat16) for _ in range(3))
+    LSE = torch.zeros((B, H, L), dtype=torch.float32)
+    for out16, odt in ((True, torch.float32), (True, torch.float16), (False, torch.bfloat16)):
+        plan = cq.cqsa_plan(L, H, d, False, 0, cq.make_opts(inputs_on_device=False, out16=out16))
+        O = torch.zeros((B, L, H, d), dtype=odt)
+        with pytest.raises(cq.CqsaError) as e:
+            cq.cqsa_forward(plan, Q, K, V, O, LSE)
+        assert e.value.status == -1 and "O has the wrong dtype" in str(e.value)
