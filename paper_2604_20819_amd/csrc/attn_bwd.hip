@@ -326,14 +326,15 @@ __global__ void __launch_bounds__(64 * dq_waves<D>(), (lds_row_elems<D>() > 128 
     }
 }
 
-// Above d = 160 the dK/dV accumulators of a whole row (2 x d/32 blocks) and
-// the wave's K rows do not fit in registers: the columns of dK and dV are
-// then split over two halves of an 8-wave work group (waves w and w + 4 own
-// the same 32 keys), each half recomputing S and dP over the full d and
-// accumulating its half of the columns; the halves share the work group's
-// Q/dO tiles and V rows, and the 8 waves give two per SIMD where the padded
-// LDS rows allow one work group per CU.
-template <int D> constexpr int dkdv_splits() { return D > 160 ? 2 : 1; }
+// From d = 160 the LDS rows are padded to 256 elements, which leaves one
+// work group per CU, and above 160 the dK/dV accumulators of a whole row
+// (2 x d/32 blocks) and the wave's K rows do not fit in registers.  There the
+// columns of dK and dV are split over two halves of an 8-wave work group
+// (waves w and w + 4 own the same 32 keys; the first half takes the extra
+// block of an odd d/32), each half recomputing S and dP over the full d and
+// accumulating its columns; the halves share the work group's Q/dO tiles and
+// V rows, and the 8 waves run two per SIMD.
+template <int D> constexpr int dkdv_splits() { return D >= 160 ? 2 : 1; }
 
 template <typename E, int D>
 __global__ void __launch_bounds__(256 * dkdv_splits<D>(), (lds_row_elems<D>() > 128 ? 1 : 2)) attn_bwd_dkdv(const BwdArgs a) {
