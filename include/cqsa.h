@@ -56,7 +56,9 @@ typedef enum { CQSA_MEM_HOST = 0, CQSA_MEM_DEVICE = 1 } cqsa_mem;
 
 /* A caller-owned tensor: `data` points at element [0,0,0,0] of a dense
  * row-major [B, L, H, d] array of `dtype`, in host memory (pinned memory is
- * recommended, pageable works) or device memory as `where` says. */
+ * recommended, pageable works) or device memory as `where` says.  `data`
+ * must be 16-byte aligned (the kernels move rows in 16-byte vectors); a
+ * misaligned tensor is rejected with CQSA_ERR_INVALID_ARG. */
 typedef struct {
   void* data;
   cqsa_dtype dtype;

@@ -5,6 +5,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <cstdint>
 #include <cstring>
 
 namespace cqsa {
@@ -163,6 +164,8 @@ cqsa_status check_tensor(const cqsa_tensor* t, const char* name, const cqsa_plan
   std::string n(name);
   if (!t) return fail(CQSA_ERR_INVALID_ARG, n + " is NULL");
   if (!t->data) return fail(CQSA_ERR_INVALID_ARG, n + ".data is NULL");
+  if (reinterpret_cast<uintptr_t>(t->data) % 16 != 0)
+    return fail(CQSA_ERR_INVALID_ARG, n + ".data must be 16-byte aligned");
   if (t->dtype != want) return fail(CQSA_ERR_INVALID_ARG, n + " has the wrong dtype");
   if (t->where != where)
     return fail(CQSA_ERR_INVALID_ARG, n + " residency differs from the plan");

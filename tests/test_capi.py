@@ -459,3 +459,20 @@ def test_out16_output_dtype_checked_before_any_device_work():
         with pytest.raises(cq.CqsaError) as e:
             cq.cqsa_forward(plan, Q, K, V, O, LSE)
         assert e.value.status == -1 and "O has the wrong dtype" in str(e.value)
+
+
+def test_misaligned_tensor_rejected_before_any_device_work():
+    """Tensor data must be 16-byte aligned (rows move in 16-byte vectors): a
+    contiguous view two bytes into its storage is an argument error, raised
+    before any device call (host-resident tensors only)."""
+    B, L, H, d = 1, 256, 2, 64
+    n = B * L * H * d
+    plan = cq.cqsa_plan(L, H, d, False, 0, cq.make_opts(inputs_on_device=False))
+    good = [torch.zeros((B, L, H, d), dtype=torch.bfloat16) for _ in range(2)]
+    bad = torch.zeros(n + 8, dtype=torch.bfloat16)[1:1 + n].view(B, L, H, d)
+    assert bad.is_contiguous() and bad.data_ptr() % 16 == 2
+    O = torch.zeros((B, L, H, d), dtype=torch.float32)
+    LSE = torch.zeros((B, H, L), dtype=torch.float32)
+    with pytest.raises(cq.CqsaError) as e:
+        cq.cqsa_forward(plan, bad, *good, O, LSE)
+    assert e.value.status == -1 and "Q.data must be 16-byte aligned" in str(e.value)
