@@ -44,7 +44,8 @@ extern "C" {
 typedef enum {
   CQSA_OK = 0,
   CQSA_ERR_INVALID_ARG = -1, /* bad pointer, shape, dtype or option; no device work done */
-  CQSA_ERR_UNSUPPORTED = -2, /* valid but not built (e.g. d not in {64,128}) */
+  CQSA_ERR_UNSUPPORTED = -2, /* valid but not built (e.g. d not a multiple of 32 in [32, 256],
+                                fp32 inputs to the backward) */
   CQSA_ERR_BUDGET = -3,      /* no depth <= max_depth fits the device budget */
   CQSA_ERR_DEVICE_OOM = -4,  /* a device allocation failed */
   CQSA_ERR_HIP = -5,         /* a HIP runtime call failed (no device, launch error, ...) */
@@ -91,8 +92,9 @@ typedef struct {
   int32_t inputs_on_device;  /* 1: Q, K, V (and dO) are device-resident; 0: host-resident (1) */
   int32_t acc_on_device;     /* 1: accumulator/outputs on device; 0: on host, merged by host
                                 threads; -1: on the device when some depth in [min_depth,
-                                max_depth] fits the budget there, else on the host (forward
-                                plans only; query cqsa_plan_acc_on_device) (1) */
+                                max_depth] fits the budget there, else on the host (query
+                                cqsa_plan_acc_on_device).  For the backward, O, LSE, dQ, dK
+                                and dV follow this residency (1) */
   int32_t with_backward;     /* 1: the footprint must also fit cqsa_backward (0) */
   int32_t tasks_per_slot;    /* forward tasks staged, launched and merged together, in [0, 32]:
                                 0 = automatic: with inputs read in place, every task up to 32
@@ -235,10 +237,19 @@ cqsa_status cqsa_forward(const cqsa_plan_t* plan, const cqsa_tensor* Q, const cq
                          float scale, void* hip_stream);
 
 /* Decomposed backward in the global-LSE form (App. A.1, Eq. "globallse"),
- * equal to Alg. 2.  Q, K, V, dO: inputs matching the plan; O, LSE: the
- * forward's outputs; dQ, dK, dV: fp32 [B, L, H, d], overwritten.  This build
- * supports device-resident tensors only (CQSA_ERR_UNSUPPORTED otherwise) and a
- * plan made with with_backward = 1 or an uncapped budget. */
+ * equal to Alg. 2.  Q, K, V, dO: inputs matching the plan, resident where the
+ * plan's inputs are (inputs_on_device); O, LSE: the forward's outputs, and
+ * dQ, dK, dV: fp32 [B, L, H, d], overwritten, all resident where the plan's
+ * accumulator is (acc_on_device; Sec. 4.1 keeps Q, K, V in host memory, and
+ * Table "recovery" runs forward+backward with the accumulator on the host).
+ * Host-resident inputs are staged task by task through the device slots (a
+ * token the previously staged task also holds is copied on the device);
+ * D = rowsum(dO * O) is computed from chunks of host-resident O or dO;
+ * host-resident gradients are computed per task on the device, copied back
+ * and added into dQ, dK, dV on host threads, and the call then blocks until
+ * they are complete.  Needs a 16-bit dtype and a plan made with
+ * with_backward = 1 or an uncapped budget; the OOM guardrail of cqsa_forward
+ * applies (fewer staging slots, then deeper plans). */
 cqsa_status cqsa_backward(const cqsa_plan_t* plan, const cqsa_tensor* Q, const cqsa_tensor* K,
                           const cqsa_tensor* V, const cqsa_tensor* O, const float* LSE,
                           cqsa_mem lse_where, const cqsa_tensor* dO, cqsa_tensor* dQ,

@@ -102,6 +102,55 @@ def attention_backward(Q, K, V, dO, causal, scale=None):
     return dQ, dK, dV, O, LSE
 
 
+def attention_backward_rows(Q, K, V, dO, causal, q_rows, k_rows, scale=None, row_chunk=64):
+    """The gradients of `attention_backward` on a subset of rows, for long
+    sequences: dQ on query rows q_rows and dK, dV on key rows k_rows.
+
+    Same definitions (App. A.1, Eq. "globallse").  A dQ row needs only its own
+    query's scores; a dK or dV row sums over every query that keeps the key,
+    so every query row is visited once, row_chunk at a time: its scores give
+    its LSE, P row, O row and D, and its contribution to the sampled keys'
+    sums is added before the next chunk.  Memory is row_chunk * L scores;
+    time is O(L^2 d) per (b, h).
+
+    q_rows, k_rows: int arrays shared by every head, or lists of H arrays.
+    Returns dQ [B, len(q_rows), H, d] and dK, dV [B, len(k_rows), H, d], float64.
+    """
+    Q = np.asarray(Q)
+    B, L, H, d = Q.shape
+    alpha = _scale(d, scale)
+    per_head = lambda r: ([np.asarray(x, dtype=np.int64) for x in r]
+                          if isinstance(r, (list, tuple)) else [np.asarray(r, dtype=np.int64)] * H)
+    qr_h, kr_h = per_head(q_rows), per_head(k_rows)
+    dQ = np.zeros((B, len(qr_h[0]), H, d))
+    dK = np.zeros((B, len(kr_h[0]), H, d))
+    dV = np.zeros((B, len(kr_h[0]), H, d))
+    for b in range(B):
+        for h in range(H):
+            k = _f64(K[b, :, h, :]); v = _f64(V[b, :, h, :])
+            kr = kr_h[h]
+            qpos = {int(r): i for i, r in enumerate(qr_h[h])}
+            for c0 in range(0, L, row_chunk):
+                r = np.arange(c0, min(L, c0 + row_chunk))
+                q = _f64(Q[b, r, h, :]); do = _f64(dO[b, r, h, :])
+                s = alpha * (q @ k.T)                                  # [r, L]
+                if causal:
+                    s = np.where(np.arange(L)[None, :] <= r[:, None], s, -np.inf)
+                m = s.max(axis=1, keepdims=True)
+                lse = m + np.log(np.exp(s - m).sum(axis=1, keepdims=True))
+                p = np.exp(s - lse)                                    # rows sum to 1
+                D = (do * (p @ v)).sum(axis=1, keepdims=True)
+                # the sampled keys' columns of dS for these queries
+                ds_k = p[:, kr] * (do @ v[kr].T - D)
+                dK[b, :, h, :] += alpha * (ds_k.T @ q)
+                dV[b, :, h, :] += p[:, kr].T @ do
+                sel = [i for i, x in enumerate(r) if int(x) in qpos]
+                if sel:
+                    ds = p[sel] * (do[sel] @ v.T - D[sel])
+                    dQ[b, [qpos[int(r[i])] for i in sel], h, :] = alpha * (ds @ k)
+    return dQ, dK, dV
+
+
 def rel_l2(x, ref):
     """Relative error ||x - ref||_2 / ||ref||_2 over the whole tensor, the
     metric read into Section 4.2's "relative error"."""

@@ -270,11 +270,22 @@ def _stream_of(*ts):
     return ctypes.c_void_p(0)
 
 
+def _check_lse(plan, LSE, O):
+    """The C ABI takes LSE as a bare float pointer: its shape, dtype, layout and
+    residency are checked here, before any call."""
+    if LSE.dtype != _torch().float32 or not LSE.is_contiguous():
+        raise ValueError("LSE must be a contiguous float32 tensor")
+    want = (plan.opts.B, plan.H, plan.L)
+    if tuple(LSE.shape) != want:
+        raise ValueError(f"LSE must have shape (B, H, L) = {want}, got {tuple(LSE.shape)}")
+    if LSE.is_cuda != O.is_cuda or (LSE.is_cuda and LSE.device != O.device):
+        raise ValueError("LSE must live where O lives")
+
+
 def cqsa_forward(plan, Q, K, V, O, LSE, scale=0.0, stream=None):
     """O (fp32 [B,L,H,d], or the input dtype with out16) and LSE (fp32 [B,H,L]) are
     written in place."""
-    if not (LSE.is_contiguous() and LSE.dtype == _torch().float32):
-        raise ValueError("LSE must be a contiguous float32 tensor")
+    _check_lse(plan, LSE, O)
     tq, tk, tv, to = (as_cqsa_tensor(x) for x in (Q, K, V, O))
     s = stream if stream is not None else _stream_of(O, Q)
     _check(lib().cqsa_forward(plan.handle, ctypes.byref(tq), ctypes.byref(tk), ctypes.byref(tv),
@@ -284,7 +295,9 @@ def cqsa_forward(plan, Q, K, V, O, LSE, scale=0.0, stream=None):
 
 
 def cqsa_backward(plan, Q, K, V, O, LSE, dO, dQ, dK, dV, scale=0.0, stream=None):
-    """dQ, dK, dV (fp32 [B,L,H,d]) are overwritten."""
+    """dQ, dK, dV (fp32 [B,L,H,d]) are overwritten.  Q, K, V, dO live where the
+    plan's inputs do; O, LSE, dQ, dK, dV where its accumulator does."""
+    _check_lse(plan, LSE, O)
     ts = [as_cqsa_tensor(x) for x in (Q, K, V, O, dO, dQ, dK, dV)]
     s = stream if stream is not None else _stream_of(dQ, Q)
     _check(lib().cqsa_backward(plan.handle, *(ctypes.byref(t) for t in ts[:4]),

@@ -30,7 +30,10 @@ constexpr float kLog2e = 1.4426950408889634f;
 // d = 96 and 128 8 waves gained nothing, at 192 and up they spill more).
 template <int D> constexpr int dq_waves() { return D == 160 ? 8 : 4; }
 
-template <typename E, int D>
+// LOCAL (BwdArgs::local_out) is a template parameter: a run-time branch in
+// the epilogue changes the register allocation of the whole kernel (the
+// dK/dV kernel at d = 128 then spills).
+template <typename E, int D, bool LOCAL>
 __global__ void __launch_bounds__(64 * dq_waves<D>(), (lds_row_elems<D>() > 128 ? 1 : 2)) attn_bwd_dq(const BwdArgs a) {
   constexpr int WAVES = dq_waves<D>(), NT = 64 * WAVES;
   constexpr int BM = 32 * WAVES, BN = 64;
@@ -311,13 +314,15 @@ __global__ void __launch_bounds__(64 * dq_waves<D>(), (lds_row_elems<D>() > 128 
     nrow = row2;
   }
   if (!qvalid) return;
-  float* dst = a.dq + (int64_t(b) * a.Lg + gq) * rs + int64_t(h) * D;
+  // global rows accumulate (a task holds a token once and the dQ launches of
+  // a call are ordered on one stream); a task-local buffer is stored
+  float* dst = a.dq + (LOCAL ? int64_t(b) * L + myq : int64_t(b) * a.Lg + gq) * rs + int64_t(h) * D;
 #pragma unroll
   for (int db = 0; db < DB; ++db)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       f32x4* p = (f32x4*)(dst + 32 * db + 8 * i + 4 * half);
-      f32x4 v = *p;
+      f32x4 v = LOCAL ? f32x4{0.f, 0.f, 0.f, 0.f} : *p;
       v[0] += a.scale * dq[db][4 * i];
       v[1] += a.scale * dq[db][4 * i + 1];
       v[2] += a.scale * dq[db][4 * i + 2];
@@ -336,7 +341,7 @@ __global__ void __launch_bounds__(64 * dq_waves<D>(), (lds_row_elems<D>() > 128 
 // V rows, and the 8 waves run two per SIMD.
 template <int D> constexpr int dkdv_splits() { return D >= 160 ? 2 : 1; }
 
-template <typename E, int D>
+template <typename E, int D, bool LOCAL>
 __global__ void __launch_bounds__(256 * dkdv_splits<D>(), (lds_row_elems<D>() > 128 ? 1 : 2)) attn_bwd_dkdv(const BwdArgs a) {
   // 32-query tiles (two per 64-token summary block) keep the registers and
   // LDS within two work groups per CU (one above d = 128)
@@ -684,16 +689,22 @@ __global__ void __launch_bounds__(256 * dkdv_splits<D>(), (lds_row_elems<D>() > 
   }
   __builtin_amdgcn_s_waitcnt(0x0F70);  // the V fill has landed even when no tile was live
   if (!kvalid) return;
-  const int64_t gk = run_global(runs_s, a.n_runs, mykey);
-  float* dkp = a.dk + (int64_t(b) * a.Lg + gk) * rs + int64_t(h) * D;
-  float* dvp = a.dv + (int64_t(b) * a.Lg + gk) * rs + int64_t(h) * D;
+  // global rows accumulate; a task-local buffer is stored (as for dQ)
+  const int64_t orow = LOCAL ? int64_t(b) * L + mykey
+                             : int64_t(b) * a.Lg + run_global(runs_s, a.n_runs, mykey);
+  float* dkp = a.dk + orow * rs + int64_t(h) * D;
+  float* dvp = a.dv + orow * rs + int64_t(h) * D;
 #pragma unroll
   for (int db = 0; db < DBO; ++db) {
     if (NSPLIT > 1 && db0 + db >= DB) break;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int off = 32 * (db0 + db) + 8 * i + 4 * half;
-      f32x4 x = *(f32x4*)(dkp + off), y = *(f32x4*)(dvp + off);
+      f32x4 x = f32x4{0.f, 0.f, 0.f, 0.f}, y = x;
+      if (!LOCAL) {
+        x = *(f32x4*)(dkp + off);
+        y = *(f32x4*)(dvp + off);
+      }
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         x[j] += a.scale * dk[db][4 * i + j];
@@ -710,7 +721,10 @@ static hipError_t launch_dq_t(const BwdArgs& a, hipStream_t s) {
   constexpr int rows = 32 * dq_waves<D>();
   const int64_t n = ((a.L + rows - 1) / rows) * int64_t(a.H) * a.B;
   if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL((attn_bwd_dq<E, D>), dim3(unsigned(n)), dim3(64 * dq_waves<D>()), 0, s, a);
+  if (a.local_out)
+    hipLaunchKernelGGL((attn_bwd_dq<E, D, true>), dim3(unsigned(n)), dim3(64 * dq_waves<D>()), 0, s, a);
+  else
+    hipLaunchKernelGGL((attn_bwd_dq<E, D, false>), dim3(unsigned(n)), dim3(64 * dq_waves<D>()), 0, s, a);
   return hipGetLastError();
 }
 
@@ -718,7 +732,10 @@ template <typename E, int D>
 static hipError_t launch_dkdv_t(const BwdArgs& a, hipStream_t s) {
   const int64_t n = ((a.L + 127) / 128) * int64_t(a.H) * a.B;
   if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL((attn_bwd_dkdv<E, D>), dim3(unsigned(n)), dim3(256 * dkdv_splits<D>()), 0, s, a);
+  if (a.local_out)
+    hipLaunchKernelGGL((attn_bwd_dkdv<E, D, true>), dim3(unsigned(n)), dim3(256 * dkdv_splits<D>()), 0, s, a);
+  else
+    hipLaunchKernelGGL((attn_bwd_dkdv<E, D, false>), dim3(unsigned(n)), dim3(256 * dkdv_splits<D>()), 0, s, a);
   return hipGetLastError();
 }
 

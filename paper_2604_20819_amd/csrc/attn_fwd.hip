@@ -22,6 +22,13 @@
 // Running maxima are rounded up to integers in the log2 domain, so every
 // rescale is an exact power of two and 16-bit P is rounded identically
 // whichever task, or the undecomposed call, produced it.
+//
+// Two row sums: l adds the fp32 weights (it gives the log-sum-exp), lt adds
+// the 16-bit weights the P.V product actually consumes.  Both are task
+// statistics merged with the same power-of-two factors, and O = acc / lt is
+// the exactly normalised average of V rows under the rounded weights (a
+// one-hot row returns its V row) whatever the decomposition: every task
+// rounds the same weights to the same values.
 #include "hip_common.hpp"
 #include "kernels.hpp"
 
@@ -66,7 +73,6 @@ __global__ void __launch_bounds__(64 * fwd_waves<D>(), (lds_row_elems<D>() > 128
   const DevTask tk = a.tasks[tj];
   const int L = int(tk.L_local);
   const int64_t nstrips = (L + BM - 1) / BM;
-  // strips in the task's launch order (most live key tiles first)
   // strips in the task's launch order (most live key tiles first; the plan
   // builds this table for BM-row strips, BM = fwd_rows_per_wg)
   const int strip = ((const int32_t*)(a.tab + tk.qorder_off))[work % nstrips];
@@ -233,7 +239,7 @@ __global__ void __launch_bounds__(64 * fwd_waves<D>(), (lds_row_elems<D>() > 128
   for (int db = 0; db < DB; ++db)
 #pragma unroll
     for (int r = 0; r < 16; ++r) o[db][r] = 0.f;
-  float m_run = -INFINITY, l_run = 0.f;
+  float m_run = -INFINITY, l_run = 0.f, lt_run = 0.f;
 
   __syncthreads();  // runs_s visible
   const uint32_t qbits = qvalid ? run_bits(runs_s, n_runs, myq) : 0u;
@@ -335,6 +341,7 @@ __global__ void __launch_bounds__(64 * fwd_waves<D>(), (lds_row_elems<D>() > 128
       // integer maxima change rarely: rescale only when some lane's did
       if (__builtin_amdgcn_ballot_w64(alpha != 1.f) != 0ull) {
         l_run *= alpha;
+        lt_run *= alpha;
 #pragma unroll
         for (int db = 0; db < DB; ++db)
 #pragma unroll
@@ -357,6 +364,7 @@ __global__ void __launch_bounds__(64 * fwd_waves<D>(), (lds_row_elems<D>() > 128
 #pragma unroll
         for (int e = 0; e < 8; ++e) pv[e] = s[kb][8 * sub + e];
         const vec8 pb = pack8<E>(pv);
+        lt_run = sum8<E>(pb, lt_run);
         const int row = 32 * kb + 16 * sub + 4 * half + ((lane & 15) >> 2);
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
@@ -389,6 +397,7 @@ __global__ void __launch_bounds__(64 * fwd_waves<D>(), (lds_row_elems<D>() > 128
   }
 
   const float l_tot = l_run + swap_halves(l_run);
+  const float lt_tot = lt_run + swap_halves(lt_run);
   if (!qvalid) return;
   if (MODE == kModeStats) {
     float* accp = a.acc + tj * a.acc_stride + (int64_t(b) * L + myq) * rs + int64_t(h) * D;
@@ -403,9 +412,10 @@ __global__ void __launch_bounds__(64 * fwd_waves<D>(), (lds_row_elems<D>() > 128
       const int64_t si = tj * a.st_stride + (int64_t(b) * a.H + h) * L + myq;
       a.m[si] = m_run;
       a.l[si] = l_tot;
+      a.lt[si] = lt_tot;
     }
   } else {
-    const float inv = 1.f / l_tot;
+    const float inv = 1.f / lt_tot;
     float* op = a.acc + (int64_t(b) * L + myq) * rs + int64_t(h) * D;
 #pragma unroll
     for (int db = 0; db < DB; ++db)
@@ -521,6 +531,7 @@ __global__ void __launch_bounds__(256) attn_fwd_f32(const FwdArgs a) {
       const int64_t si = tj * a.st_stride + (int64_t(b) * a.H + h) * L + myq;
       a.m[si] = m_run;
       a.l[si] = l_run;
+      a.lt[si] = l_run;  // fp32 weights are not rounded
     }
   } else {
     const float inv = 1.f / l_run;

@@ -1,25 +1,80 @@
 // cqsa_backward: decomposed backward in the global-LSE form (App. A.1,
 // Eq. "globallse"), equal to Alg. 2.
 //
-// caller stream : D = rowsum(dO * O) over the full sequence, zero dQ/dK/dV;
-//                 per task wait "staged", run the key-parallel dK/dV kernel,
-//                 which adds the task's rows into the global fp32 dK and dV;
-// second stream : per task the query-parallel dQ kernel, adding into dQ.
-//                 Each stream keeps the tasks in order and a task holds each
-//                 token once, so these read-modify-writes never race;
+// Q, K, V, dO sit where the plan's inputs do; O, LSE, dQ, dK, dV where its
+// accumulator does (the forward's outputs), each on the host or the device.
+//
+// caller stream : D = rowsum(dO * O) over the full sequence (host-resident O
+//                 or dO arrive in chunks through the staging slots); zero
+//                 dQ/dK/dV when they are device-resident; per task wait
+//                 "staged", run the key-parallel dK/dV kernel;
+// second stream : per task the query-parallel dQ kernel;
 // copy stream   : gather each task's runs of Q, K, V, dO into slot t % S once
-//                 both kernels of the slot's previous task are done (staged
-//                 plans only: a plan that reads its inputs in place passes
-//                 the caller's tensors and the task's block row table).
-// Depth 0 reads the caller's tensors in place (the undecomposed backward).
+//                 both kernels of the slot's previous task are done: a gather
+//                 kernel from device-resident inputs, host-to-device copies
+//                 from host-resident ones (tokens the previously staged task
+//                 also holds come from its staged rows on the device); a plan
+//                 that reads device-resident inputs in place stages nothing;
+// device gradients: each kernel's epilogue adds the task's rows into the
+//                 global fp32 gradients.  Each stream keeps the tasks in order
+//                 and a task holds each token once, so these read-modify-writes
+//                 never race;
+// host gradients: the kernels store the task's rows in the slot's own
+//                 gradient buffers; the auxiliary stream copies them to pinned
+//                 host memory and a host thread adds them into dQ, dK, dV at
+//                 their global rows, task after task (App. A.3, accumulator on
+//                 the host).
+// Depth 0 on device-resident inputs reads the caller's tensors in place (the
+// undecomposed backward).
 #include <algorithm>
+#include <chrono>
 #include <cmath>
+#include <cstring>
 
 #include "guard.hpp"
 #include "kernels.hpp"
 #include "runtime.hpp"
+#include "streamer.hpp"
 
 namespace cqsa {
+
+namespace {
+
+// dst[global rows of the task] += src[task rows] for the three gradients
+// (fp32 [B, L, H, d] and [B, Li, H, d]); rows split across host threads.
+void host_scatter_add(const Task& task, const float* const src[3], float* const dst[3], int64_t B,
+                      int64_t L, int64_t H, int64_t d) {
+  const int64_t Li = task.L_local, rw = H * d;
+  parallel_rows(B * Li, [&](int64_t lo, int64_t hi) {
+    size_t ri = 0;
+    for (int64_t x = lo; x < hi;) {
+      const int64_t b = x / Li, r = x % Li;
+      while (ri + 1 < task.runs.size() && r >= task.runs[ri].local_start + task.runs[ri].length)
+        ++ri;
+      while (ri > 0 && r < task.runs[ri].local_start) --ri;
+      const Run& run = task.runs[ri];
+      // rows [r, r + n) of this batch element lie in one run: one span each
+      const int64_t n = std::min({hi - x, Li - r, run.local_start + run.length - r});
+      const int64_t g = run.global_start + (r - run.local_start);
+      for (int t = 0; t < 3; ++t) {
+        const float* s = src[t] + (b * Li + r) * rw;
+        float* o = dst[t] + (b * L + g) * rw;
+        for (int64_t k = 0; k < n * rw; ++k) o[k] += s[k];
+      }
+      x += n;
+    }
+  });
+}
+
+void host_zero(float* const p[3], int64_t n) {
+  for (int t = 0; t < 3; ++t)
+    parallel_rows(n / 4096 + 1, [&](int64_t lo, int64_t hi) {
+      const int64_t a = lo * 4096, b = std::min(n, hi * 4096);
+      if (b > a) std::memset(p[t] + a, 0, size_t(b - a) * sizeof(float));
+    });
+}
+
+}  // namespace
 
 cqsa_status backward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_tensor* K,
                           const cqsa_tensor* V, const cqsa_tensor* O, const float* LSE,
@@ -27,8 +82,6 @@ cqsa_status backward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa
                           cqsa_tensor* dK, cqsa_tensor* dV, float scale, hipStream_t st) {
   if (!p) return fail(CQSA_ERR_INVALID_ARG, "cqsa_backward: plan is NULL");
   const cqsa_plan_opts& o = p->opts;
-  if (!o.inputs_on_device || !o.acc_on_device)
-    return fail(CQSA_ERR_UNSUPPORTED, "cqsa_backward: device-resident plans only");
   if (o.dtype == CQSA_F32)
     return fail(CQSA_ERR_UNSUPPORTED, "cqsa_backward: fp16 and bf16 inputs only");
   if (p->g.d % 32 != 0 || p->g.d > 256)
@@ -37,18 +90,21 @@ cqsa_status backward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa
     return fail(CQSA_ERR_INVALID_ARG,
                 "cqsa_backward: the plan's budget was fitted without the backward "
                 "(plan with with_backward = 1)");
+  const bool dev_in = o.inputs_on_device != 0, dev_acc = o.acc_on_device == 1;
+  const cqsa_mem in_where = dev_in ? CQSA_MEM_DEVICE : CQSA_MEM_HOST;
+  const cqsa_mem acc_where = dev_acc ? CQSA_MEM_DEVICE : CQSA_MEM_HOST;
   cqsa_status s;
-  const cqsa_mem dev = CQSA_MEM_DEVICE;
-  if ((s = check_tensor(Q, "Q", p, o.dtype, dev)) != CQSA_OK) return s;
-  if ((s = check_tensor(K, "K", p, o.dtype, dev)) != CQSA_OK) return s;
-  if ((s = check_tensor(V, "V", p, o.dtype, dev)) != CQSA_OK) return s;
-  if ((s = check_tensor(dO, "dO", p, o.dtype, dev)) != CQSA_OK) return s;
-  if ((s = check_tensor(O, "O", p, CQSA_F32, dev)) != CQSA_OK) return s;
-  if ((s = check_tensor(dQ, "dQ", p, CQSA_F32, dev)) != CQSA_OK) return s;
-  if ((s = check_tensor(dK, "dK", p, CQSA_F32, dev)) != CQSA_OK) return s;
-  if ((s = check_tensor(dV, "dV", p, CQSA_F32, dev)) != CQSA_OK) return s;
+  if ((s = check_tensor(Q, "Q", p, o.dtype, in_where)) != CQSA_OK) return s;
+  if ((s = check_tensor(K, "K", p, o.dtype, in_where)) != CQSA_OK) return s;
+  if ((s = check_tensor(V, "V", p, o.dtype, in_where)) != CQSA_OK) return s;
+  if ((s = check_tensor(dO, "dO", p, o.dtype, in_where)) != CQSA_OK) return s;
+  if ((s = check_tensor(O, "O", p, CQSA_F32, acc_where)) != CQSA_OK) return s;
+  if ((s = check_tensor(dQ, "dQ", p, CQSA_F32, acc_where)) != CQSA_OK) return s;
+  if ((s = check_tensor(dK, "dK", p, CQSA_F32, acc_where)) != CQSA_OK) return s;
+  if ((s = check_tensor(dV, "dV", p, CQSA_F32, acc_where)) != CQSA_OK) return s;
   if (!LSE) return fail(CQSA_ERR_INVALID_ARG, "LSE is NULL");
-  if (lse_where != CQSA_MEM_DEVICE) return fail(CQSA_ERR_INVALID_ARG, "LSE must be on the device");
+  if (lse_where != acc_where)
+    return fail(CQSA_ERR_INVALID_ARG, "LSE residency must equal the output residency");
 
   DevCtx* C = device_ctx(&s);
   if (!C) return s;
@@ -60,10 +116,10 @@ cqsa_status backward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa
   const float sc = scale > 0.f ? scale : float(1.0 / std::sqrt(double(d)));
   const int depth = p->depth;
   const int64_t ntask = int64_t(p->tasks.size());
-  const bool direct = depth == 0;
-  // kernels address the runs inside the caller's tensors: nothing is staged
-  const bool in_place = !direct && o.read_in_place == 1;
-  const bool staged = !direct && !in_place;
+  const bool staged = bwd_staged(o, depth);
+  // device-resident inputs not staged: read in place (decomposed) or the
+  // caller's tensors themselves (undecomposed)
+  const bool in_place = !staged && depth > 0;
 
   CallRecord& rec = call_record();
   rec.reset();
@@ -76,74 +132,157 @@ cqsa_status backward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa
     CQSA_HIP(hipEventRecord(rec.wall0, st));
   }
 
+  // ---- workspace: [plan image][D][LSE copy, host LSE only][slot 0]...[slot S-1];
+  // a slot holds the staged Q, K, V, dO (staged plans) and then the task's
+  // own dQ, dK, dV (host gradients), each sized for the longest task
   const uint64_t tab_bytes = align_up(p->packed.size());
-  const uint64_t d_bytes = align_up(uint64_t(B) * H * L * 4);
+  const uint64_t stat_bytes = align_up(uint64_t(B) * H * L * 4);
+  const uint64_t lse_bytes = dev_acc ? 0 : stat_bytes;
   const uint64_t slot_bytes = bwd_slot_bytes(p->g, o, p->max_L_local, staged);
   const int64_t nslot = std::min<int64_t>(o.n_slots, std::max<int64_t>(1, ntask));
-  const uint64_t total = tab_bytes + d_bytes + uint64_t(nslot) * slot_bytes;
+  const uint64_t total = tab_bytes + stat_bytes + lse_bytes + uint64_t(nslot) * slot_bytes;
   Workspace ws;
   if ((s = acquire_workspace(C, total, &ws)) != CQSA_OK) return s;
   rec.stats.workspace_bytes = total;
-  rec.stats.resident_tasks = staged ? nslot : 0;
+  rec.stats.resident_tasks = (staged || !dev_acc) ? nslot : 0;
   char* base = (char*)ws.ptr;
   char* d_tab = base;
   float* d_D = (float*)(base + tab_bytes);
-  const uint64_t in_b = align_up(uint64_t(B) * p->max_L_local * H * d * elem);
+  const float* d_lse = dev_acc ? LSE : (const float*)(base + tab_bytes + stat_bytes);
+  const uint64_t in_b = staged ? align_up(uint64_t(B) * p->max_L_local * H * d * elem) : 0;
+  const uint64_t g_b = align_up(uint64_t(B) * p->max_L_local * H * d * 4);
+  auto slot_base = [&](int64_t si) {
+    return base + tab_bytes + stat_bytes + lse_bytes + uint64_t(si) * slot_bytes;
+  };
 
-  while (C->sync_events.size() < size_t(4 * nslot + 3)) {
+  while (C->sync_events.size() < size_t(5 * nslot + 4)) {
     hipEvent_t e;
     CQSA_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
     C->sync_events.push_back(e);
   }
   hipEvent_t ev_start = C->sync_events[0];
   hipEvent_t ev_tab = C->sync_events[1];
-  hipEvent_t* ev_staged = &C->sync_events[2];
-  hipEvent_t* ev_free = &C->sync_events[2 + nslot];      // dK/dV kernel done with the slot
-  hipEvent_t* ev_free_q = &C->sync_events[2 + 2 * nslot]; // dQ kernel done with the slot
-  hipEvent_t ev_pre = C->sync_events[2 + 3 * nslot];      // preprocess and zero fill done
+  hipEvent_t ev_pre = C->sync_events[2];
+  hipEvent_t ev_join = C->sync_events[3];
+  hipEvent_t* ev_staged = &C->sync_events[4];
+  hipEvent_t* ev_free = &C->sync_events[4 + nslot];      // dK/dV kernel done with the slot
+  hipEvent_t* ev_free_q = &C->sync_events[4 + 2 * nslot]; // dQ kernel done with the slot
+  hipEvent_t* ev_d2h = &C->sync_events[4 + 3 * nslot];    // the slot's gradients copied out
+  hipEvent_t* ev_chunk = &C->sync_events[4 + 4 * nslot];  // preprocess done with the slot
+  const hipStream_t cs = C->copy, qs = C->lane, ms = C->aux;
   if (C->ws_free_valid) CQSA_HIP(hipStreamWaitEvent(st, C->ws_free, 0));
   CQSA_HIP(hipEventRecord(ev_start, st));
-  CQSA_HIP(hipStreamWaitEvent(C->copy, ev_start, 0));
-  if ((s = upload_image(C, p->packed, d_tab, C->copy)) != CQSA_OK) return s;
-  CQSA_HIP(hipEventRecord(ev_tab, C->copy));
+  CQSA_HIP(hipStreamWaitEvent(cs, ev_start, 0));
+  if ((s = upload_image(C, p->packed, d_tab, cs)) != CQSA_OK) return s;
+  if (!dev_acc) {
+    CQSA_HIP(hipMemcpyAsync((void*)d_lse, LSE, uint64_t(B) * H * L * 4, hipMemcpyHostToDevice, cs));
+    rec.stats.h2d_bytes += uint64_t(B) * H * L * 4;
+  }
+  CQSA_HIP(hipEventRecord(ev_tab, cs));
 
-  // preprocess and zero-fill on the caller's stream
-  std::pair<hipEvent_t, hipEvent_t> sp{nullptr, nullptr};
-  if (rec.timing) {
-    sp = {rec.make(), rec.make()};
-    CQSA_HIP(hipEventRecord(sp.first, st));
+  auto span_begin = [&](hipStream_t sm) -> std::pair<hipEvent_t, hipEvent_t> {
+    std::pair<hipEvent_t, hipEvent_t> sp{nullptr, nullptr};
+    if (rec.timing) {
+      sp = {rec.make(), rec.make()};
+      if (hipEventRecord(sp.first, sm) != hipSuccess) sp = {nullptr, nullptr};
+    }
+    return sp;
+  };
+  auto span_end = [&](std::pair<hipEvent_t, hipEvent_t> sp, hipStream_t sm, Stage k) {
+    if (sp.first && hipEventRecord(sp.second, sm) == hipSuccess) rec.spans[k].push_back(sp);
+  };
+
+  // ---- D = rowsum(dO * O) on the caller's stream ----
+  if (dev_in && dev_acc) {
+    auto sp = span_begin(st);
+    CQSA_HIP(launch_bwd_preprocess(dO->data, (const float*)O->data, d_D, o.dtype, B, L, H, int(d),
+                                   L, st));
+    span_end(sp, st, kStFinal);
+  } else {
+    // rows of one batch element in chunks of the longest task's length: a
+    // host-resident dO chunk goes to the slot's staged-input area, a
+    // host-resident O chunk to its gradient area (both at least that large)
+    const int64_t crows = std::max<int64_t>(1, p->max_L_local);
+    int64_t c = 0;
+    for (int64_t b = 0; b < B; ++b)
+      for (int64_t g0 = 0; g0 < L; g0 += crows, ++c) {
+        const int64_t n = std::min(crows, L - g0);
+        const int64_t si = c % nslot;
+        char* sb = slot_base(si);
+        if (c >= nslot) CQSA_HIP(hipStreamWaitEvent(cs, ev_chunk[si], 0));
+        const uint64_t off_in = uint64_t(b * L + g0) * row_bytes;
+        const uint64_t off_o = uint64_t(b * L + g0) * H * d * 4;
+        const void* pdo = (const char*)dO->data + off_in;
+        const float* po = (const float*)((const char*)O->data + off_o);
+        auto sp = span_begin(cs);
+        if (!dev_in) {
+          CQSA_HIP(hipMemcpyAsync(sb, pdo, n * row_bytes, hipMemcpyHostToDevice, cs));
+          pdo = sb;
+          rec.stats.h2d_bytes += uint64_t(n) * row_bytes;
+        }
+        if (!dev_acc) {
+          char* dst = sb + 4 * in_b;
+          CQSA_HIP(hipMemcpyAsync(dst, po, n * H * d * 4, hipMemcpyHostToDevice, cs));
+          po = (const float*)dst;
+          rec.stats.h2d_bytes += uint64_t(n) * H * d * 4;
+        }
+        span_end(sp, cs, kStStage);
+        CQSA_HIP(hipEventRecord(ev_staged[si], cs));
+        CQSA_HIP(hipStreamWaitEvent(st, ev_staged[si], 0));
+        auto sq = span_begin(st);
+        CQSA_HIP(launch_bwd_preprocess(pdo, po, d_D + b * H * L + g0, o.dtype, 1, n, H, int(d), L,
+                                       st));
+        span_end(sq, st, kStFinal);
+        CQSA_HIP(hipEventRecord(ev_chunk[si], st));
+      }
+    // task staging reuses the slots once every chunk is consumed
+    CQSA_HIP(hipEventRecord(ev_pre, st));
+    CQSA_HIP(hipStreamWaitEvent(cs, ev_pre, 0));
   }
-  CQSA_HIP(launch_bwd_preprocess(dO->data, (const float*)O->data, d_D, o.dtype, B, L, H, int(d), st));
-  if (rec.timing) {
-    CQSA_HIP(hipEventRecord(sp.second, st));
-    rec.spans[kStFinal].push_back(sp);
-    sp = {rec.make(), rec.make()};
-    CQSA_HIP(hipEventRecord(sp.first, st));
-  }
-  // the fused scatter-adds accumulate into zeroed gradients
-  CQSA_HIP(launch_fill_zero((float*)dQ->data, B * L * H * d, st));
-  CQSA_HIP(launch_fill_zero((float*)dK->data, B * L * H * d, st));
-  CQSA_HIP(launch_fill_zero((float*)dV->data, B * L * H * d, st));
-  if (rec.timing) {
-    CQSA_HIP(hipEventRecord(sp.second, st));
-    rec.spans[kStMerge].push_back(sp);
+
+  HostMerger merger;
+  float* const hgrad[3] = {(float*)dQ->data, (float*)dK->data, (float*)dV->data};
+  char* pin = nullptr;
+  const uint64_t pin_slot = 3 * g_b;
+  if (dev_acc) {
+    // the fused scatter-adds accumulate into zeroed gradients
+    auto sp = span_begin(st);
+    for (int x = 0; x < 3; ++x) CQSA_HIP(launch_fill_zero(hgrad[x], B * L * H * d, st));
+    span_end(sp, st, kStMerge);
+  } else {
+    void* pv = nullptr;
+    if ((s = acquire_pinned(C, size_t(pin_slot * nslot), &pv)) != CQSA_OK) return s;
+    pin = (char*)pv;
+    // the host zero-fill runs on the merge thread while the device computes
+    const int64_t n = B * L * H * d;
+    merger.push([=, &rec]() -> bool {
+      auto t0 = std::chrono::steady_clock::now();
+      host_zero(hgrad, n);
+      auto t1 = std::chrono::steady_clock::now();
+      rec.host_merge_ms += std::chrono::duration<double, std::milli>(t1 - t0).count();
+      return true;
+    });
   }
   CQSA_HIP(hipStreamWaitEvent(st, ev_tab, 0));
   // dQ kernels run on the second compute stream (they write dQ only, the dK/dV
   // kernels on the caller's stream write dK and dV only): a task's two kernels
   // overlap, and each stream keeps its own tasks in order.
-  const hipStream_t qs = C->lane;
   CQSA_HIP(hipEventRecord(ev_pre, st));
   CQSA_HIP(hipStreamWaitEvent(qs, ev_pre, 0));
 
   std::vector<bool> used(nslot, false);
+  std::vector<int64_t> last_item(nslot, -1);
+  const Task* prev_task = nullptr;
+  const char* prev_sb = nullptr;
+  const char* srcs[4] = {(const char*)Q->data, (const char*)K->data, (const char*)V->data,
+                         (const char*)dO->data};
   for (int64_t t = 0; t < ntask; ++t) {
     const Task& task = p->tasks[t];
     const int64_t Li = task.L_local;
     if (Li == 0) continue;
     const int64_t si = t % nslot;
     const TableOffsets& to = p->table_off[t];
-    char* sb = base + tab_bytes + d_bytes + uint64_t(si) * slot_bytes;
+    char* sb = slot_base(si);
     BwdArgs a{};
     if (!staged) {
       a.q = Q->data; a.k = K->data; a.v = V->data; a.dO = dO->data;
@@ -151,28 +290,52 @@ cqsa_status backward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa
       a.rows = (const int32_t*)(d_tab + to.rows);
     } else {
       if (used[si]) {
-        CQSA_HIP(hipStreamWaitEvent(C->copy, ev_free[si], 0));
-        CQSA_HIP(hipStreamWaitEvent(C->copy, ev_free_q[si], 0));
+        CQSA_HIP(hipStreamWaitEvent(cs, ev_free[si], 0));
+        CQSA_HIP(hipStreamWaitEvent(cs, ev_free_q[si], 0));
       }
-      StageArgs sa{};
-      sa.src[0] = Q->data; sa.src[1] = K->data; sa.src[2] = V->data; sa.src[3] = dO->data;
-      for (int x = 0; x < 4; ++x) sa.dst[x] = sb + x * in_b;
-      sa.n_tensors = 4; sa.row_bytes = row_bytes; sa.Li = Li; sa.Lg = L; sa.B = int32_t(B);
-      sa.runs = d_tab + to.runs; sa.n_runs = int32_t(task.runs.size());
-      if (rec.timing) {
-        sp = {rec.make(), rec.make()};
-        CQSA_HIP(hipEventRecord(sp.first, C->copy));
+      char* dsts[4] = {sb, sb + in_b, sb + 2 * in_b, sb + 3 * in_b};
+      auto sp = span_begin(cs);
+      if (dev_in) {
+        StageArgs sa{};
+        for (int x = 0; x < 4; ++x) {
+          sa.src[x] = srcs[x];
+          sa.dst[x] = dsts[x];
+        }
+        sa.n_tensors = 4; sa.row_bytes = row_bytes; sa.Li = Li; sa.Lg = L; sa.B = int32_t(B);
+        sa.runs = d_tab + to.runs; sa.n_runs = int32_t(task.runs.size());
+        CQSA_HIP(launch_stage(sa, cs));
+        rec.stats.d2d_bytes += uint64_t(4) * B * Li * row_bytes;
+      } else {
+        // host inputs: tokens the previously staged task also holds come
+        // from its staged rows (intact until a later staging on this copy
+        // stream overwrites them), the rest over the host link
+        const bool can_reuse = prev_task && prev_sb != sb;
+        const int64_t Lp = can_reuse ? prev_task->L_local : 0;
+        for (const StagePiece& pc : stage_pieces(task, can_reuse ? prev_task : nullptr)) {
+          for (int x = 0; x < 4; ++x)
+            for (int64_t b = 0; b < B; ++b) {
+              char* dst = dsts[x] + (b * Li + pc.dst) * row_bytes;
+              if (pc.reuse)
+                CQSA_HIP(hipMemcpyAsync(dst, prev_sb + x * in_b + (b * Lp + pc.src) * row_bytes,
+                                        pc.length * row_bytes, hipMemcpyDeviceToDevice, cs));
+              else
+                CQSA_HIP(hipMemcpyAsync(dst, srcs[x] + (b * L + pc.src) * row_bytes,
+                                        pc.length * row_bytes, hipMemcpyHostToDevice, cs));
+            }
+          const uint64_t moved = uint64_t(4) * B * pc.length * row_bytes;
+          if (pc.reuse)
+            rec.stats.d2d_bytes += moved;
+          else
+            rec.stats.h2d_bytes += moved;
+        }
+        prev_task = &task;
+        prev_sb = sb;
       }
-      CQSA_HIP(launch_stage(sa, C->copy));
-      rec.stats.d2d_bytes += uint64_t(4) * B * Li * row_bytes;
-      if (rec.timing) {
-        CQSA_HIP(hipEventRecord(sp.second, C->copy));
-        rec.spans[kStStage].push_back(sp);
-      }
-      CQSA_HIP(hipEventRecord(ev_staged[si], C->copy));
+      span_end(sp, cs, kStStage);
+      CQSA_HIP(hipEventRecord(ev_staged[si], cs));
       CQSA_HIP(hipStreamWaitEvent(st, ev_staged[si], 0));
       CQSA_HIP(hipStreamWaitEvent(qs, ev_staged[si], 0));
-      a.q = sa.dst[0]; a.k = sa.dst[1]; a.v = sa.dst[2]; a.dO = sa.dst[3];
+      a.q = dsts[0]; a.k = dsts[1]; a.v = dsts[2]; a.dO = dsts[3];
     }
     a.L = int32_t(Li); a.B = int32_t(B); a.H = int32_t(H); a.causal = p->g.causal;
     a.scale_log2 = sc * 1.4426950408889634f; a.scale = sc;
@@ -181,37 +344,73 @@ cqsa_status backward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa
     a.korder = (const int32_t*)(d_tab + to.korder);
     a.blk_or = (const uint32_t*)(d_tab + to.blk_or);
     a.blk_and = (const uint32_t*)(d_tab + to.blk_and);
-    a.lse = LSE; a.D = d_D; a.Lg = L;
-    a.dq = (float*)dQ->data; a.dk = (float*)dK->data; a.dv = (float*)dV->data;
-    std::pair<hipEvent_t, hipEvent_t> sk{nullptr, nullptr}, sq{nullptr, nullptr};
-    if (rec.timing) {
-      sk = {rec.make(), rec.make()};
-      sq = {rec.make(), rec.make()};
-      CQSA_HIP(hipEventRecord(sk.first, st));
-      CQSA_HIP(hipEventRecord(sq.first, qs));
+    a.lse = d_lse; a.D = d_D; a.Lg = L;
+    float* tg[3] = {nullptr, nullptr, nullptr};
+    if (dev_acc) {
+      a.local_out = 0;
+      a.dq = hgrad[0]; a.dk = hgrad[1]; a.dv = hgrad[2];
+    } else {
+      // the task's own gradients; the slot's previous ones must be copied out
+      for (int x = 0; x < 3; ++x) tg[x] = (float*)(sb + 4 * in_b + x * g_b);
+      a.local_out = 1;
+      a.dq = tg[0]; a.dk = tg[1]; a.dv = tg[2];
+      if (used[si]) {
+        CQSA_HIP(hipStreamWaitEvent(st, ev_d2h[si], 0));
+        CQSA_HIP(hipStreamWaitEvent(qs, ev_d2h[si], 0));
+      }
     }
+    std::pair<hipEvent_t, hipEvent_t> sk = span_begin(st), sq = span_begin(qs);
     CQSA_HIP(launch_bwd_dkdv(o.dtype, int(d), a, st));
     CQSA_HIP(launch_bwd_dq(o.dtype, int(d), a, qs));
     rec.stats.inner_launches += 2;
-    if (rec.timing) {
-      CQSA_HIP(hipEventRecord(sk.second, st));
-      CQSA_HIP(hipEventRecord(sq.second, qs));
-      rec.spans[kStInner].push_back(sk);
-      rec.spans[kStInner].push_back(sq);
-    }
-    if (staged) {
-      CQSA_HIP(hipEventRecord(ev_free[si], st));
-      CQSA_HIP(hipEventRecord(ev_free_q[si], qs));
+    span_end(sk, st, kStInner);
+    span_end(sq, qs, kStInner);
+    CQSA_HIP(hipEventRecord(ev_free[si], st));
+    CQSA_HIP(hipEventRecord(ev_free_q[si], qs));
+    if (!dev_acc) {
+      // the slot's pinned staging must have been added by its last job
+      if (!merger.wait_done(last_item[si])) return fail(CQSA_ERR_HIP, "host scatter-add failed");
+      float* hp[3];
+      for (int x = 0; x < 3; ++x) hp[x] = (float*)(pin + uint64_t(si) * pin_slot + x * g_b);
+      CQSA_HIP(hipStreamWaitEvent(ms, ev_free[si], 0));
+      CQSA_HIP(hipStreamWaitEvent(ms, ev_free_q[si], 0));
+      const uint64_t bytes = uint64_t(B) * Li * H * d * 4;
+      auto sp = span_begin(ms);
+      for (int x = 0; x < 3; ++x)
+        CQSA_HIP(hipMemcpyAsync(hp[x], tg[x], bytes, hipMemcpyDeviceToHost, ms));
+      span_end(sp, ms, kStD2H);
+      rec.stats.d2h_bytes += 3 * bytes;
+      CQSA_HIP(hipEventRecord(ev_d2h[si], ms));
+      const hipEvent_t wait_ev = ev_d2h[si];
+      const Task* tp = &task;
+      const float* const srcp[3] = {hp[0], hp[1], hp[2]};
+      last_item[si] = merger.push([=, &rec]() -> bool {
+        if (hipEventSynchronize(wait_ev) != hipSuccess) return false;
+        auto t0 = std::chrono::steady_clock::now();  // the adds alone, not the wait
+        host_scatter_add(*tp, srcp, hgrad, B, L, H, d);
+        auto t1 = std::chrono::steady_clock::now();
+        rec.host_merge_ms += std::chrono::duration<double, std::milli>(t1 - t0).count();
+        return true;
+      });
     }
     used[si] = true;
   }
-  // join the dQ stream back into the caller's stream
-  CQSA_HIP(hipEventRecord(ev_pre, qs));
-  CQSA_HIP(hipStreamWaitEvent(st, ev_pre, 0));
+  // join the dQ stream (and the gradient copies) back into the caller's stream
+  CQSA_HIP(hipEventRecord(ev_join, qs));
+  CQSA_HIP(hipStreamWaitEvent(st, ev_join, 0));
+  if (!dev_acc) {
+    CQSA_HIP(hipEventRecord(ev_join, ms));
+    CQSA_HIP(hipStreamWaitEvent(st, ev_join, 0));
+  }
   if (rec.timing) CQSA_HIP(hipEventRecord(rec.wall1, st));
   CQSA_HIP(hipEventRecord(C->ws_free, st));
   C->ws_free_valid = true;
   release_workspace(C, &ws, st);
+  if (!dev_acc) {
+    if (!merger.finish()) return fail(CQSA_ERR_HIP, "host scatter-add: event wait failed");
+    hipError_t e = hipStreamSynchronize(st);
+    if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+  }
   return CQSA_OK;
 }
 

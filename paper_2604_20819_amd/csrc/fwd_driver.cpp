@@ -23,48 +23,27 @@
 // its staged rows).  Depth 0 on device-resident tensors is the undecomposed
 // call: one kernel that writes O and LSE directly.
 #include <algorithm>
+#include <chrono>
 #include <cmath>
-#include <condition_variable>
-#include <deque>
-#include <functional>
-#include <thread>
 
 #include "guard.hpp"
 #include "kernels.hpp"
 #include "runtime.hpp"
+#include "streamer.hpp"
 
 namespace cqsa {
 
 namespace {
 
-int host_threads() {
-  unsigned n = std::thread::hardware_concurrency();
-  if (n == 0) n = 4;
-  return int(std::min(16u, n));
-}
-
-template <typename F>
-void parallel_rows(int64_t n, F f) {
-  const int nt = int(std::min<int64_t>(host_threads(), std::max<int64_t>(1, n / 256)));
-  if (nt <= 1) {
-    f(int64_t(0), n);
-    return;
-  }
-  std::vector<std::thread> th;
-  for (int i = 0; i < nt; ++i) {
-    const int64_t a = n * i / nt, b = n * (i + 1) / nt;
-    th.emplace_back([=] { f(a, b); });
-  }
-  for (auto& t : th) t.join();
-}
-
 // Max-shifted merge of one task's statistics into the host accumulator
-// (Eq. "merge", log2 domain, null rows skipped).  A row whose running max is
+// (Eq. "merge", log2 domain, null rows skipped); l and lt (the sums of the
+// fp32 and of the rounded weights) merge with the same factors.  A row whose running max is
 // still -inf has had no contribution yet: the first one is written, not
 // blended, so the accumulator needs no zero fill beforehand (every token has
 // a kept key in some task, so every row is written before finalisation).
 void host_merge(const Task& task, const float* acc_i, const float* m_i, const float* l_i,
-                float* acc, float* m, float* l, int64_t B, int64_t L, int64_t H, int64_t d) {
+                const float* lt_i, float* acc, float* m, float* l, float* lt, int64_t B,
+                int64_t L, int64_t H, int64_t d) {
   const int64_t Li = task.L_local;
   parallel_rows(B * Li, [&](int64_t lo, int64_t hi) {
     size_t ri = 0;
@@ -85,6 +64,7 @@ void host_merge(const Task& task, const float* acc_i, const float* m_i, const fl
         if (mo == -INFINITY) {
           for (int64_t k = 0; k < d; ++k) dst[k] = src[k];
           l[gi] = l_i[si];
+          lt[gi] = lt_i[si];
           m[gi] = mi;
           continue;
         }
@@ -93,121 +73,28 @@ void host_merge(const Task& task, const float* acc_i, const float* m_i, const fl
         const float fi = std::exp2(mi - mn);
         for (int64_t k = 0; k < d; ++k) dst[k] = dst[k] * fo + src[k] * fi;
         l[gi] = l[gi] * fo + l_i[si] * fi;
+        lt[gi] = lt[gi] * fo + lt_i[si] * fi;
         m[gi] = mn;
       }
     }
   });
 }
 
-void host_finalize(float* acc, float* m, const float* l, int64_t B, int64_t L, int64_t H,
-                   int64_t d) {
+// O = acc / lt, LSE = m + log l (natural log).
+void host_finalize(float* acc, float* m, const float* l, const float* lt, int64_t B, int64_t L,
+                   int64_t H, int64_t d) {
   parallel_rows(B * L, [&](int64_t lo, int64_t hi) {
     for (int64_t x = lo; x < hi; ++x) {
       const int64_t b = x / L, g = x % L;
       for (int64_t h = 0; h < H; ++h) {
         const int64_t gi = (b * H + h) * L + g;
-        const float inv = 1.f / l[gi];
+        const float inv = 1.f / lt[gi];
         float* row = acc + ((b * L + g) * H + h) * d;
         for (int64_t k = 0; k < d; ++k) row[k] *= inv;
         m[gi] = (m[gi] + std::log2(l[gi])) * 0.69314718055994530942f;
       }
     }
   });
-}
-
-// One consumer thread that runs host merges strictly in submission order
-// (merges of different tasks touch shared rows).
-class HostMerger {
- public:
-  ~HostMerger() { finish(); }
-  // Queues a job; returns its sequence number.
-  int64_t push(std::function<bool()> job) {
-    std::unique_lock<std::mutex> g(mu_);
-    if (!th_.joinable()) th_ = std::thread([this] { run(); });
-    q_.push_back(std::move(job));
-    cv_.notify_all();
-    return pushed_++;
-  }
-  // Blocks until job `id` (and all before it) finished; false on failure.
-  bool wait_done(int64_t id) {
-    std::unique_lock<std::mutex> g(mu_);
-    cv_.wait(g, [&] { return done_ > id || !ok_; });
-    return ok_;
-  }
-  bool finish() {
-    {
-      std::unique_lock<std::mutex> g(mu_);
-      stop_ = true;
-      cv_.notify_all();
-    }
-    if (th_.joinable()) th_.join();
-    return ok_;
-  }
-
- private:
-  void run() {
-    for (;;) {
-      std::function<bool()> job;
-      {
-        std::unique_lock<std::mutex> g(mu_);
-        cv_.wait(g, [&] { return !q_.empty() || stop_; });
-        if (q_.empty()) return;
-        job = std::move(q_.front());
-        q_.pop_front();
-      }
-      const bool ok = ok_ && job();
-      std::unique_lock<std::mutex> g(mu_);
-      if (!ok) ok_ = false;
-      ++done_;
-      cv_.notify_all();
-    }
-  }
-  std::mutex mu_;
-  std::condition_variable cv_;
-  std::deque<std::function<bool()>> q_;
-  std::thread th_;
-  int64_t pushed_ = 0, done_ = 0;
-  bool stop_ = false, ok_ = true;
-};
-
-// One piece of a task's staging: local rows [dst, dst + length) of the task
-// come either from the host tensors at global row `src`, or, when the task
-// staged just before holds the same tokens, from its staged rows at its local
-// row `src` (device to device).
-struct StagePiece {
-  int64_t dst, src, length;
-  bool reuse;
-};
-
-// Splits `cur`'s runs against the runs of the previously staged task `prev`
-// (both ascending in global order): overlapping tokens are reused, the rest
-// comes from the host.  Consecutive tasks in quorum order share chunks (at
-// depth 1 with I = (0, 1, 3), task q + 1 holds chunk q + 1 of task q).
-std::vector<StagePiece> stage_pieces(const Task& cur, const Task* prev) {
-  std::vector<StagePiece> out;
-  size_t pi = 0;
-  for (const Run& r : cur.runs) {
-    int64_t g = r.global_start;
-    const int64_t end = r.global_start + r.length;
-    while (g < end) {
-      // first run of prev that ends after g
-      while (prev && pi < prev->runs.size() &&
-             prev->runs[pi].global_start + prev->runs[pi].length <= g)
-        ++pi;
-      const Run* pr = (prev && pi < prev->runs.size()) ? &prev->runs[pi] : nullptr;
-      const int64_t dst = r.local_start + (g - r.global_start);
-      if (pr && pr->global_start <= g) {
-        const int64_t e = std::min(end, pr->global_start + pr->length);
-        out.push_back({dst, pr->local_start + (g - pr->global_start), e - g, true});
-        g = e;
-      } else {
-        const int64_t e = pr ? std::min(end, pr->global_start) : end;
-        out.push_back({dst, g, e - g, false});
-        g = e;
-      }
-    }
-  }
-  return out;
 }
 
 }  // namespace
@@ -256,14 +143,14 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
   }
 
   // ---- workspace layout ----
-  // [plan image][running l][slot 0]...[slot S-1]; a slot holds group_size
-  // task sub-slots {Q, K, V, acc, m, l} ({acc, m, l} when the inputs are
-  // read in place), each sized for the longest task.
+  // [plan image][running l, lt][slot 0]...[slot S-1]; a slot holds group_size
+  // task sub-slots {Q, K, V, acc, m, l, lt} ({acc, m, l, lt} when the inputs
+  // are read in place), each sized for the longest task.
   const int64_t ngroup = int64_t(p->groups.size());
   const int64_t gsz = p->fp.group_size;
   const uint64_t tab_bytes = align_up(p->packed.size());
-  const uint64_t gl_bytes =
-      (acc_dev && !direct && ngroup > 1) ? align_up(uint64_t(B) * H * L * 4) : 0;
+  const uint64_t gl_one = align_up(uint64_t(B) * H * L * 4);
+  const uint64_t gl_bytes = (acc_dev && !direct && ngroup > 1) ? 2 * gl_one : 0;
   const uint64_t sub_bytes = direct ? 0 : fwd_slot_bytes(p->g, o, p->max_L_local, !in_place, true);
   std::vector<int64_t> slot_tasks;
   if (!direct) slot_tasks = fwd_slot_tasks(ntask, int32_t(gsz), o.n_slots);
@@ -280,6 +167,7 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
   char* base = (char*)ws.ptr;
   char* d_tab = base;
   float* d_gl = gl_bytes ? (float*)(base + tab_bytes) : nullptr;
+  float* d_glt = gl_bytes ? (float*)(base + tab_bytes + gl_one) : nullptr;
   const uint64_t in_b = in_place ? 0 : align_up(uint64_t(B) * p->max_L_local * H * d * elem);
   const uint64_t acc_b = align_up(uint64_t(B) * p->max_L_local * H * d * 4);
   const uint64_t st_b = align_up(uint64_t(B) * p->max_L_local * H * 4);
@@ -329,7 +217,7 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
   if (direct) {
     FwdArgs a{};
     a.q = Q->data; a.k = K->data; a.v = V->data;
-    a.acc = Od; a.m = LSE; a.l = nullptr;
+    a.acc = Od; a.m = LSE; a.l = nullptr; a.lt = nullptr;
     a.tab = d_tab; a.tasks = d_tasks; a.ntask = 1;
     a.B = int32_t(B); a.H = int32_t(H); a.causal = p->g.causal; a.scale_log2 = scale_log2;
     const int64_t wgs = ((L + rows_wg - 1) / rows_wg) * B * H;
@@ -339,20 +227,23 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
     rec.stats.inner_launches = 1;
   } else {
     // running global state: acc in the O buffer, m (log2) in the LSE buffer,
-    // l in the workspace (device) or on the host
+    // l and lt in the workspace (device) or on the host
     float* acc = Od;
     float* m = LSE;
     float* l = d_gl;
-    std::vector<float> l_host;
+    float* lt = d_glt;
+    std::vector<float> l_host, lt_host;
     char* pin = nullptr;
     uint64_t pin_slot = 0;
     if (!acc_dev) {
       // running max -inf marks rows not yet merged (host_merge writes their
       // first contribution), so acc itself needs no fill
       l_host.assign(size_t(B * H * L), 0.f);
+      lt_host.assign(size_t(B * H * L), 0.f);
       l = l_host.data();
+      lt = lt_host.data();
       std::fill(m, m + B * H * L, -INFINITY);
-      pin_slot = acc_b + 2 * st_b;
+      pin_slot = acc_b + 3 * st_b;
       void* pv = nullptr;
       if ((s = acquire_pinned(C, size_t(pin_slot * nslot), &pv)) != CQSA_OK) return s;
       pin = (char*)pv;
@@ -452,6 +343,7 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
       a.acc = (float*)(sb + 3 * in_b);
       a.m = (float*)(sb + 3 * in_b + acc_b);
       a.l = (float*)(sb + 3 * in_b + acc_b + st_b);
+      a.lt = (float*)(sb + 3 * in_b + acc_b + 2 * st_b);
       a.acc_stride = a.st_stride = int64_t(sub_bytes / 4);
       a.tab = d_tab; a.tasks = d_tasks + G.task0; a.ntask = int32_t(G.count);
       a.B = int32_t(B); a.H = int32_t(H); a.causal = p->g.causal; a.scale_log2 = scale_log2;
@@ -470,9 +362,9 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
         cb.segs = (const DevSeg*)(d_tab + G.seg_off); cb.n_seg = G.n_seg;
         cb.contribs = (const DevContrib*)(d_tab + G.contrib_off);
         cb.tasks = d_tasks + G.task0;
-        cb.acc_i = a.acc; cb.m_i = a.m; cb.l_i = a.l;
+        cb.acc_i = a.acc; cb.m_i = a.m; cb.l_i = a.l; cb.lt_i = a.lt;
         cb.acc_stride = a.acc_stride; cb.st_stride = a.st_stride;
-        cb.acc = acc; cb.m = m; cb.l = l; cb.L = L;
+        cb.acc = acc; cb.m = m; cb.l = l; cb.lt = lt; cb.L = L;
         cb.B = int32_t(B); cb.H = int32_t(H); cb.d = int32_t(d); cb.final = G.final ? 1 : 0;
         if (G.blocks > 0) {
           auto sp = span_begin(ms);
@@ -493,20 +385,22 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
         float* h_acc = (float*)hp;
         float* h_m = (float*)(hp + acc_b);
         float* h_l = (float*)(hp + acc_b + st_b);
+        float* h_lt = (float*)(hp + acc_b + 2 * st_b);
         CQSA_HIP(hipStreamWaitEvent(ms, ev_inner[si], 0));
         auto sp = span_begin(ms);
         CQSA_HIP(hipMemcpyAsync(h_acc, a.acc, rows * d * 4, hipMemcpyDeviceToHost, ms));
         CQSA_HIP(hipMemcpyAsync(h_m, a.m, rows * 4, hipMemcpyDeviceToHost, ms));
         CQSA_HIP(hipMemcpyAsync(h_l, a.l, rows * 4, hipMemcpyDeviceToHost, ms));
+        CQSA_HIP(hipMemcpyAsync(h_lt, a.lt, rows * 4, hipMemcpyDeviceToHost, ms));
         span_end(sp, ms, kStD2H);
-        rec.stats.d2h_bytes += rows * (d + 2) * 4;
+        rec.stats.d2h_bytes += rows * (d + 3) * 4;
         CQSA_HIP(hipEventRecord(ev_free[si], ms));
         const hipEvent_t wait_ev = ev_free[si];
         const Task* tp = &p->tasks[t];
         last_item[si] = merger.push([=, &rec]() -> bool {
           if (hipEventSynchronize(wait_ev) != hipSuccess) return false;
           auto t0 = std::chrono::steady_clock::now();  // the merge alone, not the wait
-          host_merge(*tp, h_acc, h_m, h_l, acc, m, l, B, L, H, d);
+          host_merge(*tp, h_acc, h_m, h_l, h_lt, acc, m, l, lt, B, L, H, d);
           auto t1 = std::chrono::steady_clock::now();
           rec.host_merge_ms += std::chrono::duration<double, std::milli>(t1 - t0).count();
           return true;
@@ -517,7 +411,7 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
     if (!acc_dev) {
       if (!merger.finish()) return fail(CQSA_ERR_HIP, "host merge: event wait failed");
       auto t0 = std::chrono::steady_clock::now();
-      host_finalize(acc, m, l, B, L, H, d);
+      host_finalize(acc, m, l, lt, B, L, H, d);
       auto t1 = std::chrono::steady_clock::now();
       rec.host_final_ms += std::chrono::duration<double, std::milli>(t1 - t0).count();
     }

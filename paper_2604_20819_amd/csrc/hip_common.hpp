@@ -65,6 +65,34 @@ __device__ __forceinline__ f16x8 pack8<F16>(const float* x) {
   return r;
 }
 
+// Running sum of the 8 packed 16-bit values of an MFMA operand, as fp32:
+// four dot products with (1, 1) (v_dot2c_f32_{bf16,f16}); the products are
+// exact, so this adds exactly the rounded values the product consumes.
+typedef __attribute__((__vector_size__(2 * sizeof(__bf16)))) __bf16 bf16x2;
+typedef __attribute__((__vector_size__(2 * sizeof(_Float16)))) _Float16 f16x2;
+template <typename E>
+__device__ __forceinline__ float sum8(const typename E::vec8& x, float acc);
+template <>
+__device__ __forceinline__ float sum8<BF16>(const bf16x8& x, float acc) {
+  const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const bf16x2 p = {x[2 * i], x[2 * i + 1]};
+    acc = __builtin_amdgcn_fdot2_f32_bf16(p, one, acc, false);
+  }
+  return acc;
+}
+template <>
+__device__ __forceinline__ float sum8<F16>(const f16x8& x, float acc) {
+  const f16x2 one = {(_Float16)1.0f, (_Float16)1.0f};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const f16x2 p = {x[2 * i], x[2 * i + 1]};
+    acc = __builtin_amdgcn_fdot2(p, one, acc, false);
+  }
+  return acc;
+}
+
 template <typename V>
 __device__ __forceinline__ V bitcast_u4(const u32x4& u) {
   return __builtin_bit_cast(V, u);

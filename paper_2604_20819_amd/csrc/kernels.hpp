@@ -11,8 +11,8 @@ namespace cqsa {
 
 // Epilogue of the inner forward kernel.
 enum FwdMode : int {
-  kModeStats = 0,  // write task-local (acc_i, m_i, l_i) for recomposition
-  kModeFinal = 1,  // single task covering all tokens: write O = acc/l and LSE
+  kModeStats = 0,  // write task-local (acc_i, m_i, l_i, lt_i) for recomposition
+  kModeFinal = 1,  // single task covering all tokens: write O = acc/lt and LSE
 };
 
 // One launch of the inner forward kernel over `ntask` tasks (a launch group).
@@ -20,9 +20,12 @@ enum FwdMode : int {
 // elements.  Inputs read in place (in_place = 1): q/k/v are the caller's
 // [B, Lg, H, d] tensors and task j's local token t is the global row its runs
 // give (block row table DevTask::row_off).  Task j's statistics are acc_j
-// [B, L_j, H, d] at acc + j * acc_stride, m_j and l_j [B, H, L_j] at
-// m/l + j * st_stride.  In final mode the single task spans all L tokens:
-// q/k/v are the caller's tensors, acc is O and m is LSE.
+// [B, L_j, H, d] at acc + j * acc_stride, m_j, l_j and lt_j [B, H, L_j] at
+// m/l/lt + j * st_stride.  l sums the fp32 weights exp2(s - m) and gives the
+// log-sum-exp; lt sums the same weights rounded to the input dtype, exactly
+// the values the P.V product consumes, and normalises O (equal to l for fp32
+// inputs).  In final mode the single task spans all L tokens: q/k/v are the
+// caller's tensors, acc is O and m is LSE.
 struct FwdArgs {
   const void* q;
   const void* k;
@@ -31,6 +34,7 @@ struct FwdArgs {
   float* acc;
   float* m;             // log2 domain (stats) or natural-log LSE (final)
   float* l;             // stats only
+  float* lt;            // stats only
   int64_t acc_stride, st_stride;
   const char* tab;      // packed plan image (DevTask offsets are relative to it)
   const DevTask* tasks; // the launch's tasks
@@ -44,7 +48,8 @@ struct FwdArgs {
 
 // Gather-merge of one launch group's task statistics into the global
 // accumulator (App. A.1, Eq. "merge"), fused with the finalisation
-// O = acc / l, LSE = m + log l when the group is the last one.
+// O = acc / lt, LSE = m + log l when the group is the last one (l and lt are
+// merged with the same factors; FwdArgs says what each sums).
 struct CombineArgs {
   const DevSeg* segs;        // the group's segments, ascending blk0
   int32_t n_seg;
@@ -53,10 +58,12 @@ struct CombineArgs {
   const float* acc_i;        // task j's statistics at + j * acc_stride / st_stride
   const float* m_i;
   const float* l_i;
+  const float* lt_i;
   int64_t acc_stride, st_stride;
   float* acc;                // [B, L, H, d] running acc, or O when final
   float* m;                  // [B, H, L] running max (log2), or LSE when final
-  float* l;                  // [B, H, L] running sum
+  float* l;                  // [B, H, L] running sum of the fp32 weights
+  float* lt;                 // [B, H, L] running sum of the rounded weights
   int64_t L;
   int32_t B, H, d;
   int32_t final;
@@ -84,7 +91,11 @@ struct BwdArgs {
   const float* lse;     // [B, H, Lg] global natural-log LSE from the forward
   const float* D;       // [B, H, Lg] global rowsum(dO * O)
   int64_t Lg;           // global sequence length
-  float* dq;            // [B, Lg, H, d] global fp32 gradients (scatter-added)
+  int32_t local_out;    // 0: dq/dk/dv are the global [B, Lg, H, d] fp32 gradients and
+                        //    the task's rows are added at their global rows;
+                        // 1: they are the task's own [B, L, H, d] fp32 buffers and
+                        //    the task's rows are stored at their local rows
+  float* dq;
   float* dk;
   float* dv;
 };
@@ -114,8 +125,12 @@ hipError_t launch_stage(const StageArgs& a, hipStream_t s);
 hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t s);
 // dst[i] = src[i] rounded to the 16-bit dtype `dt` (nearest even), i < n.
 hipError_t launch_cast_out(const float* src, void* dst, int64_t n, cqsa_dtype dt, hipStream_t s);
+// D[(b * H + h) * ld + g] = sum_d dO * O over rows g < L of B batch elements
+// of [B, L, H, d] inputs (ld = L for whole tensors; a chunk of rows passes
+// its first output and the full sequence length).
 hipError_t launch_bwd_preprocess(const void* dO, const float* O, float* D, cqsa_dtype dt,
-                                 int64_t B, int64_t L, int64_t H, int d, hipStream_t s);
+                                 int64_t B, int64_t L, int64_t H, int d, int64_t ld,
+                                 hipStream_t s);
 hipError_t launch_bwd_dkdv(cqsa_dtype dt, int d, const BwdArgs& a, hipStream_t s);
 hipError_t launch_bwd_dq(cqsa_dtype dt, int d, const BwdArgs& a, hipStream_t s);
 

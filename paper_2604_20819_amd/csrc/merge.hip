@@ -1,6 +1,8 @@
 // Recomposition (App. A.1): the max-shifted merge of Eq. "merge" of a launch
-// group's task statistics (acc_i, m_i, l_i) into the global accumulator, fused
-// with the finalisation O = acc / l, LSE = m + log l after the last group.
+// group's task statistics (acc_i, m_i, l_i, lt_i) into the global
+// accumulator, fused with the finalisation O = acc / lt, LSE = m + log l
+// after the last group (l sums the fp32 weights, lt the rounded weights the
+// inner kernel's P.V product consumed; both merge with the same factors).
 //
 // Gather form: every work group owns kCombinePairs consecutive (token, head)
 // pairs of one elementary segment and one batch element.  A segment lies
@@ -14,7 +16,7 @@
 // Statistics are in the log2 domain with integer-valued maxima (the inner
 // kernels round running maxima up to integers), so every factor
 // 2^(m_i - m') is an exact power of two.  A task row with no kept key carries
-// m_i = -inf and l_i = 0: a null contribution with factor 0.
+// m_i = -inf and l_i = lt_i = 0: a null contribution with factor 0.
 #include "hip_common.hpp"
 #include "kernels.hpp"
 
@@ -52,10 +54,11 @@ __global__ void __launch_bounds__(256) combine_kernel(const CombineArgs a) {
     const int64_t r = pr / H;
     const int h = int(pr % H);
     const int64_t gi = (int64_t(b) * H + h) * a.L + sg.g0 + r;
-    float mg = -INFINITY, lg = 0.f;
+    float mg = -INFINITY, lg = 0.f, ltg = 0.f;
     if (glob) {
       mg = a.m[gi];
       lg = a.l[gi];
+      ltg = a.lt[gi];
     }
     float mx = mg;
     for (int k = 0; k < nc; ++k) {
@@ -65,7 +68,7 @@ __global__ void __launch_bounds__(256) combine_kernel(const CombineArgs a) {
       mx = fmaxf(mx, mk);
     }
     const float fg = mg == -INFINITY ? 0.f : fast_exp2(mg - mx);
-    float lsum = lg * fg;
+    float lsum = lg * fg, ltsum = ltg * fg;
     fac_s[0][tid] = fg;
     for (int k = 0; k < nc; ++k) {
       const DevContrib c = a.contribs[sg.c_off + k];
@@ -74,15 +77,17 @@ __global__ void __launch_bounds__(256) combine_kernel(const CombineArgs a) {
       const float mk = a.m_i[si];
       const float f = mk == -INFINITY ? 0.f : fast_exp2(mk - mx);
       lsum += a.l_i[si] * f;
+      ltsum += a.lt_i[si] * f;
       fac_s[k + 1][tid] = f;
     }
     if (a.final) {
-      inv_s[tid] = 1.f / lsum;
+      inv_s[tid] = 1.f / ltsum;
       a.m[gi] = (mx + __log2f(lsum)) * 0.69314718055994530942f;
     } else {
       inv_s[tid] = 1.f;
       a.m[gi] = mx;
       a.l[gi] = lsum;
+      a.lt[gi] = ltsum;
     }
   }
   __syncthreads();

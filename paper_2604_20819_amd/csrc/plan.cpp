@@ -120,8 +120,6 @@ cqsa_status validate_plan_args(int64_t L, int32_t H, int32_t d, const cqsa_plan_
     return bad(CQSA_ERR_INVALID_ARG, "tasks_per_slot must be in [0, 32]");
   if (o.tasks_per_slot > 1 && o.acc_on_device != 1)
     return bad(CQSA_ERR_UNSUPPORTED, "tasks_per_slot > 1 needs the accumulator on the device");
-  if (o.with_backward && (!o.inputs_on_device || o.acc_on_device != 1))
-    return bad(CQSA_ERR_UNSUPPORTED, "the backward supports device-resident tensors only");
   if (o.read_in_place < -1 || o.read_in_place > 1)
     return bad(CQSA_ERR_INVALID_ARG, "read_in_place must be -1 (auto), 0 or 1");
   if (o.read_in_place == 1 && !o.inputs_on_device)
@@ -235,13 +233,21 @@ uint64_t fwd_slot_bytes(const Geometry& g, const cqsa_plan_opts& o, int64_t Lmax
   const uint64_t rows = uint64_t(o.B) * uint64_t(Lmax) * uint64_t(g.H);
   uint64_t s = 0;
   if (staged) s += 3 * align_up(rows * g.d * dtype_size(o.dtype));
-  if (stats) s += align_up(rows * g.d * 4) + 2 * align_up(rows * 4);
+  if (stats) s += align_up(rows * g.d * 4) + 3 * align_up(rows * 4);  // acc, m, l, lt
   return s;
 }
 
 uint64_t bwd_slot_bytes(const Geometry& g, const cqsa_plan_opts& o, int64_t Lmax, bool staged) {
   const uint64_t rows = uint64_t(o.B) * uint64_t(Lmax) * uint64_t(g.H);
-  return staged ? 4 * align_up(rows * g.d * dtype_size(o.dtype)) : 0;
+  // staged Q, K, V, dO; with host-resident gradients the task's own fp32
+  // dQ, dK, dV, copied back to the host and scatter-added there
+  uint64_t s = staged ? 4 * align_up(rows * g.d * dtype_size(o.dtype)) : 0;
+  if (o.acc_on_device != 1) s += 3 * align_up(rows * g.d * 4);
+  return s;
+}
+
+bool bwd_staged(const cqsa_plan_opts& o, int32_t depth) {
+  return !o.inputs_on_device || (depth > 0 && o.read_in_place != 1);
 }
 
 bool direct_forward(const cqsa_plan_opts& o, int32_t depth) {
@@ -467,15 +473,19 @@ Footprint footprint(const Geometry& g, const cqsa_plan_opts& o, int32_t depth,
   // result sits in the workspace
   f.resident_fwd = (o.inputs_on_device ? 3 * in_bytes : 0) +
                    (o.acc_on_device ? f32_full + stat_full + (o.out16 ? in_bytes : 0) : 0);
-  f.resident_bwd = 4 * in_bytes + f32_full + stat_full + 3 * f32_full;
+  // backward: Q, K, V, dO follow the inputs' residency; O, LSE, dQ, dK, dV
+  // the accumulator's
+  f.resident_bwd = (o.inputs_on_device ? 4 * in_bytes : 0) +
+                   (o.acc_on_device == 1 ? f32_full + stat_full + 3 * f32_full : 0);
   // slot i holds as many task sub-slots (each sized for the longest task) as
   // the largest group that uses it (groups k with k % n_slots == i)
   const bool staged = o.read_in_place != 1;
   f.slot_fwd = direct ? 0 : fwd_slot_bytes(g, o, Lmax, staged, true);
-  f.slot_bwd = bwd_slot_bytes(g, o, Lmax, depth > 0 && staged);
-  // running row sums l, needed while more than one group merges on device
-  f.global_fwd = (o.acc_on_device && !direct && f.groups > 1) ? stat_full : 0;
-  f.global_bwd = stat_full;  // D = rowsum(dO * O)
+  f.slot_bwd = bwd_slot_bytes(g, o, Lmax, bwd_staged(o, depth));
+  // running row sums l and lt, needed while more than one group merges on device
+  f.global_fwd = (o.acc_on_device && !direct && f.groups > 1) ? 2 * stat_full : 0;
+  // D = rowsum(dO * O), and a device copy of a host-resident LSE
+  f.global_bwd = stat_full + (o.acc_on_device == 1 ? 0 : stat_full);
   f.tables = align_up(image_bytes);
   const uint64_t subslots_fwd = uint64_t(fwd_subslots(ntask, f.group_size, o.n_slots));
   const uint64_t slots_bwd = uint64_t(std::min<int64_t>(o.n_slots, ntask));

@@ -159,6 +159,10 @@ bool is_perfect_difference_set(const int32_t* I, int32_t l, int32_t c);
 uint64_t fwd_slot_bytes(const Geometry& g, const cqsa_plan_opts& o, int64_t Lmax, bool staged,
                         bool stats);
 uint64_t bwd_slot_bytes(const Geometry& g, const cqsa_plan_opts& o, int64_t Lmax, bool staged);
+// Whether the backward gathers each task's Q, K, V, dO into a staging slot
+// (host-resident inputs always; device-resident ones unless read in place or
+// undecomposed).
+bool bwd_staged(const cqsa_plan_opts& o, int32_t depth);
 // Packs the plan image: the DevTask records, every task's runs and block
 // summaries, and every group's segments and contributions (filling the
 // groups' offsets and combine block counts for H heads).

@@ -2,6 +2,7 @@
 // the caller-allocator hook, per-stage timing, and the C-ABI entry points
 // that are not planning or compute.
 #include "runtime.hpp"
+#include "streamer.hpp"
 
 #include <algorithm>
 #include <cmath>
@@ -173,6 +174,34 @@ cqsa_status check_tensor(const cqsa_tensor* t, const char* name, const cqsa_plan
     return fail(CQSA_ERR_INVALID_ARG, n + " shape differs from the plan");
   return CQSA_OK;
 }
+
+std::vector<StagePiece> stage_pieces(const Task& cur, const Task* prev) {
+  std::vector<StagePiece> out;
+  size_t pi = 0;
+  for (const Run& r : cur.runs) {
+    int64_t g = r.global_start;
+    const int64_t end = r.global_start + r.length;
+    while (g < end) {
+      // first run of prev that ends after g
+      while (prev && pi < prev->runs.size() &&
+             prev->runs[pi].global_start + prev->runs[pi].length <= g)
+        ++pi;
+      const Run* pr = (prev && pi < prev->runs.size()) ? &prev->runs[pi] : nullptr;
+      const int64_t dst = r.local_start + (g - r.global_start);
+      if (pr && pr->global_start <= g) {
+        const int64_t e = std::min(end, pr->global_start + pr->length);
+        out.push_back({dst, pr->local_start + (g - pr->global_start), e - g, true});
+        g = e;
+      } else {
+        const int64_t e = pr ? std::min(end, pr->global_start) : end;
+        out.push_back({dst, g, e - g, false});
+        g = e;
+      }
+    }
+  }
+  return out;
+}
+
 
 }  // namespace cqsa
 

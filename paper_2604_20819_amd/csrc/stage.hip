@@ -28,10 +28,12 @@ __global__ void __launch_bounds__(256) fill_zero_kernel(float* p, int64_t n4) {
     ((f32x4*)p)[i] = f32x4{0.f, 0.f, 0.f, 0.f};
 }
 
-// D[b, h, g] = sum_d dO[b, g, h, d] * O[b, g, h, d]; 16 lanes per (b, g, h).
+// D[b, h, g] = sum_d dO[b, g, h, d] * O[b, g, h, d]; 16 lanes per (b, g, h);
+// output row stride ld.
 template <typename T, int D>
 __global__ void __launch_bounds__(256) preprocess_kernel(const T* dO, const float* O, float* Dout,
-                                                         int64_t B, int64_t L, int64_t H) {
+                                                         int64_t B, int64_t L, int64_t H,
+                                                         int64_t ld) {
   constexpr int EPL = D / 16;  // elements per lane
   const int64_t row = (int64_t(blockIdx.x) * blockDim.x + threadIdx.x) / 16;
   const int sub = threadIdx.x & 15;
@@ -49,7 +51,7 @@ __global__ void __launch_bounds__(256) preprocess_kernel(const T* dO, const floa
   acc += __shfl_xor(acc, 8);
   if (ok && sub == 0) {
     const int64_t h = row % H, g = (row / H) % L, b = row / (H * L);
-    Dout[(b * H + h) * L + g] = acc;
+    Dout[(b * H + h) * ld + g] = acc;
   }
 }
 
@@ -71,7 +73,8 @@ hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t s) {
 }
 
 hipError_t launch_bwd_preprocess(const void* dO, const float* O, float* D, cqsa_dtype dt,
-                                 int64_t B, int64_t L, int64_t H, int d, hipStream_t s) {
+                                 int64_t B, int64_t L, int64_t H, int d, int64_t ld,
+                                 hipStream_t s) {
   const int64_t rows = B * L * H;
   const unsigned blocks = unsigned((rows * 16 + 255) / 256);
   if (rows == 0) return hipSuccess;
@@ -80,10 +83,10 @@ hipError_t launch_bwd_preprocess(const void* dO, const float* O, float* D, cqsa_
   case DD:                                                                               \
     if (dt == CQSA_BF16)                                                                 \
       hipLaunchKernelGGL((preprocess_kernel<__bf16, DD>), dim3(blocks), dim3(256), 0, s, \
-                         (const __bf16*)dO, O, D, B, L, H);                              \
+                         (const __bf16*)dO, O, D, B, L, H, ld);                              \
     else if (dt == CQSA_F16)                                                             \
       hipLaunchKernelGGL((preprocess_kernel<_Float16, DD>), dim3(blocks), dim3(256), 0,  \
-                         s, (const _Float16*)dO, O, D, B, L, H);                         \
+                         s, (const _Float16*)dO, O, D, B, L, H, ld);                         \
     else                                                                                 \
       return hipErrorInvalidValue;                                                       \
     break;

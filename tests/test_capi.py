@@ -114,9 +114,13 @@ def test_automatic_accumulator_residency():
     p = cq.cqsa_plan(1 << 20, 8, 128, False, 4 * GB,
                      cq.make_opts(acc_on_device=None, inputs_on_device=False, depth=3))
     assert p.acc_on_device == 0 and p.depth == 3
-    with pytest.raises(cq.CqsaError) as e:
-        cq.cqsa_plan(4096, 4, 128, False, 0, cq.make_opts(acc_on_device=None, with_backward=True))
-    assert e.value.status == -2
+    # with the backward: the gradients follow the accumulator (Table
+    # "recovery": fwd+bwd with the accumulator on the host)
+    p = cq.cqsa_plan(4096, 4, 128, False, 0, cq.make_opts(acc_on_device=None, with_backward=True))
+    assert p.acc_on_device == 1
+    p = cq.cqsa_plan(1 << 20, 8, 128, True, 8 * GB,
+                     cq.make_opts(acc_on_device=None, inputs_on_device=False, with_backward=True))
+    assert p.acc_on_device == 0 and p.modelled_device_bytes <= 8 * GB
 
 
 def test_read_in_place_choice_and_errors():
@@ -290,7 +294,9 @@ def test_footprint_model_closed_form(tps, want_g, subslots, in_place):
     """Footprint of the bf16 L=32768 H=16 d=128 depth-1 plan, recomputed here
     from the workspace layout the header documents: with g tasks per slot and
     two slots, slot i holds the largest group k = i (mod 2); a task sub-slot
-    holds the statistics, plus the staged Q, K, V unless they are read in place."""
+    holds the statistics (acc, m, l and the rounded-weight sum lt), plus the
+    staged Q, K, V unless they are read in place; with more than one launch
+    group the running l and lt sit in the workspace."""
     L, H, d, B = 32768, 16, 128, 1
     p = cq.cqsa_plan(L, H, d, False, 0, cq.make_opts(depth=1, tasks_per_slot=tps,
                                                        read_in_place=in_place))
@@ -298,10 +304,10 @@ def test_footprint_model_closed_form(tps, want_g, subslots, in_place):
     al = lambda x: (x + 255) // 256 * 256
     Lmax = max(p.task(t)["L_local"] for t in range(p.num_tasks))
     rows = B * Lmax * H
-    sub = (0 if in_place else 3 * al(rows * d * 2)) + al(rows * d * 4) + 2 * al(rows * 4)
+    sub = (0 if in_place else 3 * al(rows * d * 2)) + al(rows * d * 4) + 3 * al(rows * 4)
     resident = 3 * al(B * L * H * d * 2) + al(B * L * H * d * 4) + al(B * L * H * 4)
     groups = -(-7 // want_g)
-    running_l = al(B * H * L * 4) if groups > 1 else 0
+    running_l = 2 * al(B * H * L * 4) if groups > 1 else 0
     want = resident + subslots * sub + running_l + al(_image_bytes(p, want_g))
     assert p.modelled_device_bytes == want
 
@@ -392,15 +398,20 @@ def test_backward_argument_errors_without_device_work():
     capped = cq.cqsa_plan(64, 1, 64, False, 10 ** 9, cq.make_opts(depth=1))
     st, msg = _backward_status(capped)
     assert st == -1 and "with_backward" in msg
-    # host-resident plans and fp32 plans are not built for the backward
-    host = cq.cqsa_plan(64, 1, 64, False, 0, cq.make_opts(depth=1, inputs_on_device=False,
-                                                          acc_on_device=False))
-    assert _backward_status(host)[0] == -2
+    # fp32 plans are not built for the backward
     f32 = cq.cqsa_plan(64, 1, 64, False, 0, cq.make_opts(dtype="f32", depth=1))
     assert _backward_status(f32, dt="f32")[0] == -2
     # tensor residency, dtype and shape; LSE pointer and residency
     st, msg = _backward_status(ok, dO=_desc("bf16", cq.CQSA_MEM_HOST))
     assert st == -1 and "dO" in msg and "residency" in msg
+    # a host-resident plan: inputs on the host, O, LSE and gradients too
+    host = cq.cqsa_plan(64, 1, 64, False, 0, cq.make_opts(depth=1, inputs_on_device=False,
+                                                          acc_on_device=False, with_backward=True))
+    h = cq.CQSA_MEM_HOST
+    st, msg = _backward_status(host, where=h, dQ=_desc("f32", cq.CQSA_MEM_DEVICE), lse_where=h)
+    assert st == -1 and "dQ" in msg and "residency" in msg
+    st, msg = _backward_status(host, where=h)
+    assert st == -1 and "LSE" in msg
     st, msg = _backward_status(ok, dK=_desc("bf16", cq.CQSA_MEM_DEVICE))
     assert st == -1 and "dK" in msg and "dtype" in msg
     st, msg = _backward_status(ok, V=_desc("bf16", cq.CQSA_MEM_DEVICE, L=65))
@@ -476,3 +487,30 @@ def test_misaligned_tensor_rejected_before_any_device_work():
     with pytest.raises(cq.CqsaError) as e:
         cq.cqsa_forward(plan, bad, *good, O, LSE)
     assert e.value.status == -1 and "Q.data must be 16-byte aligned" in str(e.value)
+
+
+def test_lse_checked_by_the_binding_before_any_call():
+    """The C ABI takes LSE as a bare float pointer, so the Python binding checks
+    its dtype, layout, shape (B, H, L) and residency (that of O) in both
+    wrappers before calling the library: an undersized LSE would otherwise be
+    written out of bounds, a bf16 or strided one misread."""
+    import torch
+    B, L, H, d = 2, 64, 3, 64
+    plan = cq.cqsa_plan(L, H, d, False, 0, cq.make_opts(B=B, depth=1, with_backward=True))
+    x = torch.zeros((B, L, H, d), dtype=torch.bfloat16)
+    O = torch.zeros((B, L, H, d), dtype=torch.float32)
+    good = torch.zeros((B, H, L), dtype=torch.float32)
+    bad = [torch.zeros((B, H, L - 1), dtype=torch.float32),          # undersized
+           torch.zeros((B, L, H), dtype=torch.float32),              # wrong layout
+           torch.zeros((B, H, L), dtype=torch.bfloat16),             # wrong dtype
+           torch.zeros((B, H, 2 * L), dtype=torch.float32)[..., ::2]]  # strided
+    for lse in bad:
+        with pytest.raises(ValueError, match="LSE"):
+            cq.cqsa_forward(plan, x, x, x, O, lse)
+        with pytest.raises(ValueError, match="LSE"):
+            cq.cqsa_backward(plan, x, x, x, O, lse, x, O, O, O)
+    # the good LSE passes the binding; the library then refuses the host
+    # tensors of this device plan with a status, not a crash
+    with pytest.raises(cq.CqsaError) as e:
+        cq.cqsa_forward(plan, x, x, x, O, good)
+    assert e.value.status == -1

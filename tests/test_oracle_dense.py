@@ -102,6 +102,10 @@ def test_row_subsets_and_per_head_rows():
     O, LSE = dense.attention_forward(Q, K, V, causal=True)
     rows = np.array([0, 5, 33, 69])
     Os, LSEs = dense.attention_forward(Q, K, V, causal=True, rows=rows, row_chunk=3)
+    # a row subset in chunks of 3 rows hands BLAS other matrix shapes than the
+    # full call, so its blocking, and the float64 summation order of each dot
+    # product, differ: equal up to a few ulps of the sums (rtol 1e-12), not to
+    # the last bit
     np.testing.assert_allclose(Os, O[:, rows], rtol=1e-12, atol=1e-14)
     np.testing.assert_allclose(LSEs, LSE[:, :, rows], rtol=1e-12, atol=1e-14)
     per = [np.array([1, 2, 68]), np.array([0, 40, 69])]
@@ -114,3 +118,25 @@ def test_row_subsets_and_per_head_rows():
 def test_rel_l2():
     assert dense.rel_l2(np.array([3.0, 4.0]), np.array([3.0, 4.0])) == 0.0
     assert abs(dense.rel_l2(np.array([3.0, 5.0]), np.array([3.0, 4.0])) - 0.2) < 1e-15
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_backward_rows_equal_the_full_backward(causal):
+    """attention_backward_rows (sampled query rows for dQ, sampled key rows
+    for dK and dV, one pass over query chunks) against the full-matrix
+    attention_backward, itself pinned by autograd and finite differences."""
+    rng = np.random.default_rng(11)
+    Q, K, V, dO = _rand(rng, 2, 70, 3, 8)
+    gQ, gK, gV, _, _ = dense.attention_backward(Q, K, V, dO, causal)
+    qr, kr = np.array([0, 9, 33, 69]), np.array([0, 1, 50, 68, 69])
+    dQ, dK, dV = dense.attention_backward_rows(Q, K, V, dO, causal, qr, kr, row_chunk=16)
+    np.testing.assert_allclose(dQ, gQ[:, qr], rtol=1e-11, atol=1e-13)
+    np.testing.assert_allclose(dK, gK[:, kr], rtol=1e-11, atol=1e-13)
+    np.testing.assert_allclose(dV, gV[:, kr], rtol=1e-11, atol=1e-13)
+    per_q = [np.array([3, 4]), np.array([0, 69]), np.array([10, 20])]
+    per_k = [np.array([69, 5]), np.array([7, 8]), np.array([0, 1])]
+    dQ, dK, dV = dense.attention_backward_rows(Q, K, V, dO, causal, per_q, per_k, row_chunk=7)
+    for h in range(3):
+        np.testing.assert_allclose(dQ[:, :, h], gQ[:, per_q[h], h], rtol=1e-11, atol=1e-13)
+        np.testing.assert_allclose(dK[:, :, h], gK[:, per_k[h], h], rtol=1e-11, atol=1e-13)
+        np.testing.assert_allclose(dV[:, :, h], gV[:, per_k[h], h], rtol=1e-11, atol=1e-13)
