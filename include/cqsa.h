@@ -255,6 +255,39 @@ cqsa_status cqsa_backward(const cqsa_plan_t* plan, const cqsa_tensor* Q, const c
                           cqsa_mem lse_where, const cqsa_tensor* dO, cqsa_tensor* dQ,
                           cqsa_tensor* dK, cqsa_tensor* dV, float scale, void* hip_stream);
 
+/* Bytes of the fixed device scratch array that cqsa_forward_noalloc works in
+ * (64 MiB; one array per GPU the library runs on, held until the process
+ * ends). */
+#define CQSA_NOALLOC_SCRATCH_BYTES (64u << 20)
+
+/* cqsa_forward for callers that cannot allocate: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation.  Same
+ * arguments, results and ordering as cqsa_forward (bit-identical outputs), but
+ * the call allocates nothing: no hipMalloc, no hipFree, no pinned host memory,
+ * no caller-allocator call, no new streams or events (those it records into
+ * exist from the device's set-up).  Its workspace is a fixed device
+ * array of CQSA_NOALLOC_SCRATCH_BYTES per GPU, looked up once per device when
+ * the library first runs there.  The plan image is copied from the plan
+ * itself (pageable host memory), so the copy may block the host until the
+ * stream reaches it.
+ * Limits, each reported as CQSA_ERR_INVALID_ARG before any device work:
+ *   - the plan must keep O and LSE on the device (acc_on_device = 1);
+ *   - the call's workspace (the plan image plus the task statistics and, for
+ *     staged plans, the staged inputs) must fit CQSA_NOALLOC_SCRATCH_BYTES;
+ *   - at most 3 staging slots;
+ *   - per-stage timing (cqsa_set_timing) is not recorded.
+ * No OOM guardrail runs (nothing is allocated).  Nothing in the scratch has
+ * to start at zero: each call writes every byte it reads before reading it.
+ * Every call on a GPU shares that GPU's scratch and finds the previous
+ * call's contents there.  Two calls whose device work overlapped on one GPU
+ * would race in it, so each call's device work waits for the previous
+ * no-allocation call's (an event the library records at the end of every
+ * call): calls from different streams or host threads queue, they do not
+ * overlap. */
+cqsa_status cqsa_forward_noalloc(const cqsa_plan_t* plan, const cqsa_tensor* Q,
+                                 const cqsa_tensor* K, const cqsa_tensor* V, cqsa_tensor* O,
+                                 float* LSE, cqsa_mem lse_where, float scale, void* hip_stream);
+
 /* Route the library's device workspace through a caller allocator (e.g. a
  * framework's caching allocator).  alloc(bytes, ctx) returns device memory or
  * NULL (reported as CQSA_ERR_DEVICE_OOM); release(ptr, ctx) frees it.  Passing

@@ -98,6 +98,10 @@ _SIGS = {
                                     ctypes.POINTER(cqsa_tensor), ctypes.POINTER(cqsa_tensor),
                                     ctypes.POINTER(cqsa_tensor), ctypes.c_void_p, ctypes.c_int,
                                     ctypes.c_float, ctypes.c_void_p]),
+    "cqsa_forward_noalloc": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(cqsa_tensor),
+                                            ctypes.POINTER(cqsa_tensor), ctypes.POINTER(cqsa_tensor),
+                                            ctypes.POINTER(cqsa_tensor), ctypes.c_void_p, ctypes.c_int,
+                                            ctypes.c_float, ctypes.c_void_p]),
     "cqsa_backward": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(cqsa_tensor),
                                      ctypes.POINTER(cqsa_tensor), ctypes.POINTER(cqsa_tensor),
                                      ctypes.POINTER(cqsa_tensor), ctypes.c_void_p, ctypes.c_int,
@@ -292,6 +296,20 @@ def cqsa_forward(plan, Q, K, V, O, LSE, scale=0.0, stream=None):
                               ctypes.byref(to), ctypes.c_void_p(LSE.data_ptr()),
                               CQSA_MEM_DEVICE if LSE.is_cuda else CQSA_MEM_HOST,
                               float(scale), s), "cqsa_forward")
+
+
+def cqsa_forward_noalloc(plan, Q, K, V, O, LSE, scale=0.0, stream=None):
+    """cqsa_forward working in the device's fixed scratch array: allocates
+    nothing (for graph capture and serving loops); see include/cqsa.h for its
+    limits."""
+    _check_lse(plan, LSE, O)
+    tq, tk, tv, to = (as_cqsa_tensor(x) for x in (Q, K, V, O))
+    s = stream if stream is not None else _stream_of(O, Q)
+    _check(lib().cqsa_forward_noalloc(plan.handle, ctypes.byref(tq), ctypes.byref(tk),
+                                      ctypes.byref(tv), ctypes.byref(to),
+                                      ctypes.c_void_p(LSE.data_ptr()),
+                                      CQSA_MEM_DEVICE if LSE.is_cuda else CQSA_MEM_HOST,
+                                      float(scale), s), "cqsa_forward_noalloc")
 
 
 def cqsa_backward(plan, Q, K, V, O, LSE, dO, dQ, dK, dV, scale=0.0, stream=None):

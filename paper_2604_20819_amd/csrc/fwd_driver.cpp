@@ -99,9 +99,13 @@ void host_finalize(float* acc, float* m, const float* l, const float* lt, int64_
 
 }  // namespace
 
+// noalloc: the cqsa_forward_noalloc contract -- the workspace is the device's
+// scratch array, the plan image is copied straight from the plan, and nothing
+// is allocated (no workspace, pinned host buffer, timing event or new
+// synchronisation event).
 cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_tensor* K,
                          const cqsa_tensor* V, cqsa_tensor* O, float* LSE, cqsa_mem lse_where,
-                         float scale, hipStream_t st) {
+                         float scale, hipStream_t st, bool noalloc) {
   if (!p) return fail(CQSA_ERR_INVALID_ARG, "cqsa_forward: plan is NULL");
   const cqsa_plan_opts& o = p->opts;
   const cqsa_mem in_where = o.inputs_on_device ? CQSA_MEM_DEVICE : CQSA_MEM_HOST;
@@ -114,6 +118,11 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
   if (!LSE) return fail(CQSA_ERR_INVALID_ARG, "LSE is NULL");
   if (lse_where != acc_where)
     return fail(CQSA_ERR_INVALID_ARG, "LSE residency must equal the output residency");
+
+  if (noalloc && !o.acc_on_device)
+    return fail(CQSA_ERR_INVALID_ARG,
+                "cqsa_forward_noalloc: the plan must keep O and LSE on the device "
+                "(a host accumulator needs pinned staging)");
 
   DevCtx* C = device_ctx(&s);
   if (!C) return s;
@@ -133,6 +142,7 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
 
   CallRecord& rec = call_record();
   rec.reset();
+  if (noalloc) rec.timing = false;  // timing events would be created per call
   rec.stats.depth = depth;
   rec.stats.num_tasks = ntask;
   rec.stats.modelled_device_bytes = p->fp.peak;
@@ -160,8 +170,22 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
   // fp32 result when O is 16-bit: [B, L, H, d] after the slots
   const uint64_t o32_bytes = o.out16 ? align_up(uint64_t(B) * L * H * d * 4) : 0;
   const uint64_t total = tab_bytes + gl_bytes + slot_off[nslot] + o32_bytes;
+  const size_t events = size_t(4 * std::max<int64_t>(nslot, 1) + 3);
   Workspace ws;
-  if ((s = acquire_workspace(C, total, &ws)) != CQSA_OK) return s;
+  if (noalloc) {
+    if (total > CQSA_NOALLOC_SCRATCH_BYTES)
+      return fail(CQSA_ERR_INVALID_ARG,
+                  "cqsa_forward_noalloc: the call's workspace (" + std::to_string(total) +
+                      " bytes) exceeds the " + std::to_string(CQSA_NOALLOC_SCRATCH_BYTES) +
+                      "-byte scratch");
+    if (events > C->sync_events.size())
+      return fail(CQSA_ERR_INVALID_ARG,
+                  "cqsa_forward_noalloc: at most 3 staging slots (the set-up events)");
+    ws.ptr = C->scratch;
+    ws.bytes = total;
+  } else if ((s = acquire_workspace(C, total, &ws)) != CQSA_OK) {
+    return s;
+  }
   rec.stats.workspace_bytes = total;
   rec.stats.resident_tasks = direct ? 0 : fwd_subslots(ntask, int32_t(gsz), o.n_slots);
   char* base = (char*)ws.ptr;
@@ -176,7 +200,7 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
   const int rows_wg = fwd_rows_per_wg(o.dtype, int(d));
 
   // ---- ordering against the caller's stream and the previous call ----
-  while (C->sync_events.size() < size_t(4 * std::max<int64_t>(nslot, 1) + 3)) {
+  while (C->sync_events.size() < events) {
     hipEvent_t e;
     CQSA_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
     C->sync_events.push_back(e);
@@ -186,7 +210,10 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
   hipEvent_t* ev_staged = &C->sync_events[2];
   hipEvent_t* ev_free = &C->sync_events[2 + nslot];
   hipEvent_t* ev_inner = &C->sync_events[2 + 2 * nslot];
-  if (C->ws_free_valid) CQSA_HIP(hipStreamWaitEvent(st, C->ws_free, 0));
+  // after the previous call's last use of the same workspace
+  hipEvent_t& ws_free = noalloc ? C->scratch_free : C->ws_free;
+  bool& ws_free_valid = noalloc ? C->scratch_free_valid : C->ws_free_valid;
+  if (ws_free_valid) CQSA_HIP(hipStreamWaitEvent(st, ws_free, 0));
   // With nothing to stage and a single launch group (the direct call, or
   // inputs read in place with every task in one launch) the whole call runs
   // on the caller's stream: each hop between streams costs the GPU an event
@@ -199,7 +226,13 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
     CQSA_HIP(hipEventRecord(ev_start, st));
     CQSA_HIP(hipStreamWaitEvent(cs, ev_start, 0));
   }
-  if ((s = upload_image(C, p->packed, d_tab, cs)) != CQSA_OK) return s;
+  if (noalloc) {
+    // from the plan's own (pageable) memory: no pinned staging ring
+    if (!p->packed.empty())
+      CQSA_HIP(hipMemcpyAsync(d_tab, p->packed.data(), p->packed.size(), hipMemcpyHostToDevice, cs));
+  } else if ((s = upload_image(C, p->packed, d_tab, cs)) != CQSA_OK) {
+    return s;
+  }
 
   auto span_begin = [&](hipStream_t sm) -> std::pair<hipEvent_t, hipEvent_t> {
     std::pair<hipEvent_t, hipEvent_t> sp{nullptr, nullptr};
@@ -428,9 +461,9 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
     span_end(sp, st, kStFinal);
   }
   if (rec.timing) CQSA_HIP(hipEventRecord(rec.wall1, st));
-  CQSA_HIP(hipEventRecord(C->ws_free, st));
-  C->ws_free_valid = true;
-  release_workspace(C, &ws, st);
+  CQSA_HIP(hipEventRecord(ws_free, st));
+  ws_free_valid = true;
+  if (!noalloc) release_workspace(C, &ws, st);
   if (!acc_dev) {
     hipError_t e = hipStreamSynchronize(st);
     if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
@@ -447,11 +480,28 @@ extern "C" cqsa_status cqsa_forward(const cqsa_plan_t* plan, const cqsa_tensor* 
   cqsa::clear_error();
   try {
     return cqsa::run_guarded(plan, false, [&](const cqsa_plan_t* q) {
-      return cqsa::forward_impl(q, Q, K, V, O, LSE, lse_where, scale, (hipStream_t)hip_stream);
+      return cqsa::forward_impl(q, Q, K, V, O, LSE, lse_where, scale, (hipStream_t)hip_stream,
+                                false);
     });
   } catch (const std::exception& e) {
     return cqsa::fail(CQSA_ERR_INTERNAL, std::string("cqsa_forward: ") + e.what());
   } catch (...) {
     return cqsa::fail(CQSA_ERR_INTERNAL, "cqsa_forward: unknown exception");
+  }
+}
+
+extern "C" cqsa_status cqsa_forward_noalloc(const cqsa_plan_t* plan, const cqsa_tensor* Q,
+                                            const cqsa_tensor* K, const cqsa_tensor* V,
+                                            cqsa_tensor* O, float* LSE, cqsa_mem lse_where,
+                                            float scale, void* hip_stream) {
+  cqsa::clear_error();
+  try {
+    // no guardrail: nothing is allocated, so nothing can run out of memory
+    return cqsa::forward_impl(plan, Q, K, V, O, LSE, lse_where, scale, (hipStream_t)hip_stream,
+                              true);
+  } catch (const std::exception& e) {
+    return cqsa::fail(CQSA_ERR_INTERNAL, std::string("cqsa_forward_noalloc: ") + e.what());
+  } catch (...) {
+    return cqsa::fail(CQSA_ERR_INTERNAL, "cqsa_forward_noalloc: unknown exception");
   }
 }

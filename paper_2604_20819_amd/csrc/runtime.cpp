@@ -11,6 +11,11 @@
 
 namespace cqsa {
 
+// Workspace of cqsa_forward_noalloc.  In host code this name is a host-side
+// stand-in, not a device address: host code uses only the address that
+// hipGetSymbolAddress returns for the current device (DevCtx::scratch).
+static __device__ __align__(256) char scratch[CQSA_NOALLOC_SCRATCH_BYTES];
+
 namespace {
 std::mutex g_ctx_mu;
 DevCtx g_ctx[64];
@@ -36,8 +41,25 @@ DevCtx* device_ctx(cqsa_status* st) {
     if ((e = hipStreamCreateWithFlags(&c->copy, hipStreamNonBlocking)) != hipSuccess ||
         (e = hipStreamCreateWithFlags(&c->aux, hipStreamNonBlocking)) != hipSuccess ||
         (e = hipStreamCreateWithFlags(&c->lane, hipStreamNonBlocking)) != hipSuccess ||
-        (e = hipEventCreateWithFlags(&c->ws_free, hipEventDisableTiming)) != hipSuccess) {
+        (e = hipEventCreateWithFlags(&c->ws_free, hipEventDisableTiming)) != hipSuccess ||
+        (e = hipEventCreateWithFlags(&c->scratch_free, hipEventDisableTiming)) != hipSuccess) {
       *st = hip_fail(e, "creating library streams");
+      return nullptr;
+    }
+    while (c->sync_events.size() < kSetupEvents) {
+      hipEvent_t ev;
+      if ((e = hipEventCreateWithFlags(&ev, hipEventDisableTiming)) != hipSuccess) {
+        *st = hip_fail(e, "creating library events");
+        return nullptr;
+      }
+      c->sync_events.push_back(ev);
+    }
+    // this device's copy of the scratch array (the device is current here)
+    if ((e = hipGetSymbolAddress(&c->scratch, HIP_SYMBOL(scratch))) != hipSuccess ||
+        c->scratch == nullptr) {
+      c->scratch = nullptr;
+      *st = hip_fail(e == hipSuccess ? hipErrorInvalidSymbol : e,
+                     "hipGetSymbolAddress of the no-allocation scratch");
       return nullptr;
     }
     c->ready = true;

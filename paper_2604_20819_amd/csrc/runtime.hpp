@@ -36,8 +36,18 @@ struct DevCtx {
   bool img_valid[2] = {false, false};
   int img_next = 0;
   std::vector<hipEvent_t> sync_events;  // reusable non-timing events
+  // the fixed scratch array of cqsa_forward_noalloc on this device (its device
+  // address, from hipGetSymbolAddress at set-up) and the event after the
+  // last no-allocation call's last use of it
+  void* scratch = nullptr;
+  hipEvent_t scratch_free = nullptr;
+  bool scratch_free_valid = false;
   std::mutex mu;
 };
+
+// Non-timing events created with the context, so that a call that must not
+// allocate finds its synchronisation events in place.
+constexpr size_t kSetupEvents = 16;
 
 DevCtx* device_ctx(cqsa_status* st);  // context of the current device (created on first use)
 
