@@ -4,8 +4,8 @@ Allocation failures are forced from the host: a caller allocator (the
 cqsa_set_allocator hook) refuses requests above a limit and returns NULL, so
 the library sees CQSA_ERR_DEVICE_OOM before it enqueues any work.  With an
 automatic depth the call must then succeed with fewer resident task working
-sets or a deeper plan, and match the unconstrained result; a forced depth
-must report the failure.
+sets or a deeper plan, and match both the float64 oracle and the
+unconstrained result; a forced depth must report the failure.
 """
 import numpy as np
 import pytest
@@ -14,6 +14,8 @@ import torch
 import paper_2604_20819_amd as cq
 from paper_2604_20819_amd import synth
 from tests.gpu_util import need_gpu, rel_l2, say
+from tests.test_gpu_backward import _check_grads, oracle_grads
+from tests.test_gpu_forward import _check_vs_oracle
 
 pytestmark = pytest.mark.gpu
 
@@ -88,6 +90,7 @@ def test_forward_guardrail_lowers_residency_then_deepens():
     for O, LSE in ((O1, L1), (O2, L2)):
         assert rel_l2(O.numpy(), O0.numpy()) <= 2e-5
         assert np.abs(LSE.numpy() - L0.numpy()).max() <= 1e-5
+        _check_vs_oracle(O, LSE, Q, K, V, False, "bf16")
 
 
 def test_forward_guardrail_reaches_a_deeper_level():
@@ -115,6 +118,7 @@ def test_forward_guardrail_reaches_a_deeper_level():
     assert st["depth"] == 2 and st["workspace_bytes"] < smallest_depth1
     assert rel_l2(O.numpy(), O0.numpy()) <= 2e-5
     assert np.abs(LSE.numpy() - L0.numpy()).max() <= 1e-5
+    _check_vs_oracle(O, LSE, Q, K, V, False, "bf16")
 
 
 def test_forced_depth_reports_the_failure_and_exhaustion_is_reported():
@@ -172,3 +176,42 @@ def test_backward_guardrail():
     say(f"  fallbacks {st['guard_steps']}, depth {st['depth']}, resident {st['resident_tasks']}")
     for g, r in zip(got, ref):
         assert rel_l2(g.numpy(), r.numpy()) <= 1e-3
+    _check_grads(got, oracle_grads(Q, K, V, dO, True), "bf16")
+
+
+def test_host_resident_backward_guardrail():
+    """With every tensor in host memory the backward's staging slots hold the
+    task's inputs and its own gradients; a workspace refusal drops to one
+    slot (or a deeper plan), and the gradients still match float64."""
+    need_gpu()
+    L, H, d = 2500, 2, 64
+    Q, K, V, dO = synth.make_inputs(45, 1, L, H, d, "bf16", with_dO=True)
+    q, k, v, do = (x.pin_memory() for x in (Q, K, V, dO))
+    plan = cq.cqsa_plan(L, H, d, True, 0, cq.make_opts(dtype="bf16", with_backward=True,
+                                                       inputs_on_device=False,
+                                                       acc_on_device=False))
+    O = torch.empty((1, L, H, d), dtype=torch.float32, pin_memory=True)
+    LSE = torch.empty((1, H, L), dtype=torch.float32, pin_memory=True)
+    cq.cqsa_forward(plan, q, k, v, O, LSE)
+
+    def grads():
+        g = [torch.empty((1, L, H, d), dtype=torch.float32, pin_memory=True) for _ in range(3)]
+        cq.cqsa_backward(plan, q, k, v, O, LSE, do, *g)
+        return g
+
+    cq.cqsa_set_timing(True)
+    try:
+        ref = grads()
+        full = cq.cqsa_last_stats()["workspace_bytes"]
+        with LimitedAllocator(full - 1) as a:
+            say(f"guardrail host backward: workspace {full} B, limit {full - 1} B")
+            got = grads()
+            st = cq.cqsa_last_stats()
+            assert a.refused >= 1 and st["guard_steps"] >= 1 and st["workspace_bytes"] < full
+            assert not a.held
+    finally:
+        cq.cqsa_set_timing(False)
+    say(f"  fallbacks {st['guard_steps']}, depth {st['depth']}, resident {st['resident_tasks']}")
+    for g, r in zip(got, ref):
+        assert rel_l2(g.numpy(), r.numpy()) <= 1e-3
+    _check_grads(got, oracle_grads(Q, K, V, dO, True), "bf16")

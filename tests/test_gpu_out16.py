@@ -4,13 +4,16 @@ With out16 the forward computes the same fp32 result as with an fp32 O and
 rounds it once, to nearest even, into an O of the input dtype.  torch's
 float32 -> bfloat16 / float16 conversions round the same way, so the 16-bit
 O must equal the fp32 call's O converted by torch bit for bit, and LSE must
-be identical.  Parity of the fp32 result with the oracle is covered by the
-forward tests.
+be identical.  Against the float64 oracle the 16-bit O carries the fp32
+result's error (max-abs bound 1e-2) plus one rounding to the output dtype
+(half an ulp: at most 2^-8 |O| for bf16, 2^-11 |O| for fp16), elementwise.
 """
+import numpy as np
 import pytest
 import torch
 
 import paper_2604_20819_amd as cq
+from oracle import dense
 from paper_2604_20819_amd import synth
 from tests.gpu_util import need_gpu, say
 
@@ -54,6 +57,13 @@ def test_out16_equals_rounded_fp32(dt, B, L, H, d, causal, depth, rip, host_in):
     assert o16.dtype == tdt
     assert torch.equal(o16, o32.to(tdt))
     assert torch.equal(l16, l32)
+    Of, Lf = dense.attention_forward(synth.as_f64(Q), synth.as_f64(K), synth.as_f64(V), causal)
+    half_ulp = {"bf16": 2.0 ** -8, "f16": 2.0 ** -11}[dt]
+    err = np.abs(o16.double().numpy() - Of)
+    say(f"  max |O16 - O64| = {err.max():.3e}, max |LSE - LSE64| = "
+        f"{np.abs(l16.double().numpy() - Lf).max():.3e}")
+    assert (err <= 1e-2 + half_ulp * np.abs(Of)).all()
+    assert np.abs(l16.double().numpy() - Lf).max() <= 1e-4
 
 
 def test_out16_back_to_back_calls_share_the_workspace():
