@@ -8,9 +8,9 @@ memory, a 4 GB device budget (CQS depth 2, 49 tasks of about 192600 tokens,
 accumulator on the host).  Q, K, V are i.i.d. N(0,1) from a fixed seed, cast
 to bf16.  One step = one pass of the whole forward hot path: plan the call,
 stage every task's runs over the host link (reusing the tokens the previous
-task also holds), one inner-kernel launch per task on two alternating
-compute streams, copy each task's statistics back, merge them on host
-threads, finalise.  `value` is algorithmic TFLOP/s = 4 d B H L^2 / step time
+task also holds), one inner-kernel launch per task (launches this long run
+one after another on the caller's stream), copy each task's statistics back,
+merge them on host threads, finalise.  `value` is algorithmic TFLOP/s = 4 d B H L^2 / step time
 with the inputs already in (host) memory; the host-link rates ride along.
 
 The same line also carries:

@@ -14,10 +14,13 @@
  *   - Every call returns cqsa_status: 0 on success, a negative code on error.
  *     No C++ exception or abort crosses this boundary.  On error the contents
  *     of outputs are unspecified and cqsa_last_error() describes the failure.
- *   - Tensors are dense row-major [B, L, H, d] (d fastest); the caller owns
- *     them.  LSE and the softmax statistics are [B, H, L] fp32.
- *   - Outputs O, dQ, dK, dV are fp32 and LSE is the natural-log log-sum-exp
- *     of the scaled scores (Section 4.1: statistics, merge and output are
+ *   - Tensors are dense row-major [B, L, H, d] (d fastest), with no stride
+ *     arguments: a task's run of tokens is then one contiguous span per batch
+ *     element, which staging copies in one transfer and the kernels address
+ *     with one row offset.  The caller owns them.  LSE and the softmax
+ *     statistics are [B, H, L] fp32.
+ *   - Outputs O (unless the plan asks for a 16-bit O), dQ, dK, dV are fp32
+ *     and LSE is the natural-log log-sum-exp of the scaled scores (Section 4.1: statistics, merge and output are
  *     fp32; App. A.1: lse = m + log l).
  *   - Inputs are fp32, fp16 or bf16.  Head dimension d: 32, 64, 96, ..., 256
  *     for the forward (the head dims the paper's forward covers, Sec. 5,
