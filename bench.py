@@ -149,6 +149,18 @@ def time_steps(step, steps, warmup, torch):
     return (time.perf_counter() - t0) * 1e3 / steps, out
 
 
+def warm_gpu(torch, seconds):
+    """Dense fp16 products for about `seconds`, so that timing starts at
+    working clocks."""
+    a = torch.randn((8192, 8192), device="cuda", dtype=torch.float16)
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < seconds:
+        for _ in range(10):
+            a = (a @ a).clamp_(-1, 1)
+        torch.cuda.synchronize()
+    del a
+
+
 def mean(stats, key):
     return sum(s[key] for s in stats) / len(stats)
 
@@ -421,17 +433,22 @@ def sweep(args):
         dQ, dK, dV = (torch.empty((B, L, H, d), dtype=torch.float32, device="cuda")
                       for _ in range(3))
         flops = 4.0 * d * B * H * pairs(L, True)
-        steps = 5 if L <= (1 << 17) else 2
+        # short calls take more steps, and a second of warm-up work before the
+        # first length brings the GPU's clocks up (the first sub-millisecond
+        # calls of a process otherwise run up to 1.7x slower)
+        steps = 20 if L <= (1 << 15) else 5 if L <= (1 << 17) else 2
+        if L == 8192:
+            warm_gpu(torch, 1.0)
         row = {"L": L}
         for depth, tag in ((1, "decomposed"), (0, "undecomposed")):
             plan = cq.cqsa_plan(L, H, d, True, 0, cq.make_opts(B=B, dtype="f16", depth=depth,
                                                                 with_backward=True))
-            ms, _ = time_steps(lambda: cq.cqsa_forward(plan, q, k, v, O, LSE), steps, 1, torch)
+            ms, _ = time_steps(lambda: cq.cqsa_forward(plan, q, k, v, O, LSE), steps, 3, torch)
 
             def fb():
                 cq.cqsa_forward(plan, q, k, v, O, LSE)
                 cq.cqsa_backward(plan, q, k, v, O, LSE, do, dQ, dK, dV)
-            msb, _ = time_steps(fb, steps, 1, torch)
+            msb, _ = time_steps(fb, steps, 3, torch)
             row.update({f"{tag}_fwd_ms": round(ms, 3),
                         f"{tag}_fwd_tflops": round(flops / (ms * 1e-3) / 1e12, 2),
                         f"{tag}_fwd_bwd_ms": round(msb, 3),

@@ -126,6 +126,19 @@ typedef struct {
                                 result is kept in the workspace, and the footprint counts it.
                                 Needs a 16-bit dtype, acc_on_device = 1 and with_backward = 0
                                 (the backward reads the fp32 O).  0: O is fp32 (0) */
+  int32_t bwd_tasks_per_launch; /* backward tasks run by one dQ and one dK/dV launch, in
+                                [0, 32].  Applies when the inputs are read in place and O, LSE,
+                                dQ, dK, dV are device-resident (acc_on_device = 1) at depth
+                                >= 1: the tasks of a launch store their gradients in task-local
+                                fp32 buffers in the workspace (3 x B x L_max x H x d x 4 bytes
+                                per task) and one gather-merge per launch adds them into dQ, dK,
+                                dV in task order.  0 = automatic: every task up to 32 when
+                                with_backward = 1, reduced until the budget fits, else 1;
+                                >= 1 forced (> 1 needs inputs_on_device = 1 and neither
+                                read_in_place nor acc_on_device set to 0; where the
+                                conditions above do not hold, 1 applies).  With 1, each
+                                task's launches add its rows into the gradients directly, tasks
+                                one after another.  Every setting gives the same bits (0) */
 } cqsa_plan_opts;
 
 /* One contiguous run of a task's tokens: global tokens
@@ -178,11 +191,14 @@ typedef struct {
                                        backward: preprocess span (D = rowsum(dO * O)) */
   double ms_d2h;                    /* sum of statistics device-to-host spans */
   int64_t tiles_full, tiles_clear, tiles_mixed; /* 128x128 tile census of the plan */
-  int64_t merge_launches;           /* device merge launches (forward) */
+  int64_t merge_launches;           /* device merge launches (forward merges, or the backward's
+                                       gradient merges) */
   double ms_inner_busy;             /* time at least one inner kernel ran (union of its spans) */
   int64_t guard_steps;              /* OOM guardrail fallbacks this call took (0: the plan ran) */
-  int64_t resident_tasks;           /* task working sets held at once (forward sub-slots or
-                                       backward staging slots; 0 for the undecomposed path) */
+  int64_t resident_tasks;           /* task working sets held at once (forward sub-slots,
+                                       backward staging slots, or the backward tasks per launch
+                                       whose local gradients the workspace holds; 0 for the
+                                       undecomposed path and for one in-place task per launch) */
 } cqsa_run_stats;
 
 /* Fill `o` with the defaults listed in cqsa_plan_opts. */
@@ -208,6 +224,9 @@ cqsa_status cqsa_plan_get_task(const cqsa_plan_t* plan, int64_t t, cqsa_task* ou
 uint64_t cqsa_plan_modelled_device_bytes(const cqsa_plan_t* plan);
 /* Forward tasks per staging slot and launch group the plan chose; -1 if plan is NULL. */
 int32_t cqsa_plan_tasks_per_slot(const cqsa_plan_t* plan);
+/* Backward tasks per dQ and dK/dV launch the plan chose (bwd_tasks_per_launch);
+ * -1 if plan is NULL. */
+int32_t cqsa_plan_bwd_tasks_per_launch(const cqsa_plan_t* plan);
 /* Where the plan keeps the accumulator and outputs: 1 device, 0 host (the choice of an
  * automatic acc_on_device = -1; App. A.3, residency); -1 if plan is NULL. */
 int32_t cqsa_plan_acc_on_device(const cqsa_plan_t* plan);

@@ -47,7 +47,7 @@ class cqsa_plan_opts(ctypes.Structure):
                 ("with_backward", ctypes.c_int32), ("tasks_per_slot", ctypes.c_int32),
                 ("n_level_sets", ctypes.c_int32), ("level_sets", cqsa_interest_set * 4),
                 ("read_in_place", ctypes.c_int32),
-                ("out16", ctypes.c_int32)]
+                ("out16", ctypes.c_int32), ("bwd_tasks_per_launch", ctypes.c_int32)]
 
 
 class cqsa_run(ctypes.Structure):
@@ -88,6 +88,7 @@ _SIGS = {
     "cqsa_plan_get_task": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.POINTER(cqsa_task)]),
     "cqsa_plan_modelled_device_bytes": (ctypes.c_uint64, [ctypes.c_void_p]),
     "cqsa_plan_tasks_per_slot": (ctypes.c_int32, [ctypes.c_void_p]),
+    "cqsa_plan_bwd_tasks_per_launch": (ctypes.c_int32, [ctypes.c_void_p]),
     "cqsa_plan_acc_on_device": (ctypes.c_int32, [ctypes.c_void_p]),
     "cqsa_plan_reads_in_place": (ctypes.c_int32, [ctypes.c_void_p]),
     "cqsa_plan_tile_census": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(ctypes.c_int64),
@@ -148,12 +149,14 @@ def cqsa_plan_opts_default():
 
 def make_opts(B=1, dtype="bf16", c=7, interest=(0, 1, 3), depth=-1, min_depth=1, max_depth=4,
               n_slots=2, inputs_on_device=True, acc_on_device=True, with_backward=False,
-              tasks_per_slot=0, levels=None, read_in_place=None, out16=False):
+              tasks_per_slot=0, levels=None, read_in_place=None, out16=False,
+              bwd_tasks_per_launch=0):
     """levels: optional list of (c, interest) per depth (the last repeats below).
     acc_on_device=None asks the planner to choose the accumulator residency;
     read_in_place=None lets it choose whether the kernels read the caller's
     tensors in place (True) or gather each task's runs first (False).
-    out16=True makes cqsa_forward write O in the input dtype."""
+    out16=True makes cqsa_forward write O in the input dtype.
+    bwd_tasks_per_launch: 0 automatic, n >= 1 backward tasks per launch."""
     o = cqsa_plan_opts_default()
     o.B = B
     o.dtype = {"f32": CQSA_F32, "f16": CQSA_F16, "bf16": CQSA_BF16}[dtype]
@@ -168,6 +171,7 @@ def make_opts(B=1, dtype="bf16", c=7, interest=(0, 1, 3), depth=-1, min_depth=1,
     o.tasks_per_slot = int(tasks_per_slot)
     o.read_in_place = -1 if read_in_place is None else int(bool(read_in_place))
     o.out16 = int(bool(out16))
+    o.bwd_tasks_per_launch = int(bwd_tasks_per_launch)
     if levels:
         if len(levels) > 4:
             raise ValueError("at most 4 level sets")
@@ -208,6 +212,10 @@ class Plan:
     @property
     def tasks_per_slot(self):
         return lib().cqsa_plan_tasks_per_slot(self.handle)
+
+    @property
+    def bwd_tasks_per_launch(self):
+        return lib().cqsa_plan_bwd_tasks_per_launch(self.handle)
 
     @property
     def acc_on_device(self):

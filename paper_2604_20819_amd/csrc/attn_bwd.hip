@@ -4,9 +4,11 @@
 //   dV = P^T dO,  dK = alpha dS^T Q  (key-parallel kernel, 4 products)
 //   dQ = alpha dS K                  (query-parallel kernel, 3 products)
 // The paper shows this equals Alg. 2; because every (query, key) pair is kept
-// by exactly one task, task gradients add, and each kernel's epilogue adds its
-// task-local rows straight into the global fp32 gradients (tasks are ordered
-// on one stream and a task holds each token once, so no atomics are needed).
+// by exactly one task, task gradients add.  A launch of one task may add its
+// rows straight into the global fp32 gradients (tasks are ordered on one
+// stream and a task holds each token once, so no atomics are needed); a
+// launch of several tasks stores each task's rows in its own buffer, and a
+// gather-merge sums them in task order.
 //
 // Tile verdicts, masks and ascending-order causal tests follow the forward.
 // Fully masked tiles are skipped before any load: a skipped tile leaves
@@ -56,17 +58,21 @@ __global__ void __launch_bounds__(64 * dq_waves<D>(), (lds_row_elems<D>() > 128 
   const int tid = threadIdx.x, lane = tid & 63, half = lane >> 5;
   // uniform per wave, so per-wave loads and branches stay scalar
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int L = a.L;
+  int64_t work = xcd_remap(blockIdx.x, gridDim.x);
+  const int tj = find_task(a.tasks, a.ntask, BM, int64_t(a.H) * a.B, work);
+  const DevTask tk = a.tasks[tj];
+  const int L = int(tk.L_local);
   const int64_t nstrips = (L + BM - 1) / BM;
-  const int64_t work = xcd_remap(blockIdx.x, nstrips * a.H * a.B);
   // strips in the task's launch order (most live key tiles first; the plan
   // builds this table for BM-row strips, BM = dq_rows_per_wg)
-  const int strip = a.qorder[work % nstrips];
+  const int strip = ((const int32_t*)(a.tab + tk.dqorder_off))[work % nstrips];
   const int h = int((work / nstrips) % a.H);
   const int b = int(work / (nstrips * a.H));
-  const DevRun* runs_g = (const DevRun*)a.runs;
+  const int n_runs = tk.n_runs;
+  const DevRun* runs_g = (const DevRun*)(a.tab + tk.runs_off);
+  const DevBlock* blks = (const DevBlock*)(a.tab + tk.sum_off);
   const bool in_place = a.in_place != 0;
-  for (int i = tid; i < a.n_runs; i += NT) runs_s[i] = runs_g[i];
+  for (int i = tid; i < n_runs; i += NT) runs_s[i] = runs_g[i];
 
   // token rows: consecutive when staged, the runs' global rows when the
   // caller's tensors are read in place (as in the forward)
@@ -87,8 +93,8 @@ __global__ void __launch_bounds__(64 * dq_waves<D>(), (lds_row_elems<D>() > 128 
   // its branch are wave-uniform
   int64_t qrow = myq;
   if (in_place && q0w < L) {
-    const int32_t br = a.rows[q0w >> 6];
-    qrow = br != kNoRow ? int64_t(br) + (myq & 63) : (qvalid ? run_global(runs_g, a.n_runs, myq) : 0);
+    const int32_t br = blks[q0w >> 6].row;
+    qrow = br != kNoRow ? int64_t(br) + (myq & 63) : (qvalid ? run_global(runs_g, n_runs, myq) : 0);
   }
   vec8 qf[DK], of[DK];
 #pragma unroll
@@ -106,13 +112,13 @@ __global__ void __launch_bounds__(64 * dq_waves<D>(), (lds_row_elems<D>() > 128 
   const int qb0 = strip * (BM / 64), qb1 = lastq_wg / 64;
   uint32_t qor = 0u, qand = 0xFFFFFFFFu;
   for (int qb = qb0; qb <= qb1; ++qb) {
-    qor |= a.blk_or[qb];
-    qand &= a.blk_and[qb];
+    qor |= blks[qb].bor;
+    qand &= blks[qb].band;
   }
   const bool wave_live = q0w < L;
   const int wq1 = wave_live ? (q0w + 31 < L ? q0w + 31 : L - 1) : 0;
-  const uint32_t wor = wave_live ? a.blk_or[q0w / 64] : 0u;
-  const uint32_t wand = wave_live ? a.blk_and[q0w / 64] : 0u;
+  const uint32_t wor = wave_live ? blks[q0w / 64].bor : 0u;
+  const uint32_t wand = wave_live ? blks[q0w / 64].band : 0u;
   const int nkt = (L + BN - 1) / BN;
   // Tile skipping as in the forward: a window of 64 tiles' summaries (and
   // first rows, kNoRow across a run boundary) per vector load (lane i = tile
@@ -125,9 +131,10 @@ __global__ void __launch_bounds__(64 * dq_waves<D>(), (lds_row_elems<D>() > 128 
     const int k = k0 + lane;
     Window w{0xFFFFFFFFu, 0u, 0};
     if (k < nkt) {
-      w.an = a.blk_and[k];
-      w.on = a.blk_or[k];
-      w.row = in_place ? a.rows[k] : k * BN;
+      const u32x4 x = *(const u32x4*)(blks + k);  // one DevBlock
+      w.on = x[0];
+      w.an = x[1];
+      w.row = in_place ? int32_t(x[2]) : k * BN;
     }
     return w;
   };
@@ -189,7 +196,7 @@ __global__ void __launch_bounds__(64 * dq_waves<D>(), (lds_row_elems<D>() > 128 
         const int key = kt * BN + row;
         const int ch = (ln % CHUNKS) ^ swz(row);
         const uint32_t vo =
-            key < L ? uint32_t((run_global(runs_s, a.n_runs, key) * rs + ch * 8) * 2) : kOobOffset;
+            key < L ? uint32_t((run_global(runs_s, n_runs, key) * rs + ch * 8) * 2) : kOobOffset;
         const int off = (NDMA * wave + j) * 1024;
         buf_load16_lds(rk, kb + off, vo);
         buf_load16_lds(rv, vb + off, vo);
@@ -199,7 +206,7 @@ __global__ void __launch_bounds__(64 * dq_waves<D>(), (lds_row_elems<D>() > 128 
   auto sstore = [&](int buf, int kt, uint32_t kor_t) {
     if ((qor & kor_t) != 0u && tid < BN) {
       const int key = kt * BN + tid;
-      kbits_s[buf][tid] = key < L ? run_bits(runs_s, a.n_runs, key) : 0u;
+      kbits_s[buf][tid] = key < L ? run_bits(runs_s, n_runs, key) : 0u;
     }
   };
 
@@ -210,8 +217,8 @@ __global__ void __launch_bounds__(64 * dq_waves<D>(), (lds_row_elems<D>() > 128 
     for (int r = 0; r < 16; ++r) dq[db][r] = 0.f;
 
   __syncthreads();
-  const uint32_t qbits = qvalid ? run_bits(runs_s, a.n_runs, myq) : 0u;
-  const int64_t gq = qvalid ? run_global(runs_s, a.n_runs, myq) : 0;
+  const uint32_t qbits = qvalid ? run_bits(runs_s, n_runs, myq) : 0u;
+  const int64_t gq = qvalid ? run_global(runs_s, n_runs, myq) : 0;
   const int64_t si = (int64_t(b) * a.H + h) * a.Lg + gq;
   const float lse2 = qvalid ? a.lse[si] * kLog2e : 0.f;
   const float Dq = qvalid ? a.D[si] : 0.f;
@@ -314,19 +321,21 @@ __global__ void __launch_bounds__(64 * dq_waves<D>(), (lds_row_elems<D>() > 128 
     nrow = row2;
   }
   if (!qvalid) return;
-  // global rows accumulate (a task holds a token once and the dQ launches of
-  // a call are ordered on one stream); a task-local buffer is stored
-  float* dst = a.dq + (LOCAL ? int64_t(b) * L + myq : int64_t(b) * a.Lg + gq) * rs + int64_t(h) * D;
+  // global rows accumulate (a single task holds a token once and the dQ
+  // launches of a call are ordered on one stream); a task-local buffer is
+  // stored.  The scaled value is rounded before the addition (no fused
+  // multiply-add), so accumulating here and summing task-local buffers later
+  // in task order give the same bits.
+  float* dst = (LOCAL ? a.dq + tj * a.out_stride + (int64_t(b) * L + myq) * rs
+                      : a.dq + (int64_t(b) * a.Lg + gq) * rs) + int64_t(h) * D;
 #pragma unroll
   for (int db = 0; db < DB; ++db)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       f32x4* p = (f32x4*)(dst + 32 * db + 8 * i + 4 * half);
       f32x4 v = LOCAL ? f32x4{0.f, 0.f, 0.f, 0.f} : *p;
-      v[0] += a.scale * dq[db][4 * i];
-      v[1] += a.scale * dq[db][4 * i + 1];
-      v[2] += a.scale * dq[db][4 * i + 2];
-      v[3] += a.scale * dq[db][4 * i + 3];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) v[j] += mul_rounded(a.scale, dq[db][4 * i + j]);
       *p = v;
     }
 }
@@ -371,21 +380,25 @@ __global__ void __launch_bounds__(256 * dkdv_splits<D>(), (lds_row_elems<D>() > 
   const int tid = threadIdx.x, lane = tid & 63, half = lane >> 5;
   // uniform per wave, so per-wave loads and branches stay scalar
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int L = a.L;
+  int64_t work = xcd_remap(blockIdx.x, gridDim.x);
+  const int tj = find_task(a.tasks, a.ntask, BK, int64_t(a.H) * a.B, work);
+  const DevTask tk = a.tasks[tj];
+  const int L = int(tk.L_local);
   const int64_t nstrips = (L + BK - 1) / BK;
-  const int64_t work = xcd_remap(blockIdx.x, nstrips * a.H * a.B);
   // the wave's 32 keys are the kw-th of the strip; it owns dK, dV columns
   // from 32-column block db0 (both fixed at 4 waves, no split)
   const int kw = NSPLIT > 1 ? (wave & 3) : wave;
   const int db0 = NSPLIT > 1 ? (wave >> 2) * DBO : 0;
   // key strips in the task's launch order (most live query tiles first)
   static_assert(BK == kStrip, "strip tables are built for kStrip-row strips");
-  const int strip = a.korder[work % nstrips];
+  const int strip = ((const int32_t*)(a.tab + tk.korder_off))[work % nstrips];
   const int h = int((work / nstrips) % a.H);
   const int b = int(work / (nstrips * a.H));
-  const DevRun* runs_g = (const DevRun*)a.runs;
+  const int n_runs = tk.n_runs;
+  const DevRun* runs_g = (const DevRun*)(a.tab + tk.runs_off);
+  const DevBlock* blks = (const DevBlock*)(a.tab + tk.sum_off);
   const bool in_place = a.in_place != 0;
-  for (int i = tid; i < a.n_runs; i += NT) runs_s[i] = runs_g[i];
+  for (int i = tid; i < n_runs; i += NT) runs_s[i] = runs_g[i];
 
   // token rows: consecutive when staged, the runs' global rows when the
   // caller's tensors are read in place
@@ -406,16 +419,20 @@ __global__ void __launch_bounds__(256 * dkdv_splits<D>(), (lds_row_elems<D>() > 
   // its branch are wave-uniform
   int64_t krow = mykey;
   if (in_place && k0w < L) {
-    const int32_t br = a.rows[k0w >> 6];
-    krow = br != kNoRow ? int64_t(br) + (mykey & 63) : (kvalid ? run_global(runs_g, a.n_runs, mykey) : 0);
+    const int32_t br = blks[k0w >> 6].row;
+    krow = br != kNoRow ? int64_t(br) + (mykey & 63) : (kvalid ? run_global(runs_g, n_runs, mykey) : 0);
   }
   // the wave's K rows stay in registers (B operands of S = Q K^T); the
   // strip's V rows (B operands of dP = dO V^T) go to LDS once
+  // every lane loads (keys past the task read row 0, then take zeros): a
+  // select rather than a branch around the loads
   vec8 kf[DK];
+  const int64_t kr = kvalid ? krow : 0;
 #pragma unroll
   for (int ks = 0; ks < DK; ++ks) {
-    u32x4 u = {0u, 0u, 0u, 0u};
-    if (kvalid) u = *(const u32x4*)(Kg + krow * rs + ks * 16 + half * 8);
+    u32x4 u = *(const u32x4*)(Kg + kr * rs + ks * 16 + half * 8);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) u[e] = kvalid ? u[e] : 0u;
     kf[ks] = bitcast_u4<vec8>(u);
   }
   {
@@ -424,7 +441,7 @@ __global__ void __launch_bounds__(256 * dkdv_splits<D>(), (lds_row_elems<D>() > 
     const int vb0 = strip * 2, vb1 = ((strip * BK + BK < L ? strip * BK + BK : L) - 1) >> 6;
     int32_t vrow = strip * BK;
     if (in_place) {
-      const int32_t r0 = a.rows[vb0], r1 = a.rows[vb1];
+      const int32_t r0 = blks[vb0].row, r1 = blks[vb1].row;
       vrow = (r0 != kNoRow && (vb1 == vb0 || r1 == r0 + 64)) ? r0 : kNoRow;
     }
     const int64_t vrows = int64_t(L) - int64_t(strip) * BK;
@@ -441,7 +458,7 @@ __global__ void __launch_bounds__(256 * dkdv_splits<D>(), (lds_row_elems<D>() > 
         // per-lane rows from the slice base (the runs in global memory: the
         // LDS copy is not visible yet); tokens past the task end read zero
         const int key = strip * BK + row;
-        vo = key < L ? uint32_t((run_global(runs_g, a.n_runs, key) * rs + ch * 8) * 2) : kOobOffset;
+        vo = key < L ? uint32_t((run_global(runs_g, n_runs, key) * rs + ch * 8) * 2) : kOobOffset;
       }
       buf_load16_lds(rv, vs + (NV * wave + j) * 1024, vo);
     }
@@ -449,12 +466,12 @@ __global__ void __launch_bounds__(256 * dkdv_splits<D>(), (lds_row_elems<D>() > 
 
   const int lastk_wg = (strip * BK + BK < L ? strip * BK + BK : L) - 1;
   const int kb0 = strip * 2, kb1 = lastk_wg / 64;
-  const uint32_t kor = a.blk_or[kb0] | a.blk_or[kb1];
-  const uint32_t kand = a.blk_and[kb0] & a.blk_and[kb1];
+  const uint32_t kor = blks[kb0].bor | blks[kb1].bor;
+  const uint32_t kand = blks[kb0].band & blks[kb1].band;
   const bool wave_live = k0w < L;
   const int wk1 = wave_live ? (k0w + 31 < L ? k0w + 31 : L - 1) : 0;
-  const uint32_t wor = wave_live ? a.blk_or[k0w / 64] : 0u;
-  const uint32_t wand = wave_live ? a.blk_and[k0w / 64] : 0u;
+  const uint32_t wor = wave_live ? blks[k0w / 64].bor : 0u;
+  const uint32_t wand = wave_live ? blks[k0w / 64].band : 0u;
   const int nqt = (L + BQ - 1) / BQ;
   const int first_key = strip * BK;
   const int64_t stat_base = (int64_t(b) * a.H + h) * a.Lg;
@@ -471,10 +488,11 @@ __global__ void __launch_bounds__(256 * dkdv_splits<D>(), (lds_row_elems<D>() > 
     const int t = t0 + lane;
     Window w{0xFFFFFFFFu, 0u, 0};
     if (t < nqt) {
-      w.an = a.blk_and[t >> 1];
-      w.on = a.blk_or[t >> 1];
+      const u32x4 x = *(const u32x4*)(blks + (t >> 1));  // one DevBlock
+      w.on = x[0];
+      w.an = x[1];
       if (in_place) {
-        const int32_t r = a.rows[t >> 1];
+        const int32_t r = int32_t(x[2]);
         w.row = r != kNoRow ? r + (t & 1) * BQ : kNoRow;
       } else {
         w.row = t * BQ;
@@ -507,25 +525,24 @@ __global__ void __launch_bounds__(256 * dkdv_splits<D>(), (lds_row_elems<D>() > 
   // as zero) straight into LDS, and, for the first BQ threads, the query's
   // global LSE (log2 units), D and group bits into registers (LSE = +inf
   // past the task gives P = 0), stored to LDS after the compute.
-  uint32_t goff[NDMA];
-#pragma unroll
-  for (int j = 0; j < NDMA; ++j) {
-    const int row = RPI * (NDMA * wave + j) + lane / CHUNKS;
-    goff[j] = uint32_t((row * rs + ((lane % CHUNKS) ^ swz(row)) * 8) * 2);
-  }
   float lse_r = INFINITY, d_r = 0.f;
-  uint32_t qb_r = 0u;
   auto gload = [&](int buf, int qt, int32_t trow) {
     if (trow != kNoRow) {
-      // consecutive rows from trow
+      // consecutive rows from trow; the per-lane offsets are recomputed per
+      // tile from an opaque copy of the lane index (kept out of registers
+      // across the tile loop)
       const int64_t rows = int64_t(L) - int64_t(qt) * BQ;
       const __amdgpu_buffer_rsrc_t rq = row_rsrc(Qg + int64_t(trow) * rs, rows, rs * 2, D * 2);
       const __amdgpu_buffer_rsrc_t ro = row_rsrc(Og + int64_t(trow) * rs, rows, rs * 2, D * 2);
+      int ln = lane;
+      asm volatile("" : "+v"(ln));
 #pragma unroll
       for (int j = 0; j < NDMA; ++j) {
+        const int row = RPI * (NDMA * wave + j) + ln / CHUNKS;
+        const uint32_t go = uint32_t((row * rs + ((ln % CHUNKS) ^ swz(row)) * 8) * 2);
         const int off = (NDMA * wave + j) * 1024;
-        buf_load16_lds(rq, qs[buf] + off, goff[j]);
-        buf_load16_lds(ro, os[buf] + off, goff[j]);
+        buf_load16_lds(rq, qs[buf] + off, go);
+        buf_load16_lds(ro, os[buf] + off, go);
       }
     } else {
       // across a run boundary: per-lane rows from the slice base
@@ -541,7 +558,7 @@ __global__ void __launch_bounds__(256 * dkdv_splits<D>(), (lds_row_elems<D>() > 
         const int q = qt * BQ + row;
         const int ch = (ln % CHUNKS) ^ swz(row);
         const uint32_t vo =
-            q < L ? uint32_t((run_global(runs_s, a.n_runs, q) * rs + ch * 8) * 2) : kOobOffset;
+            q < L ? uint32_t((run_global(runs_s, n_runs, q) * rs + ch * 8) * 2) : kOobOffset;
         const int off = (NDMA * wave + j) * 1024;
         buf_load16_lds(rq, qs[buf] + off, vo);
         buf_load16_lds(ro, os[buf] + off, vo);
@@ -551,20 +568,21 @@ __global__ void __launch_bounds__(256 * dkdv_splits<D>(), (lds_row_elems<D>() > 
       const int q = qt * BQ + tid;
       lse_r = INFINITY;
       d_r = 0.f;
-      qb_r = 0u;
       if (q < L) {
-        const int64_t g = run_global(runs_s, a.n_runs, q);
+        const int64_t g = run_global(runs_s, n_runs, q);
         lse_r = a.lse[stat_base + g] * kLog2e;
         d_r = a.D[stat_base + g];
-        qb_r = run_bits(runs_s, a.n_runs, q);
       }
     }
   };
-  auto sstore = [&](int buf) {
+  // the group bits come from the runs in LDS here rather than with the loads
+  // (one register fewer across the tile's compute)
+  auto sstore = [&](int buf, int qt) {
     if (tid < BQ) {
+      const int q = qt * BQ + tid;
       lse_s[buf][tid] = lse_r;
       d_s[buf][tid] = d_r;
-      qbits_s[buf][tid] = qb_r;
+      qbits_s[buf][tid] = q < L ? run_bits(runs_s, n_runs, q) : 0u;
     }
   };
 
@@ -578,14 +596,14 @@ __global__ void __launch_bounds__(256 * dkdv_splits<D>(), (lds_row_elems<D>() > 
     }
 
   __syncthreads();  // runs_s visible
-  const uint32_t kbits = kvalid ? run_bits(runs_s, a.n_runs, mykey) : 0u;
+  const uint32_t kbits = kvalid ? run_bits(runs_s, n_runs, mykey) : 0u;
 
   uint32_t qor = 0u, qand = 0u, nor = 0u, nand = 0u;
   int32_t qrow = 0, nrow = 0;
   int qt = next_live(causal ? first_key / BQ : 0, qor, qand, qrow);
   if (qt < nqt) {
     gload(0, qt, qrow);
-    sstore(0);
+    sstore(0, qt);
   }
   int qn = qt < nqt ? next_live(qt + 1, nor, nand, nrow) : nqt;
   int buf = 0;
@@ -672,7 +690,7 @@ __global__ void __launch_bounds__(256 * dkdv_splits<D>(), (lds_row_elems<D>() > 
     uint32_t or2 = 0u, and2 = 0u;
     int32_t row2 = 0;
     if (qn < nqt) {
-      sstore(buf ^ 1);
+      sstore(buf ^ 1, qn);
       if (qc < nqt) {
         qc2 = pick(qc, cw, or2, and2, row2);
         if (qc2 < 0) qc2 = next_live(qc + 64, or2, and2, row2);
@@ -689,11 +707,12 @@ __global__ void __launch_bounds__(256 * dkdv_splits<D>(), (lds_row_elems<D>() > 
   }
   __builtin_amdgcn_s_waitcnt(0x0F70);  // the V fill has landed even when no tile was live
   if (!kvalid) return;
-  // global rows accumulate; a task-local buffer is stored (as for dQ)
-  const int64_t orow = LOCAL ? int64_t(b) * L + mykey
-                             : int64_t(b) * a.Lg + run_global(runs_s, a.n_runs, mykey);
-  float* dkp = a.dk + orow * rs + int64_t(h) * D;
-  float* dvp = a.dv + orow * rs + int64_t(h) * D;
+  // global rows accumulate; a task-local buffer is stored (as for dQ, the
+  // scaled dK is rounded before the addition)
+  const int64_t orow = LOCAL ? tj * a.out_stride + (int64_t(b) * L + mykey) * rs
+                             : (int64_t(b) * a.Lg + run_global(runs_s, n_runs, mykey)) * rs;
+  float* dkp = a.dk + orow + int64_t(h) * D;
+  float* dvp = a.dv + orow + int64_t(h) * D;
 #pragma unroll
   for (int db = 0; db < DBO; ++db) {
     if (NSPLIT > 1 && db0 + db >= DB) break;
@@ -707,7 +726,7 @@ __global__ void __launch_bounds__(256 * dkdv_splits<D>(), (lds_row_elems<D>() > 
       }
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        x[j] += a.scale * dk[db][4 * i + j];
+        x[j] += mul_rounded(a.scale, dk[db][4 * i + j]);
         y[j] += dv[db][4 * i + j];
       }
       *(f32x4*)(dkp + off) = x;
@@ -717,10 +736,7 @@ __global__ void __launch_bounds__(256 * dkdv_splits<D>(), (lds_row_elems<D>() > 
 }
 
 template <typename E, int D>
-static hipError_t launch_dq_t(const BwdArgs& a, hipStream_t s) {
-  constexpr int rows = 32 * dq_waves<D>();
-  const int64_t n = ((a.L + rows - 1) / rows) * int64_t(a.H) * a.B;
-  if (n == 0) return hipSuccess;
+static hipError_t launch_dq_t(const BwdArgs& a, int64_t n, hipStream_t s) {
   if (a.local_out)
     hipLaunchKernelGGL((attn_bwd_dq<E, D, true>), dim3(unsigned(n)), dim3(64 * dq_waves<D>()), 0, s, a);
   else
@@ -729,9 +745,7 @@ static hipError_t launch_dq_t(const BwdArgs& a, hipStream_t s) {
 }
 
 template <typename E, int D>
-static hipError_t launch_dkdv_t(const BwdArgs& a, hipStream_t s) {
-  const int64_t n = ((a.L + 127) / 128) * int64_t(a.H) * a.B;
-  if (n == 0) return hipSuccess;
+static hipError_t launch_dkdv_t(const BwdArgs& a, int64_t n, hipStream_t s) {
   if (a.local_out)
     hipLaunchKernelGGL((attn_bwd_dkdv<E, D, true>), dim3(unsigned(n)), dim3(256 * dkdv_splits<D>()), 0, s, a);
   else
@@ -741,14 +755,14 @@ static hipError_t launch_dkdv_t(const BwdArgs& a, hipStream_t s) {
 
 #define CQSA_BWD_SWITCH(LAUNCH)                                        \
   switch (d) {                                                         \
-    case 32: return dt == CQSA_BF16 ? LAUNCH<BF16, 32>(a, s) : LAUNCH<F16, 32>(a, s);    \
-    case 64: return dt == CQSA_BF16 ? LAUNCH<BF16, 64>(a, s) : LAUNCH<F16, 64>(a, s);    \
-    case 96: return dt == CQSA_BF16 ? LAUNCH<BF16, 96>(a, s) : LAUNCH<F16, 96>(a, s);    \
-    case 128: return dt == CQSA_BF16 ? LAUNCH<BF16, 128>(a, s) : LAUNCH<F16, 128>(a, s); \
-    case 160: return dt == CQSA_BF16 ? LAUNCH<BF16, 160>(a, s) : LAUNCH<F16, 160>(a, s); \
-    case 192: return dt == CQSA_BF16 ? LAUNCH<BF16, 192>(a, s) : LAUNCH<F16, 192>(a, s); \
-    case 224: return dt == CQSA_BF16 ? LAUNCH<BF16, 224>(a, s) : LAUNCH<F16, 224>(a, s); \
-    case 256: return dt == CQSA_BF16 ? LAUNCH<BF16, 256>(a, s) : LAUNCH<F16, 256>(a, s); \
+    case 32: return dt == CQSA_BF16 ? LAUNCH<BF16, 32>(a, wgs, s) : LAUNCH<F16, 32>(a, wgs, s);    \
+    case 64: return dt == CQSA_BF16 ? LAUNCH<BF16, 64>(a, wgs, s) : LAUNCH<F16, 64>(a, wgs, s);    \
+    case 96: return dt == CQSA_BF16 ? LAUNCH<BF16, 96>(a, wgs, s) : LAUNCH<F16, 96>(a, wgs, s);    \
+    case 128: return dt == CQSA_BF16 ? LAUNCH<BF16, 128>(a, wgs, s) : LAUNCH<F16, 128>(a, wgs, s); \
+    case 160: return dt == CQSA_BF16 ? LAUNCH<BF16, 160>(a, wgs, s) : LAUNCH<F16, 160>(a, wgs, s); \
+    case 192: return dt == CQSA_BF16 ? LAUNCH<BF16, 192>(a, wgs, s) : LAUNCH<F16, 192>(a, wgs, s); \
+    case 224: return dt == CQSA_BF16 ? LAUNCH<BF16, 224>(a, wgs, s) : LAUNCH<F16, 224>(a, wgs, s); \
+    case 256: return dt == CQSA_BF16 ? LAUNCH<BF16, 256>(a, wgs, s) : LAUNCH<F16, 256>(a, wgs, s); \
   }                                                                    \
   return hipErrorInvalidValue;
 
@@ -770,15 +784,23 @@ int dq_rows_per_wg(int d) {
   return 128;
 }
 
-hipError_t launch_bwd_dq(cqsa_dtype dt, int d, const BwdArgs& a, hipStream_t s) {
-  if (a.n_runs > kMaxRuns) return hipErrorInvalidValue;
-  if (dt != CQSA_BF16 && dt != CQSA_F16) return hipErrorInvalidValue;
+// Launch checks: a task table, a grid that fits, and global accumulation
+// only for a single task (tasks of one launch may share tokens).
+static bool bwd_launch_ok(cqsa_dtype dt, const BwdArgs& a, int64_t wgs) {
+  if (dt != CQSA_BF16 && dt != CQSA_F16) return false;
+  if (a.ntask < 1 || !a.tasks || !a.tab || wgs > 0x7fffffff) return false;
+  return a.local_out != 0 || a.ntask == 1;
+}
+
+hipError_t launch_bwd_dq(cqsa_dtype dt, int d, const BwdArgs& a, int64_t wgs, hipStream_t s) {
+  if (wgs == 0) return hipSuccess;
+  if (!bwd_launch_ok(dt, a, wgs)) return hipErrorInvalidValue;
   CQSA_BWD_SWITCH(launch_dq_t)
 }
 
-hipError_t launch_bwd_dkdv(cqsa_dtype dt, int d, const BwdArgs& a, hipStream_t s) {
-  if (a.n_runs > kMaxRuns) return hipErrorInvalidValue;
-  if (dt != CQSA_BF16 && dt != CQSA_F16) return hipErrorInvalidValue;
+hipError_t launch_bwd_dkdv(cqsa_dtype dt, int d, const BwdArgs& a, int64_t wgs, hipStream_t s) {
+  if (wgs == 0) return hipSuccess;
+  if (!bwd_launch_ok(dt, a, wgs)) return hipErrorInvalidValue;
   CQSA_BWD_SWITCH(launch_dkdv_t)
 }
 #undef CQSA_BWD_SWITCH

@@ -15,10 +15,16 @@
 //                 from host-resident ones (tokens the previously staged task
 //                 also holds come from its staged rows on the device); a plan
 //                 that reads device-resident inputs in place stages nothing;
-// device gradients: each kernel's epilogue adds the task's rows into the
-//                 global fp32 gradients.  Each stream keeps the tasks in order
-//                 and a task holds each token once, so these read-modify-writes
-//                 never race;
+// device gradients, several tasks per launch (inputs read in place): per
+//                 launch group one dK/dV launch (caller's stream) and one dQ
+//                 launch (second stream) over all its tasks store every task's
+//                 rows in its own buffer, and a gather-merge on the caller's
+//                 stream adds them into dQ, dK, dV in task order;
+// device gradients, one task per launch: each kernel's epilogue adds the
+//                 task's rows into the global fp32 gradients.  Each stream
+//                 keeps the tasks in order and a task holds each token once,
+//                 so these read-modify-writes never race (undecomposed, the
+//                 single task's rows are stored);
 // host gradients: the kernels store the task's rows in the slot's own
 //                 gradient buffers; the auxiliary stream copies them to pinned
 //                 host memory and a host thread adds them into dQ, dK, dV at
@@ -140,11 +146,17 @@ cqsa_status backward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa
   const uint64_t lse_bytes = dev_acc ? 0 : stat_bytes;
   const uint64_t slot_bytes = bwd_slot_bytes(p->g, o, p->max_L_local, staged);
   const int64_t nslot = std::min<int64_t>(o.n_slots, std::max<int64_t>(1, ntask));
-  const uint64_t total = tab_bytes + stat_bytes + lse_bytes + uint64_t(nslot) * slot_bytes;
+  // several tasks per launch: their local dQ, dK, dV after the slots
+  const bool batched = !p->bwd_groups.empty();
+  const bool direct = depth == 0 && !staged && dev_acc;  // the single task stores its rows
+  const int64_t gmax = batched ? p->fp.bwd_group_size : 0;
+  const uint64_t loc_b = align_up(uint64_t(B) * p->max_L_local * H * d * 4);
+  const uint64_t total = tab_bytes + stat_bytes + lse_bytes + uint64_t(nslot) * slot_bytes +
+                         3 * uint64_t(gmax) * loc_b;
   Workspace ws;
   if ((s = acquire_workspace(C, total, &ws)) != CQSA_OK) return s;
   rec.stats.workspace_bytes = total;
-  rec.stats.resident_tasks = (staged || !dev_acc) ? nslot : 0;
+  rec.stats.resident_tasks = batched ? gmax : (staged || !dev_acc) ? nslot : 0;
   char* base = (char*)ws.ptr;
   char* d_tab = base;
   float* d_D = (float*)(base + tab_bytes);
@@ -244,12 +256,12 @@ cqsa_status backward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa
   float* const hgrad[3] = {(float*)dQ->data, (float*)dK->data, (float*)dV->data};
   char* pin = nullptr;
   const uint64_t pin_slot = 3 * g_b;
-  if (dev_acc) {
+  if (dev_acc && !batched && !direct) {
     // the fused scatter-adds accumulate into zeroed gradients
     auto sp = span_begin(st);
     for (int x = 0; x < 3; ++x) CQSA_HIP(launch_fill_zero(hgrad[x], B * L * H * d, st));
     span_end(sp, st, kStMerge);
-  } else {
+  } else if (!dev_acc) {
     void* pv = nullptr;
     if ((s = acquire_pinned(C, size_t(pin_slot * nslot), &pv)) != CQSA_OK) return s;
     pin = (char*)pv;
@@ -270,13 +282,73 @@ cqsa_status backward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa
   CQSA_HIP(hipEventRecord(ev_pre, st));
   CQSA_HIP(hipStreamWaitEvent(qs, ev_pre, 0));
 
+  // work groups of a launch over tasks [t0, t0 + n): each task's strips
+  auto wgs_of = [&](int64_t t0, int64_t n, int64_t rows) {
+    int64_t w = 0;
+    for (int64_t t = t0; t < t0 + n; ++t) w += (p->tasks[t].L_local + rows - 1) / rows * B * H;
+    return w;
+  };
+  auto common_args = [&](BwdArgs& a, int64_t t0, int64_t n) {
+    a.tab = d_tab;
+    a.tasks = (const DevTask*)d_tab + t0;
+    a.ntask = int32_t(n);
+    a.B = int32_t(B); a.H = int32_t(H); a.causal = p->g.causal;
+    a.scale_log2 = sc * 1.4426950408889634f; a.scale = sc;
+    a.lse = d_lse; a.D = d_D; a.Lg = L;
+  };
+  const int64_t dq_rows = dq_rows_per_wg(int(d));
+  if (batched) {
+    float* loc = (float*)(base + tab_bytes + stat_bytes + lse_bytes + uint64_t(nslot) * slot_bytes);
+    const int64_t stride = int64_t(loc_b / 4);
+    float* lg[3] = {loc, loc + gmax * stride, loc + 2 * gmax * stride};
+    for (size_t k = 0; k < p->bwd_groups.size(); ++k) {
+      const Group& gr = p->bwd_groups[k];
+      BwdArgs a{};
+      a.q = Q->data; a.k = K->data; a.v = V->data; a.dO = dO->data;
+      a.in_place = 1;
+      common_args(a, gr.task0, gr.count);
+      a.local_out = 1;
+      a.out_stride = stride;
+      a.dq = lg[0]; a.dk = lg[1]; a.dv = lg[2];
+      // the previous group's merge has read the local buffers (it runs on the
+      // caller's stream, ahead of this group's dK/dV launch)
+      if (k > 0) {
+        CQSA_HIP(hipEventRecord(ev_pre, st));
+        CQSA_HIP(hipStreamWaitEvent(qs, ev_pre, 0));
+      }
+      std::pair<hipEvent_t, hipEvent_t> sk = span_begin(st), sq = span_begin(qs);
+      CQSA_HIP(launch_bwd_dkdv(o.dtype, int(d), a, wgs_of(gr.task0, gr.count, kStrip), st));
+      CQSA_HIP(launch_bwd_dq(o.dtype, int(d), a, wgs_of(gr.task0, gr.count, dq_rows), qs));
+      rec.stats.inner_launches += 2;
+      span_end(sk, st, kStInner);
+      span_end(sq, qs, kStInner);
+      CQSA_HIP(hipEventRecord(ev_join, qs));
+      CQSA_HIP(hipStreamWaitEvent(st, ev_join, 0));
+      GradMergeArgs m{};
+      m.segs = (const DevSeg*)(d_tab + gr.seg_off);
+      m.n_seg = gr.n_seg;
+      m.contribs = (const DevContrib*)(d_tab + gr.contrib_off);
+      m.tasks = (const DevTask*)d_tab + gr.task0;
+      for (int x = 0; x < 3; ++x) {
+        m.src[x] = lg[x];
+        m.dst[x] = hgrad[x];
+      }
+      m.stride = stride;
+      m.L = L; m.B = int32_t(B); m.H = int32_t(H); m.d = int32_t(d);
+      auto sm = span_begin(st);
+      CQSA_HIP(launch_grad_merge(m, gr.blocks, st));
+      rec.stats.merge_launches += 1;
+      span_end(sm, st, kStMerge);
+    }
+  }
+
   std::vector<bool> used(nslot, false);
   std::vector<int64_t> last_item(nslot, -1);
   const Task* prev_task = nullptr;
   const char* prev_sb = nullptr;
   const char* srcs[4] = {(const char*)Q->data, (const char*)K->data, (const char*)V->data,
                          (const char*)dO->data};
-  for (int64_t t = 0; t < ntask; ++t) {
+  for (int64_t t = 0; t < (batched ? 0 : ntask); ++t) {
     const Task& task = p->tasks[t];
     const int64_t Li = task.L_local;
     if (Li == 0) continue;
@@ -287,7 +359,6 @@ cqsa_status backward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa
     if (!staged) {
       a.q = Q->data; a.k = K->data; a.v = V->data; a.dO = dO->data;
       a.in_place = in_place ? 1 : 0;
-      a.rows = (const int32_t*)(d_tab + to.rows);
     } else {
       if (used[si]) {
         CQSA_HIP(hipStreamWaitEvent(cs, ev_free[si], 0));
@@ -337,17 +408,11 @@ cqsa_status backward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa
       CQSA_HIP(hipStreamWaitEvent(qs, ev_staged[si], 0));
       a.q = dsts[0]; a.k = dsts[1]; a.v = dsts[2]; a.dO = dsts[3];
     }
-    a.L = int32_t(Li); a.B = int32_t(B); a.H = int32_t(H); a.causal = p->g.causal;
-    a.scale_log2 = sc * 1.4426950408889634f; a.scale = sc;
-    a.runs = d_tab + to.runs; a.n_runs = int32_t(task.runs.size());
-    a.qorder = (const int32_t*)(d_tab + to.dqorder);
-    a.korder = (const int32_t*)(d_tab + to.korder);
-    a.blk_or = (const uint32_t*)(d_tab + to.blk_or);
-    a.blk_and = (const uint32_t*)(d_tab + to.blk_and);
-    a.lse = d_lse; a.D = d_D; a.Lg = L;
+    common_args(a, t, 1);
     float* tg[3] = {nullptr, nullptr, nullptr};
     if (dev_acc) {
-      a.local_out = 0;
+      // undecomposed, local rows are the global rows: the task stores them
+      a.local_out = direct ? 1 : 0;
       a.dq = hgrad[0]; a.dk = hgrad[1]; a.dv = hgrad[2];
     } else {
       // the task's own gradients; the slot's previous ones must be copied out
@@ -360,8 +425,8 @@ cqsa_status backward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa
       }
     }
     std::pair<hipEvent_t, hipEvent_t> sk = span_begin(st), sq = span_begin(qs);
-    CQSA_HIP(launch_bwd_dkdv(o.dtype, int(d), a, st));
-    CQSA_HIP(launch_bwd_dq(o.dtype, int(d), a, qs));
+    CQSA_HIP(launch_bwd_dkdv(o.dtype, int(d), a, wgs_of(t, 1, kStrip), st));
+    CQSA_HIP(launch_bwd_dq(o.dtype, int(d), a, wgs_of(t, 1, dq_rows), qs));
     rec.stats.inner_launches += 2;
     span_end(sk, st, kStInner);
     span_end(sq, qs, kStInner);

@@ -109,6 +109,29 @@ cqsa_status cqsa_plan(int64_t L, int32_t H, int32_t d, int32_t causal,
           break;
         }
       }
+      // backward launch groups: with inputs read in place and device-resident
+      // gradients, every task (up to 32) in one dQ and one dK/dV launch whose
+      // task-local gradients a gather-merge sums, reduced until the budget fits
+      p->bwd_groups.clear();
+      const int32_t bf = o.bwd_tasks_per_launch;
+      if (bwd_batchable(o, dep) && (bf > 1 || (bf == 0 && o.with_backward)) && ntask > 1) {
+        const int32_t b_hi = int32_t(std::min<int64_t>(bf > 0 ? bf : kMaxContrib, ntask));
+        for (int32_t gb = b_hi; gb >= 2; --gb) {
+          std::vector<Group> bg = make_groups(ntask, gb);
+          // the merge of the last group covers only the tokens its tasks hold
+          for (Group& x : bg) x.final = false;
+          std::vector<uint8_t> im = p->packed;
+          pack_groups(sc, H, &bg, &im);
+          Footprint f = footprint(g, o, dep, tasks, p->fp.group_size, im.size(), gb);
+          if (fits(f) || bf > 0) {
+            ok = ok && fits(f);
+            p->fp = f;
+            p->packed = std::move(im);
+            p->bwd_groups = std::move(bg);
+            break;
+          }
+        }
+      }
       p->tasks = std::move(tasks);
       return ok;
     };
@@ -180,6 +203,10 @@ cqsa_status cqsa_plan_get_task(const cqsa_plan_t* p, int64_t t, cqsa_task* out) 
 uint64_t cqsa_plan_modelled_device_bytes(const cqsa_plan_t* p) { return p ? p->fp.peak : 0; }
 
 int32_t cqsa_plan_tasks_per_slot(const cqsa_plan_t* p) { return p ? p->fp.group_size : -1; }
+
+int32_t cqsa_plan_bwd_tasks_per_launch(const cqsa_plan_t* p) {
+  return p ? p->fp.bwd_group_size : -1;
+}
 
 cqsa_status cqsa_plan_tile_census(const cqsa_plan_t* p, int64_t* full, int64_t* clear,
                                   int64_t* mixed) {

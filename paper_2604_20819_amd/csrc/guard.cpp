@@ -8,8 +8,9 @@
 // 1, increase the depth by one and re-establish n_cap.  Here n_cap is the
 // number of forward sub-slots (tasks per launch group x staging slots, each
 // holding one task's staged inputs and statistics) or, for the backward, the
-// staging slots.  The reduction halves the tasks per launch group, then
-// drops staging slots one at a time; a new depth restarts from the
+// tasks per launch (each holding its task-local gradients) and the staging
+// slots.  The reduction halves the tasks per launch group, then drops staging
+// slots one at a time; a new depth restarts from the
 // automatic group size and the requested slot count.  A forced depth is
 // never changed: its failure is reported, as the paper does for explicit
 // depths.  The configuration that succeeded is kept with the plan and tried
@@ -28,11 +29,11 @@ namespace cqsa {
 namespace {
 
 struct Config {
-  int32_t depth, group, slots;
+  int32_t depth, group, slots, bgroup;
 };
 
 Config config_of(const cqsa_plan_t* p) {
-  return Config{p->depth, p->fp.group_size, p->opts.n_slots};
+  return Config{p->depth, p->fp.group_size, p->opts.n_slots, p->fp.bwd_group_size};
 }
 
 // The next configuration after an allocation failure, or false when none
@@ -42,6 +43,10 @@ bool next_config(Config& c, bool backward, const cqsa_plan_opts& o) {
     c.group /= 2;
     return true;
   }
+  if (backward && c.bgroup > 1) {
+    c.bgroup /= 2;
+    return true;
+  }
   if (c.slots > 1) {
     c.slots -= 1;
     return true;
@@ -49,6 +54,7 @@ bool next_config(Config& c, bool backward, const cqsa_plan_opts& o) {
   if (c.depth < o.max_depth) {
     c.depth += 1;
     c.group = 0;  // automatic at the new depth
+    c.bgroup = 0;
     c.slots = o.n_slots;
     return true;
   }
@@ -59,6 +65,7 @@ std::shared_ptr<const cqsa_plan_s> build(const cqsa_plan_t* p, const Config& c, 
   cqsa_plan_opts o = p->opts;
   o.depth = c.depth;
   o.tasks_per_slot = c.group;
+  o.bwd_tasks_per_launch = c.bgroup;
   o.n_slots = c.slots;
   cqsa_plan_t* out = nullptr;
   // the budget no longer applies: the allocation itself is the test

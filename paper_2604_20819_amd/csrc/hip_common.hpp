@@ -123,6 +123,15 @@ constexpr int lds_row_elems() {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// a * b rounded to fp32 on its own: the opaque copy keeps the compiler from
+// fusing the product into a following addition (an FMA rounds once), so a sum
+// of such products is the same whichever code adds them.
+__device__ __forceinline__ float mul_rounded(float a, float b) {
+  float t = a * b;
+  asm volatile("" : "+v"(t));
+  return t;
+}
+
 // Value held by lane l^32 (the other half of the wave).
 __device__ __forceinline__ float swap_halves(float v) {
   auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(uint32_t, v),

@@ -69,35 +69,51 @@ struct CombineArgs {
   int32_t final;
 };
 
-// Inner backward kernels over one task (App. A.1, Eq. "globallse").
+// Inner backward kernels over the tasks of one launch (App. A.1, Eq.
+// "globallse").  Work groups take the tasks' strips in task order (task j's
+// strips precede task j + 1's), and each reads its task's runs, summaries,
+// block rows and strip order from the plan image through its DevTask record.
 struct BwdArgs {
-  const void* q;        // [B, L, H, d] staged task rows, or, when in_place, the
-  const void* k;        // caller's [B, Lg, H, d] tensors with local token t at
-  const void* v;        // the global row its runs give
+  const void* q;        // [B, L, H, d] staged rows of the launch's single task, or,
+  const void* k;        // when in_place, the caller's [B, Lg, H, d] tensors with
+  const void* v;        // local token t of a task at the global row its runs give
   const void* dO;
   int32_t in_place;
-  const int32_t* rows;  // block row table (records.hpp), used when in_place
-  const int32_t* qorder; // dQ query-strip launch order (records.hpp, DevTask::dqorder_off)
-  const int32_t* korder; // key-strip launch order
-  int32_t L;            // task length
+  const char* tab;      // packed plan image (DevTask offsets are relative to it)
+  const DevTask* tasks; // the launch's tasks
+  int32_t ntask;
   int32_t B, H;
   int32_t causal;
   float scale_log2;     // softmax scale * log2(e)
   float scale;          // softmax scale (dQ = scale dS K, dK = scale dS^T Q)
-  const void* runs;     // DevRun[n_runs]
-  int32_t n_runs;
-  const uint32_t* blk_or;
-  const uint32_t* blk_and;
   const float* lse;     // [B, H, Lg] global natural-log LSE from the forward
   const float* D;       // [B, H, Lg] global rowsum(dO * O)
   int64_t Lg;           // global sequence length
   int32_t local_out;    // 0: dq/dk/dv are the global [B, Lg, H, d] fp32 gradients and
-                        //    the task's rows are added at their global rows;
-                        // 1: they are the task's own [B, L, H, d] fp32 buffers and
-                        //    the task's rows are stored at their local rows
+                        //    the (single) task's rows are added at their global rows;
+                        // 1: task j's own [B, L_j, H, d] fp32 buffers sit at
+                        //    dq/dk/dv + j * out_stride and its rows are stored at
+                        //    their local rows
+  int64_t out_stride;   // elements
   float* dq;
   float* dk;
   float* dv;
+};
+
+// Gather-merge of one launch group's task-local gradients (task j's at
+// + j * stride) into the global fp32 dQ, dK, dV: every token's rows are the
+// sum of its contributions in task order, added to the running value when an
+// earlier group touched the token.
+struct GradMergeArgs {
+  const DevSeg* segs;   // the group's segments, ascending blk0
+  int32_t n_seg;
+  const DevContrib* contribs;
+  const DevTask* tasks; // the group's tasks (for L_j)
+  const float* src[3];  // task-local dq, dk, dv of the group's first task
+  int64_t stride;       // elements between consecutive tasks' buffers
+  float* dst[3];        // global [B, L, H, d] dQ, dK, dV
+  int64_t L;
+  int32_t B, H, d;
 };
 
 // Copy the rows of a task's runs from up to four [B, Lg, H, d] tensors into
@@ -131,7 +147,11 @@ hipError_t launch_cast_out(const float* src, void* dst, int64_t n, cqsa_dtype dt
 hipError_t launch_bwd_preprocess(const void* dO, const float* O, float* D, cqsa_dtype dt,
                                  int64_t B, int64_t L, int64_t H, int d, int64_t ld,
                                  hipStream_t s);
-hipError_t launch_bwd_dkdv(cqsa_dtype dt, int d, const BwdArgs& a, hipStream_t s);
-hipError_t launch_bwd_dq(cqsa_dtype dt, int d, const BwdArgs& a, hipStream_t s);
+// `wgs` = total work groups: sum over the launch's tasks of
+// ceil(L_j / rows) * B * H with rows = kStrip (dK/dV) or dq_rows_per_wg(d) (dQ).
+hipError_t launch_bwd_dkdv(cqsa_dtype dt, int d, const BwdArgs& a, int64_t wgs, hipStream_t s);
+hipError_t launch_bwd_dq(cqsa_dtype dt, int d, const BwdArgs& a, int64_t wgs, hipStream_t s);
+// `blocks` as for launch_combine.
+hipError_t launch_grad_merge(const GradMergeArgs& a, int64_t blocks, hipStream_t s);
 
 }  // namespace cqsa

@@ -131,6 +131,63 @@ __global__ void __launch_bounds__(256) combine_kernel(const CombineArgs a) {
   }
 }
 
+// Gradient recomposition of a launch group: every (token, head) row of dQ,
+// dK and dV is the sum of the group's task-local rows that hold the token, in
+// task order, added to the running value when an earlier group touched the
+// token (task gradients add: each kept pair belongs to one task).  Work
+// groups own kCombinePairs consecutive (token, head) pairs of one segment and
+// batch element, as in the combine; the rows are contiguous in every buffer,
+// 16 bytes per thread per pass.
+template <int D>
+__global__ void __launch_bounds__(256) grad_merge_kernel(const GradMergeArgs a) {
+  constexpr int P = kCombinePairs;
+  constexpr int F4 = D / 4;
+  constexpr int NF = P * F4 / 256;
+  static_assert(P * F4 % 256 == 0, "merge tiling");
+  const int tid = threadIdx.x;
+  const int b = blockIdx.y;
+  const int64_t blk = blockIdx.x;
+  int lo = 0, hi = a.n_seg - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (a.segs[mid].blk0 <= blk) lo = mid; else hi = mid - 1;
+  }
+  const DevSeg sg = a.segs[lo];
+  const int H = a.H;
+  const int64_t pair0 = (blk - sg.blk0) * P;
+  const int64_t npair64 = sg.len * H - pair0;
+  const int npair = npair64 < P ? int(npair64) : P;
+  const int nc = sg.n_c < kMaxContrib ? sg.n_c : kMaxContrib;
+  const bool glob = sg.has_global != 0;
+  const int64_t row_g = (int64_t(b) * a.L + sg.g0) * H + pair0;  // first pair's row
+#pragma unroll 1
+  for (int t = 0; t < 3; ++t) {
+    float* dst = a.dst[t] + row_g * D;
+    f32x4 acc[NF];
+#pragma unroll
+    for (int i = 0; i < NF; ++i) {
+      const int f = tid + 256 * i, p = f / F4;
+      acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (glob && p < npair) acc[i] = *(const f32x4*)(dst + int64_t(p) * D + (f % F4) * 4);
+    }
+    for (int k = 0; k < nc; ++k) {
+      const DevContrib c = a.contribs[sg.c_off + k];
+      const int64_t Lj = a.tasks[c.j].L_local;
+      const float* src = a.src[t] + c.j * a.stride + ((int64_t(b) * Lj + c.local_start) * H + pair0) * D;
+#pragma unroll
+      for (int i = 0; i < NF; ++i) {
+        const int f = tid + 256 * i, p = f / F4;
+        if (p < npair) acc[i] += *(const f32x4*)(src + int64_t(p) * D + (f % F4) * 4);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < NF; ++i) {
+      const int f = tid + 256 * i, p = f / F4;
+      if (p < npair) *(f32x4*)(dst + int64_t(p) * D + (f % F4) * 4) = acc[i];
+    }
+  }
+}
+
 // fp32 result rounded to a 16-bit output dtype (nearest even): 8 elements
 // per thread, one 32-byte read and one 16-byte write.
 template <typename T>
@@ -180,6 +237,28 @@ hipError_t launch_combine(const CombineArgs& a, int64_t blocks, hipStream_t s) {
     case 192: hipLaunchKernelGGL(combine_kernel<192>, grid, dim3(256), 0, s, a); break;
     case 224: hipLaunchKernelGGL(combine_kernel<224>, grid, dim3(256), 0, s, a); break;
     case 256: hipLaunchKernelGGL(combine_kernel<256>, grid, dim3(256), 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace cqsa
+
+namespace cqsa {
+
+hipError_t launch_grad_merge(const GradMergeArgs& a, int64_t blocks, hipStream_t s) {
+  if (blocks <= 0 || a.B <= 0) return hipSuccess;
+  if (a.n_seg < 1 || blocks > 0x7fffffff || a.B > 65535) return hipErrorInvalidValue;
+  const dim3 grid(unsigned(blocks), unsigned(a.B));
+  switch (a.d) {
+    case 32: hipLaunchKernelGGL(grad_merge_kernel<32>, grid, dim3(256), 0, s, a); break;
+    case 64: hipLaunchKernelGGL(grad_merge_kernel<64>, grid, dim3(256), 0, s, a); break;
+    case 96: hipLaunchKernelGGL(grad_merge_kernel<96>, grid, dim3(256), 0, s, a); break;
+    case 128: hipLaunchKernelGGL(grad_merge_kernel<128>, grid, dim3(256), 0, s, a); break;
+    case 160: hipLaunchKernelGGL(grad_merge_kernel<160>, grid, dim3(256), 0, s, a); break;
+    case 192: hipLaunchKernelGGL(grad_merge_kernel<192>, grid, dim3(256), 0, s, a); break;
+    case 224: hipLaunchKernelGGL(grad_merge_kernel<224>, grid, dim3(256), 0, s, a); break;
+    case 256: hipLaunchKernelGGL(grad_merge_kernel<256>, grid, dim3(256), 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

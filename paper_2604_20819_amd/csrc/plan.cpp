@@ -120,6 +120,13 @@ cqsa_status validate_plan_args(int64_t L, int32_t H, int32_t d, const cqsa_plan_
     return bad(CQSA_ERR_INVALID_ARG, "tasks_per_slot must be in [0, 32]");
   if (o.tasks_per_slot > 1 && o.acc_on_device != 1)
     return bad(CQSA_ERR_UNSUPPORTED, "tasks_per_slot > 1 needs the accumulator on the device");
+  if (o.bwd_tasks_per_launch < 0 || o.bwd_tasks_per_launch > kMaxContrib)
+    return bad(CQSA_ERR_INVALID_ARG, "bwd_tasks_per_launch must be in [0, 32]");
+  if (o.bwd_tasks_per_launch > 1 &&
+      (o.inputs_on_device != 1 || o.read_in_place == 0 || o.acc_on_device == 0))
+    return bad(CQSA_ERR_UNSUPPORTED,
+               "bwd_tasks_per_launch > 1 needs device-resident inputs read in place and "
+               "device-resident outputs");
   if (o.read_in_place < -1 || o.read_in_place > 1)
     return bad(CQSA_ERR_INVALID_ARG, "read_in_place must be -1 (auto), 0 or 1");
   if (o.read_in_place == 1 && !o.inputs_on_device)
@@ -421,11 +428,29 @@ void pack_image(const std::vector<Task>& tasks, const SegmentCover& sc, int32_t 
     o.qorder = put(query_strip_order(k, causal, fwd_rows));
     o.dqorder = put(query_strip_order(k, causal, dq_rows));
     o.korder = put(key_strip_order(k, causal));
+    o.blocks = reserve(nb * sizeof(DevBlock));
+    for (size_t i = 0; i < nb; ++i) {
+      DevBlock x{k.blk_or[i], k.blk_and[i], 0, 0u};
+      std::memcpy(&x.row, im.data() + o.rows + i * 4, 4);
+      std::memcpy(im.data() + o.blocks + i * sizeof(DevBlock), &x, sizeof(x));
+    }
     DevTask d{k.L_local, int64_t(o.runs), int64_t(o.blk_or), int64_t(o.blk_and), int64_t(o.rows),
-              int64_t(o.qorder), int64_t(o.dqorder), int64_t(o.korder), int32_t(k.runs.size()), 0};
+              int64_t(o.qorder), int64_t(o.dqorder), int64_t(o.korder), int64_t(o.blocks),
+              int32_t(k.runs.size()), 0};
     std::memcpy(im.data() + hdr + t * sizeof(DevTask), &d, sizeof(d));
     offs->push_back(o);
   }
+  pack_groups(sc, H, groups, image);
+}
+
+void pack_groups(const SegmentCover& sc, int32_t H, std::vector<Group>* groups,
+                 std::vector<uint8_t>* image) {
+  std::vector<uint8_t>& im = *image;
+  auto reserve = [&](uint64_t bytes) {
+    const uint64_t at = im.size();
+    im.resize(align_up(at + bytes), 0);
+    return at;
+  };
   const size_t nseg = sc.cover.size();
   for (Group& g : *groups) {
     const int32_t t0 = int32_t(g.task0), t1 = int32_t(g.task0 + g.count);
@@ -456,8 +481,17 @@ void pack_image(const std::vector<Task>& tasks, const SegmentCover& sc, int32_t 
   }
 }
 
+bool bwd_batchable(const cqsa_plan_opts& o, int32_t depth) {
+  return depth > 0 && o.inputs_on_device && o.read_in_place == 1 && o.acc_on_device == 1;
+}
+
+uint64_t bwd_local_task_bytes(const Geometry& g, const cqsa_plan_opts& o, int64_t Lmax) {
+  return 3 * align_up(uint64_t(o.B) * uint64_t(Lmax) * uint64_t(g.H) * uint64_t(g.d) * 4);
+}
+
 Footprint footprint(const Geometry& g, const cqsa_plan_opts& o, int32_t depth,
-                    const std::vector<Task>& tasks, int32_t group_size, uint64_t image_bytes) {
+                    const std::vector<Task>& tasks, int32_t group_size, uint64_t image_bytes,
+                    int32_t bwd_group) {
   Footprint f;
   int64_t Lmax = 0;
   for (const Task& t : tasks) Lmax = std::max(Lmax, t.L_local);
@@ -486,12 +520,17 @@ Footprint footprint(const Geometry& g, const cqsa_plan_opts& o, int32_t depth,
   f.global_fwd = (o.acc_on_device && !direct && f.groups > 1) ? 2 * stat_full : 0;
   // D = rowsum(dO * O), and a device copy of a host-resident LSE
   f.global_bwd = stat_full + (o.acc_on_device == 1 ? 0 : stat_full);
+  // task-local gradients of one backward launch group of several tasks
+  f.bwd_group_size = std::max<int32_t>(1, bwd_group);
+  f.bwd_local = f.bwd_group_size > 1 ? uint64_t(f.bwd_group_size) * bwd_local_task_bytes(g, o, Lmax)
+                                     : 0;
   f.tables = align_up(image_bytes);
   const uint64_t subslots_fwd = uint64_t(fwd_subslots(ntask, f.group_size, o.n_slots));
   const uint64_t slots_bwd = uint64_t(std::min<int64_t>(o.n_slots, ntask));
   uint64_t peak_fwd = f.resident_fwd + subslots_fwd * f.slot_fwd + f.global_fwd + f.tables;
   uint64_t peak_bwd = o.with_backward
-                          ? f.resident_bwd + slots_bwd * f.slot_bwd + f.global_bwd + f.tables
+                          ? f.resident_bwd + slots_bwd * f.slot_bwd + f.global_bwd + f.bwd_local +
+                                f.tables
                           : 0;
   f.peak = std::max(peak_fwd, peak_bwd);
   return f;

@@ -46,6 +46,7 @@ struct TableOffsets {
   uint64_t qorder = 0;  // int32[n_strips] forward query strips, longest first
   uint64_t dqorder = 0; // int32[n_strips] dQ query strips, longest first
   uint64_t korder = 0;  // int32[n_strips] key strips, longest first
+  uint64_t blocks = 0;  // DevBlock[n_blocks] (OR, AND, row interleaved)
 };
 
 // A launch group: tasks [task0, task0 + count) are staged into one slot,
@@ -78,6 +79,8 @@ struct Footprint {
   uint64_t peak = 0;           // modelled peak device bytes
   int32_t group_size = 1;      // tasks per forward staging slot
   int64_t groups = 1;          // forward launch groups
+  int32_t bwd_group_size = 1;  // backward tasks per dQ and dK/dV launch
+  uint64_t bwd_local = 0;      // task-local gradients of one backward launch group
 };
 
 struct Geometry {
@@ -100,6 +103,8 @@ struct cqsa_plan_s {
   std::vector<uint8_t> packed;
   std::vector<cqsa::TableOffsets> table_off;
   std::vector<cqsa::Group> groups;
+  // backward launch groups (bwd_batched plans only; merge tables in `packed`)
+  std::vector<cqsa::Group> bwd_groups;
   // lazily computed census
   mutable std::once_flag census_once;
   mutable int64_t census[3] = {0, 0, 0};
@@ -134,9 +139,18 @@ LevelSet level_set(const cqsa_plan_opts& o, int32_t level);
 std::vector<Task> build_tasks(int64_t L, const cqsa_plan_opts& o, int32_t depth);
 
 // Footprint of running `tasks` under `o` with `group_size` tasks per forward
-// slot and a plan image of `image_bytes` (mirrors the runtime's allocations).
+// slot, `bwd_group` tasks per backward launch and a plan image of
+// `image_bytes` (mirrors the runtime's allocations).
 Footprint footprint(const Geometry& g, const cqsa_plan_opts& o, int32_t depth,
-                    const std::vector<Task>& tasks, int32_t group_size, uint64_t image_bytes);
+                    const std::vector<Task>& tasks, int32_t group_size, uint64_t image_bytes,
+                    int32_t bwd_group = 1);
+
+// Whether the backward can run several tasks per launch with task-local
+// gradients and a gather-merge: inputs read in place, device-resident
+// outputs and gradients, depth >= 1.
+bool bwd_batchable(const cqsa_plan_opts& o, int32_t depth);
+// Bytes of one backward task's local dQ, dK, dV (each sized for the longest task).
+uint64_t bwd_local_task_bytes(const Geometry& g, const cqsa_plan_opts& o, int64_t Lmax);
 
 // True when the forward writes O directly from one undecomposed launch.
 bool direct_forward(const cqsa_plan_opts& o, int32_t depth);
@@ -171,6 +185,10 @@ bool bwd_staged(const cqsa_plan_opts& o, int32_t depth);
 void pack_image(const std::vector<Task>& tasks, const SegmentCover& sc, int32_t H, bool causal,
                 int32_t fwd_rows, int32_t dq_rows, std::vector<Group>* groups,
                 std::vector<uint8_t>* image, std::vector<TableOffsets>* offs);
+// Appends the segments and contributions of `groups` to the image (filling
+// their offsets and block counts for H heads).
+void pack_groups(const SegmentCover& sc, int32_t H, std::vector<Group>* groups,
+                 std::vector<uint8_t>* image);
 
 // Query rows per work group of the inner forward and dQ kernels.
 int fwd_rows_per_wg(cqsa_dtype dt, int d);

@@ -34,8 +34,18 @@ struct DevTask {
   int64_t dqorder_off;// int32[ceil(L_local / R)] dQ query strips of R rows, R the dQ
                       // kernel's strip height (dq_rows_per_wg), most live key tiles first
   int64_t korder_off; // int32[ceil(L_local / kStrip)] key strips, most live query tiles first
+  int64_t sum_off;    // DevBlock[ceil(L_local / 64)]: the three block tables above, interleaved
   int32_t n_runs;
   int32_t pad;
+};
+
+// One 64-token block's OR, AND and row, read with one 16-byte load (the
+// backward kernels' tile windows).
+struct DevBlock {
+  uint32_t bor;
+  uint32_t band;
+  int32_t row;
+  uint32_t pad;
 };
 
 // Keys of the strip a dK/dV work group owns.  Strips of a (task, b, h) run in
@@ -72,7 +82,8 @@ struct DevContrib {
 };
 
 static_assert(sizeof(DevRun) == 32, "DevRun layout");
-static_assert(sizeof(DevTask) == 72, "DevTask layout");
+static_assert(sizeof(DevTask) == 80, "DevTask layout");
+static_assert(sizeof(DevBlock) == 16, "DevBlock layout");
 static_assert(sizeof(DevSeg) == 40, "DevSeg layout");
 static_assert(sizeof(DevContrib) == 16, "DevContrib layout");
 

@@ -151,11 +151,13 @@ def test_read_in_place_choice_and_errors():
     with pytest.raises(cq.CqsaError) as e:
         cq.cqsa_plan(4096, 4, 64, False, 0, o)
     assert e.value.status == -1
-    # in place the backward holds no staging slots: the forward's sub-slots
-    # are the peak, and they shrink by the three staged inputs
+    # in place, one backward task per launch holds no staging slots: the
+    # forward's sub-slots are the peak, and they shrink by the three staged
+    # inputs
     kw = dict(B=2, with_backward=True, depth=1)
-    a = cq.cqsa_plan(65536, 16, 128, True, 0, cq.make_opts(**kw))
+    a = cq.cqsa_plan(65536, 16, 128, True, 0, cq.make_opts(bwd_tasks_per_launch=1, **kw))
     b = cq.cqsa_plan(65536, 16, 128, True, 0, cq.make_opts(read_in_place=False, **kw))
+    assert a.bwd_tasks_per_launch == 1 and b.bwd_tasks_per_launch == 1
     assert a.modelled_device_bytes < b.modelled_device_bytes
 
 
@@ -166,7 +168,8 @@ def test_struct_layouts_match_the_header(tmp_path):
     import subprocess
     if shutil.which("gcc") is None:
         pytest.skip("gcc not available")
-    checks = {"cqsa_plan_opts": ["B", "interest", "tasks_per_slot", "n_level_sets", "level_sets"],
+    checks = {"cqsa_plan_opts": ["B", "interest", "tasks_per_slot", "n_level_sets", "level_sets",
+                                 "out16", "bwd_tasks_per_launch"],
               "cqsa_interest_set": ["c", "l", "interest"],
               "cqsa_tensor": ["data", "B", "d"], "cqsa_task": ["quorum", "runs", "block_and"],
               "cqsa_run": ["global_start", "bits"],
@@ -257,32 +260,43 @@ def test_workload_depths(L, H, d, causal, budget, kw, want):
             assert q.modelled_device_bytes > budget
 
 
-def _image_bytes(p, g):
+def _image_bytes(p, g, bwd_g=1):
     """Plan image size from the layout the planner documents: DevTask records
-    (72 bytes), per-task runs, block summaries (OR, AND), block row table and
+    (80 bytes), per-task runs, block summaries (OR, AND), block row table,
     the three strip orders (one int32 per strip: the forward's 256-query
-    strips at bf16 d = 128, and the backward's 128-token strips), per-group
-    segments and contributions."""
+    strips at bf16 d = 128, and the backward's 128-token strips) and the
+    interleaved block records (16 bytes per block), then per forward group
+    the segments and contributions, and per backward launch group (when it
+    holds several tasks) those of its tokens."""
     al = lambda x: (x + 255) // 256 * 256
     tasks = [p.task(t) for t in range(p.num_tasks)]
-    size = al(len(tasks) * 72)
+    size = al(len(tasks) * 80)
     for tk in tasks:
-        size += al(len(tk["runs"]) * 32) + 3 * al(len(tk["block_or"]) * 4)
+        nb = len(tk["block_or"])
+        size += al(len(tk["runs"]) * 32) + 3 * al(nb * 4) + al(nb * 16)
         size += al(-(-tk["L_local"] // 256) * 4) + 2 * al(-(-tk["L_local"] // 128) * 4)
     bounds = sorted({0, p.L} | {r[0] for tk in tasks for r in tk["runs"]}
                     | {r[0] + r[1] for tk in tasks for r in tk["runs"]})
     segs = list(zip(bounds[:-1], bounds[1:]))
     holders = [[t for t, tk in enumerate(tasks)
                 if any(r[0] <= s0 < r[0] + r[1] for r in tk["runs"])] for s0, _ in segs]
-    for t0 in range(0, len(tasks), g):
-        final = t0 + g >= len(tasks)
-        n_seg = n_con = 0
-        for hs in holders:
-            k = sum(1 for t in hs if t0 <= t < t0 + g)
-            if k or final:
-                n_seg += 1
-                n_con += k
-        size += al(n_seg * 40) + al(n_con * 16)
+
+    def groups(gs, final_all):
+        n = 0
+        for t0 in range(0, len(tasks), gs):
+            final = final_all and t0 + gs >= len(tasks)
+            n_seg = n_con = 0
+            for hs in holders:
+                k = sum(1 for t in hs if t0 <= t < t0 + gs)
+                if k or final:
+                    n_seg += 1
+                    n_con += k
+            n += al(n_seg * 40) + al(n_con * 16)
+        return n
+
+    size += groups(g, True)
+    if bwd_g > 1:
+        size += groups(bwd_g, False)
     return size
 
 
@@ -310,6 +324,54 @@ def test_footprint_model_closed_form(tps, want_g, subslots, in_place):
     running_l = 2 * al(B * H * L * 4) if groups > 1 else 0
     want = resident + subslots * sub + running_l + al(_image_bytes(p, want_g))
     assert p.modelled_device_bytes == want
+
+
+def test_backward_launch_groups():
+    """Backward tasks per launch.  Inputs read in place with device-resident
+    gradients and with_backward: every task (up to 32) in one dQ and one dK/dV
+    launch, their task-local fp32 dQ, dK, dV (3 x B x L_max x H x d x 4 bytes
+    each) counted in the backward's peak, which is then the modelled one;
+    reduced until a capped budget fits.  One per launch otherwise."""
+    al = lambda x: (x + 255) // 256 * 256
+    L, H, d, B = 32768, 16, 128, 1
+    p = cq.cqsa_plan(L, H, d, False, 0, cq.make_opts(depth=1, with_backward=True))
+    assert p.bwd_tasks_per_launch == 7
+    Lmax = max(p.task(t)["L_local"] for t in range(p.num_tasks))
+    f32 = al(B * L * H * d * 4)
+    resident = 4 * al(B * L * H * d * 2) + f32 + al(B * H * L * 4) + 3 * f32
+    local = 7 * 3 * al(B * Lmax * H * d * 4)
+    want = resident + al(B * H * L * 4) + local + al(_image_bytes(p, 7, 7))
+    assert p.modelled_device_bytes == want
+    one = cq.cqsa_plan(L, H, d, False, 0, cq.make_opts(depth=1, with_backward=True,
+                                                       bwd_tasks_per_launch=1))
+    assert one.bwd_tasks_per_launch == 1 and one.modelled_device_bytes < want
+    # a budget between them: fewer tasks per launch, the same depth
+    budget = (one.modelled_device_bytes + want) // 2
+    mid = cq.cqsa_plan(L, H, d, False, budget, cq.make_opts(with_backward=True))
+    assert mid.depth == 1 and 1 < mid.bwd_tasks_per_launch < 7
+    assert mid.modelled_device_bytes <= budget
+    # 49 tasks at depth 2: 32 per launch
+    p = cq.cqsa_plan(L, H, d, False, 0, cq.make_opts(depth=2, with_backward=True))
+    assert p.bwd_tasks_per_launch == 32
+    # forced
+    p = cq.cqsa_plan(L, H, d, False, 0, cq.make_opts(depth=1, with_backward=True,
+                                                     bwd_tasks_per_launch=3))
+    assert p.bwd_tasks_per_launch == 3
+    # not batched: staged inputs, host accumulator, no with_backward, undecomposed
+    for kw in (dict(read_in_place=False), dict(acc_on_device=False),
+               dict(inputs_on_device=False, acc_on_device=False)):
+        p = cq.cqsa_plan(L, H, d, False, 0, cq.make_opts(depth=1, with_backward=True, **kw))
+        assert p.bwd_tasks_per_launch == 1, kw
+    assert cq.cqsa_plan(L, H, d, False, 0, cq.make_opts(depth=1)).bwd_tasks_per_launch == 1
+    assert cq.cqsa_plan(L, H, d, False, 0, cq.make_opts(
+        depth=0, with_backward=True)).bwd_tasks_per_launch == 1
+    # refused: out of range, or forced above 1 where it cannot apply
+    for kw, status in [(dict(bwd_tasks_per_launch=33), -1), (dict(bwd_tasks_per_launch=-1), -1),
+                       (dict(bwd_tasks_per_launch=2, read_in_place=False), -2),
+                       (dict(bwd_tasks_per_launch=2, acc_on_device=False), -2)]:
+        with pytest.raises(cq.CqsaError) as e:
+            cq.cqsa_plan(L, H, d, False, 0, cq.make_opts(depth=1, with_backward=True, **kw))
+        assert e.value.status == status and "bwd_tasks_per_launch" in str(e.value)
 
 
 def test_group_size_rules():

@@ -179,6 +179,47 @@ def test_backward_guardrail():
     _check_grads(got, oracle_grads(Q, K, V, dO, True), "bf16")
 
 
+def test_batched_backward_guardrail():
+    """Read in place, the backward's resident task working sets are the
+    task-local gradients of one launch group: a refused workspace halves the
+    tasks per launch (7 -> 3), and since every grouping adds the same values in
+    the same order the gradients keep their bits."""
+    need_gpu()
+    L, H, d = 2500, 2, 128
+    Q, K, V, dO = synth.make_inputs(45, 1, L, H, d, "bf16", with_dO=True)
+    q, k, v, do = (x.cuda() for x in (Q, K, V, dO))
+    plan = cq.cqsa_plan(L, H, d, True, 0, cq.make_opts(dtype="bf16", with_backward=True))
+    assert plan.reads_in_place == 1 and plan.bwd_tasks_per_launch == 7
+    O = torch.empty((1, L, H, d), dtype=torch.float32, device="cuda")
+    LSE = torch.empty((1, H, L), dtype=torch.float32, device="cuda")
+    cq.cqsa_forward(plan, q, k, v, O, LSE)
+
+    def grads():
+        g = [torch.empty((1, L, H, d), dtype=torch.float32, device="cuda") for _ in range(3)]
+        cq.cqsa_backward(plan, q, k, v, O, LSE, do, *g)
+        torch.cuda.synchronize()
+        return [x.cpu() for x in g]
+
+    cq.cqsa_set_timing(True)
+    try:
+        ref = grads()
+        st0 = cq.cqsa_last_stats()
+        full = st0["workspace_bytes"]
+        with LimitedAllocator(full - 1) as a:
+            say(f"guardrail batched backward: workspace {full} B, limit {full - 1} B")
+            got = grads()
+            st = cq.cqsa_last_stats()
+            assert a.refused >= 1 and st["guard_steps"] == 1 and st["workspace_bytes"] < full
+    finally:
+        cq.cqsa_set_timing(False)
+    say(f"  fallbacks {st['guard_steps']}, depth {st['depth']}, resident {st0['resident_tasks']}"
+        f" -> {st['resident_tasks']}")
+    assert st0["resident_tasks"] == 7 and st["resident_tasks"] == 3 and st["depth"] == 1
+    for g, r in zip(got, ref):
+        assert torch.equal(g, r)
+    _check_grads(got, oracle_grads(Q, K, V, dO, True), "bf16")
+
+
 def test_host_resident_backward_guardrail():
     """With every tensor in host memory the backward's staging slots hold the
     task's inputs and its own gradients; a workspace refusal drops to one

@@ -97,7 +97,10 @@ def test_backward_in_place_equals_staged(dt, B, L, H, d, causal, depth):
         cq.cqsa_set_timing(False)
     assert got[-1].reads_in_place == 1 and ref[-1].reads_in_place == 0
     assert st["d2d_bytes"] == 0 and st0["d2d_bytes"] > 0
-    assert st["resident_tasks"] == 0 and st0["resident_tasks"] > 0
+    # in place, the task-local gradients of a launch's tasks are what the
+    # workspace holds (none with one task per launch)
+    gs = got[-1].bwd_tasks_per_launch
+    assert st["resident_tasks"] == (gs if gs > 1 else 0) and st0["resident_tasks"] > 0
     for name, g, r in zip(("O", "LSE", "dQ", "dK", "dV"), got[:5], ref[:5]):
         assert torch.equal(g, r), name
     assert all(np.isfinite(g.numpy()).all() for g in got[2:5])
