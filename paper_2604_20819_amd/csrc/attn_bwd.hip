@@ -127,16 +127,15 @@ __global__ void __launch_bounds__(64 * dq_waves<D>(), (lds_row_elems<D>() > 128 
     uint32_t an, on;
     int32_t row;
   };
+  // The window's words stay as loaded until pick() uses them after the
+  // tile's compute: arithmetic on them, or a default written over a
+  // conditionally loaded register, would make the wave wait here for the
+  // load (and, in order, for every tile load issued after it).  Lanes past
+  // the last tile read the last tile's record; pick() ignores them.
   auto window = [&](int k0) {
-    const int k = k0 + lane;
-    Window w{0xFFFFFFFFu, 0u, 0};
-    if (k < nkt) {
-      const u32x4 x = *(const u32x4*)(blks + k);  // one DevBlock
-      w.on = x[0];
-      w.an = x[1];
-      w.row = in_place ? int32_t(x[2]) : k * BN;
-    }
-    return w;
+    const int k = k0 + lane < nkt ? k0 + lane : nkt - 1;
+    const u32x3 x = *(const u32x3*)(blks + k);
+    return Window{x[1], x[0], int32_t(x[2])};
   };
   auto pick = [&](int k0, const Window& w, uint32_t& kor_out, uint32_t& kand_out,
                   int32_t& row_out) -> int {
@@ -147,7 +146,7 @@ __global__ void __launch_bounds__(64 * dq_waves<D>(), (lds_row_elems<D>() > 128 
     const int i = __builtin_ctzll(m);
     kand_out = __builtin_amdgcn_readlane(w.an, i);
     kor_out = __builtin_amdgcn_readlane(w.on, i);
-    row_out = __builtin_amdgcn_readlane(w.row, i);
+    row_out = in_place ? __builtin_amdgcn_readlane(w.row, i) : (k0 + i) * BN;
     return k0 + i;
   };
   auto next_live = [&](int kt, uint32_t& kor_out, uint32_t& kand_out, int32_t& row_out) -> int {
@@ -349,12 +348,24 @@ __global__ void __launch_bounds__(64 * dq_waves<D>(), (lds_row_elems<D>() > 128 
 // accumulating its columns; the halves share the work group's Q/dO tiles and
 // V rows, and the 8 waves run two per SIMD.
 template <int D> constexpr int dkdv_splits() { return D >= 160 ? 2 : 1; }
+// Groups of 32 keys per work group.  At d = 96 and 128 a work group of 8
+// waves owns a 256-key strip: each 32-query tile it loads (Q and dO rows)
+// then feeds twice the products, which halves the tile traffic per product;
+// the LDS (a 64 KB V strip and the double-buffered tiles) leaves one work
+// group per CU, two waves per SIMD as before.  Elsewhere 4 groups (a 128-key
+// strip).
+template <int D> constexpr int dkdv_key_waves() { return (D == 96 || D == 128) ? 8 : 4; }
+template <int D> constexpr int dkdv_waves() { return dkdv_key_waves<D>() * dkdv_splits<D>(); }
+template <int D> constexpr int dkdv_wgs_per_cu() {
+  return (lds_row_elems<D>() > 128 || dkdv_key_waves<D>() > 4) ? 1 : 2;
+}
 
 template <typename E, int D, bool LOCAL>
-__global__ void __launch_bounds__(256 * dkdv_splits<D>(), (lds_row_elems<D>() > 128 ? 1 : 2)) attn_bwd_dkdv(const BwdArgs a) {
+__global__ void __launch_bounds__(64 * dkdv_waves<D>(), dkdv_wgs_per_cu<D>()) attn_bwd_dkdv(const BwdArgs a) {
   // 32-query tiles (two per 64-token summary block) keep the registers and
-  // LDS within two work groups per CU (one above d = 128)
-  constexpr int BK = 128, BQ = 32;
+  // LDS within two waves per SIMD
+  constexpr int KW = dkdv_key_waves<D>();
+  constexpr int BK = 32 * KW, BQ = 32;
   // Q and dO tiles: rows of DP elements (d padded as in the forward) with
   // the forward's swizzle (chunk ch of row r in slot ch ^ swz(r)),
   // conflict-free for the row reads and the transpose reads; filled by
@@ -363,18 +374,23 @@ __global__ void __launch_bounds__(256 * dkdv_splits<D>(), (lds_row_elems<D>() > 
   constexpr int P2 = DP * 2;
   constexpr int DK = D / 16, DB = D / 32, CHUNKS = DP / 8;
   constexpr int NSPLIT = dkdv_splits<D>(), DBO = (DB + NSPLIT - 1) / NSPLIT;
-  constexpr int WAVES = 4 * NSPLIT, NT = 64 * WAVES;
+  constexpr int WAVES = KW * NSPLIT, NT = 64 * WAVES;
   constexpr int RPI = 64 / CHUNKS, NDMA = BQ / RPI / WAVES;
+  static_assert(NDMA >= 1 && NDMA * RPI * WAVES == BQ, "tile loads");
+  static_assert(2 * NDMA < 16, "vmcnt immediate");
   typedef typename E::vec8 vec8;
   auto swz = [](int r) { return 2 * (r & 3) + ((r >> 2) & 1); };
 
-  // double-buffered query tiles (Q, dO) with their per-query statistics
-  __shared__ __attribute__((aligned(1024))) char qs[2][BQ * P2];
-  __shared__ __attribute__((aligned(1024))) char os[2][BQ * P2];
+  // a ring of NBUF query tiles (Q, dO) with their per-query statistics,
+  // filled NBUF - 1 tiles ahead of the compute (two ahead for the 256-key
+  // strips, whose single work group per CU leaves the LDS for a third tile)
+  constexpr int NBUF = KW == 8 ? 3 : 2, AHEAD = NBUF - 1;
+  __shared__ __attribute__((aligned(1024))) char qs[NBUF][BQ * P2];
+  __shared__ __attribute__((aligned(1024))) char os[NBUF][BQ * P2];
   __shared__ __attribute__((aligned(1024))) char vs[BK * P2];   // the strip's V rows, swizzled
-  __shared__ __attribute__((aligned(16))) float lse_s[2][BQ];
-  __shared__ __attribute__((aligned(16))) float d_s[2][BQ];
-  __shared__ __attribute__((aligned(16))) uint32_t qbits_s[2][BQ];
+  __shared__ __attribute__((aligned(16))) float lse_s[NBUF][BQ];  // natural-log LSE
+  __shared__ __attribute__((aligned(16))) float d_s[NBUF][BQ];
+  __shared__ __attribute__((aligned(16))) uint32_t qbits_s[NBUF][BQ];
   __shared__ DevRun runs_s[kMaxRuns];
 
   const int tid = threadIdx.x, lane = tid & 63, half = lane >> 5;
@@ -389,8 +405,8 @@ __global__ void __launch_bounds__(256 * dkdv_splits<D>(), (lds_row_elems<D>() > 
   // from 32-column block db0 (both fixed at 4 waves, no split)
   const int kw = NSPLIT > 1 ? (wave & 3) : wave;
   const int db0 = NSPLIT > 1 ? (wave >> 2) * DBO : 0;
-  // key strips in the task's launch order (most live query tiles first)
-  static_assert(BK == kStrip, "strip tables are built for kStrip-row strips");
+  // key strips in the task's launch order (most live query tiles first; the
+  // plan builds this table for BK-row strips, BK = dkdv_rows_per_wg)
   const int strip = ((const int32_t*)(a.tab + tk.korder_off))[work % nstrips];
   const int h = int((work / nstrips) % a.H);
   const int b = int(work / (nstrips * a.H));
@@ -437,12 +453,14 @@ __global__ void __launch_bounds__(256 * dkdv_splits<D>(), (lds_row_elems<D>() > 
   }
   {
     // the strip's rows are consecutive from vrow unless, read in place, one
-    // of its two blocks crosses a run boundary or they lie in different runs
-    const int vb0 = strip * 2, vb1 = ((strip * BK + BK < L ? strip * BK + BK : L) - 1) >> 6;
+    // of its blocks crosses a run boundary or they lie in different runs
+    const int vb0 = strip * (BK / 64), vb1 = ((strip * BK + BK < L ? strip * BK + BK : L) - 1) >> 6;
     int32_t vrow = strip * BK;
     if (in_place) {
-      const int32_t r0 = blks[vb0].row, r1 = blks[vb1].row;
-      vrow = (r0 != kNoRow && (vb1 == vb0 || r1 == r0 + 64)) ? r0 : kNoRow;
+      const int32_t r0 = blks[vb0].row;
+      bool one = r0 != kNoRow;
+      for (int vb = vb0 + 1; vb <= vb1; ++vb) one = one && blks[vb].row == r0 + 64 * (vb - vb0);
+      vrow = one ? r0 : kNoRow;
     }
     const int64_t vrows = int64_t(L) - int64_t(strip) * BK;
     const __amdgpu_buffer_rsrc_t rv =
@@ -465,9 +483,12 @@ __global__ void __launch_bounds__(256 * dkdv_splits<D>(), (lds_row_elems<D>() > 
   }
 
   const int lastk_wg = (strip * BK + BK < L ? strip * BK + BK : L) - 1;
-  const int kb0 = strip * 2, kb1 = lastk_wg / 64;
-  const uint32_t kor = blks[kb0].bor | blks[kb1].bor;
-  const uint32_t kand = blks[kb0].band & blks[kb1].band;
+  const int kb0 = strip * (BK / 64), kb1 = lastk_wg / 64;
+  uint32_t kor = 0u, kand = 0xFFFFFFFFu;
+  for (int kb = kb0; kb <= kb1; ++kb) {
+    kor |= blks[kb].bor;
+    kand &= blks[kb].band;
+  }
   const bool wave_live = k0w < L;
   const int wk1 = wave_live ? (k0w + 31 < L ? k0w + 31 : L - 1) : 0;
   const uint32_t wor = wave_live ? blks[k0w / 64].bor : 0u;
@@ -484,24 +505,17 @@ __global__ void __launch_bounds__(256 * dkdv_splits<D>(), (lds_row_elems<D>() > 
     uint32_t an, on;
     int32_t row;
   };
+  // raw words until pick(), as in the dQ kernel (tile t lies in block t / 2)
   auto window = [&](int t0) {
-    const int t = t0 + lane;
-    Window w{0xFFFFFFFFu, 0u, 0};
-    if (t < nqt) {
-      const u32x4 x = *(const u32x4*)(blks + (t >> 1));  // one DevBlock
-      w.on = x[0];
-      w.an = x[1];
-      if (in_place) {
-        const int32_t r = int32_t(x[2]);
-        w.row = r != kNoRow ? r + (t & 1) * BQ : kNoRow;
-      } else {
-        w.row = t * BQ;
-      }
-    }
-    return w;
+    const int t = t0 + lane < nqt ? t0 + lane : nqt - 1;
+    const u32x3 x = *(const u32x3*)(blks + (t >> 1));
+    return Window{x[1], x[0], int32_t(x[2])};
   };
+  // row_out: the tile's first row in the Q and dO the kernel reads (local
+  // when staged); grow_out: its first global row when its queries lie in one
+  // run (for the statistics), else kNoRow
   auto pick = [&](int t0, const Window& w, uint32_t& qor_out, uint32_t& qand_out,
-                  int32_t& row_out) -> int {
+                  int32_t& row_out, int32_t& grow_out) -> int {
     const int t = t0 + lane;
     const bool ok = t < nqt && !(causal && t * BQ + BQ - 1 < first_key) && (kand & w.an) == 0u;
     const uint64_t m = __builtin_amdgcn_ballot_w64(ok);
@@ -509,40 +523,70 @@ __global__ void __launch_bounds__(256 * dkdv_splits<D>(), (lds_row_elems<D>() > 
     const int i = __builtin_ctzll(m);
     qand_out = __builtin_amdgcn_readlane(w.an, i);
     qor_out = __builtin_amdgcn_readlane(w.on, i);
-    row_out = __builtin_amdgcn_readlane(w.row, i);
+    const int32_t r = __builtin_amdgcn_readlane(w.row, i);
+    const int32_t grow = r != kNoRow ? r + ((t0 + i) & 1) * BQ : kNoRow;
+    row_out = in_place ? grow : (t0 + i) * BQ;
+    grow_out = grow;
     return t0 + i;
   };
-  auto next_live = [&](int t, uint32_t& qor_out, uint32_t& qand_out, int32_t& row_out) -> int {
+  auto next_live = [&](int t, uint32_t& qor_out, uint32_t& qand_out, int32_t& row_out,
+                       int32_t& grow_out) -> int {
     for (; t < nqt; t += 64) {
-      const int r = pick(t, window(t), qor_out, qand_out, row_out);
+      const int r = pick(t, window(t), qor_out, qand_out, row_out, grow_out);
       if (r >= 0) return r;
     }
     return nqt;
   };
 
-  // Query-tile loads for the next tile, issued right after a tile barrier:
-  // Q and dO rows through per-tile buffer resources (rows past the task read
-  // as zero) straight into LDS, and, for the first BQ threads, the query's
-  // global LSE (log2 units), D and group bits into registers (LSE = +inf
-  // past the task gives P = 0), stored to LDS after the compute.
-  float lse_r = INFINITY, d_r = 0.f;
-  auto gload = [&](int buf, int qt, int32_t trow) {
+  // Query-tile loads, issued right after a tile barrier, all straight into
+  // LDS with no register results, so nothing waits for them before the
+  // barrier of the iteration that computes the tile: first, for the first BQ
+  // threads, the queries' global LSE and D (rows past the task read zero:
+  // their Q and dO rows are zero, so they add nothing), then the Q and dO
+  // rows through per-tile buffer resources (rows past the task read zero).
+  // per-lane DMA offsets kept in registers across the tile loop (a register
+  // a DMA load addressed must not be rewritten while the load is in flight,
+  // so per-tile temporaries would make the wave wait for it)
+  uint32_t goff[NDMA];
+#pragma unroll
+  for (int j = 0; j < NDMA; ++j) {
+    const int row = RPI * (NDMA * wave + j) + lane / CHUNKS;
+    goff[j] = uint32_t((row * rs + ((lane % CHUNKS) ^ swz(row)) * 8) * 2);
+  }
+  const uint32_t soff = uint32_t(lane) * 4;
+  auto gload = [&](int buf, int qt, int32_t trow, int32_t grow) {
+    if (tid < BQ) {
+      lds_ptr lse_d = (lds_ptr)lse_s[buf], d_d = (lds_ptr)d_s[buf];
+      if (grow != kNoRow) {
+        // the tile's queries are consecutive global rows from grow
+        const int64_t n = int64_t(L) - int64_t(qt) * BQ;
+        const __amdgpu_buffer_rsrc_t rl = row_rsrc(a.lse + stat_base + grow, 1, 0, (n < BQ ? n : BQ) * 4);
+        const __amdgpu_buffer_rsrc_t rd = row_rsrc(a.D + stat_base + grow, 1, 0, (n < BQ ? n : BQ) * 4);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rl, lse_d, 4, soff, 0, 0, 0);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rd, d_d, 4, soff, 0, 0, 0);
+      } else {
+        const __amdgpu_buffer_rsrc_t rl = row_rsrc(a.lse + stat_base, 1, 0, a.Lg * 4);
+        const __amdgpu_buffer_rsrc_t rd = row_rsrc(a.D + stat_base, 1, 0, a.Lg * 4);
+        const int q = qt * BQ + tid;
+        const uint32_t so = q < L ? uint32_t(run_global(runs_s, n_runs, q) * 4) : kOobOffset;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rl, lse_d, 4, so, 0, 0, 0);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rd, d_d, 4, so, 0, 0, 0);
+        // this rare path's offsets are temporaries: wait here, so that the
+        // compiler need not make every later iteration wait before reusing
+        // their registers
+        __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+      }
+    }
     if (trow != kNoRow) {
-      // consecutive rows from trow; the per-lane offsets are recomputed per
-      // tile from an opaque copy of the lane index (kept out of registers
-      // across the tile loop)
+      // consecutive rows from trow
       const int64_t rows = int64_t(L) - int64_t(qt) * BQ;
       const __amdgpu_buffer_rsrc_t rq = row_rsrc(Qg + int64_t(trow) * rs, rows, rs * 2, D * 2);
       const __amdgpu_buffer_rsrc_t ro = row_rsrc(Og + int64_t(trow) * rs, rows, rs * 2, D * 2);
-      int ln = lane;
-      asm volatile("" : "+v"(ln));
 #pragma unroll
       for (int j = 0; j < NDMA; ++j) {
-        const int row = RPI * (NDMA * wave + j) + ln / CHUNKS;
-        const uint32_t go = uint32_t((row * rs + ((ln % CHUNKS) ^ swz(row)) * 8) * 2);
         const int off = (NDMA * wave + j) * 1024;
-        buf_load16_lds(rq, qs[buf] + off, go);
-        buf_load16_lds(ro, os[buf] + off, go);
+        buf_load16_lds(rq, qs[buf] + off, goff[j]);
+        buf_load16_lds(ro, os[buf] + off, goff[j]);
       }
     } else {
       // across a run boundary: per-lane rows from the slice base
@@ -563,25 +607,13 @@ __global__ void __launch_bounds__(256 * dkdv_splits<D>(), (lds_row_elems<D>() > 
         buf_load16_lds(rq, qs[buf] + off, vo);
         buf_load16_lds(ro, os[buf] + off, vo);
       }
-    }
-    if (tid < BQ) {
-      const int q = qt * BQ + tid;
-      lse_r = INFINITY;
-      d_r = 0.f;
-      if (q < L) {
-        const int64_t g = run_global(runs_s, n_runs, q);
-        lse_r = a.lse[stat_base + g] * kLog2e;
-        d_r = a.D[stat_base + g];
-      }
+      __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0), as for the statistics
     }
   };
-  // the group bits come from the runs in LDS here rather than with the loads
-  // (one register fewer across the tile's compute)
+  // the group bits come from the runs in LDS
   auto sstore = [&](int buf, int qt) {
     if (tid < BQ) {
       const int q = qt * BQ + tid;
-      lse_s[buf][tid] = lse_r;
-      d_s[buf][tid] = d_r;
       qbits_s[buf][tid] = q < L ? run_bits(runs_s, n_runs, q) : 0u;
     }
   };
@@ -598,25 +630,42 @@ __global__ void __launch_bounds__(256 * dkdv_splits<D>(), (lds_row_elems<D>() > 
   __syncthreads();  // runs_s visible
   const uint32_t kbits = kvalid ? run_bits(runs_s, n_runs, mykey) : 0u;
 
-  uint32_t qor = 0u, qand = 0u, nor = 0u, nand = 0u;
-  int32_t qrow = 0, nrow = 0;
-  int qt = next_live(causal ? first_key / BQ : 0, qor, qand, qrow);
-  if (qt < nqt) {
-    gload(0, qt, qrow);
-    sstore(0, qt);
+  // tl[0] is the tile being computed, tl[1 .. AHEAD] the next live ones
+  // (nqt: none); tor, tand, trw hold their block summaries and first rows
+  int tl[NBUF];
+  uint32_t tor[NBUF], tand[NBUF];
+  int32_t trw[NBUF], tgr[NBUF];
+  tl[0] = next_live(causal ? first_key / BQ : 0, tor[0], tand[0], trw[0], tgr[0]);
+#pragma unroll
+  for (int k = 1; k < NBUF; ++k) {
+    tor[k] = tand[k] = 0u;
+    trw[k] = tgr[k] = 0;
+    tl[k] = tl[k - 1] < nqt ? next_live(tl[k - 1] + 1, tor[k], tand[k], trw[k], tgr[k]) : nqt;
   }
-  int qn = qt < nqt ? next_live(qt + 1, nor, nand, nrow) : nqt;
+#pragma unroll
+  for (int k = 0; k < AHEAD; ++k)
+    if (tl[k] < nqt) {
+      gload(k, tl[k], trw[k], tgr[k]);
+      sstore(k, tl[k]);
+    }
   int buf = 0;
-  while (qt < nqt) {
-    // this wave's tile loads have landed; after the barrier every wave's
-    // have, and every wave is done with the other buffers
-    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
-    lds_barrier();
-    // summary window after qn (used after the compute), then the loads of qn
-    const int qc = qn + 1;
-    const Window cw = window(qc);
-    if (qn < nqt) gload(buf ^ 1, qn, nrow);
+  while (tl[0] < nqt) {
+    const int qt = tl[0];
+    // this wave's loads of tile qt have landed: only the loads of the tiles
+    // after it, 2 NDMA per tile (those of wave 0 follow its two statistics
+    // loads, which are older), may still be in flight.  After the barrier
+    // every wave's have, and every wave is done with the buffer refilled next.
+    if (AHEAD == 2 && tl[1] < nqt)
+      __builtin_amdgcn_s_waitcnt(0x0F70 | (2 * NDMA));  // vmcnt(2 NDMA)
+    else
+      __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+    lds_barrier_dma_in_flight();
+    // the loads of the last tile ahead
+    const int qc = tl[AHEAD] + 1;
+    const int bl = (buf + AHEAD) % NBUF;
+    if (tl[AHEAD] < nqt) gload(bl, tl[AHEAD], trw[AHEAD], tgr[AHEAD]);
     const int q0 = qt * BQ;
+    const uint32_t qor = tor[0], qand = tand[0];
     const bool wfull = !wave_live || (wand & qand) != 0u || (causal && q0 + BQ - 1 < k0w);
     if (!wfull) {
       const bool wclear = (wor & qor) == 0u && (!causal || q0 >= wk1);
@@ -650,7 +699,7 @@ __global__ void __launch_bounds__(256 * dkdv_splits<D>(), (lds_row_elems<D>() > 
 #pragma unroll
           for (int ii = 0; ii < 2; ++ii) {
             const int ql = 32 * qb + 8 * (2 * sub + ii) + 4 * half;
-            const f32x4 l4 = *(const f32x4*)(&lse_s[buf][ql]);
+            const f32x4 l4 = *(const f32x4*)(&lse_s[buf][ql]) * kLog2e;
             const f32x4 d4 = *(const f32x4*)(&d_s[buf][ql]);
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
@@ -688,22 +737,45 @@ __global__ void __launch_bounds__(256 * dkdv_splits<D>(), (lds_row_elems<D>() > 
     }
     int qc2 = nqt;
     uint32_t or2 = 0u, and2 = 0u;
-    int32_t row2 = 0;
-    if (qn < nqt) {
-      sstore(buf ^ 1, qn);
+    int32_t row2 = 0, grow2 = 0;
+    if (tl[AHEAD] < nqt) {
+      sstore(bl, tl[AHEAD]);
       if (qc < nqt) {
-        qc2 = pick(qc, cw, or2, and2, row2);
-        if (qc2 < 0) qc2 = next_live(qc + 64, or2, and2, row2);
+        // the tile after it, when live, from one scalar load of its block's
+        // record (scalar loads are counted apart from the tile loads, so
+        // nothing here waits for those); else the vector scan, after which
+        // this wave waits for its loads (the scan's registers are reused by
+        // the next iteration, and the compiler would otherwise wait for them,
+        // and for the tile loads, on every iteration)
+        const const_u32* bw = (const_u32*)(uintptr_t)(blks + (qc >> 1));
+        const uint32_t bor = bw[0], band = bw[1];
+        const int32_t brow = int32_t(bw[2]);
+        if (!(causal && qc * BQ + BQ - 1 < first_key) && (kand & band) == 0u) {
+          qc2 = qc;
+          or2 = bor;
+          and2 = band;
+          grow2 = brow != kNoRow ? brow + (qc & 1) * BQ : kNoRow;
+          row2 = in_place ? grow2 : qc * BQ;
+        } else {
+          qc2 = next_live(qc + 1, or2, and2, row2, grow2);
+          __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+        }
       }
     }
-    buf ^= 1;
-    qt = qn;
-    qor = nor;
-    qand = nand;
-    qn = qc2;
-    nor = or2;
-    nand = and2;
-    nrow = row2;
+#pragma unroll
+    for (int k = 0; k < AHEAD; ++k) {
+      tl[k] = tl[k + 1];
+      tor[k] = tor[k + 1];
+      tand[k] = tand[k + 1];
+      trw[k] = trw[k + 1];
+      tgr[k] = tgr[k + 1];
+    }
+    tl[AHEAD] = qc2;
+    tor[AHEAD] = or2;
+    tand[AHEAD] = and2;
+    trw[AHEAD] = row2;
+    tgr[AHEAD] = grow2;
+    buf = buf + 1 == NBUF ? 0 : buf + 1;
   }
   __builtin_amdgcn_s_waitcnt(0x0F70);  // the V fill has landed even when no tile was live
   if (!kvalid) return;
@@ -747,9 +819,9 @@ static hipError_t launch_dq_t(const BwdArgs& a, int64_t n, hipStream_t s) {
 template <typename E, int D>
 static hipError_t launch_dkdv_t(const BwdArgs& a, int64_t n, hipStream_t s) {
   if (a.local_out)
-    hipLaunchKernelGGL((attn_bwd_dkdv<E, D, true>), dim3(unsigned(n)), dim3(256 * dkdv_splits<D>()), 0, s, a);
+    hipLaunchKernelGGL((attn_bwd_dkdv<E, D, true>), dim3(unsigned(n)), dim3(64 * dkdv_waves<D>()), 0, s, a);
   else
-    hipLaunchKernelGGL((attn_bwd_dkdv<E, D, false>), dim3(unsigned(n)), dim3(256 * dkdv_splits<D>()), 0, s, a);
+    hipLaunchKernelGGL((attn_bwd_dkdv<E, D, false>), dim3(unsigned(n)), dim3(64 * dkdv_waves<D>()), 0, s, a);
   return hipGetLastError();
 }
 
@@ -765,6 +837,24 @@ static hipError_t launch_dkdv_t(const BwdArgs& a, int64_t n, hipStream_t s) {
     case 256: return dt == CQSA_BF16 ? LAUNCH<BF16, 256>(a, wgs, s) : LAUNCH<F16, 256>(a, wgs, s); \
   }                                                                    \
   return hipErrorInvalidValue;
+
+int dkdv_rows_per_wg(int d) {
+  switch (d) {
+#define CQSA_KV_ROWS(DD) \
+  case DD:               \
+    return 32 * dkdv_key_waves<DD>();
+    CQSA_KV_ROWS(32)
+    CQSA_KV_ROWS(64)
+    CQSA_KV_ROWS(96)
+    CQSA_KV_ROWS(128)
+    CQSA_KV_ROWS(160)
+    CQSA_KV_ROWS(192)
+    CQSA_KV_ROWS(224)
+    CQSA_KV_ROWS(256)
+#undef CQSA_KV_ROWS
+  }
+  return 128;
+}
 
 int dq_rows_per_wg(int d) {
   switch (d) {

@@ -296,7 +296,7 @@ cqsa_status backward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa
     a.scale_log2 = sc * 1.4426950408889634f; a.scale = sc;
     a.lse = d_lse; a.D = d_D; a.Lg = L;
   };
-  const int64_t dq_rows = dq_rows_per_wg(int(d));
+  const int64_t dq_rows = dq_rows_per_wg(int(d)), kv_rows = dkdv_rows_per_wg(int(d));
   if (batched) {
     float* loc = (float*)(base + tab_bytes + stat_bytes + lse_bytes + uint64_t(nslot) * slot_bytes);
     const int64_t stride = int64_t(loc_b / 4);
@@ -317,7 +317,7 @@ cqsa_status backward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa
         CQSA_HIP(hipStreamWaitEvent(qs, ev_pre, 0));
       }
       std::pair<hipEvent_t, hipEvent_t> sk = span_begin(st), sq = span_begin(qs);
-      CQSA_HIP(launch_bwd_dkdv(o.dtype, int(d), a, wgs_of(gr.task0, gr.count, kStrip), st));
+      CQSA_HIP(launch_bwd_dkdv(o.dtype, int(d), a, wgs_of(gr.task0, gr.count, kv_rows), st));
       CQSA_HIP(launch_bwd_dq(o.dtype, int(d), a, wgs_of(gr.task0, gr.count, dq_rows), qs));
       rec.stats.inner_launches += 2;
       span_end(sk, st, kStInner);
@@ -425,7 +425,7 @@ cqsa_status backward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa
       }
     }
     std::pair<hipEvent_t, hipEvent_t> sk = span_begin(st), sq = span_begin(qs);
-    CQSA_HIP(launch_bwd_dkdv(o.dtype, int(d), a, wgs_of(t, 1, kStrip), st));
+    CQSA_HIP(launch_bwd_dkdv(o.dtype, int(d), a, wgs_of(t, 1, kv_rows), st));
     CQSA_HIP(launch_bwd_dq(o.dtype, int(d), a, wgs_of(t, 1, dq_rows), qs));
     rec.stats.inner_launches += 2;
     span_end(sk, st, kStInner);

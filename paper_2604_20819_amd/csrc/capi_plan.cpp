@@ -97,7 +97,7 @@ cqsa_status cqsa_plan(int64_t L, int32_t H, int32_t d, int32_t causal,
         std::vector<uint8_t> image;
         std::vector<TableOffsets> offs;
         pack_image(tasks, sc, H, causal != 0, fwd_rows_per_wg(o.dtype, d), dq_rows_per_wg(d),
-                   &groups, &image, &offs);
+                   dkdv_rows_per_wg(d), &groups, &image, &offs);
         Footprint f = footprint(g, o, dep, tasks, gs, image.size());
         ok = fits(f);
         if (ok || gs == 1 || o.tasks_per_slot > 0) {

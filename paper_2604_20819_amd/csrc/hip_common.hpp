@@ -24,8 +24,13 @@ typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
 typedef __attribute__((__vector_size__(4 * sizeof(short)))) short i16x4;
 typedef __attribute__((__vector_size__(4 * sizeof(uint32_t)))) uint32_t u32x4;
 typedef __attribute__((__vector_size__(2 * sizeof(uint32_t)))) uint32_t u32x2;
+typedef uint32_t u32x3 __attribute__((ext_vector_type(3)));
 
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+typedef __attribute__((address_space(3))) void* lds_ptr;
+// Words read through the constant address space: a load at a wave-uniform
+// address is then a scalar load (tables that no kernel writes).
+typedef const __attribute__((address_space(4))) uint32_t const_u32;
 
 // Input element tags.
 struct BF16 {
@@ -162,6 +167,15 @@ __device__ __forceinline__ u32x4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t v
 __device__ __forceinline__ void buf_load16_lds(__amdgpu_buffer_rsrc_t r, void* lds, uint32_t voff) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16, voff, 0,
                                            0, 0);
+}
+
+// Work-group barrier after this wave's own LDS reads and writes have
+// completed (lgkmcnt(0)) that leaves LDS DMA loads (buffer_load ... lds,
+// counted by vmcnt) in flight: the compiler's fences would wait for them.
+// The caller waits (vmcnt) for the DMA loads the next phase reads.  The
+// memory clobber keeps the compiler from moving memory accesses across it.
+__device__ __forceinline__ void lds_barrier_dma_in_flight() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
 // Work-group barrier that orders LDS only.  __syncthreads() also orders

@@ -148,7 +148,8 @@ hipError_t launch_bwd_preprocess(const void* dO, const float* O, float* D, cqsa_
                                  int64_t B, int64_t L, int64_t H, int d, int64_t ld,
                                  hipStream_t s);
 // `wgs` = total work groups: sum over the launch's tasks of
-// ceil(L_j / rows) * B * H with rows = kStrip (dK/dV) or dq_rows_per_wg(d) (dQ).
+// ceil(L_j / rows) * B * H with rows = dkdv_rows_per_wg(d) (dK/dV) or
+// dq_rows_per_wg(d) (dQ).
 hipError_t launch_bwd_dkdv(cqsa_dtype dt, int d, const BwdArgs& a, int64_t wgs, hipStream_t s);
 hipError_t launch_bwd_dq(cqsa_dtype dt, int d, const BwdArgs& a, int64_t wgs, hipStream_t s);
 // `blocks` as for launch_combine.

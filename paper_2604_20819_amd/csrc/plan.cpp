@@ -363,16 +363,17 @@ std::vector<int32_t> query_strip_order(const Task& t, bool causal, int32_t rows)
   return longest_first(live);
 }
 
-std::vector<int32_t> key_strip_order(const Task& t, bool causal) {
+std::vector<int32_t> key_strip_order(const Task& t, bool causal, int32_t rows) {
   const int64_t L = t.L_local, nq = (L + 31) / 32;
-  const int64_t ns = (L + kStrip - 1) / kStrip;
+  const int64_t ns = (L + rows - 1) / rows;
   std::vector<uint32_t> tile_and(static_cast<size_t>(nq));  // 32-query tile q lies in block q / 2
   for (int64_t q = 0; q < nq; ++q) tile_and[size_t(q)] = t.blk_and[size_t(q / 2)];
   const ValuePrefix vp(tile_and);
   std::vector<int64_t> live(size_t(ns), 0);
   for (int64_t s = 0; s < ns; ++s) {
-    const int64_t first = s * kStrip, last = std::min(L, (s + 1) * kStrip) - 1;
-    const uint32_t kand = t.blk_and[size_t(2 * s)] & t.blk_and[size_t(last / kBlock)];
+    const int64_t first = s * rows, last = std::min<int64_t>(L, (s + 1) * rows) - 1;
+    uint32_t kand = 0xFFFFFFFFu;  // AND over the strip's blocks
+    for (int64_t b = first / kBlock; b <= last / kBlock; ++b) kand &= t.blk_and[size_t(b)];
     // causally, tile q is dead when its last query, 32 q + 31, precedes the
     // strip's first key (a multiple of 32): the first live tile is first / 32
     const int64_t q0 = causal ? first / 32 : 0;
@@ -382,7 +383,7 @@ std::vector<int32_t> key_strip_order(const Task& t, bool causal) {
 }
 
 void pack_image(const std::vector<Task>& tasks, const SegmentCover& sc, int32_t H, bool causal,
-                int32_t fwd_rows, int32_t dq_rows, std::vector<Group>* groups,
+                int32_t fwd_rows, int32_t dq_rows, int32_t kv_rows, std::vector<Group>* groups,
                 std::vector<uint8_t>* image, std::vector<TableOffsets>* offs) {
   std::vector<uint8_t>& im = *image;
   im.clear();
@@ -427,7 +428,7 @@ void pack_image(const std::vector<Task>& tasks, const SegmentCover& sc, int32_t 
     };
     o.qorder = put(query_strip_order(k, causal, fwd_rows));
     o.dqorder = put(query_strip_order(k, causal, dq_rows));
-    o.korder = put(key_strip_order(k, causal));
+    o.korder = put(key_strip_order(k, causal, kv_rows));
     o.blocks = reserve(nb * sizeof(DevBlock));
     for (size_t i = 0; i < nb; ++i) {
       DevBlock x{k.blk_or[i], k.blk_and[i], 0, 0u};

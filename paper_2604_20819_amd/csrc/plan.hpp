@@ -183,25 +183,27 @@ bool bwd_staged(const cqsa_plan_opts& o, int32_t depth);
 // `fwd_rows` and `dq_rows` are the forward and dQ kernels' query-strip
 // heights (fwd_rows_per_wg, dq_rows_per_wg).
 void pack_image(const std::vector<Task>& tasks, const SegmentCover& sc, int32_t H, bool causal,
-                int32_t fwd_rows, int32_t dq_rows, std::vector<Group>* groups,
+                int32_t fwd_rows, int32_t dq_rows, int32_t kv_rows, std::vector<Group>* groups,
                 std::vector<uint8_t>* image, std::vector<TableOffsets>* offs);
 // Appends the segments and contributions of `groups` to the image (filling
 // their offsets and block counts for H heads).
 void pack_groups(const SegmentCover& sc, int32_t H, std::vector<Group>* groups,
                  std::vector<uint8_t>* image);
 
-// Query rows per work group of the inner forward and dQ kernels.
+// Query rows per work group of the inner forward and dQ kernels, and key
+// rows per work group of the dK/dV kernel.
 int fwd_rows_per_wg(cqsa_dtype dt, int d);
 int dq_rows_per_wg(int d);
+int dkdv_rows_per_wg(int d);
 
 // Strip orders of one task for its kernels' launch order (longest first):
 // query strips of `rows` rows (a multiple of 64) by the 64-key tiles live for
-// them, and 128-key strips by the 32-query tiles live for them, with the
-// kernels' liveness rule (a tile is skipped when the AND of the strip's block
-// summaries and of the tile's shares a bit, or when it lies causally past the
-// strip).  Ties keep strip order.
+// them, and key strips of `rows` rows (a multiple of 64) by the 32-query
+// tiles live for them, with the kernels' liveness rule (a tile is skipped
+// when the AND of the strip's block summaries and of the tile's shares a
+// bit, or when it lies causally past the strip).  Ties keep strip order.
 std::vector<int32_t> query_strip_order(const Task& t, bool causal, int32_t rows);
-std::vector<int32_t> key_strip_order(const Task& t, bool causal);
+std::vector<int32_t> key_strip_order(const Task& t, bool causal, int32_t rows);
 
 inline uint64_t align_up(uint64_t x, uint64_t a = 256) { return (x + a - 1) / a * a; }
 

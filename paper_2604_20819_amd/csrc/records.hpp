@@ -33,7 +33,8 @@ struct DevTask {
                       // forward's strip height (fwd_rows_per_wg), most live key tiles first
   int64_t dqorder_off;// int32[ceil(L_local / R)] dQ query strips of R rows, R the dQ
                       // kernel's strip height (dq_rows_per_wg), most live key tiles first
-  int64_t korder_off; // int32[ceil(L_local / kStrip)] key strips, most live query tiles first
+  int64_t korder_off; // int32[ceil(L_local / R)] dK/dV key strips of R rows, R the dK/dV
+                      // kernel's strip height (dkdv_rows_per_wg), most live query tiles first
   int64_t sum_off;    // DevBlock[ceil(L_local / 64)]: the three block tables above, interleaved
   int32_t n_runs;
   int32_t pad;
@@ -48,10 +49,9 @@ struct DevBlock {
   uint32_t pad;
 };
 
-// Keys of the strip a dK/dV work group owns.  Strips of a (task, b, h) run in
-// the order of the task's strip tables (forward, dQ, dK/dV), longest first,
-// so a launch ends with its shortest strips.
-constexpr int kStrip = 128;
+// Strips of a (task, b, h) run in the order of the task's strip tables
+// (forward, dQ, dK/dV), longest first, so a launch ends with its shortest
+// strips.
 
 // Block row table: entry i is the global row of local token 64 i when the
 // tokens of block i (up to the task end) lie in one run, so they are
