@@ -356,12 +356,13 @@ template <int D> constexpr int dkdv_splits() { return D >= 160 ? 2 : 1; }
 // strip).
 template <int D> constexpr int dkdv_key_waves() { return (D == 96 || D == 128) ? 8 : 4; }
 template <int D> constexpr int dkdv_waves() { return dkdv_key_waves<D>() * dkdv_splits<D>(); }
-template <int D> constexpr int dkdv_wgs_per_cu() {
-  return (lds_row_elems<D>() > 128 || dkdv_key_waves<D>() > 4) ? 1 : 2;
-}
+// Minimum waves per SIMD the compiler must allow for (the second launch
+// bound): two, which caps the registers at 256, except where one work group
+// of the padded rows holds a CU.
+template <int D> constexpr int dkdv_min_waves() { return lds_row_elems<D>() > 128 ? 1 : 2; }
 
 template <typename E, int D, bool LOCAL>
-__global__ void __launch_bounds__(64 * dkdv_waves<D>(), dkdv_wgs_per_cu<D>()) attn_bwd_dkdv(const BwdArgs a) {
+__global__ void __launch_bounds__(64 * dkdv_waves<D>(), dkdv_min_waves<D>()) attn_bwd_dkdv(const BwdArgs a) {
   // 32-query tiles (two per 64-token summary block) keep the registers and
   // LDS within two waves per SIMD
   constexpr int KW = dkdv_key_waves<D>();
@@ -377,7 +378,6 @@ __global__ void __launch_bounds__(64 * dkdv_waves<D>(), dkdv_wgs_per_cu<D>()) at
   constexpr int WAVES = KW * NSPLIT, NT = 64 * WAVES;
   constexpr int RPI = 64 / CHUNKS, NDMA = BQ / RPI / WAVES;
   static_assert(NDMA >= 1 && NDMA * RPI * WAVES == BQ, "tile loads");
-  static_assert(2 * NDMA < 16, "vmcnt immediate");
   typedef typename E::vec8 vec8;
   auto swz = [](int r) { return 2 * (r & 3) + ((r >> 2) & 1); };
 
@@ -385,6 +385,7 @@ __global__ void __launch_bounds__(64 * dkdv_waves<D>(), dkdv_wgs_per_cu<D>()) at
   // filled NBUF - 1 tiles ahead of the compute (two ahead for the 256-key
   // strips, whose single work group per CU leaves the LDS for a third tile)
   constexpr int NBUF = KW == 8 ? 3 : 2, AHEAD = NBUF - 1;
+  static_assert(NBUF == 2 || 2 * NDMA < 16, "vmcnt immediate");
   __shared__ __attribute__((aligned(1024))) char qs[NBUF][BQ * P2];
   __shared__ __attribute__((aligned(1024))) char os[NBUF][BQ * P2];
   __shared__ __attribute__((aligned(1024))) char vs[BK * P2];   // the strip's V rows, swizzled
@@ -656,7 +657,7 @@ __global__ void __launch_bounds__(64 * dkdv_waves<D>(), dkdv_wgs_per_cu<D>()) at
     // loads, which are older), may still be in flight.  After the barrier
     // every wave's have, and every wave is done with the buffer refilled next.
     if (AHEAD == 2 && tl[1] < nqt)
-      __builtin_amdgcn_s_waitcnt(0x0F70 | (2 * NDMA));  // vmcnt(2 NDMA)
+      __builtin_amdgcn_s_waitcnt(0x0F70 | ((2 * NDMA) & 15));  // vmcnt(2 NDMA)
     else
       __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
     lds_barrier_dma_in_flight();

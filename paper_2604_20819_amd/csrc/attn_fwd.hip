@@ -52,17 +52,26 @@ __global__ void __launch_bounds__(64 * fwd_waves<D>(), (lds_row_elems<D>() > 128
   // loads: one wave instruction fills 1 KB, lane i its i-th 16 bytes.
   constexpr int DP = lds_row_elems<D>(); // LDS row elements (d padded)
   constexpr int RB = DP * 2;             // LDS row bytes
-  constexpr int KBYTES = BN * RB, VBYTES = BN * RB, STAGE = KBYTES + VBYTES;
+  constexpr int KBYTES = BN * RB, VBYTES = BN * RB;
   constexpr int DK = D / 16;             // k-steps of S^T = K Q^T
   constexpr int DB = D / 32;             // 32-wide d blocks of O^T
   constexpr int CHUNKS = DP / 8;         // 16-byte chunks per LDS row
   constexpr int RPI = 64 / CHUNKS;       // rows per 1 KB load instruction
   constexpr int NDMA = BN / RPI / WAVES; // load instructions per wave per tensor
+  static_assert(NDMA >= 1, "tile loads");
   typedef typename E::vec8 vec8;
   auto swz = [](int r) { return 2 * (r & 3) + ((r >> 2) & 1); };
 
-  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
-  __shared__ __attribute__((aligned(16))) uint32_t kbits_s[2][BN];
+  // a ring of NBUF key tiles (K, V), filled NBUF - 1 tiles ahead of the
+  // compute: three at d = 96 and 128, whose 8-wave work group per CU leaves
+  // the LDS for a third tile, two elsewhere
+  constexpr int NBUF = (WAVES == 8 && DP <= 128) ? 3 : 2, AHEAD = NBUF - 1;
+  // loads of one tile per wave (the vmcnt that leaves them in flight)
+  constexpr int TILE_OPS = 2 * NDMA;
+  static_assert(NBUF == 2 || TILE_OPS < 16, "vmcnt immediate");
+  __shared__ __attribute__((aligned(1024))) char kst[NBUF][KBYTES];
+  __shared__ __attribute__((aligned(1024))) char vst[NBUF][VBYTES];
+  __shared__ __attribute__((aligned(16))) uint32_t kbits_s[NBUF][BN];
   __shared__ DevRun runs_s[kMaxRuns];
 
   const int tid = threadIdx.x, lane = tid & 63, half = lane >> 5;
@@ -79,9 +88,7 @@ __global__ void __launch_bounds__(64 * fwd_waves<D>(), (lds_row_elems<D>() > 128
   const int h = int((work / nstrips) % a.H);
   const int b = int(work / (nstrips * a.H));
   const int n_runs = tk.n_runs;
-  const uint32_t* blk_or = (const uint32_t*)(a.tab + tk.or_off);
-  const uint32_t* blk_and = (const uint32_t*)(a.tab + tk.and_off);
-  const int32_t* blk_row = (const int32_t*)(a.tab + tk.row_off);
+  const DevBlock* blks = (const DevBlock*)(a.tab + tk.sum_off);
   const DevRun* runs_g = (const DevRun*)(a.tab + tk.runs_off);
   const bool in_place = a.in_place != 0;
 
@@ -106,7 +113,7 @@ __global__ void __launch_bounds__(64 * fwd_waves<D>(), (lds_row_elems<D>() > 128
   // its branch are wave-uniform
   int64_t qrow = myq;
   if (in_place && q0w < L) {
-    const int32_t br = blk_row[q0w >> 6];
+    const int32_t br = blks[q0w >> 6].row;
     qrow = br != kNoRow ? int64_t(br) + (myq & 63) : (qvalid ? run_global(runs_g, n_runs, myq) : 0);
   }
 
@@ -123,13 +130,13 @@ __global__ void __launch_bounds__(64 * fwd_waves<D>(), (lds_row_elems<D>() > 128
   const int qb0 = strip * (BM / 64), qb1 = lastq_wg / 64;
   uint32_t qor = 0u, qand = 0xFFFFFFFFu;
   for (int qb = qb0; qb <= qb1; ++qb) {
-    qor |= blk_or[qb];
-    qand &= blk_and[qb];
+    qor |= blks[qb].bor;
+    qand &= blks[qb].band;
   }
   const bool wave_live = q0w < L;
   const int wq1 = wave_live ? (q0w + 31 < L ? q0w + 31 : L - 1) : 0;
-  const uint32_t wor = wave_live ? blk_or[q0w / 64] : 0u;
-  const uint32_t wand = wave_live ? blk_and[q0w / 64] : 0u;
+  const uint32_t wor = wave_live ? blks[q0w / 64].bor : 0u;
+  const uint32_t wand = wave_live ? blks[q0w / 64].band : 0u;
 
   const int nkt = (L + BN - 1) / BN;
   // Tile skipping (App. A.2): a key tile is live for the strip unless it is
@@ -144,15 +151,15 @@ __global__ void __launch_bounds__(64 * fwd_waves<D>(), (lds_row_elems<D>() > 128
     uint32_t an, on;  // this lane's tile summaries (AND, OR)
     int32_t row;
   };
+  // The window's words stay as loaded until pick() uses them after the
+  // tile's compute: arithmetic on them, or a default written over a
+  // conditionally loaded register, would make the wave wait for the load
+  // (and, in order, for every tile load issued after it).  Lanes past the
+  // last tile read the last tile's record; pick() ignores them.
   auto window = [&](int k0) {
-    const int k = k0 + lane;
-    Window w{0xFFFFFFFFu, 0u, 0};
-    if (k < nkt) {
-      w.an = blk_and[k];
-      w.on = blk_or[k];
-      w.row = in_place ? blk_row[k] : k * BN;
-    }
-    return w;
+    const int k = k0 + lane < nkt ? k0 + lane : nkt - 1;
+    const u32x3 x = *(const u32x3*)(blks + k);
+    return Window{x[1], x[0], int32_t(x[2])};
   };
   // First live tile in [k0, k0 + 64), or -1; its summaries in kor_out/kand_out
   // and its first row in row_out.
@@ -165,7 +172,7 @@ __global__ void __launch_bounds__(64 * fwd_waves<D>(), (lds_row_elems<D>() > 128
     const int i = __builtin_ctzll(m);
     kand_out = __builtin_amdgcn_readlane(w.an, i);
     kor_out = __builtin_amdgcn_readlane(w.on, i);
-    row_out = __builtin_amdgcn_readlane(w.row, i);
+    row_out = in_place ? __builtin_amdgcn_readlane(w.row, i) : (k0 + i) * BN;
     return k0 + i;
   };
   // First live tile at or after kt (blocking; walks windows).
@@ -190,8 +197,8 @@ __global__ void __launch_bounds__(64 * fwd_waves<D>(), (lds_row_elems<D>() > 128
     goff[j] = uint32_t((row * rs + ch * 8) * 2);
   }
   auto gload = [&](int buf, int kt, int32_t trow) {
-    char* kb = smem + buf * STAGE;
-    char* vb = kb + KBYTES;
+    char* kb = kst[buf];
+    char* vb = vst[buf];
     if (trow != kNoRow) {
       // the tile's tokens are consecutive rows from trow
       const int64_t rows = int64_t(L) - int64_t(kt) * BN;
@@ -224,6 +231,10 @@ __global__ void __launch_bounds__(64 * fwd_waves<D>(), (lds_row_elems<D>() > 128
         buf_load16_lds(rk, kb + off, vo);
         buf_load16_lds(rv, vb + off, vo);
       }
+      // this rare path's offsets are temporaries: wait here, so that the
+      // compiler need not make every later iteration wait before reusing
+      // their registers
+      __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
     }
   };
   auto sstore = [&](int buf, int kt, uint32_t kor_t) {
@@ -244,34 +255,50 @@ __global__ void __launch_bounds__(64 * fwd_waves<D>(), (lds_row_elems<D>() > 128
   __syncthreads();  // runs_s visible
   const uint32_t qbits = qvalid ? run_bits(runs_s, n_runs, myq) : 0u;
 
-  uint32_t kor = 0u, kand = 0u, nor = 0u, nand = 0u;
-  int32_t krow = 0, nrow = 0;
-  int kt = next_live(0, kor, kand, krow);
-  if (kt < nkt) {
-    gload(0, kt, krow);
-    sstore(0, kt, kor);
+  // tl[0] is the tile being computed, tl[1 .. AHEAD] the next live ones
+  // (nkt: none); tor, tand, trw hold their block summaries and first rows
+  int tl[NBUF];
+  uint32_t tor[NBUF], tand[NBUF];
+  int32_t trw[NBUF];
+  tl[0] = next_live(0, tor[0], tand[0], trw[0]);
+#pragma unroll
+  for (int k = 1; k < NBUF; ++k) {
+    tor[k] = tand[k] = 0u;
+    trw[k] = 0;
+    tl[k] = tl[k - 1] < nkt ? next_live(tl[k - 1] + 1, tor[k], tand[k], trw[k]) : nkt;
   }
-  int kn = kt < nkt ? next_live(kt + 1, nor, nand, nrow) : nkt;
+#pragma unroll
+  for (int k = 0; k < AHEAD; ++k)
+    if (tl[k] < nkt) {
+      gload(k, tl[k], trw[k]);
+      sstore(k, tl[k], tor[k]);
+    }
   int buf = 0;
-  while (kt < nkt) {
-    // this wave's tile loads have landed; after the barrier every wave's
-    // have, and every wave is done with the other buffer
-    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
-    lds_barrier();
-    // summary window after kn (used after this tile's compute), then the
-    // loads of tile kn into the other buffer
-    const int kc = kn + 1;
-    const Window cw = window(kc);
-    if (kn < nkt) gload(buf ^ 1, kn, nrow);
+  while (tl[0] < nkt) {
+    const int kt = tl[0];
+    // this wave's loads of tile kt have landed: only those of the tile after
+    // it (2 NDMA) may still be in flight.  After the barrier every wave's
+    // have, and every wave is done with the buffer refilled next; the
+    // barrier itself leaves the DMA loads in flight.
+    if (AHEAD == 2 && tl[1] < nkt)
+      __builtin_amdgcn_s_waitcnt(0x0F70 | (TILE_OPS & 15));  // vmcnt(2 NDMA)
+    else
+      __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+    lds_barrier_dma_in_flight();
+    // the loads of the last tile ahead
+    const int kc = tl[AHEAD] + 1;
+    const int bl = (buf + AHEAD) % NBUF;
+    if (tl[AHEAD] < nkt) gload(bl, tl[AHEAD], trw[AHEAD]);
 
     // ---- compute on tile kt (wave-uniform verdict) ----
+    const uint32_t kor = tor[0], kand = tand[0];
     const int k0 = kt * BN, k1 = (k0 + BN - 1 < L ? k0 + BN - 1 : L - 1);
     const bool wfull = !wave_live || (wand & kand) != 0u || (causal && k0 > wq1);
     if (!wfull) {
       const bool wclear = (wor & kor) == 0u && (!causal || k1 <= q0w) && (k0 + BN <= L);
       const bool use_bits = (qor & kor) != 0u;
-      const char* Kb = smem + buf * STAGE;
-      const char* Vb = Kb + KBYTES;
+      const char* Kb = kst[buf];
+      const char* Vb = vst[buf];
       // the two 32-key blocks' accumulation chains alternate, so consecutive
       // products never depend on each other
       f32x16 s[2];
@@ -375,25 +402,45 @@ __global__ void __launch_bounds__(64 * fwd_waves<D>(), (lds_row_elems<D>() > 128
         }
       }
     }
-    // ---- group bits of the next tile, next live tile ----
+    // ---- group bits of the last tile ahead, the live tile after it ----
     int kc2 = nkt;
     uint32_t or2 = 0u, and2 = 0u;
     int32_t row2 = 0;
-    if (kn < nkt) {
-      sstore(buf ^ 1, kn, nor);
-      if (kc < nkt) {
-        kc2 = pick(kc, cw, or2, and2, row2);
-        if (kc2 < 0) kc2 = next_live(kc + 64, or2, and2, row2);
+    if (tl[AHEAD] < nkt) {
+      sstore(bl, tl[AHEAD], tor[AHEAD]);
+      if (kc < nkt && !(causal && kc * BN > lastq_wg)) {
+        // when live, from one scalar load of its block's record (scalar
+        // loads are counted apart from the tile loads, so nothing here waits
+        // for those); else the vector scan, after which this wave waits for
+        // its loads (the scan's registers are reused by the next iteration,
+        // and the compiler would otherwise wait for them, and for the tile
+        // loads, on every iteration)
+        const const_u32* bw = (const_u32*)(uintptr_t)(blks + kc);
+        const uint32_t bor = bw[0], band = bw[1];
+        const int32_t brow = int32_t(bw[2]);
+        if ((qand & band) == 0u) {
+          kc2 = kc;
+          or2 = bor;
+          and2 = band;
+          row2 = in_place ? brow : kc * BN;
+        } else {
+          kc2 = next_live(kc + 1, or2, and2, row2);
+          __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+        }
       }
     }
-    buf ^= 1;
-    kt = kn;
-    kor = nor;
-    kand = nand;
-    kn = kc2;
-    nor = or2;
-    nand = and2;
-    nrow = row2;
+#pragma unroll
+    for (int k = 0; k < AHEAD; ++k) {
+      tl[k] = tl[k + 1];
+      tor[k] = tor[k + 1];
+      tand[k] = tand[k + 1];
+      trw[k] = trw[k + 1];
+    }
+    tl[AHEAD] = kc2;
+    tor[AHEAD] = or2;
+    tand[AHEAD] = and2;
+    trw[AHEAD] = row2;
+    buf = buf + 1 == NBUF ? 0 : buf + 1;
   }
 
   const float l_tot = l_run + swap_halves(l_run);
@@ -453,7 +500,7 @@ __global__ void __launch_bounds__(256) attn_fwd_f32(const FwdArgs a) {
   const int b = int(work / (nstrips * a.H));
   const int n_runs = tk.n_runs;
   const DevRun* runs_g = (const DevRun*)(a.tab + tk.runs_off);
-  const int32_t* blk_row = (const int32_t*)(a.tab + tk.row_off);
+  const DevBlock* blks = (const DevBlock*)(a.tab + tk.sum_off);
   const bool in_place = a.in_place != 0;
   for (int i = tid; i < n_runs; i += 256) runs_s[i] = runs_g[i];
   // token rows as in the MFMA kernel: consecutive when staged, the runs'
@@ -467,7 +514,7 @@ __global__ void __launch_bounds__(256) attn_fwd_f32(const FwdArgs a) {
   const float c = a.scale_log2;
   const int myq = strip * QPB + ql;
   const bool qvalid = myq < L;
-  const int64_t qrow = !qvalid ? 0 : in_place ? in_place_row(blk_row, runs_g, n_runs, myq) : myq;
+  const int64_t qrow = !qvalid ? 0 : in_place ? in_place_row(blks, runs_g, n_runs, myq) : myq;
   float q[SL], o[SL];
 #pragma unroll
   for (int i = 0; i < SL; ++i) {

@@ -206,9 +206,9 @@ __device__ __forceinline__ int64_t run_global(const DevRun* runs, int n, int64_t
 
 // Tensor row of local token r when the inputs are read in place: from the
 // block row table when r's 64-token block lies in one run, else from the runs.
-__device__ __forceinline__ int64_t in_place_row(const int32_t* rows, const DevRun* runs, int n,
+__device__ __forceinline__ int64_t in_place_row(const DevBlock* blks, const DevRun* runs, int n,
                                                 int r) {
-  const int32_t g = rows[r >> 6];
+  const int32_t g = blks[r >> 6].row;
   return g != kNoRow ? int64_t(g) + (r & 63) : run_global(runs, n, r);
 }
 

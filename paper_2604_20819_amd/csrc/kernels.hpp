@@ -19,7 +19,7 @@ enum FwdMode : int {
 // Staged inputs: task j's rows are [B, L_j, H, d] at q/k/v + j * in_stride
 // elements.  Inputs read in place (in_place = 1): q/k/v are the caller's
 // [B, Lg, H, d] tensors and task j's local token t is the global row its runs
-// give (block row table DevTask::row_off).  Task j's statistics are acc_j
+// give (the block rows of DevTask::sum_off).  Task j's statistics are acc_j
 // [B, L_j, H, d] at acc + j * acc_stride, m_j, l_j and lt_j [B, H, L_j] at
 // m/l/lt + j * st_stride.  l sums the fp32 weights exp2(s - m) and gives the
 // log-sum-exp; lt sums the same weights rounded to the input dtype, exactly

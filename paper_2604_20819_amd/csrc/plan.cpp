@@ -402,13 +402,10 @@ void pack_image(const std::vector<Task>& tasks, const SegmentCover& sc, int32_t 
       DevRun r{k.runs[i].local_start, k.runs[i].global_start, k.runs[i].length, k.runs[i].bits, 0u};
       std::memcpy(im.data() + o.runs + i * sizeof(DevRun), &r, sizeof(r));
     }
-    o.blk_or = reserve(k.blk_or.size() * 4);
-    std::memcpy(im.data() + o.blk_or, k.blk_or.data(), k.blk_or.size() * 4);
-    o.blk_and = reserve(k.blk_and.size() * 4);
-    std::memcpy(im.data() + o.blk_and, k.blk_and.data(), k.blk_and.size() * 4);
-    // block row table for kernels that read the caller's tensors in place
+    // block records: summaries and the block row table for kernels that
+    // read the caller's tensors in place
     const size_t nb = k.blk_or.size();
-    o.rows = reserve(nb * 4);
+    o.blocks = reserve(nb * sizeof(DevBlock));
     size_t ri = 0;
     for (size_t i = 0; i < nb; ++i) {
       const int64_t t0 = int64_t(i) * kBlock;
@@ -418,7 +415,8 @@ void pack_image(const std::vector<Task>& tasks, const SegmentCover& sc, int32_t 
       const int32_t row = t1 <= r.local_start + r.length
                               ? int32_t(r.global_start + (t0 - r.local_start))
                               : kNoRow;
-      std::memcpy(im.data() + o.rows + i * 4, &row, 4);
+      const DevBlock x{k.blk_or[i], k.blk_and[i], row, 0u};
+      std::memcpy(im.data() + o.blocks + i * sizeof(DevBlock), &x, sizeof(x));
     }
     // strip launch orders, longest first: the forward's strips, dQ's and dK/dV's
     auto put = [&](const std::vector<int32_t>& v) {
@@ -429,15 +427,8 @@ void pack_image(const std::vector<Task>& tasks, const SegmentCover& sc, int32_t 
     o.qorder = put(query_strip_order(k, causal, fwd_rows));
     o.dqorder = put(query_strip_order(k, causal, dq_rows));
     o.korder = put(key_strip_order(k, causal, kv_rows));
-    o.blocks = reserve(nb * sizeof(DevBlock));
-    for (size_t i = 0; i < nb; ++i) {
-      DevBlock x{k.blk_or[i], k.blk_and[i], 0, 0u};
-      std::memcpy(&x.row, im.data() + o.rows + i * 4, 4);
-      std::memcpy(im.data() + o.blocks + i * sizeof(DevBlock), &x, sizeof(x));
-    }
-    DevTask d{k.L_local, int64_t(o.runs), int64_t(o.blk_or), int64_t(o.blk_and), int64_t(o.rows),
-              int64_t(o.qorder), int64_t(o.dqorder), int64_t(o.korder), int64_t(o.blocks),
-              int32_t(k.runs.size()), 0};
+    DevTask d{k.L_local, int64_t(o.runs), int64_t(o.qorder), int64_t(o.dqorder),
+              int64_t(o.korder), int64_t(o.blocks), int32_t(k.runs.size()), 0};
     std::memcpy(im.data() + hdr + t * sizeof(DevTask), &d, sizeof(d));
     offs->push_back(o);
   }

@@ -40,13 +40,10 @@ struct Task {
 // Offsets of one task's tables inside the packed table image (bytes).
 struct TableOffsets {
   uint64_t runs = 0;    // DevRun[n_runs]: {local_start, global_start, length, bits, pad}
-  uint64_t blk_or = 0;  // uint32[n_blocks]
-  uint64_t blk_and = 0; // uint32[n_blocks]
-  uint64_t rows = 0;    // int32[n_blocks] block row table (records.hpp, kNoRow)
   uint64_t qorder = 0;  // int32[n_strips] forward query strips, longest first
   uint64_t dqorder = 0; // int32[n_strips] dQ query strips, longest first
   uint64_t korder = 0;  // int32[n_strips] key strips, longest first
-  uint64_t blocks = 0;  // DevBlock[n_blocks] (OR, AND, row interleaved)
+  uint64_t blocks = 0;  // DevBlock[n_blocks]: block OR, AND and row (records.hpp, kNoRow)
 };
 
 // A launch group: tasks [task0, task0 + count) are staged into one slot,

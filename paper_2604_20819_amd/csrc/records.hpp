@@ -26,22 +26,19 @@ struct DevRun {
 struct DevTask {
   int64_t L_local;
   int64_t runs_off;   // DevRun[n_runs]
-  int64_t or_off;     // uint32[ceil(L_local / 64)] block OR of the group bits
-  int64_t and_off;    // uint32[ceil(L_local / 64)] block AND of the group bits
-  int64_t row_off;    // int32[ceil(L_local / 64)] block rows (see kNoRow)
   int64_t qorder_off; // int32[ceil(L_local / R)] forward query strips of R rows, R the
                       // forward's strip height (fwd_rows_per_wg), most live key tiles first
   int64_t dqorder_off;// int32[ceil(L_local / R)] dQ query strips of R rows, R the dQ
                       // kernel's strip height (dq_rows_per_wg), most live key tiles first
   int64_t korder_off; // int32[ceil(L_local / R)] dK/dV key strips of R rows, R the dK/dV
                       // kernel's strip height (dkdv_rows_per_wg), most live query tiles first
-  int64_t sum_off;    // DevBlock[ceil(L_local / 64)]: the three block tables above, interleaved
+  int64_t sum_off;    // DevBlock[ceil(L_local / 64)]: each 64-token block's summaries and row
   int32_t n_runs;
   int32_t pad;
 };
 
-// One 64-token block's OR, AND and row, read with one 16-byte load (the
-// backward kernels' tile windows).
+// One 64-token block: the OR and the AND of its tokens' group bits, and its
+// row in the block row table (see kNoRow); a tile window reads one per lane.
 struct DevBlock {
   uint32_t bor;
   uint32_t band;
@@ -82,7 +79,7 @@ struct DevContrib {
 };
 
 static_assert(sizeof(DevRun) == 32, "DevRun layout");
-static_assert(sizeof(DevTask) == 80, "DevTask layout");
+static_assert(sizeof(DevTask) == 56, "DevTask layout");
 static_assert(sizeof(DevBlock) == 16, "DevBlock layout");
 static_assert(sizeof(DevSeg) == 40, "DevSeg layout");
 static_assert(sizeof(DevContrib) == 16, "DevContrib layout");
