@@ -26,11 +26,12 @@ namespace cqsa {
 
 constexpr float kLog2e = 1.4426950408889634f;
 
-// Waves per dQ work group: 8 over a 256-query strip at d = 160, where the
-// padded LDS rows leave one work group per CU and 4 waves would run one wave
-// per SIMD (a 40 B spill costs less); 4 over a 128-query strip elsewhere (at
-// d = 96 and 128 8 waves gained nothing, at 192 and up they spill more).
-template <int D> constexpr int dq_waves() { return D == 160 ? 8 : 4; }
+// Waves per dQ work group: 8 over a 256-query strip at d = 96, 128 and 160
+// (at 96 and 128 the work group's single slot per CU leaves the LDS for a
+// third K/V tile; at 160 the padded LDS rows leave one work group per CU and 4
+// waves would run one wave per SIMD, where a 40 B spill costs less); 4 over a
+// 128-query strip elsewhere (at 192 and up 8 waves spill more).
+template <int D> constexpr int dq_waves() { return (D >= 96 && D <= 160) ? 8 : 4; }
 
 // LOCAL (BwdArgs::local_out) is a template parameter: a run-time branch in
 // the epilogue changes the register allocation of the whole kernel (the
@@ -45,14 +46,20 @@ __global__ void __launch_bounds__(64 * dq_waves<D>(), (lds_row_elems<D>() > 128 
   // direct buffer-to-LDS loads (lane i's 16 bytes at +16 i of a 1 KB block).
   constexpr int DP = lds_row_elems<D>();
   constexpr int RB = DP * 2;
-  constexpr int KBYTES = BN * RB, VBYTES = BN * RB, STAGE = KBYTES + VBYTES;
+  constexpr int KBYTES = BN * RB, VBYTES = BN * RB;
   constexpr int DK = D / 16, DB = D / 32, CHUNKS = DP / 8;
   constexpr int RPI = 64 / CHUNKS, NDMA = BN / RPI / WAVES;
   typedef typename E::vec8 vec8;
   auto swz = [](int r) { return 2 * (r & 3) + ((r >> 2) & 1); };
 
-  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
-  __shared__ __attribute__((aligned(16))) uint32_t kbits_s[2][BN];
+  // a ring of NBUF key tiles (K, V) filled NBUF - 1 tiles ahead of the
+  // compute: three for the 8-wave work groups of unpadded rows, two elsewhere
+  constexpr int NBUF = (WAVES == 8 && DP <= 128) ? 3 : 2, AHEAD = NBUF - 1;
+  constexpr int TILE_OPS = 2 * NDMA;  // this wave's loads of one tile
+  static_assert(NBUF == 2 || TILE_OPS < 16, "vmcnt immediate");
+  __shared__ __attribute__((aligned(1024))) char kst[NBUF][KBYTES];
+  __shared__ __attribute__((aligned(1024))) char vst[NBUF][VBYTES];
+  __shared__ __attribute__((aligned(16))) uint32_t kbits_s[NBUF][BN];
   __shared__ DevRun runs_s[kMaxRuns];
 
   const int tid = threadIdx.x, lane = tid & 63, half = lane >> 5;
@@ -168,8 +175,8 @@ __global__ void __launch_bounds__(64 * dq_waves<D>(), (lds_row_elems<D>() > 128 
     goff[j] = uint32_t((row * rs + ((lane % CHUNKS) ^ swz(row)) * 8) * 2);
   }
   auto gload = [&](int buf, int kt, int32_t trow) {
-    char* kb = smem + buf * STAGE;
-    char* vb = kb + KBYTES;
+    char* kb = kst[buf];
+    char* vb = vst[buf];
     if (trow != kNoRow) {
       // consecutive rows from trow
       const int64_t rows = int64_t(L) - int64_t(kt) * BN;
@@ -200,6 +207,10 @@ __global__ void __launch_bounds__(64 * dq_waves<D>(), (lds_row_elems<D>() > 128 
         buf_load16_lds(rk, kb + off, vo);
         buf_load16_lds(rv, vb + off, vo);
       }
+      // this rare path's offsets are temporaries: wait here, so that the
+      // compiler need not make every later iteration wait before reusing
+      // their registers
+      __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
     }
   };
   auto sstore = [&](int buf, int kt, uint32_t kor_t) {
@@ -222,31 +233,48 @@ __global__ void __launch_bounds__(64 * dq_waves<D>(), (lds_row_elems<D>() > 128 
   const float lse2 = qvalid ? a.lse[si] * kLog2e : 0.f;
   const float Dq = qvalid ? a.D[si] : 0.f;
 
-  uint32_t kor = 0u, kand = 0u, nor = 0u, nand = 0u;
-  int32_t krow = 0, nrow = 0;
-  int kt = next_live(0, kor, kand, krow);
-  if (kt < nkt) {
-    gload(0, kt, krow);
-    sstore(0, kt, kor);
+  // tl[0] is the tile being computed, tl[1 .. AHEAD] the next live ones
+  // (nkt: none); tor, tand, trw hold their block summaries and first rows
+  int tl[NBUF];
+  uint32_t tor[NBUF], tand[NBUF];
+  int32_t trw[NBUF];
+  tl[0] = next_live(0, tor[0], tand[0], trw[0]);
+#pragma unroll
+  for (int k = 1; k < NBUF; ++k) {
+    tor[k] = tand[k] = 0u;
+    trw[k] = 0;
+    tl[k] = tl[k - 1] < nkt ? next_live(tl[k - 1] + 1, tor[k], tand[k], trw[k]) : nkt;
   }
-  int kn = kt < nkt ? next_live(kt + 1, nor, nand, nrow) : nkt;
+#pragma unroll
+  for (int k = 0; k < AHEAD; ++k)
+    if (tl[k] < nkt) {
+      gload(k, tl[k], trw[k]);
+      sstore(k, tl[k], tor[k]);
+    }
   int buf = 0;
-  while (kt < nkt) {
-    // this wave's tile loads have landed; after the barrier every wave's
-    // have, and every wave is done with the other buffer
-    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
-    lds_barrier();
-    // summary window after kn (used after the compute), then the loads of kn
-    const int kc = kn + 1;
-    const Window cw = window(kc);
-    if (kn < nkt) gload(buf ^ 1, kn, nrow);
+  while (tl[0] < nkt) {
+    const int kt = tl[0];
+    // this wave's loads of tile kt have landed: only those of the tile after
+    // it may still be in flight.  After the barrier every wave's have, and
+    // every wave is done with the buffer refilled next; the barrier leaves
+    // the DMA loads in flight.
+    if (AHEAD == 2 && tl[1] < nkt)
+      __builtin_amdgcn_s_waitcnt(0x0F70 | (TILE_OPS & 15));  // vmcnt(2 NDMA)
+    else
+      __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+    lds_barrier_dma_in_flight();
+    // the loads of the last tile ahead
+    const int kc = tl[AHEAD] + 1;
+    const int bl = (buf + AHEAD) % NBUF;
+    if (tl[AHEAD] < nkt) gload(bl, tl[AHEAD], trw[AHEAD]);
+    const uint32_t kor = tor[0], kand = tand[0];
     const int k0 = kt * BN, k1 = (k0 + BN - 1 < L ? k0 + BN - 1 : L - 1);
     const bool wfull = !wave_live || (wand & kand) != 0u || (causal && k0 > wq1);
     if (!wfull) {
       const bool wclear = (wor & kor) == 0u && (!causal || k1 <= q0w) && (k0 + BN <= L);
       const bool use_bits = (qor & kor) != 0u;
-      const char* Kb = smem + buf * STAGE;
-      const char* Vb = Kb + KBYTES;
+      const char* Kb = kst[buf];
+      const char* Vb = vst[buf];
       // one 32-key block at a time: S^T, dP^T, dS^T, then its dQ^T products
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
@@ -303,21 +331,38 @@ __global__ void __launch_bounds__(64 * dq_waves<D>(), (lds_row_elems<D>() > 128 
     int kc2 = nkt;
     uint32_t or2 = 0u, and2 = 0u;
     int32_t row2 = 0;
-    if (kn < nkt) {
-      sstore(buf ^ 1, kn, nor);
-      if (kc < nkt) {
-        kc2 = pick(kc, cw, or2, and2, row2);
-        if (kc2 < 0) kc2 = next_live(kc + 64, or2, and2, row2);
+    if (tl[AHEAD] < nkt) {
+      sstore(bl, tl[AHEAD], tor[AHEAD]);
+      if (kc < nkt && !(causal && kc * BN > lastq_wg)) {
+        // when live, from one scalar load of its block's record; else the
+        // vector scan, after which this wave waits for its loads (as in the
+        // forward)
+        const const_u32* bw = (const_u32*)(uintptr_t)(blks + kc);
+        const uint32_t bor = bw[0], band = bw[1];
+        const int32_t brow = int32_t(bw[2]);
+        if ((qand & band) == 0u) {
+          kc2 = kc;
+          or2 = bor;
+          and2 = band;
+          row2 = in_place ? brow : kc * BN;
+        } else {
+          kc2 = next_live(kc + 1, or2, and2, row2);
+          __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+        }
       }
     }
-    buf ^= 1;
-    kt = kn;
-    kor = nor;
-    kand = nand;
-    kn = kc2;
-    nor = or2;
-    nand = and2;
-    nrow = row2;
+#pragma unroll
+    for (int k = 0; k < AHEAD; ++k) {
+      tl[k] = tl[k + 1];
+      tor[k] = tor[k + 1];
+      tand[k] = tand[k + 1];
+      trw[k] = trw[k + 1];
+    }
+    tl[AHEAD] = kc2;
+    tor[AHEAD] = or2;
+    tand[AHEAD] = and2;
+    trw[AHEAD] = row2;
+    buf = buf + 1 == NBUF ? 0 : buf + 1;
   }
   if (!qvalid) return;
   // global rows accumulate (a single task holds a token once and the dQ

@@ -264,8 +264,8 @@ def _image_bytes(p, g, bwd_g=1):
     """Plan image size from the layout the planner documents: DevTask records
     (56 bytes), per-task runs, block records (OR, AND and row: 16 bytes per
     block) and the three strip orders (one int32 per strip: at bf16 d = 128
-    the forward's 256-query strips, dQ's 128-query strips and dK/dV's
-    256-key strips), then per forward group the segments and contributions,
+    the forward's and dQ's 256-query strips and dK/dV's 256-key strips),
+    then per forward group the segments and contributions,
     and per backward launch group (when it holds several tasks) those of its
     tokens."""
     al = lambda x: (x + 255) // 256 * 256
@@ -274,8 +274,7 @@ def _image_bytes(p, g, bwd_g=1):
     for tk in tasks:
         nb = len(tk["block_or"])
         size += al(len(tk["runs"]) * 32) + al(nb * 16)
-        size += al(-(-tk["L_local"] // 256) * 4) + al(-(-tk["L_local"] // 128) * 4)
-        size += al(-(-tk["L_local"] // 256) * 4)
+        size += 3 * al(-(-tk["L_local"] // 256) * 4)
     bounds = sorted({0, p.L} | {r[0] for tk in tasks for r in tk["runs"]}
                     | {r[0] + r[1] for tk in tasks for r in tk["runs"]})
     segs = list(zip(bounds[:-1], bounds[1:]))
