@@ -133,7 +133,8 @@ typedef struct {
                                 fp32 buffers in the workspace (3 x B x L_max x H x d x 4 bytes
                                 per task) and one gather-merge per launch adds them into dQ, dK,
                                 dV in task order.  0 = automatic: every task up to 32 when
-                                with_backward = 1, reduced until the budget fits, else 1;
+                                with_backward = 1, reduced until the budget fits, over
+                                balanced splits only (49 tasks: 25 per launch), else 1;
                                 >= 1 forced (> 1 needs inputs_on_device = 1 and neither
                                 read_in_place nor acc_on_device set to 0; where the
                                 conditions above do not hold, 1 applies).  With 1, each

@@ -111,12 +111,17 @@ cqsa_status cqsa_plan(int64_t L, int32_t H, int32_t d, int32_t causal,
       }
       // backward launch groups: with inputs read in place and device-resident
       // gradients, every task (up to 32) in one dQ and one dK/dV launch whose
-      // task-local gradients a gather-merge sums, reduced until the budget fits
+      // task-local gradients a gather-merge sums, reduced until the budget
+      // fits.  The automatic size takes only balanced splits (49 tasks: 25 +
+      // 24, not 32 + 17): the same launches, and task-local buffers for the
+      // larger half only.
       p->bwd_groups.clear();
       const int32_t bf = o.bwd_tasks_per_launch;
       if (bwd_batchable(o, dep) && (bf > 1 || (bf == 0 && o.with_backward)) && ntask > 1) {
         const int32_t b_hi = int32_t(std::min<int64_t>(bf > 0 ? bf : kMaxContrib, ntask));
         for (int32_t gb = b_hi; gb >= 2; --gb) {
+          const int64_t n_groups = (ntask + gb - 1) / gb;
+          if (bf == 0 && (ntask + n_groups - 1) / n_groups != gb) continue;
           std::vector<Group> bg = make_groups(ntask, gb);
           // the merge of the last group covers only the tokens its tasks hold
           for (Group& x : bg) x.final = false;

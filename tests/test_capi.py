@@ -350,9 +350,14 @@ def test_backward_launch_groups():
     mid = cq.cqsa_plan(L, H, d, False, budget, cq.make_opts(with_backward=True))
     assert mid.depth == 1 and 1 < mid.bwd_tasks_per_launch < 7
     assert mid.modelled_device_bytes <= budget
-    # 49 tasks at depth 2: 32 per launch
+    # 49 tasks at depth 2: two launches, split evenly (25 + 24)
     p = cq.cqsa_plan(L, H, d, False, 0, cq.make_opts(depth=2, with_backward=True))
-    assert p.bwd_tasks_per_launch == 32
+    assert p.bwd_tasks_per_launch == 25
+    # automatic sizes under a budget are balanced splits of the 7 tasks: 7, 4, 3 or 2
+    for frac in (0.2, 0.4, 0.6, 0.8):
+        q = cq.cqsa_plan(L, H, d, False, int(one.modelled_device_bytes + frac * (want - one.modelled_device_bytes)),
+                         cq.make_opts(depth=1, with_backward=True))
+        assert q.bwd_tasks_per_launch in (1, 2, 3, 4, 7), frac
     # forced
     p = cq.cqsa_plan(L, H, d, False, 0, cq.make_opts(depth=1, with_backward=True,
                                                      bwd_tasks_per_launch=3))
