@@ -200,6 +200,15 @@ typedef struct {
                                        backward staging slots, or the backward tasks per launch
                                        whose local gradients the workspace holds; 0 for the
                                        undecomposed path and for one in-place task per launch) */
+  /* The inner forward's own tile decisions (App. A.2), counted on the device
+   * when tile counting is enabled (cqsa_set_tile_counting) for a cqsa_forward
+   * with 16-bit inputs, else -1.  Unit: one wave of 32 consecutive local
+   * queries (every wave holding a query of its task) against one 64-key tile
+   * its work group visits, summed over tasks, batch elements and heads:
+   * masked (every pair masked for the wave: skipped), clear (no pair masked:
+   * no mask work), mixed (per-pair tests).  cqsa_plan_fwd_tile_decisions
+   * gives the counts the block summaries predict. */
+  int64_t kernel_tiles_masked, kernel_tiles_clear, kernel_tiles_mixed;
 } cqsa_run_stats;
 
 /* Fill `o` with the defaults listed in cqsa_plan_opts. */
@@ -238,6 +247,19 @@ int32_t cqsa_plan_reads_in_place(const cqsa_plan_t* plan);
 /* Pooled 128x128 tile census over causal-retained tiles of every task (App. A.2). */
 cqsa_status cqsa_plan_tile_census(const cqsa_plan_t* plan, int64_t* full, int64_t* clear,
                                   int64_t* mixed);
+/* The inner forward's tile decisions this plan predicts, in the unit of
+ * cqsa_run_stats.kernel_tiles_* (App. A.2 verdicts from the 64-token block
+ * summaries, at the 16-bit kernel's work-group and wave shapes for the plan's
+ * d): a work group of R query rows (R = 256 at d = 96 ... 192, else 128)
+ * visits key tile t unless t is causally past its last query or the AND of
+ * its blocks' summaries meets tile t's; a visited tile is masked for a wave
+ * when the wave's block AND meets the tile's or it is causally past the
+ * wave's last query, clear when the wave's block OR misses the tile's, the
+ * tile lies causally below the wave's first query and holds 64 keys, mixed
+ * otherwise.  Summed over tasks times B x H.  CQSA_ERR_UNSUPPORTED for fp32
+ * plans (their kernel is not counted). */
+cqsa_status cqsa_plan_fwd_tile_decisions(const cqsa_plan_t* plan, int64_t* masked,
+                                         int64_t* clear, int64_t* mixed);
 void cqsa_plan_destroy(cqsa_plan_t* plan);                 /* NULL is a no-op */
 
 /* Decomposed forward (Alg. 1 computed with the max-shifted merge of App. A.1).
@@ -321,6 +343,13 @@ cqsa_status cqsa_set_allocator(void* (*alloc)(size_t bytes, void* ctx),
 /* Enable (1) or disable (0) per-stage HIP-event timing for later calls on
  * this thread. */
 cqsa_status cqsa_set_timing(int32_t enable);
+
+/* Enable (1) or disable (0) counting the inner forward's tile decisions
+ * (cqsa_run_stats.kernel_tiles_*) for later cqsa_forward calls on this
+ * thread (a diagnostic: the kernels add one atomic per wave; the counters
+ * live in a small device buffer per GPU and a pinned host copy per thread,
+ * both allocated on first use; cqsa_forward_noalloc does not count). */
+cqsa_status cqsa_set_tile_counting(int32_t enable);
 
 /* Statistics of the last cqsa_forward/cqsa_backward on this thread; waits for
  * that call's timing events to complete. */

@@ -74,7 +74,8 @@ class cqsa_run_stats(ctypes.Structure):
                 ("tiles_full", ctypes.c_int64), ("tiles_clear", ctypes.c_int64),
                 ("tiles_mixed", ctypes.c_int64), ("merge_launches", ctypes.c_int64),
                 ("ms_inner_busy", ctypes.c_double), ("guard_steps", ctypes.c_int64),
-                ("resident_tasks", ctypes.c_int64)]
+                ("resident_tasks", ctypes.c_int64), ("kernel_tiles_masked", ctypes.c_int64),
+                ("kernel_tiles_clear", ctypes.c_int64), ("kernel_tiles_mixed", ctypes.c_int64)]
 
 
 # Every symbol include/cqsa.h declares, with its ctypes signature.
@@ -94,6 +95,9 @@ _SIGS = {
     "cqsa_plan_tile_census": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(ctypes.c_int64),
                                              ctypes.POINTER(ctypes.c_int64),
                                              ctypes.POINTER(ctypes.c_int64)]),
+    "cqsa_plan_fwd_tile_decisions": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(ctypes.c_int64),
+                                                    ctypes.POINTER(ctypes.c_int64),
+                                                    ctypes.POINTER(ctypes.c_int64)]),
     "cqsa_plan_destroy": (None, [ctypes.c_void_p]),
     "cqsa_forward": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(cqsa_tensor),
                                     ctypes.POINTER(cqsa_tensor), ctypes.POINTER(cqsa_tensor),
@@ -111,6 +115,7 @@ _SIGS = {
                                      ctypes.c_float, ctypes.c_void_p]),
     "cqsa_set_allocator": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
     "cqsa_set_timing": (ctypes.c_int, [ctypes.c_int32]),
+    "cqsa_set_tile_counting": (ctypes.c_int, [ctypes.c_int32]),
     "cqsa_last_stats": (ctypes.c_int, [ctypes.POINTER(cqsa_run_stats)]),
     "cqsa_release_workspace": (ctypes.c_int, []),
     "cqsa_last_error": (ctypes.c_char_p, []),
@@ -243,6 +248,14 @@ class Plan:
                                            ctypes.byref(m)), "cqsa_plan_tile_census")
         return f.value, c.value, m.value
 
+    def fwd_tile_decisions(self):
+        """(masked, clear, mixed) the inner forward's tile decisions should
+        count (cqsa_plan_fwd_tile_decisions)."""
+        f, c, m = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+        _check(lib().cqsa_plan_fwd_tile_decisions(self.handle, ctypes.byref(f), ctypes.byref(c),
+                                                  ctypes.byref(m)), "cqsa_plan_fwd_tile_decisions")
+        return f.value, c.value, m.value
+
 
 def cqsa_plan(L, H, d, causal, device_budget_bytes=0, opts=None):
     """Plan a call (host only).  opts: a cqsa_plan_opts (make_opts) or None."""
@@ -335,6 +348,10 @@ def cqsa_backward(plan, Q, K, V, O, LSE, dO, dQ, dK, dV, scale=0.0, stream=None)
 
 def cqsa_set_timing(enable):
     _check(lib().cqsa_set_timing(int(bool(enable))), "cqsa_set_timing")
+
+
+def cqsa_set_tile_counting(enable):
+    _check(lib().cqsa_set_tile_counting(int(bool(enable))), "cqsa_set_tile_counting")
 
 
 def cqsa_last_stats():

@@ -42,7 +42,9 @@ namespace cqsa {
 // work groups fit three to a CU, and for d = 224, 256, which would spill.
 template <int D> constexpr int fwd_waves() { return (D >= 96 && D <= 192) ? 8 : 4; }
 
-template <typename E, int D, int MODE>
+// COUNT: the launch counts its tile decisions (FwdArgs::tile_count); a
+// separate instance, so that the kernel without counting does no counting work
+template <typename E, int D, int MODE, bool COUNT>
 __global__ void __launch_bounds__(64 * fwd_waves<D>(), (lds_row_elems<D>() > 128 ? 1 : 2)) attn_fwd_mfma(const FwdArgs a) {
   constexpr int WAVES = fwd_waves<D>(), NT = 64 * WAVES;
   constexpr int BM = 32 * WAVES, BN = 64;
@@ -274,6 +276,8 @@ __global__ void __launch_bounds__(64 * fwd_waves<D>(), (lds_row_elems<D>() > 128
       sstore(k, tl[k], tor[k]);
     }
   int buf = 0;
+  // this wave's tile decisions (wave-uniform): masked for the wave, clear, mixed
+  uint32_t n_masked = 0u, n_clear = 0u, n_mixed = 0u;
   while (tl[0] < nkt) {
     const int kt = tl[0];
     // this wave's loads of tile kt have landed: only those of the tile after
@@ -294,8 +298,13 @@ __global__ void __launch_bounds__(64 * fwd_waves<D>(), (lds_row_elems<D>() > 128
     const uint32_t kor = tor[0], kand = tand[0];
     const int k0 = kt * BN, k1 = (k0 + BN - 1 < L ? k0 + BN - 1 : L - 1);
     const bool wfull = !wave_live || (wand & kand) != 0u || (causal && k0 > wq1);
+    if (COUNT) n_masked += wfull ? 1u : 0u;
     if (!wfull) {
       const bool wclear = (wor & kor) == 0u && (!causal || k1 <= q0w) && (k0 + BN <= L);
+      if (COUNT) {
+        n_clear += wclear ? 1u : 0u;
+        n_mixed += wclear ? 0u : 1u;
+      }
       const bool use_bits = (qor & kor) != 0u;
       const char* Kb = kst[buf];
       const char* Vb = vst[buf];
@@ -445,6 +454,11 @@ __global__ void __launch_bounds__(64 * fwd_waves<D>(), (lds_row_elems<D>() > 128
 
   const float l_tot = l_run + swap_halves(l_run);
   const float lt_tot = lt_run + swap_halves(lt_run);
+  if (COUNT && wave_live && lane == 0) {
+    atomicAdd(a.tile_count + 0, (unsigned long long)n_masked);
+    atomicAdd(a.tile_count + 1, (unsigned long long)n_clear);
+    atomicAdd(a.tile_count + 2, (unsigned long long)n_mixed);
+  }
   if (!qvalid) return;
   if (MODE == kModeStats) {
     float* accp = a.acc + tj * a.acc_stride + (int64_t(b) * L + myq) * rs + int64_t(h) * D;
@@ -592,12 +606,20 @@ __global__ void __launch_bounds__(256) attn_fwd_f32(const FwdArgs a) {
   }
 }
 
+template <typename E, int D, int MODE>
+static void launch_mfma_mode(const FwdArgs& a, int64_t n, hipStream_t s) {
+  if (a.tile_count)
+    hipLaunchKernelGGL((attn_fwd_mfma<E, D, MODE, true>), dim3(unsigned(n)), dim3(64 * fwd_waves<D>()), 0, s, a);
+  else
+    hipLaunchKernelGGL((attn_fwd_mfma<E, D, MODE, false>), dim3(unsigned(n)), dim3(64 * fwd_waves<D>()), 0, s, a);
+}
+
 template <typename E, int D>
 static hipError_t launch_mfma(FwdMode mode, const FwdArgs& a, int64_t n, hipStream_t s) {
   if (mode == kModeStats)
-    hipLaunchKernelGGL((attn_fwd_mfma<E, D, kModeStats>), dim3(unsigned(n)), dim3(64 * fwd_waves<D>()), 0, s, a);
+    launch_mfma_mode<E, D, kModeStats>(a, n, s);
   else
-    hipLaunchKernelGGL((attn_fwd_mfma<E, D, kModeFinal>), dim3(unsigned(n)), dim3(64 * fwd_waves<D>()), 0, s, a);
+    launch_mfma_mode<E, D, kModeFinal>(a, n, s);
   return hipGetLastError();
 }
 

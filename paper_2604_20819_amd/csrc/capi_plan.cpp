@@ -225,6 +225,23 @@ cqsa_status cqsa_plan_tile_census(const cqsa_plan_t* p, int64_t* full, int64_t* 
   return CQSA_OK;
 }
 
+cqsa_status cqsa_plan_fwd_tile_decisions(const cqsa_plan_t* p, int64_t* masked, int64_t* clear,
+                                         int64_t* mixed) {
+  clear_error();
+  if (!p || !masked || !clear || !mixed)
+    return fail(CQSA_ERR_INVALID_ARG, "cqsa_plan_fwd_tile_decisions: NULL argument");
+  if (p->opts.dtype == CQSA_F32)
+    return fail(CQSA_ERR_UNSUPPORTED, "cqsa_plan_fwd_tile_decisions: fp32 plans are not counted");
+  int64_t acc[3] = {0, 0, 0};
+  const int32_t rows = fwd_rows_per_wg(p->opts.dtype, p->g.d);
+  for (const Task& t : p->tasks) fwd_tile_decisions(t, p->g.causal != 0, rows, acc);
+  const int64_t bh = int64_t(p->opts.B) * p->g.H;
+  *masked = acc[0] * bh;
+  *clear = acc[1] * bh;
+  *mixed = acc[2] * bh;
+  return CQSA_OK;
+}
+
 void cqsa_plan_destroy(cqsa_plan_t* p) { delete p; }
 
 const char* cqsa_last_error(void) { return last_error_cstr(); }

@@ -220,6 +220,11 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
   hipEvent_t& ws_free = noalloc ? C->scratch_free : C->ws_free;
   bool& ws_free_valid = noalloc ? C->scratch_free_valid : C->ws_free_valid;
   if (ws_free_valid) CQSA_HIP(hipStreamWaitEvent(st, ws_free, 0));
+  // tile-decision counters, zeroed before every inner launch (the other
+  // streams start after events recorded on st below)
+  unsigned long long* tile_count = nullptr;
+  if (!noalloc && tile_counting_enabled() && o.dtype != CQSA_F32)
+    if ((s = tile_counters_begin(C, st, &tile_count)) != CQSA_OK) return s;
   // With nothing to stage and a single launch group (the direct call, or
   // inputs read in place with every task in one launch) the whole call runs
   // on the caller's stream: each hop between streams costs the GPU an event
@@ -259,6 +264,7 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
     a.acc = Od; a.m = LSE; a.l = nullptr; a.lt = nullptr;
     a.tab = d_tab; a.tasks = d_tasks; a.ntask = 1;
     a.B = int32_t(B); a.H = int32_t(H); a.causal = p->g.causal; a.scale_log2 = scale_log2;
+    a.tile_count = tile_count;
     const int64_t wgs = ((L + rows_wg - 1) / rows_wg) * B * H;
     auto sp = span_begin(st);
     CQSA_HIP(launch_fwd(o.dtype, int(d), kModeFinal, a, wgs, st));
@@ -390,6 +396,7 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
       a.acc_stride = a.st_stride = int64_t(sub_bytes / 4);
       a.tab = d_tab; a.tasks = d_tasks + G.task0; a.ntask = int32_t(G.count);
       a.B = int32_t(B); a.H = int32_t(H); a.causal = p->g.causal; a.scale_log2 = scale_log2;
+      a.tile_count = tile_count;
       {
         auto sp = span_begin(ls);
         CQSA_HIP(launch_fwd(o.dtype, int(d), kModeStats, a, wgs, ls));
@@ -471,6 +478,7 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
     span_end(sp, st, kStFinal);
   }
   if (rec.timing) CQSA_HIP(hipEventRecord(rec.wall1, st));
+  if (tile_count && (s = tile_counters_end(C, rec, st)) != CQSA_OK) return s;
   CQSA_HIP(hipEventRecord(ws_free, st));
   ws_free_valid = true;
   if (!noalloc) release_workspace(C, &ws, st);

@@ -44,6 +44,11 @@ struct FwdArgs {
   float scale_log2;     // softmax scale * log2(e)
   int32_t in_place;     // 1: q/k/v are the caller's tensors, rows by the runs
   int64_t Lg;           // rows per batch element of q/k/v when in_place
+  // when not null, each wave adds its tile decisions over the key tiles its
+  // work group visits: [0] masked for the wave (skipped), [1] clear, [2]
+  // mixed (16-bit kernels, launched as their counting instance; waves with
+  // no query of the task add nothing)
+  unsigned long long* tile_count;
 };
 
 // Gather-merge of one launch group's task statistics into the global
@@ -141,6 +146,9 @@ hipError_t launch_stage(const StageArgs& a, hipStream_t s);
 hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t s);
 // dst[i] = src[i] rounded to the 16-bit dtype `dt` (nearest even), i < n.
 hipError_t launch_cast_out(const float* src, void* dst, int64_t n, cqsa_dtype dt, hipStream_t s);
+// Zeroes n 64-bit counters (a kernel, not a memset, so that the call stays
+// free of memset nodes).
+hipError_t launch_zero_u64(unsigned long long* p, int n, hipStream_t s);
 // D[(b * H + h) * ld + g] = sum_d dO * O over rows g < L of B batch elements
 // of [B, L, H, d] inputs (ld = L for whole tensors; a chunk of rows passes
 // its first output and the full sequence length).

@@ -264,4 +264,15 @@ hipError_t launch_grad_merge(const GradMergeArgs& a, int64_t blocks, hipStream_t
   return hipGetLastError();
 }
 
+__global__ void __launch_bounds__(64) zero_u64_kernel(unsigned long long* p, int n) {
+  const int i = threadIdx.x;
+  if (i < n) p[i] = 0ull;
+}
+
+hipError_t launch_zero_u64(unsigned long long* p, int n, hipStream_t s) {
+  if (n <= 0 || n > 64) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(zero_u64_kernel, dim3(1), dim3(64), 0, s, p, n);
+  return hipGetLastError();
+}
+
 }  // namespace cqsa

@@ -382,6 +382,35 @@ std::vector<int32_t> key_strip_order(const Task& t, bool causal, int32_t rows) {
   return longest_first(live);
 }
 
+void fwd_tile_decisions(const Task& t, bool causal, int32_t rows, int64_t out[3]) {
+  const int64_t L = t.L_local, nkt = (L + kBlock - 1) / kBlock;
+  const int64_t ns = (L + rows - 1) / rows;
+  std::vector<int64_t> visited;
+  for (int64_t s = 0; s < ns; ++s) {
+    const int64_t first = s * rows, last = std::min(L, first + rows) - 1;
+    uint32_t qand = 0xFFFFFFFFu;  // AND over the work group's blocks
+    for (int64_t b = first / kBlock; b <= last / kBlock; ++b) qand &= t.blk_and[size_t(b)];
+    // key tile k is block k: live for the work group unless causally past its
+    // last query or sharing a bit of the AND with it
+    visited.clear();
+    for (int64_t k = 0; k < nkt; ++k)
+      if (!(causal && k * kBlock > last) && (qand & t.blk_and[size_t(k)]) == 0u) visited.push_back(k);
+    for (int64_t q0 = first; q0 <= last; q0 += 32) {
+      const int64_t q1 = std::min(q0 + 31, L - 1);
+      const uint32_t wor = t.blk_or[size_t(q0 / kBlock)], wand = t.blk_and[size_t(q0 / kBlock)];
+      for (int64_t k : visited) {
+        const int64_t k0 = k * kBlock, k1 = std::min(k0 + kBlock - 1, L - 1);
+        if ((wand & t.blk_and[size_t(k)]) != 0u || (causal && k0 > q1))
+          ++out[0];
+        else if ((wor & t.blk_or[size_t(k)]) == 0u && (!causal || k1 <= q0) && k0 + kBlock <= L)
+          ++out[1];
+        else
+          ++out[2];
+      }
+    }
+  }
+}
+
 void pack_image(const std::vector<Task>& tasks, const SegmentCover& sc, int32_t H, bool causal,
                 int32_t fwd_rows, int32_t dq_rows, int32_t kv_rows, std::vector<Group>* groups,
                 std::vector<uint8_t>* image, std::vector<TableOffsets>* offs) {

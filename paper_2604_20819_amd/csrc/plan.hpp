@@ -202,6 +202,13 @@ int dkdv_rows_per_wg(int d);
 std::vector<int32_t> query_strip_order(const Task& t, bool causal, int32_t rows);
 std::vector<int32_t> key_strip_order(const Task& t, bool causal, int32_t rows);
 
+// The inner forward's tile decisions on one (batch element, head) of task t
+// (App. A.2), with the kernel's rules at `rows` query rows per work group
+// and 32 per wave: out[0] masked for a wave, out[1] clear, out[2] mixed,
+// over the 64-key tiles each work group visits and the waves holding a
+// query.  O(tiles x waves) per task.
+void fwd_tile_decisions(const Task& t, bool causal, int32_t rows, int64_t out[3]);
+
 inline uint64_t align_up(uint64_t x, uint64_t a = 256) { return (x + a - 1) / a * a; }
 
 }  // namespace cqsa

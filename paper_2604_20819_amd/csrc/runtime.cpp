@@ -2,6 +2,7 @@
 // the caller-allocator hook, per-stage timing, and the C-ABI entry points
 // that are not planning or compute.
 #include "runtime.hpp"
+#include "kernels.hpp"
 #include "streamer.hpp"
 
 #include <algorithm>
@@ -24,6 +25,7 @@ void* (*g_alloc)(size_t, void*) = nullptr;
 void (*g_release)(void*, void*) = nullptr;
 void* g_hook_ctx = nullptr;
 thread_local bool t_timing = false;
+thread_local bool t_tile_counting = false;
 thread_local CallRecord t_record;
 }  // namespace
 
@@ -169,7 +171,9 @@ void CallRecord::reset() {
   host_merge_ms = 0.0;
   host_final_ms = 0.0;
   std::memset(&stats, 0, sizeof(stats));
+  stats.kernel_tiles_masked = stats.kernel_tiles_clear = stats.kernel_tiles_mixed = -1;
   timing = t_timing;
+  counted = false;
 }
 
 hipEvent_t CallRecord::make() {
@@ -181,6 +185,32 @@ hipEvent_t CallRecord::make() {
 
 CallRecord& call_record() { return t_record; }
 bool timing_enabled() { return t_timing; }
+bool tile_counting_enabled() { return t_tile_counting; }
+
+cqsa_status tile_counters_begin(DevCtx* c, hipStream_t s, unsigned long long** out) {
+  if (!c->tile_count) {
+    void* p = nullptr;
+    CQSA_HIP(hipMalloc(&p, 64));
+    c->tile_count = (unsigned long long*)p;
+  }
+  CQSA_HIP(launch_zero_u64(c->tile_count, 3, s));
+  *out = c->tile_count;
+  return CQSA_OK;
+}
+
+cqsa_status tile_counters_end(DevCtx* c, CallRecord& rec, hipStream_t s) {
+  if (!rec.tile_host) {
+    void* p = nullptr;
+    CQSA_HIP(hipHostMalloc(&p, 64, hipHostMallocDefault));
+    rec.tile_host = (unsigned long long*)p;
+  }
+  if (!rec.tile_done) CQSA_HIP(hipEventCreateWithFlags(&rec.tile_done, hipEventDisableTiming));
+  CQSA_HIP(hipMemcpyAsync(rec.tile_host, c->tile_count, 3 * sizeof(unsigned long long),
+                          hipMemcpyDeviceToHost, s));
+  CQSA_HIP(hipEventRecord(rec.tile_done, s));
+  rec.counted = true;
+  return CQSA_OK;
+}
 
 cqsa_status check_tensor(const cqsa_tensor* t, const char* name, const cqsa_plan_t* p,
                          cqsa_dtype want, cqsa_mem where) {
@@ -249,6 +279,12 @@ cqsa_status cqsa_set_timing(int32_t enable) {
   return CQSA_OK;
 }
 
+cqsa_status cqsa_set_tile_counting(int32_t enable) {
+  clear_error();
+  t_tile_counting = enable != 0;
+  return CQSA_OK;
+}
+
 cqsa_status cqsa_last_stats(cqsa_run_stats* out) {
   clear_error();
   if (!out) return fail(CQSA_ERR_INVALID_ARG, "cqsa_last_stats: out is NULL");
@@ -291,6 +327,13 @@ cqsa_status cqsa_last_stats(cqsa_run_stats* out) {
     }
     if (ce > cs) busy += ce - cs;
     s.ms_inner_busy = busy;
+  }
+  if (r.counted) {
+    hipError_t e = hipEventSynchronize(r.tile_done);
+    if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+    s.kernel_tiles_masked = int64_t(r.tile_host[0]);
+    s.kernel_tiles_clear = int64_t(r.tile_host[1]);
+    s.kernel_tiles_mixed = int64_t(r.tile_host[2]);
   }
   *out = s;
   return CQSA_OK;

@@ -42,6 +42,9 @@ struct DevCtx {
   void* scratch = nullptr;
   hipEvent_t scratch_free = nullptr;
   bool scratch_free_valid = false;
+  // the inner forward's tile-decision counters (cqsa_set_tile_counting),
+  // allocated on first use; calls reach them in workspace order
+  unsigned long long* tile_count = nullptr;
   std::mutex mu;
 };
 
@@ -72,6 +75,11 @@ cqsa_status upload_image(DevCtx* c, const std::vector<uint8_t>& image, void* dst
 enum Stage { kStStage = 0, kStInner, kStMerge, kStFinal, kStD2H, kStCount };
 struct CallRecord {
   bool timing = false;
+  // tile counting of the last call: the counters' copy in pinned host memory
+  // (allocated on first use, per thread) and the event after that copy
+  bool counted = false;
+  unsigned long long* tile_host = nullptr;
+  hipEvent_t tile_done = nullptr;
   std::vector<hipEvent_t> owned;                       // destroyed on reset
   std::vector<std::pair<hipEvent_t, hipEvent_t>> spans[kStCount];
   hipEvent_t wall0 = nullptr, wall1 = nullptr;
@@ -83,6 +91,11 @@ struct CallRecord {
 };
 CallRecord& call_record();
 bool timing_enabled();
+bool tile_counting_enabled();
+// The device's tile counters, zeroed on stream s (allocated on first use).
+cqsa_status tile_counters_begin(DevCtx* c, hipStream_t s, unsigned long long** out);
+// Copies the counters to the call record after the work on s (the call's end).
+cqsa_status tile_counters_end(DevCtx* c, CallRecord& rec, hipStream_t s);
 
 // Checks shared by forward and backward.
 cqsa_status check_tensor(const cqsa_tensor* t, const char* name, const cqsa_plan_t* p,
