@@ -200,15 +200,19 @@ typedef struct {
                                        backward staging slots, or the backward tasks per launch
                                        whose local gradients the workspace holds; 0 for the
                                        undecomposed path and for one in-place task per launch) */
-  /* The inner forward's own tile decisions (App. A.2), counted on the device
-   * when tile counting is enabled (cqsa_set_tile_counting) for a cqsa_forward
-   * with 16-bit inputs, else -1.  Unit: one wave of 32 consecutive local
-   * queries (every wave holding a query of its task) against one 64-key tile
-   * its work group visits, summed over tasks, batch elements and heads:
+  /* The kernels' own tile decisions (App. A.2), counted on the device when
+   * tile counting is enabled (cqsa_set_tile_counting), else -1.  Forward
+   * (16-bit inputs) and the backward's dQ kernel: one wave of 32 consecutive
+   * local queries (every wave holding a query of its task) against one 64-key
+   * tile its work group visits, summed over tasks, batch elements and heads:
    * masked (every pair masked for the wave: skipped), clear (no pair masked:
    * no mask work), mixed (per-pair tests).  cqsa_plan_fwd_tile_decisions
-   * gives the counts the block summaries predict. */
+   * and cqsa_plan_bwd_tile_decisions give the counts the block summaries
+   * predict. */
   int64_t kernel_tiles_masked, kernel_tiles_clear, kernel_tiles_mixed;
+  /* Backward only: the dK/dV kernel's decisions, one group of 32 consecutive
+   * local keys against one 32-query tile its work group visits. */
+  int64_t kernel_kv_tiles_masked, kernel_kv_tiles_clear, kernel_kv_tiles_mixed;
 } cqsa_run_stats;
 
 /* Fill `o` with the defaults listed in cqsa_plan_opts. */
@@ -260,6 +264,19 @@ cqsa_status cqsa_plan_tile_census(const cqsa_plan_t* plan, int64_t* full, int64_
  * plans (their kernel is not counted). */
 cqsa_status cqsa_plan_fwd_tile_decisions(const cqsa_plan_t* plan, int64_t* masked,
                                          int64_t* clear, int64_t* mixed);
+/* The backward kernels' tile decisions this plan predicts (16-bit plans).
+ * dq[0..2]: the dQ kernel's masked, clear, mixed counts, by the rules of
+ * cqsa_plan_fwd_tile_decisions at its work-group height (256 query rows at
+ * d = 96 ... 160, else 128).  kv[0..2]: the dK/dV kernel's, for key strips of
+ * R rows (256 at d = 96, 128, else 128), groups of 32 keys and 32-query
+ * tiles: a work group visits query tile t unless t lies causally wholly
+ * before its first key or the AND of its blocks' summaries meets the
+ * summaries of t's block; a visited tile is masked for a key group when the
+ * group's block AND meets the tile's or it lies causally wholly before the
+ * group's first key, clear when the group's block OR misses the tile's and,
+ * causally, the tile starts at or after the group's last key, mixed
+ * otherwise.  Summed over tasks times B x H. */
+cqsa_status cqsa_plan_bwd_tile_decisions(const cqsa_plan_t* plan, int64_t* dq, int64_t* kv);
 void cqsa_plan_destroy(cqsa_plan_t* plan);                 /* NULL is a no-op */
 
 /* Decomposed forward (Alg. 1 computed with the max-shifted merge of App. A.1).
@@ -344,11 +361,12 @@ cqsa_status cqsa_set_allocator(void* (*alloc)(size_t bytes, void* ctx),
  * this thread. */
 cqsa_status cqsa_set_timing(int32_t enable);
 
-/* Enable (1) or disable (0) counting the inner forward's tile decisions
- * (cqsa_run_stats.kernel_tiles_*) for later cqsa_forward calls on this
- * thread (a diagnostic: the kernels add one atomic per wave; the counters
- * live in a small device buffer per GPU and a pinned host copy per thread,
- * both allocated on first use; cqsa_forward_noalloc does not count). */
+/* Enable (1) or disable (0) counting the kernels' tile decisions
+ * (cqsa_run_stats.kernel_tiles_*, kernel_kv_tiles_*) for later cqsa_forward
+ * and cqsa_backward calls on this thread (a diagnostic: the launches run
+ * counting instances of the kernels, which add one atomic per wave; the
+ * counters live in a small device buffer per GPU and a pinned host copy per
+ * thread, both allocated on first use; cqsa_forward_noalloc does not count). */
 cqsa_status cqsa_set_tile_counting(int32_t enable);
 
 /* Statistics of the last cqsa_forward/cqsa_backward on this thread; waits for

@@ -75,7 +75,9 @@ class cqsa_run_stats(ctypes.Structure):
                 ("tiles_mixed", ctypes.c_int64), ("merge_launches", ctypes.c_int64),
                 ("ms_inner_busy", ctypes.c_double), ("guard_steps", ctypes.c_int64),
                 ("resident_tasks", ctypes.c_int64), ("kernel_tiles_masked", ctypes.c_int64),
-                ("kernel_tiles_clear", ctypes.c_int64), ("kernel_tiles_mixed", ctypes.c_int64)]
+                ("kernel_tiles_clear", ctypes.c_int64), ("kernel_tiles_mixed", ctypes.c_int64),
+                ("kernel_kv_tiles_masked", ctypes.c_int64), ("kernel_kv_tiles_clear", ctypes.c_int64),
+                ("kernel_kv_tiles_mixed", ctypes.c_int64)]
 
 
 # Every symbol include/cqsa.h declares, with its ctypes signature.
@@ -97,6 +99,8 @@ _SIGS = {
                                              ctypes.POINTER(ctypes.c_int64)]),
     "cqsa_plan_fwd_tile_decisions": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(ctypes.c_int64),
                                                     ctypes.POINTER(ctypes.c_int64),
+                                                    ctypes.POINTER(ctypes.c_int64)]),
+    "cqsa_plan_bwd_tile_decisions": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(ctypes.c_int64),
                                                     ctypes.POINTER(ctypes.c_int64)]),
     "cqsa_plan_destroy": (None, [ctypes.c_void_p]),
     "cqsa_forward": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(cqsa_tensor),
@@ -255,6 +259,14 @@ class Plan:
         _check(lib().cqsa_plan_fwd_tile_decisions(self.handle, ctypes.byref(f), ctypes.byref(c),
                                                   ctypes.byref(m)), "cqsa_plan_fwd_tile_decisions")
         return f.value, c.value, m.value
+
+    def bwd_tile_decisions(self):
+        """((dQ masked, clear, mixed), (dK/dV masked, clear, mixed)) the
+        backward kernels' tile decisions should count
+        (cqsa_plan_bwd_tile_decisions)."""
+        dq, kv = (ctypes.c_int64 * 3)(), (ctypes.c_int64 * 3)()
+        _check(lib().cqsa_plan_bwd_tile_decisions(self.handle, dq, kv), "cqsa_plan_bwd_tile_decisions")
+        return tuple(dq), tuple(kv)
 
 
 def cqsa_plan(L, H, d, causal, device_budget_bytes=0, opts=None):

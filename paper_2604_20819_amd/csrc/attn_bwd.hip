@@ -36,7 +36,9 @@ template <int D> constexpr int dq_waves() { return (D >= 96 && D <= 160) ? 8 : 4
 // LOCAL (BwdArgs::local_out) is a template parameter: a run-time branch in
 // the epilogue changes the register allocation of the whole kernel (the
 // dK/dV kernel at d = 128 then spills).
-template <typename E, int D, bool LOCAL>
+// COUNT: the launch counts its tile decisions (BwdArgs::tile_count, [0..2]);
+// a separate instance, so that the kernel without counting does no counting work
+template <typename E, int D, bool LOCAL, bool COUNT>
 __global__ void __launch_bounds__(64 * dq_waves<D>(), (lds_row_elems<D>() > 128 ? 1 : 2)) attn_bwd_dq(const BwdArgs a) {
   constexpr int WAVES = dq_waves<D>(), NT = 64 * WAVES;
   constexpr int BM = 32 * WAVES, BN = 64;
@@ -252,6 +254,8 @@ __global__ void __launch_bounds__(64 * dq_waves<D>(), (lds_row_elems<D>() > 128 
       sstore(k, tl[k], tor[k]);
     }
   int buf = 0;
+  // this wave's tile decisions (wave-uniform): masked for the wave, clear, mixed
+  uint32_t n_masked = 0u, n_clear = 0u, n_mixed = 0u;
   while (tl[0] < nkt) {
     const int kt = tl[0];
     // this wave's loads of tile kt have landed: only those of the tile after
@@ -270,8 +274,13 @@ __global__ void __launch_bounds__(64 * dq_waves<D>(), (lds_row_elems<D>() > 128 
     const uint32_t kor = tor[0], kand = tand[0];
     const int k0 = kt * BN, k1 = (k0 + BN - 1 < L ? k0 + BN - 1 : L - 1);
     const bool wfull = !wave_live || (wand & kand) != 0u || (causal && k0 > wq1);
+    if (COUNT) n_masked += wfull ? 1u : 0u;
     if (!wfull) {
       const bool wclear = (wor & kor) == 0u && (!causal || k1 <= q0w) && (k0 + BN <= L);
+      if (COUNT) {
+        n_clear += wclear ? 1u : 0u;
+        n_mixed += wclear ? 0u : 1u;
+      }
       const bool use_bits = (qor & kor) != 0u;
       const char* Kb = kst[buf];
       const char* Vb = vst[buf];
@@ -364,6 +373,11 @@ __global__ void __launch_bounds__(64 * dq_waves<D>(), (lds_row_elems<D>() > 128 
     trw[AHEAD] = row2;
     buf = buf + 1 == NBUF ? 0 : buf + 1;
   }
+  if (COUNT && wave_live && lane == 0) {
+    atomicAdd(a.tile_count + 0, (unsigned long long)n_masked);
+    atomicAdd(a.tile_count + 1, (unsigned long long)n_clear);
+    atomicAdd(a.tile_count + 2, (unsigned long long)n_mixed);
+  }
   if (!qvalid) return;
   // global rows accumulate (a single task holds a token once and the dQ
   // launches of a call are ordered on one stream); a task-local buffer is
@@ -406,7 +420,9 @@ template <int D> constexpr int dkdv_waves() { return dkdv_key_waves<D>() * dkdv_
 // of the padded rows holds a CU.
 template <int D> constexpr int dkdv_min_waves() { return lds_row_elems<D>() > 128 ? 1 : 2; }
 
-template <typename E, int D, bool LOCAL>
+// COUNT: as for the dQ kernel, into BwdArgs::tile_count[3..5]; one count per
+// 32-key group (the first of the waves that share one when the columns split)
+template <typename E, int D, bool LOCAL, bool COUNT>
 __global__ void __launch_bounds__(64 * dkdv_waves<D>(), dkdv_min_waves<D>()) attn_bwd_dkdv(const BwdArgs a) {
   // 32-query tiles (two per 64-token summary block) keep the registers and
   // LDS within two waves per SIMD
@@ -695,6 +711,8 @@ __global__ void __launch_bounds__(64 * dkdv_waves<D>(), dkdv_min_waves<D>()) att
       sstore(k, tl[k]);
     }
   int buf = 0;
+  // this wave's tile decisions (wave-uniform): masked for the wave, clear, mixed
+  uint32_t n_masked = 0u, n_clear = 0u, n_mixed = 0u;
   while (tl[0] < nqt) {
     const int qt = tl[0];
     // this wave's loads of tile qt have landed: only the loads of the tiles
@@ -713,8 +731,13 @@ __global__ void __launch_bounds__(64 * dkdv_waves<D>(), dkdv_min_waves<D>()) att
     const int q0 = qt * BQ;
     const uint32_t qor = tor[0], qand = tand[0];
     const bool wfull = !wave_live || (wand & qand) != 0u || (causal && q0 + BQ - 1 < k0w);
+    if (COUNT) n_masked += wfull ? 1u : 0u;
     if (!wfull) {
       const bool wclear = (wor & qor) == 0u && (!causal || q0 >= wk1);
+      if (COUNT) {
+        n_clear += wclear ? 1u : 0u;
+        n_mixed += wclear ? 0u : 1u;
+      }
       const bool use_bits = (kor & qor) != 0u;
       const uint32_t kmask = use_bits ? kbits : 0u;
       const char* qsb = qs[buf];
@@ -824,6 +847,11 @@ __global__ void __launch_bounds__(64 * dkdv_waves<D>(), dkdv_min_waves<D>()) att
     buf = buf + 1 == NBUF ? 0 : buf + 1;
   }
   __builtin_amdgcn_s_waitcnt(0x0F70);  // the V fill has landed even when no tile was live
+  if (COUNT && wave_live && db0 == 0 && lane == 0) {
+    atomicAdd(a.tile_count + 3, (unsigned long long)n_masked);
+    atomicAdd(a.tile_count + 4, (unsigned long long)n_clear);
+    atomicAdd(a.tile_count + 5, (unsigned long long)n_mixed);
+  }
   if (!kvalid) return;
   // global rows accumulate; a task-local buffer is stored (as for dQ, the
   // scaled dK is rounded before the addition)
@@ -853,21 +881,37 @@ __global__ void __launch_bounds__(64 * dkdv_waves<D>(), dkdv_min_waves<D>()) att
   }
 }
 
+template <typename E, int D, bool LOCAL>
+static void launch_dq_l(const BwdArgs& a, int64_t n, hipStream_t s) {
+  if (a.tile_count)
+    hipLaunchKernelGGL((attn_bwd_dq<E, D, LOCAL, true>), dim3(unsigned(n)), dim3(64 * dq_waves<D>()), 0, s, a);
+  else
+    hipLaunchKernelGGL((attn_bwd_dq<E, D, LOCAL, false>), dim3(unsigned(n)), dim3(64 * dq_waves<D>()), 0, s, a);
+}
+
 template <typename E, int D>
 static hipError_t launch_dq_t(const BwdArgs& a, int64_t n, hipStream_t s) {
   if (a.local_out)
-    hipLaunchKernelGGL((attn_bwd_dq<E, D, true>), dim3(unsigned(n)), dim3(64 * dq_waves<D>()), 0, s, a);
+    launch_dq_l<E, D, true>(a, n, s);
   else
-    hipLaunchKernelGGL((attn_bwd_dq<E, D, false>), dim3(unsigned(n)), dim3(64 * dq_waves<D>()), 0, s, a);
+    launch_dq_l<E, D, false>(a, n, s);
   return hipGetLastError();
+}
+
+template <typename E, int D, bool LOCAL>
+static void launch_dkdv_l(const BwdArgs& a, int64_t n, hipStream_t s) {
+  if (a.tile_count)
+    hipLaunchKernelGGL((attn_bwd_dkdv<E, D, LOCAL, true>), dim3(unsigned(n)), dim3(64 * dkdv_waves<D>()), 0, s, a);
+  else
+    hipLaunchKernelGGL((attn_bwd_dkdv<E, D, LOCAL, false>), dim3(unsigned(n)), dim3(64 * dkdv_waves<D>()), 0, s, a);
 }
 
 template <typename E, int D>
 static hipError_t launch_dkdv_t(const BwdArgs& a, int64_t n, hipStream_t s) {
   if (a.local_out)
-    hipLaunchKernelGGL((attn_bwd_dkdv<E, D, true>), dim3(unsigned(n)), dim3(64 * dkdv_waves<D>()), 0, s, a);
+    launch_dkdv_l<E, D, true>(a, n, s);
   else
-    hipLaunchKernelGGL((attn_bwd_dkdv<E, D, false>), dim3(unsigned(n)), dim3(64 * dkdv_waves<D>()), 0, s, a);
+    launch_dkdv_l<E, D, false>(a, n, s);
   return hipGetLastError();
 }
 

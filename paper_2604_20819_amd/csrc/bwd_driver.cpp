@@ -183,6 +183,11 @@ cqsa_status backward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa
   hipEvent_t* ev_chunk = &C->sync_events[4 + 4 * nslot];  // preprocess done with the slot
   const hipStream_t cs = C->copy, qs = C->lane, ms = C->aux;
   if (C->ws_free_valid) CQSA_HIP(hipStreamWaitEvent(st, C->ws_free, 0));
+  // tile-decision counters, zeroed before every kernel (the other streams
+  // start after events recorded on st below)
+  unsigned long long* tile_count = nullptr;
+  if (tile_counting_enabled())
+    if ((s = tile_counters_begin(C, st, 6, &tile_count)) != CQSA_OK) return s;
   CQSA_HIP(hipEventRecord(ev_start, st));
   CQSA_HIP(hipStreamWaitEvent(cs, ev_start, 0));
   if ((s = upload_image(C, p->packed, d_tab, cs)) != CQSA_OK) return s;
@@ -295,6 +300,7 @@ cqsa_status backward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa
     a.B = int32_t(B); a.H = int32_t(H); a.causal = p->g.causal;
     a.scale_log2 = sc * 1.4426950408889634f; a.scale = sc;
     a.lse = d_lse; a.D = d_D; a.Lg = L;
+    a.tile_count = tile_count;
   };
   const int64_t dq_rows = dq_rows_per_wg(int(d)), kv_rows = dkdv_rows_per_wg(int(d));
   if (batched) {
@@ -468,6 +474,7 @@ cqsa_status backward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa
     CQSA_HIP(hipStreamWaitEvent(st, ev_join, 0));
   }
   if (rec.timing) CQSA_HIP(hipEventRecord(rec.wall1, st));
+  if (tile_count && (s = tile_counters_end(C, rec, st, 6)) != CQSA_OK) return s;
   CQSA_HIP(hipEventRecord(C->ws_free, st));
   C->ws_free_valid = true;
   release_workspace(C, &ws, st);

@@ -242,6 +242,26 @@ cqsa_status cqsa_plan_fwd_tile_decisions(const cqsa_plan_t* p, int64_t* masked, 
   return CQSA_OK;
 }
 
+cqsa_status cqsa_plan_bwd_tile_decisions(const cqsa_plan_t* p, int64_t* dq, int64_t* kv) {
+  clear_error();
+  if (!p || !dq || !kv)
+    return fail(CQSA_ERR_INVALID_ARG, "cqsa_plan_bwd_tile_decisions: NULL argument");
+  if (p->opts.dtype == CQSA_F32)
+    return fail(CQSA_ERR_UNSUPPORTED, "cqsa_plan_bwd_tile_decisions: the backward needs a 16-bit dtype");
+  int64_t a[3] = {0, 0, 0}, b[3] = {0, 0, 0};
+  const int32_t q_rows = dq_rows_per_wg(p->g.d), k_rows = dkdv_rows_per_wg(p->g.d);
+  for (const Task& t : p->tasks) {
+    fwd_tile_decisions(t, p->g.causal != 0, q_rows, a);
+    kv_tile_decisions(t, p->g.causal != 0, k_rows, b);
+  }
+  const int64_t bh = int64_t(p->opts.B) * p->g.H;
+  for (int i = 0; i < 3; ++i) {
+    dq[i] = a[i] * bh;
+    kv[i] = b[i] * bh;
+  }
+  return CQSA_OK;
+}
+
 void cqsa_plan_destroy(cqsa_plan_t* p) { delete p; }
 
 const char* cqsa_last_error(void) { return last_error_cstr(); }

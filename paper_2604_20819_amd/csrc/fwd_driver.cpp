@@ -224,7 +224,7 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
   // streams start after events recorded on st below)
   unsigned long long* tile_count = nullptr;
   if (!noalloc && tile_counting_enabled() && o.dtype != CQSA_F32)
-    if ((s = tile_counters_begin(C, st, &tile_count)) != CQSA_OK) return s;
+    if ((s = tile_counters_begin(C, st, 3, &tile_count)) != CQSA_OK) return s;
   // With nothing to stage and a single launch group (the direct call, or
   // inputs read in place with every task in one launch) the whole call runs
   // on the caller's stream: each hop between streams costs the GPU an event
@@ -478,7 +478,7 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
     span_end(sp, st, kStFinal);
   }
   if (rec.timing) CQSA_HIP(hipEventRecord(rec.wall1, st));
-  if (tile_count && (s = tile_counters_end(C, rec, st)) != CQSA_OK) return s;
+  if (tile_count && (s = tile_counters_end(C, rec, st, 3)) != CQSA_OK) return s;
   CQSA_HIP(hipEventRecord(ws_free, st));
   ws_free_valid = true;
   if (!noalloc) release_workspace(C, &ws, st);

@@ -103,6 +103,11 @@ struct BwdArgs {
   float* dq;
   float* dk;
   float* dv;
+  // when not null, the launches run their counting instances: each dQ wave
+  // adds its tile decisions over the key tiles its work group visits to
+  // [0] masked, [1] clear, [2] mixed, each dK/dV key group its decisions over
+  // the query tiles its work group visits to [3], [4], [5]
+  unsigned long long* tile_count;
 };
 
 // Gather-merge of one launch group's task-local gradients (task j's at

@@ -208,6 +208,10 @@ std::vector<int32_t> key_strip_order(const Task& t, bool causal, int32_t rows);
 // over the 64-key tiles each work group visits and the waves holding a
 // query.  O(tiles x waves) per task.
 void fwd_tile_decisions(const Task& t, bool causal, int32_t rows, int64_t out[3]);
+// The dK/dV kernel's tile decisions on one (batch element, head) of task t:
+// key strips of `rows` rows, groups of 32 keys, 32-query tiles (tile q's
+// summaries are those of block q / 2); out as for fwd_tile_decisions.
+void kv_tile_decisions(const Task& t, bool causal, int32_t rows, int64_t out[3]);
 
 inline uint64_t align_up(uint64_t x, uint64_t a = 256) { return (x + a - 1) / a * a; }
 

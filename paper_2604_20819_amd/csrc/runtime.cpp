@@ -172,8 +172,9 @@ void CallRecord::reset() {
   host_final_ms = 0.0;
   std::memset(&stats, 0, sizeof(stats));
   stats.kernel_tiles_masked = stats.kernel_tiles_clear = stats.kernel_tiles_mixed = -1;
+  stats.kernel_kv_tiles_masked = stats.kernel_kv_tiles_clear = stats.kernel_kv_tiles_mixed = -1;
   timing = t_timing;
-  counted = false;
+  counted = 0;
 }
 
 hipEvent_t CallRecord::make() {
@@ -187,28 +188,28 @@ CallRecord& call_record() { return t_record; }
 bool timing_enabled() { return t_timing; }
 bool tile_counting_enabled() { return t_tile_counting; }
 
-cqsa_status tile_counters_begin(DevCtx* c, hipStream_t s, unsigned long long** out) {
+cqsa_status tile_counters_begin(DevCtx* c, hipStream_t s, int n, unsigned long long** out) {
   if (!c->tile_count) {
     void* p = nullptr;
     CQSA_HIP(hipMalloc(&p, 64));
     c->tile_count = (unsigned long long*)p;
   }
-  CQSA_HIP(launch_zero_u64(c->tile_count, 3, s));
+  CQSA_HIP(launch_zero_u64(c->tile_count, n, s));
   *out = c->tile_count;
   return CQSA_OK;
 }
 
-cqsa_status tile_counters_end(DevCtx* c, CallRecord& rec, hipStream_t s) {
+cqsa_status tile_counters_end(DevCtx* c, CallRecord& rec, hipStream_t s, int n) {
   if (!rec.tile_host) {
     void* p = nullptr;
     CQSA_HIP(hipHostMalloc(&p, 64, hipHostMallocDefault));
     rec.tile_host = (unsigned long long*)p;
   }
   if (!rec.tile_done) CQSA_HIP(hipEventCreateWithFlags(&rec.tile_done, hipEventDisableTiming));
-  CQSA_HIP(hipMemcpyAsync(rec.tile_host, c->tile_count, 3 * sizeof(unsigned long long),
+  CQSA_HIP(hipMemcpyAsync(rec.tile_host, c->tile_count, size_t(n) * sizeof(unsigned long long),
                           hipMemcpyDeviceToHost, s));
   CQSA_HIP(hipEventRecord(rec.tile_done, s));
-  rec.counted = true;
+  rec.counted = n;
   return CQSA_OK;
 }
 
@@ -334,6 +335,11 @@ cqsa_status cqsa_last_stats(cqsa_run_stats* out) {
     s.kernel_tiles_masked = int64_t(r.tile_host[0]);
     s.kernel_tiles_clear = int64_t(r.tile_host[1]);
     s.kernel_tiles_mixed = int64_t(r.tile_host[2]);
+    if (r.counted >= 6) {
+      s.kernel_kv_tiles_masked = int64_t(r.tile_host[3]);
+      s.kernel_kv_tiles_clear = int64_t(r.tile_host[4]);
+      s.kernel_kv_tiles_mixed = int64_t(r.tile_host[5]);
+    }
   }
   *out = s;
   return CQSA_OK;

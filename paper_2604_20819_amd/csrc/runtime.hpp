@@ -77,7 +77,7 @@ struct CallRecord {
   bool timing = false;
   // tile counting of the last call: the counters' copy in pinned host memory
   // (allocated on first use, per thread) and the event after that copy
-  bool counted = false;
+  int counted = 0;                          // counters copied (0: none)
   unsigned long long* tile_host = nullptr;
   hipEvent_t tile_done = nullptr;
   std::vector<hipEvent_t> owned;                       // destroyed on reset
@@ -92,10 +92,13 @@ struct CallRecord {
 CallRecord& call_record();
 bool timing_enabled();
 bool tile_counting_enabled();
-// The device's tile counters, zeroed on stream s (allocated on first use).
-cqsa_status tile_counters_begin(DevCtx* c, hipStream_t s, unsigned long long** out);
-// Copies the counters to the call record after the work on s (the call's end).
-cqsa_status tile_counters_end(DevCtx* c, CallRecord& rec, hipStream_t s);
+// The device's first n tile counters (n <= 8), zeroed on stream s (allocated
+// on first use).
+cqsa_status tile_counters_begin(DevCtx* c, hipStream_t s, int n, unsigned long long** out);
+// Copies the first n counters to the call record after the work on s (the
+// call's end); cqsa_last_stats reads them: [0..2] the forward's or the dQ
+// kernel's decisions, [3..5] the dK/dV kernel's.
+cqsa_status tile_counters_end(DevCtx* c, CallRecord& rec, hipStream_t s, int n);
 
 // Checks shared by forward and backward.
 cqsa_status check_tensor(const cqsa_tensor* t, const char* name, const cqsa_plan_t* p,
