@@ -308,90 +308,120 @@ __global__ void __launch_bounds__(64 * fwd_waves<D>(), (lds_row_elems<D>() > 128
       const bool use_bits = (qor & kor) != 0u;
       const char* Kb = kst[buf];
       const char* Vb = vst[buf];
-      // the two 32-key blocks' accumulation chains alternate, so consecutive
-      // products never depend on each other
-      f32x16 s[2];
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) s[kb][r] = 0.f;
-      // K operands read two steps ahead of their products
-      auto kread = [&](int ks, int kb) {
-        const int kr = 32 * kb + (lane & 31);
-        return *(const u32x4*)(Kb + kr * RB + (((2 * ks + half) ^ swz(kr)) << 4));
-      };
-      u32x4 ka[3][2];
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        ka[0][kb] = kread(0, kb);
-        ka[1][kb] = kread(1, kb);
-      }
-#pragma unroll
-      for (int ks = 0; ks < DK; ++ks) {
-        if (ks + 2 < DK) {
-#pragma unroll
-          for (int kb = 0; kb < 2; ++kb) ka[(ks + 2) % 3][kb] = kread(ks + 2, kb);
-        }
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb) s[kb] = mfma32<E>(bitcast_u4<vec8>(ka[ks % 3][kb]), qf[ks], s[kb]);
-      }
-      // keep the reads two steps ahead of the products they feed
-      __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
-#pragma unroll
-      for (int ks = 0; ks < DK; ++ks) {
-        if (ks + 2 < DK) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-      }
-      if (!wclear) {
-        // mixed tile: the group bits of this lane's 32 keys arrive four
-        // consecutive keys per 16-byte LDS read, all issued before any is
-        // used, and the per-element test is a select (no branch, no
-        // short-circuit); with use_bits false the bits drop out of the test
-        const uint32_t qmask = use_bits ? qbits : 0u;
-        u32x4 kbv[2][4];
+      // S^T of the tile, the mixed tile's masked scores -inf; the two 32-key
+      // blocks' accumulation chains alternate, so consecutive products never
+      // depend on each other
+      auto scores = [&](f32x16(&s)[2]) {
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-          for (int i = 0; i < 4; ++i)
-            kbv[kb][i] = *(const u32x4*)(&kbits_s[buf][32 * kb + 8 * i + 4 * half]);
+          for (int r = 0; r < 16; ++r) s[kb][r] = 0.f;
+        // K operands read two steps ahead of their products
+        auto kread = [&](int ks, int kb) {
+          const int kr = 32 * kb + (lane & 31);
+          return *(const u32x4*)(Kb + kr * RB + (((2 * ks + half) ^ swz(kr)) << 4));
+        };
+        u32x4 ka[3][2];
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+          ka[0][kb] = kread(0, kb);
+          ka[1][kb] = kread(1, kb);
+        }
+#pragma unroll
+        for (int ks = 0; ks < DK; ++ks) {
+          if (ks + 2 < DK) {
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb) ka[(ks + 2) % 3][kb] = kread(ks + 2, kb);
+          }
+#pragma unroll
+          for (int kb = 0; kb < 2; ++kb) s[kb] = mfma32<E>(bitcast_u4<vec8>(ka[ks % 3][kb]), qf[ks], s[kb]);
+        }
+        // keep the reads two steps ahead of the products they feed
+        __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+        for (int ks = 0; ks < DK; ++ks) {
+          if (ks + 2 < DK) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+          __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+        }
+        if (!wclear) {
+          // mixed tile: the group bits of this lane's 32 keys arrive four
+          // consecutive keys per 16-byte LDS read, all issued before any is
+          // used, and the per-element test is a select (no branch, no
+          // short-circuit); with use_bits false the bits drop out of the test
+          const uint32_t qmask = use_bits ? qbits : 0u;
+          u32x4 kbv[2][4];
+#pragma unroll
+          for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              kbv[kb][i] = *(const u32x4*)(&kbits_s[buf][32 * kb + 8 * i + 4 * half]);
+#pragma unroll
+          for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+              const int key = k0 + 32 * kb + 8 * (r >> 2) + 4 * half + (r & 3);
+              const bool keep = (key < L) & (!causal | (key <= myq)) &
+                                ((kbv[kb][r >> 2][r & 3] & qmask) == 0u);
+              s[kb][r] = keep ? s[kb][r] : -INFINITY;
+            }
+        }
+      };
+      f32x16 s[2];
+      scores(s);
+      // The running maximum is an integer (log2) and rarely rises, so the
+      // tile first keeps it: a lane's sum of weights bounds each of them, and
+      // a sum <= 2^16 leaves P, acc, l and lt far inside fp32 (another integer
+      // shift scales them by a power of two, undone by the final division or
+      // the merge).  While some lane has no maximum yet, or when a sum exceeds
+      // the bound, the tile takes the exact maximum, with its scores
+      // recomputed if the first try overwrote them.  (At d = 192 the kernel is
+      // at its register limit and always takes the exact maximum.)
+      float psum = 0.f;
+      bool kept = false;
+      if constexpr (D != 192) {
+        if (__builtin_amdgcn_ballot_w64(m_run == -INFINITY) == 0ull) {
+#pragma unroll
+          for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+              const float p = fast_exp2(fmaf(s[kb][r], c, -m_run));
+              s[kb][r] = p;
+              psum += p;
+            }
+          kept = __builtin_amdgcn_ballot_w64(!(psum <= 65536.f)) == 0ull;
+          if (!kept) scores(s);
+        }
+      }
+      if (!kept) {
+        float smax = -INFINITY;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) smax = fmaxf(smax, s[kb][r]);
+        smax = fmaxf(smax, swap_halves(smax));
+        const float mnew = fmaxf(m_run, ceilf(smax * c));
+        const float msafe = mnew == -INFINITY ? 0.f : mnew;
+        const float alpha = fast_exp2(m_run - msafe);
+        m_run = mnew;
+        // integer maxima change rarely: rescale only when some lane's did
+        if (__builtin_amdgcn_ballot_w64(alpha != 1.f) != 0ull) {
+          l_run *= alpha;
+          lt_run *= alpha;
+#pragma unroll
+          for (int db = 0; db < DB; ++db)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
+        }
+        psum = 0.f;
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
-            const int key = k0 + 32 * kb + 8 * (r >> 2) + 4 * half + (r & 3);
-            const bool keep = (key < L) & (!causal | (key <= myq)) &
-                              ((kbv[kb][r >> 2][r & 3] & qmask) == 0u);
-            s[kb][r] = keep ? s[kb][r] : -INFINITY;
+            const float p = fast_exp2(fmaf(s[kb][r], c, -msafe));
+            s[kb][r] = p;
+            psum += p;
           }
       }
-      float smax = -INFINITY;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) smax = fmaxf(smax, s[kb][r]);
-      smax = fmaxf(smax, swap_halves(smax));
-      const float mnew = fmaxf(m_run, ceilf(smax * c));
-      const float msafe = mnew == -INFINITY ? 0.f : mnew;
-      const float alpha = fast_exp2(m_run - msafe);
-      m_run = mnew;
-      // integer maxima change rarely: rescale only when some lane's did
-      if (__builtin_amdgcn_ballot_w64(alpha != 1.f) != 0ull) {
-        l_run *= alpha;
-        lt_run *= alpha;
-#pragma unroll
-        for (int db = 0; db < DB; ++db)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
-      }
-      float psum = 0.f;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float p = fast_exp2(fmaf(s[kb][r], c, -msafe));
-          s[kb][r] = p;
-          psum += p;
-        }
       l_run += psum;
 #pragma unroll
       for (int ks2 = 0; ks2 < 4; ++ks2) {
