@@ -1,8 +1,8 @@
 // Inner forward kernels: masked flash-style attention over one CQS task.
 //
 // One launch covers the tasks of a launch group.  Each work group owns a
-// 128-query strip of one (task, batch, head) and walks the task's 64-key
-// tiles with an online softmax, emitting the local statistics (unnormalised
+// 128- or 256-query strip of one (task, batch, head) and walks the task's
+// 64-key tiles with an online softmax, emitting the local statistics (unnormalised
 // acc, row max m, row sum l) that the max-shifted merge of App. A.1
 // (Eq. "merge") recomposes across tasks.
 //
@@ -16,12 +16,14 @@
 // gfx950 design: S^T = K Q^T on v_mfma_f32_32x32x16 so each lane owns one
 // query column and its row statistics stay in-lane (one permlane32 swap per
 // tile); P^T feeds O^T = V^T P^T directly from registers, and V^T operands come
-// from row-major LDS through ds_read_b64_tr_b16.  K/V tiles are double
-// buffered in LDS and filled by direct buffer-to-LDS loads issued right after
-// each tile barrier, so they cost no registers and no LDS store instructions.
-// Running maxima are rounded up to integers in the log2 domain, so every
-// rescale is an exact power of two and 16-bit P is rounded identically
-// whichever task, or the undecomposed call, produced it.
+// from row-major LDS through ds_read_b64_tr_b16.  K/V tiles rotate through two
+// or three LDS buffers, filled by direct buffer-to-LDS loads issued right
+// after each tile barrier, so they cost no registers and no LDS store
+// instructions.  Each row's shift (the running maximum in the log2 domain) is
+// an integer, so every rescale is an exact power of two and 16-bit P is
+// rounded identically whichever task, or the undecomposed call, produced it;
+// a tile keeps the row's shift while the weights it gives stay bounded, and
+// takes the exact maximum, rounded up, otherwise.
 //
 // Two row sums: l adds the fp32 weights (it gives the log-sum-exp), lt adds
 // the 16-bit weights the P.V product actually consumes.  Both are task
