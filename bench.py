@@ -23,6 +23,11 @@ The same line also carries:
   * `roofline`: the inner forward kernel of the headline run: algorithmic
     FLOPs per launch (the 49 tasks' kept pairs sum to L^2) over the mean
     HIP-event duration of its launches, recorded on the streams they run on;
+    `inner_fwd.executed_tflops` (and `executed_*` in `kernels`) divides the
+    FLOPs the products execute instead: every computed tile in full (mixed
+    tiles' masked pairs included; the backward's dQ kernel recomputes S and
+    dP, 14 d per pair against the algorithmic 10 d), counted from the plan's
+    block summaries exactly as the kernels decide;
   * `cpu_baseline`: the float64 oracle on sampled query rows of the headline
     workload, with the rate, threads, CPU model and the extrapolated time of
     the full configuration.
@@ -389,6 +394,8 @@ def l32768_kernels(steps, warmup):
         "inner_fwd": {"bound": "mfma", "unit": "TFLOP/s", "launches_per_step": launches,
                       "ms_per_launch": round(ms_launch, 4),
                       "achieved_per_launch": round(flops / launches / (ms_launch * 1e-3) / 1e12, 2),
+                      "executed_tflops_per_launch": round(
+                          fwd_executed_flops(plan, D) / launches / (ms_launch * 1e-3) / 1e12, 2),
                       "frac": round(flops / launches / (ms_launch * 1e-3) / 1e12 / PEAK_TFLOPS, 4),
                       "undecomposed_launch": round(
                           flops / (mean(stu, "ms_inner") * 1e-3) / 1e12, 2)},
@@ -404,7 +411,10 @@ def l32768_kernels(steps, warmup):
                       "achieved_busy": round(
                           2.5 * flops / (mean(stb, "ms_inner_busy") * 1e-3) / 1e12, 2),
                       "frac": round(2.5 * flops / (mean(stb, "ms_inner_busy") * 1e-3) / 1e12
-                                    / PEAK_TFLOPS, 4)},
+                                    / PEAK_TFLOPS, 4),
+                      "executed_busy": round(
+                          bwd_executed_flops(plan, D) / (mean(stb, "ms_inner_busy") * 1e-3) / 1e12,
+                          2)},
         "bwd_preprocess": {"bound": "hbm", "unit": "GB/s", "bytes_per_launch": pre_bytes,
                            "achieved": round(pre_bytes / (mean(stb, "ms_finalize") * 1e-3) / 1e9,
                                              1)},
@@ -552,6 +562,23 @@ def headdim_sweep(args):
     print(json.dumps(out), flush=True)
 
 
+def fwd_executed_flops(plan, D):
+    """FLOPs the inner forward's products execute: 4 D per (query, key) pair of
+    every 32-query x 64-key wave tile it computes (clear or mixed), counted by
+    the plan's block summaries exactly as the kernel decides (the kernel's own
+    counters equal these counts, tests/test_gpu_tile_counts.py)."""
+    _, clear, mixed = plan.fwd_tile_decisions()
+    return (clear + mixed) * 32 * 64 * 4.0 * D
+
+
+def bwd_executed_flops(plan, D):
+    """FLOPs the backward kernels' products execute: dQ 6 D per pair of its
+    computed 32-query x 64-key wave tiles (S, dP, dQ), dK/dV 8 D per pair of
+    its computed 32-key x 32-query tiles (S, dP, dV, dK)."""
+    (_, qc, qm), (_, kc, km) = plan.bwd_tile_decisions()
+    return (qc + qm) * 32 * 64 * 6.0 * D + (kc + km) * 32 * 32 * 8.0 * D
+
+
 def headline(args):
     import torch
 
@@ -582,6 +609,7 @@ def headline(args):
     ms_launch = mean(st, "ms_inner") / launches
     per_launch = flops / launches          # the tasks' kept pairs sum to L^2
     achieved = per_launch / (ms_launch * 1e-3) / 1e12
+    executed = fwd_executed_flops(plan, D) / launches
     line = {
         "metric": METRIC,
         "value": round(flops / (ms * 1e-3) / 1e12, 2),
@@ -608,6 +636,8 @@ def headline(args):
                      "traffic": measured_traffic()},
         "inner_fwd": {"kernel": "attn_fwd_mfma<BF16, 128, stats>", "launches_per_step": launches,
                       "flops_per_launch": per_launch, "ms_per_launch": round(ms_launch, 4),
+                      "executed_flops_per_launch": executed,
+                      "executed_tflops": round(executed / (ms_launch * 1e-3) / 1e12, 2),
                       "concurrency": round(mean(st, "ms_inner") / mean(st, "ms_inner_busy"), 3),
                       "achieved_busy": round(flops / (mean(st, "ms_inner_busy") * 1e-3) / 1e12,
                                              2)},
