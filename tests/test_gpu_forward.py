@@ -195,6 +195,29 @@ def test_overflowing_scores_stay_finite():
         _check_vs_oracle(O, LSE, Q, K, V, False, "bf16")
 
 
+@pytest.mark.parametrize("dt,causal", [("bf16", False), ("f16", True)])
+def test_rising_scores_take_the_exact_maximum_again(dt, causal):
+    """Scores that climb by about 9 (log2 units) from one 64-key tile to the
+    next: a tile that keeps the row's shift finds weights far above the 2^16
+    bound on most tiles, recomputes its scores and takes the exact maximum;
+    the result must still match float64 (App. A.1), at depths 0-2."""
+    need_gpu()
+    B, L, H, d = 1, 1536, 2, 64
+    Q, K, V = synth.make_inputs(77, B, L, H, d, dt)
+    e = torch.ones(d, dtype=torch.float32) / d ** 0.5
+    ramp = (torch.arange(L, dtype=torch.float32) // 64) * 20.0   # per tile: +20 along e
+    Q = (Q.float() + 3.0 * e).to(Q.dtype)
+    K = (K.float() + ramp[None, :, None, None] * e).to(K.dtype)
+    Qf, Kf = synth.as_f64(Q), synth.as_f64(K)
+    s = np.einsum("blhd,bmhd->bhlm", Qf, Kf) / np.sqrt(d) * np.log2(np.e)
+    step = np.median(s[..., 64:128].max(-1) - s[..., :64].max(-1))
+    assert step > 8          # the bound's 16 doublings are gone within two tiles
+    for depth in (0, 1, 2):
+        say(f"rising scores dt={dt} causal={causal} depth={depth}")
+        O, LSE, _ = run_forward(Q, K, V, causal, depth=depth)
+        _check_vs_oracle(O, LSE, Q, K, V, causal, dt)
+
+
 @pytest.mark.parametrize("dt", ["bf16", "f16"])
 def test_one_hot_rows_return_the_value_row(dt):
     """Scores so peaked that every softmax row is one-hot to far below fp32
