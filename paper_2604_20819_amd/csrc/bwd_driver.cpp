@@ -7,8 +7,10 @@
 // caller stream : D = rowsum(dO * O) over the full sequence (host-resident O
 //                 or dO arrive in chunks through the staging slots); zero
 //                 dQ/dK/dV when they are device-resident; per task wait
-//                 "staged", run the key-parallel dK/dV kernel;
-// second stream : per task the query-parallel dQ kernel;
+//                 "staged", run the key-parallel dK/dV kernel, then the
+//                 query-parallel dQ kernel when the dK/dV launches span many
+//                 rounds of resident waves;
+// second stream : otherwise the dQ kernels, beside the dK/dV kernels;
 // copy stream   : gather each task's runs of Q, K, V, dO into slot t % S once
 //                 both kernels of the slot's previous task are done: a gather
 //                 kernel from device-resident inputs, host-to-device copies
@@ -16,15 +18,16 @@
 //                 also holds come from its staged rows on the device); a plan
 //                 that reads device-resident inputs in place stages nothing;
 // device gradients, several tasks per launch (inputs read in place): per
-//                 launch group one dK/dV launch (caller's stream) and one dQ
-//                 launch (second stream) over all its tasks store every task's
-//                 rows in its own buffer, and a gather-merge on the caller's
-//                 stream adds them into dQ, dK, dV in task order;
+//                 launch group one dK/dV launch and one dQ launch over all its
+//                 tasks store every task's rows in its own buffer, and a
+//                 gather-merge on the caller's stream adds them into dQ, dK,
+//                 dV in task order;
 // device gradients, one task per launch: each kernel's epilogue adds the
-//                 task's rows into the global fp32 gradients.  Each stream
-//                 keeps the tasks in order and a task holds each token once,
-//                 so these read-modify-writes never race (undecomposed, the
-//                 single task's rows are stored);
+//                 task's rows into the global fp32 gradients.  All dQ launches
+//                 of a call run on one stream, which keeps the tasks in order,
+//                 and a task holds each token once, so these
+//                 read-modify-writes never race (undecomposed, the single
+//                 task's rows are stored);
 // host gradients: the kernels store the task's rows in the slot's own
 //                 gradient buffers; the auxiliary stream copies them to pinned
 //                 host memory and a host thread adds them into dQ, dK, dV at
@@ -181,7 +184,23 @@ cqsa_status backward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa
   hipEvent_t* ev_free_q = &C->sync_events[4 + 2 * nslot]; // dQ kernel done with the slot
   hipEvent_t* ev_d2h = &C->sync_events[4 + 3 * nslot];    // the slot's gradients copied out
   hipEvent_t* ev_chunk = &C->sync_events[4 + 4 * nslot];  // preprocess done with the slot
-  const hipStream_t cs = C->copy, qs = C->lane, ms = C->aux;
+  const int64_t dq_rows = dq_rows_per_wg(int(d)), kv_rows = dkdv_rows_per_wg(int(d));
+  // work groups of a launch over tasks [t0, t0 + n): each task's strips
+  auto wgs_of = [&](int64_t t0, int64_t n, int64_t rows) {
+    int64_t w = 0;
+    for (int64_t t = t0; t < t0 + n; ++t) w += (p->tasks[t].L_local + rows - 1) / rows * B * H;
+    return w;
+  };
+  // the dQ stream, one for the whole call: the caller's stream when the
+  // longest dK/dV launch spans many rounds of resident waves (one wave per 32
+  // keys), else the second compute stream
+  int64_t kv_waves = 0;
+  if (batched)
+    for (const Group& gr : p->bwd_groups)
+      kv_waves = std::max(kv_waves, wgs_of(gr.task0, gr.count, kv_rows) * (kv_rows / 32));
+  else
+    for (int64_t t = 0; t < ntask; ++t) kv_waves = std::max(kv_waves, wgs_of(t, 1, kv_rows) * (kv_rows / 32));
+  const hipStream_t cs = C->copy, qs = serial_launch(kv_waves) ? st : C->lane, ms = C->aux;
   if (C->ws_free_valid) CQSA_HIP(hipStreamWaitEvent(st, C->ws_free, 0));
   // tile-decision counters, zeroed before every kernel (the other streams
   // start after events recorded on st below)
@@ -281,18 +300,12 @@ cqsa_status backward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa
     });
   }
   CQSA_HIP(hipStreamWaitEvent(st, ev_tab, 0));
-  // dQ kernels run on the second compute stream (they write dQ only, the dK/dV
-  // kernels on the caller's stream write dK and dV only): a task's two kernels
-  // overlap, and each stream keeps its own tasks in order.
+  // dQ kernels write dQ only and dK/dV kernels dK and dV only, so on the
+  // second stream a task's two kernels overlap; each stream keeps its own
+  // tasks in order.  (With qs the caller's stream these waits are no-ops.)
   CQSA_HIP(hipEventRecord(ev_pre, st));
   CQSA_HIP(hipStreamWaitEvent(qs, ev_pre, 0));
 
-  // work groups of a launch over tasks [t0, t0 + n): each task's strips
-  auto wgs_of = [&](int64_t t0, int64_t n, int64_t rows) {
-    int64_t w = 0;
-    for (int64_t t = t0; t < t0 + n; ++t) w += (p->tasks[t].L_local + rows - 1) / rows * B * H;
-    return w;
-  };
   auto common_args = [&](BwdArgs& a, int64_t t0, int64_t n) {
     a.tab = d_tab;
     a.tasks = (const DevTask*)d_tab + t0;
@@ -302,7 +315,6 @@ cqsa_status backward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa
     a.lse = d_lse; a.D = d_D; a.Lg = L;
     a.tile_count = tile_count;
   };
-  const int64_t dq_rows = dq_rows_per_wg(int(d)), kv_rows = dkdv_rows_per_wg(int(d));
   if (batched) {
     float* loc = (float*)(base + tab_bytes + stat_bytes + lse_bytes + uint64_t(nslot) * slot_bytes);
     const int64_t stride = int64_t(loc_b / 4);
@@ -322,12 +334,13 @@ cqsa_status backward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa
         CQSA_HIP(hipEventRecord(ev_pre, st));
         CQSA_HIP(hipStreamWaitEvent(qs, ev_pre, 0));
       }
-      std::pair<hipEvent_t, hipEvent_t> sk = span_begin(st), sq = span_begin(qs);
+      auto sk = span_begin(st);
       CQSA_HIP(launch_bwd_dkdv(o.dtype, int(d), a, wgs_of(gr.task0, gr.count, kv_rows), st));
-      CQSA_HIP(launch_bwd_dq(o.dtype, int(d), a, wgs_of(gr.task0, gr.count, dq_rows), qs));
-      rec.stats.inner_launches += 2;
       span_end(sk, st, kStInner);
+      auto sq = span_begin(qs);
+      CQSA_HIP(launch_bwd_dq(o.dtype, int(d), a, wgs_of(gr.task0, gr.count, dq_rows), qs));
       span_end(sq, qs, kStInner);
+      rec.stats.inner_launches += 2;
       CQSA_HIP(hipEventRecord(ev_join, qs));
       CQSA_HIP(hipStreamWaitEvent(st, ev_join, 0));
       GradMergeArgs m{};
@@ -430,12 +443,13 @@ cqsa_status backward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa
         CQSA_HIP(hipStreamWaitEvent(qs, ev_d2h[si], 0));
       }
     }
-    std::pair<hipEvent_t, hipEvent_t> sk = span_begin(st), sq = span_begin(qs);
+    auto sk = span_begin(st);
     CQSA_HIP(launch_bwd_dkdv(o.dtype, int(d), a, wgs_of(t, 1, kv_rows), st));
-    CQSA_HIP(launch_bwd_dq(o.dtype, int(d), a, wgs_of(t, 1, dq_rows), qs));
-    rec.stats.inner_launches += 2;
     span_end(sk, st, kStInner);
+    auto sq = span_begin(qs);
+    CQSA_HIP(launch_bwd_dq(o.dtype, int(d), a, wgs_of(t, 1, dq_rows), qs));
     span_end(sq, qs, kStInner);
+    rec.stats.inner_launches += 2;
     CQSA_HIP(hipEventRecord(ev_free[si], st));
     CQSA_HIP(hipEventRecord(ev_free_q[si], qs));
     if (!dev_acc) {

@@ -35,12 +35,6 @@ namespace cqsa {
 
 namespace {
 
-// Waves the GPU holds at once at the inner kernel's occupancy (256 CUs x 4
-// SIMDs x 2 waves), and the launch length, in rounds of them, from which
-// consecutive launches are serialised.
-constexpr int64_t kResidentWaves = 256 * 8;
-constexpr int64_t kSerialRounds = 8;
-
 // Max-shifted merge of one task's statistics into the host accumulator
 // (Eq. "merge", log2 domain, null rows skipped); l and lt (the sums of the
 // fp32 and of the rounded weights) merge with the same factors.  A row whose running max is
@@ -371,7 +365,7 @@ cqsa_status forward_impl(const cqsa_plan_t* p, const cqsa_tensor* Q, const cqsa_
       // flight would only share the GPU, so they stay on the caller's stream
       // and run one after the other.  Inner kernels write only their slot.
       const int64_t waves = wgs * (rows_wg / 32);  // one wave per 32 query rows
-      const bool alternate = waves < kSerialRounds * kResidentWaves;
+      const bool alternate = !serial_launch(waves);
       const hipStream_t ls = (alternate && (k & 1)) ? C->lane : st;
       if (ls != cs) {
         CQSA_HIP(hipEventRecord(ev_staged[si], cs));

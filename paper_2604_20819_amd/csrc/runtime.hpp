@@ -15,6 +15,17 @@
 
 namespace cqsa {
 
+// Waves the GPU holds at once at the inner kernels' occupancy (256 CUs x 4
+// SIMDs x 2 waves), and the launch length, in rounds of them, from which the
+// drivers run consecutive inner launches one after the other on the caller's
+// stream: such a launch has a negligible tail, and two of them in flight only
+// share the GPU (which costs time: in the backward, dQ beside dK/dV was 2-8 %
+// slower than the two in turn from 8 rounds up).  Shorter launches go to two
+// streams, so that one fills the other's tail.
+constexpr int64_t kResidentWaves = 256 * 8;
+constexpr int64_t kSerialRounds = 8;
+inline bool serial_launch(int64_t waves) { return waves >= kSerialRounds * kResidentWaves; }
+
 // Library-owned streams and caches of one device.  All streams use the
 // default priority.
 struct DevCtx {
@@ -22,7 +33,7 @@ struct DevCtx {
   bool ready = false;
   hipStream_t copy = nullptr;   // staging copies (H2D or D2D)
   hipStream_t aux = nullptr;    // forward merges, or statistics device -> host
-  hipStream_t lane = nullptr;   // second compute stream (odd groups, backward dQ)
+  hipStream_t lane = nullptr;   // second compute stream (short launches: odd forward groups, backward dQ)
   hipEvent_t ws_free = nullptr; // recorded after the last call's last use of the workspace
   bool ws_free_valid = false;
   void* ws = nullptr;           // cached device workspace (built-in allocator)

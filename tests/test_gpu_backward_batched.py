@@ -109,3 +109,30 @@ def test_depth2_L32768_batched_vs_undecomposed():
         say(f"  {name} vs undecomposed: {r:.3e}")
         assert r <= 1e-3, name
         assert torch.equal(g[i], g1[i]), name
+
+
+def test_long_launches_serialise_dq_after_dkdv():
+    """bf16 B=1 H=40 d=128 L=32768, non-causal, depth 1: every dK/dV launch
+    spans at least 8 rounds of the GPU's resident waves, so the dQ kernels run
+    after the dK/dV kernels on the caller's stream (one task per launch too:
+    55 key strips x 40 heads x 8 waves per task), where shorter launches run
+    them on a second stream.  All tasks in one launch and one task per launch
+    give the same bits, and both match the undecomposed call (rel-L2 <= 1e-3)."""
+    need_gpu()
+    B, L, H, d = 1, 32768, 40, 128
+    say(f"serialised dQ launches B={B} L={L} H={H} d={d}")
+    Q, K, V, dO = synth.make_inputs(20819 + 62, B, L, H, d, "bf16", with_dO=True)
+    g, plan, st = run(Q, K, V, dO, False, 1, 0)
+    assert plan.num_tasks == 7 and plan.bwd_tasks_per_launch == 7
+    # the drivers' serial-launch threshold: 8 rounds of 256 CUs x 8 waves
+    strips = -(-min(plan.task(t)["L_local"] for t in range(7)) // 256)
+    assert strips == 55 and strips * B * H * 8 >= 8 * 256 * 8
+    g1, _, st1 = run(Q, K, V, dO, False, 1, 1)
+    assert st1["inner_launches"] == 14
+    g0, _, _ = run(Q, K, V, dO, False, 0, 0)
+    for name, i in (("dQ", 0), ("dK", 1), ("dV", 2)):
+        assert np.isfinite(g[i].numpy()).all(), name
+        assert torch.equal(g[i], g1[i]), name
+        r = rel_l2(g[i].numpy(), g0[i].numpy())
+        say(f"  {name} vs undecomposed: {r:.3e}")
+        assert r <= 1e-3, name
