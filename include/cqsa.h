@@ -366,7 +366,8 @@ cqsa_status cqsa_set_timing(int32_t enable);
  * and cqsa_backward calls on this thread (a diagnostic: the launches run
  * counting instances of the kernels, which add one atomic per wave; the
  * counters live in a small device buffer per GPU and a pinned host copy per
- * thread, both allocated on first use; cqsa_forward_noalloc does not count). */
+ * thread, both allocated on first use, so counted calls that overlap on one
+ * GPU mix their counts; cqsa_forward_noalloc does not count). */
 cqsa_status cqsa_set_tile_counting(int32_t enable);
 
 /* Statistics of the last cqsa_forward/cqsa_backward on this thread; waits for
