@@ -211,7 +211,8 @@ typedef struct {
    * predict. */
   int64_t kernel_tiles_masked, kernel_tiles_clear, kernel_tiles_mixed;
   /* Backward only: the dK/dV kernel's decisions, one group of 32 consecutive
-   * local keys against one 32-query tile its work group visits. */
+   * local keys against one query tile its work group visits (64 queries at
+   * d = 96, else 32). */
   int64_t kernel_kv_tiles_masked, kernel_kv_tiles_clear, kernel_kv_tiles_mixed;
 } cqsa_run_stats;
 
@@ -268,8 +269,9 @@ cqsa_status cqsa_plan_fwd_tile_decisions(const cqsa_plan_t* plan, int64_t* maske
  * dq[0..2]: the dQ kernel's masked, clear, mixed counts, by the rules of
  * cqsa_plan_fwd_tile_decisions at its work-group height (256 query rows at
  * d = 96 ... 160, else 128).  kv[0..2]: the dK/dV kernel's, for key strips of
- * R rows (256 at d = 96, 128, else 128), groups of 32 keys and 32-query
- * tiles: a work group visits query tile t unless t lies causally wholly
+ * R rows (256 at d = 96, 128, else 128), groups of 32 keys and query tiles
+ * of T rows (64 at d = 96, one summary block; else 32, half a block):
+ * a work group visits query tile t unless t lies causally wholly
  * before its first key or the AND of its blocks' summaries meets the
  * summaries of t's block; a visited tile is masked for a key group when the
  * group's block AND meets the tile's or it lies causally wholly before the

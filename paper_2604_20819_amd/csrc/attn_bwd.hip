@@ -408,12 +408,20 @@ __global__ void __launch_bounds__(64 * dq_waves<D>(), (lds_row_elems<D>() > 128 
 // V rows, and the 8 waves run two per SIMD.
 template <int D> constexpr int dkdv_splits() { return D >= 160 ? 2 : 1; }
 // Groups of 32 keys per work group.  At d = 96 and 128 a work group of 8
-// waves owns a 256-key strip: each 32-query tile it loads (Q and dO rows)
-// then feeds twice the products, which halves the tile traffic per product;
-// the LDS (a 64 KB V strip and the double-buffered tiles) leaves one work
-// group per CU, two waves per SIMD as before.  Elsewhere 4 groups (a 128-key
-// strip).
+// waves owns a 256-key strip: each query tile it loads (Q and dO rows) then
+// feeds twice the products, which halves the tile traffic per product; the
+// LDS (a 64 KB V strip and the tiles) leaves one work group per CU, two waves
+// per SIMD as before.  Elsewhere 4 groups (a 128-key strip).
 template <int D> constexpr int dkdv_key_waves() { return (D == 96 || D == 128) ? 8 : 4; }
+// Query rows per tile: 64 (one summary block) at d = 96, 32 (two tiles per
+// block) elsewhere.  A 64-query tile halves the barriers, tile probes and
+// statistics loads per product, and its two halves are computed in turn.  At
+// d = 128 it would need a few registers more than the 256 two waves per SIMD
+// allow, and the compiler's spill code for that kernel was wrong: it saved a
+// live register under a branch's partial exec mask (waves that skip the
+// branch lost the value).  So d = 128 keeps 32-query tiles, which need no
+// spill.
+template <int D> constexpr int dkdv_qtile() { return D == 96 ? 64 : 32; }
 template <int D> constexpr int dkdv_waves() { return dkdv_key_waves<D>() * dkdv_splits<D>(); }
 // Minimum waves per SIMD the compiler must allow for (the second launch
 // bound): two, which caps the registers at 256, except where one work group
@@ -424,10 +432,9 @@ template <int D> constexpr int dkdv_min_waves() { return lds_row_elems<D>() > 12
 // 32-key group (the first of the waves that share one when the columns split)
 template <typename E, int D, bool LOCAL, bool COUNT>
 __global__ void __launch_bounds__(64 * dkdv_waves<D>(), dkdv_min_waves<D>()) attn_bwd_dkdv(const BwdArgs a) {
-  // 32-query tiles (two per 64-token summary block) keep the registers and
-  // LDS within two waves per SIMD
   constexpr int KW = dkdv_key_waves<D>();
-  constexpr int BK = 32 * KW, BQ = 32;
+  constexpr int BK = 32 * KW, BQ = dkdv_qtile<D>();
+  constexpr int TSH = BQ == 32 ? 1 : 0;  // query tile t lies in summary block t >> TSH
   // Q and dO tiles: rows of DP elements (d padded as in the forward) with
   // the forward's swizzle (chunk ch of row r in slot ch ^ swz(r)),
   // conflict-free for the row reads and the transpose reads; filled by
@@ -443,12 +450,15 @@ __global__ void __launch_bounds__(64 * dkdv_waves<D>(), dkdv_min_waves<D>()) att
   auto swz = [](int r) { return 2 * (r & 3) + ((r >> 2) & 1); };
 
   // a ring of NBUF query tiles (Q, dO) with their per-query statistics,
-  // filled NBUF - 1 tiles ahead of the compute (two ahead for the 256-key
-  // strips, whose single work group per CU leaves the LDS for a third tile)
-  constexpr int NBUF = KW == 8 ? 3 : 2, AHEAD = NBUF - 1;
+  // filled NBUF - 1 tiles ahead of the compute: three 32-query buffers for the
+  // 256-key strips of d = 128 (two tiles' compute for a tile's loads to land
+  // in), else two (a 64-query tile's loads land during the previous 64-query
+  // tile; a third 64-query buffer would not fit beside the 256-key V strip)
+  constexpr int NBUF = (KW == 8 && BQ == 32) ? 3 : 2, AHEAD = NBUF - 1;
   static_assert(NBUF == 2 || 2 * NDMA < 16, "vmcnt immediate");
-  __shared__ __attribute__((aligned(1024))) char qs[NBUF][BQ * P2];
-  __shared__ __attribute__((aligned(1024))) char os[NBUF][BQ * P2];
+  // each buffer holds the Q tile, then the dO tile: the dO rows lie a
+  // constant offset from the Q rows, so their reads share address registers
+  __shared__ __attribute__((aligned(1024))) char qos[NBUF][2 * BQ * P2];
   __shared__ __attribute__((aligned(1024))) char vs[BK * P2];   // the strip's V rows, swizzled
   __shared__ __attribute__((aligned(16))) float lse_s[NBUF][BQ];  // natural-log LSE
   __shared__ __attribute__((aligned(16))) float d_s[NBUF][BQ];
@@ -567,10 +577,10 @@ __global__ void __launch_bounds__(64 * dkdv_waves<D>(), dkdv_min_waves<D>()) att
     uint32_t an, on;
     int32_t row;
   };
-  // raw words until pick(), as in the dQ kernel (tile t lies in block t / 2)
+  // raw words until pick(), as in the dQ kernel
   auto window = [&](int t0) {
     const int t = t0 + lane < nqt ? t0 + lane : nqt - 1;
-    const u32x3 x = *(const u32x3*)(blks + (t >> 1));
+    const u32x3 x = *(const u32x3*)(blks + (t >> TSH));
     return Window{x[1], x[0], int32_t(x[2])};
   };
   // row_out: the tile's first row in the Q and dO the kernel reads (local
@@ -586,7 +596,7 @@ __global__ void __launch_bounds__(64 * dkdv_waves<D>(), dkdv_min_waves<D>()) att
     qand_out = __builtin_amdgcn_readlane(w.an, i);
     qor_out = __builtin_amdgcn_readlane(w.on, i);
     const int32_t r = __builtin_amdgcn_readlane(w.row, i);
-    const int32_t grow = r != kNoRow ? r + ((t0 + i) & 1) * BQ : kNoRow;
+    const int32_t grow = r != kNoRow ? r + (TSH ? ((t0 + i) & 1) * BQ : 0) : kNoRow;
     row_out = in_place ? grow : (t0 + i) * BQ;
     grow_out = grow;
     return t0 + i;
@@ -616,8 +626,11 @@ __global__ void __launch_bounds__(64 * dkdv_waves<D>(), dkdv_min_waves<D>()) att
     goff[j] = uint32_t((row * rs + ((lane % CHUNKS) ^ swz(row)) * 8) * 2);
   }
   const uint32_t soff = uint32_t(lane) * 4;
+  // the threads that load and store a tile's per-query statistics: wave 0
+  // for a 64-query tile (a wave-uniform branch), its first half for 32
+  const bool stat_lanes = BQ == 64 ? wave == 0 : tid < BQ;
   auto gload = [&](int buf, int qt, int32_t trow, int32_t grow) {
-    if (tid < BQ) {
+    if (stat_lanes) {
       lds_ptr lse_d = (lds_ptr)lse_s[buf], d_d = (lds_ptr)d_s[buf];
       if (grow != kNoRow) {
         // the tile's queries are consecutive global rows from grow
@@ -647,8 +660,8 @@ __global__ void __launch_bounds__(64 * dkdv_waves<D>(), dkdv_min_waves<D>()) att
 #pragma unroll
       for (int j = 0; j < NDMA; ++j) {
         const int off = (NDMA * wave + j) * 1024;
-        buf_load16_lds(rq, qs[buf] + off, goff[j]);
-        buf_load16_lds(ro, os[buf] + off, goff[j]);
+        buf_load16_lds(rq, qos[buf] + off, goff[j]);
+        buf_load16_lds(ro, qos[buf] + BQ * P2 + off, goff[j]);
       }
     } else {
       // across a run boundary: per-lane rows from the slice base
@@ -666,15 +679,15 @@ __global__ void __launch_bounds__(64 * dkdv_waves<D>(), dkdv_min_waves<D>()) att
         const uint32_t vo =
             q < L ? uint32_t((run_global(runs_s, n_runs, q) * rs + ch * 8) * 2) : kOobOffset;
         const int off = (NDMA * wave + j) * 1024;
-        buf_load16_lds(rq, qs[buf] + off, vo);
-        buf_load16_lds(ro, os[buf] + off, vo);
+        buf_load16_lds(rq, qos[buf] + off, vo);
+        buf_load16_lds(ro, qos[buf] + BQ * P2 + off, vo);
       }
       __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0), as for the statistics
     }
   };
   // the group bits come from the runs in LDS
   auto sstore = [&](int buf, int qt) {
-    if (tid < BQ) {
+    if (stat_lanes) {
       const int q = qt * BQ + tid;
       qbits_s[buf][tid] = q < L ? run_bits(runs_s, n_runs, q) : 0u;
     }
@@ -740,8 +753,8 @@ __global__ void __launch_bounds__(64 * dkdv_waves<D>(), dkdv_min_waves<D>()) att
       }
       const bool use_bits = (kor & qor) != 0u;
       const uint32_t kmask = use_bits ? kbits : 0u;
-      const char* qsb = qs[buf];
-      const char* osb = os[buf];
+      const char* qsb = qos[buf];
+      const char* osb = qsb + BQ * P2;
 #pragma unroll 1
       for (int qb = 0; qb < BQ / 32; ++qb) {
         f32x16 s, dp;
@@ -753,12 +766,16 @@ __global__ void __launch_bounds__(64 * dkdv_waves<D>(), dkdv_min_waves<D>()) att
         const int row = 32 * qb + (lane & 31);
 #pragma unroll
         for (int ks = 0; ks < DK; ++ks) {
-          const int slot = ((2 * ks + half) ^ swz(row)) << 4;
+          // 16-byte chunk 2 ks + half of the row: the swizzle changes only
+          // the chunk's low 3 bits, so writing ks >> 2 as a separate 128-byte
+          // step leaves four distinct per-lane offsets (the rest immediate)
+          const int slot = (((2 * (ks & 3) + half) ^ swz(row)) << 4) + 128 * (ks >> 2);
           const u32x4 qa = *(const u32x4*)(qsb + row * P2 + slot);
           s = mfma32<E>(bitcast_u4<vec8>(qa), kf[ks], s);
           const u32x4 oa = *(const u32x4*)(osb + row * P2 + slot);
           const int vr = kw * 32 + (lane & 31);
-          const u32x4 vb = *(const u32x4*)(vs + vr * P2 + (((2 * ks + half) ^ swz(vr)) << 4));
+          const u32x4 vb = *(const u32x4*)(vs + vr * P2 + (((2 * (ks & 3) + half) ^ swz(vr)) << 4) +
+                                           128 * (ks >> 2));
           dp = mfma32<E>(bitcast_u4<vec8>(oa), bitcast_u4<vec8>(vb), dp);
         }
         // 16 queries at a time: P and dS = P (dP - D), packed for dV and dK
@@ -794,8 +811,12 @@ __global__ void __launch_bounds__(64 * dkdv_waves<D>(), dkdv_min_waves<D>()) att
 #pragma unroll
           for (int db = 0; db < DBO; ++db) {
             if (NSPLIT > 1 && db0 + db >= DB) break;  // the last half of an odd d/32
-            const int col = 32 * (db0 + db) + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
-            const int tcol = (((col >> 3) ^ swz(trow)) << 4) + (col & 7) * 2;
+            // column 32 g + 16 ((lane >> 4) & 1) + 4 (lane & 3) of block g
+            // lies in chunk 4 g + xl; as for the row reads, g >> 1 is a
+            // separate 128-byte step
+            const int g = db0 + db;
+            const int xl = 2 * ((lane >> 4) & 1) + ((lane & 3) >> 1);
+            const int tcol = (((4 * (g & 1) + xl) ^ swz(trow)) << 4) + 128 * (g >> 1) + 8 * (lane & 1);
             const char* po = osb + trow * P2 + tcol;
             dv[db] = mfma32<E>(lds_tr_pair<E>(po, po + 8 * P2), bp, dv[db]);
             const char* pq = qsb + trow * P2 + tcol;
@@ -816,14 +837,14 @@ __global__ void __launch_bounds__(64 * dkdv_waves<D>(), dkdv_min_waves<D>()) att
         // this wave waits for its loads (the scan's registers are reused by
         // the next iteration, and the compiler would otherwise wait for them,
         // and for the tile loads, on every iteration)
-        const const_u32* bw = (const_u32*)(uintptr_t)(blks + (qc >> 1));
+        const const_u32* bw = (const_u32*)(uintptr_t)(blks + (qc >> TSH));
         const uint32_t bor = bw[0], band = bw[1];
         const int32_t brow = int32_t(bw[2]);
         if (!(causal && qc * BQ + BQ - 1 < first_key) && (kand & band) == 0u) {
           qc2 = qc;
           or2 = bor;
           and2 = band;
-          grow2 = brow != kNoRow ? brow + (qc & 1) * BQ : kNoRow;
+          grow2 = brow != kNoRow ? brow + (TSH ? (qc & 1) * BQ : 0) : kNoRow;
           row2 = in_place ? grow2 : qc * BQ;
         } else {
           qc2 = next_live(qc + 1, or2, and2, row2, grow2);
@@ -927,6 +948,24 @@ static hipError_t launch_dkdv_t(const BwdArgs& a, int64_t n, hipStream_t s) {
     case 256: return dt == CQSA_BF16 ? LAUNCH<BF16, 256>(a, wgs, s) : LAUNCH<F16, 256>(a, wgs, s); \
   }                                                                    \
   return hipErrorInvalidValue;
+
+int dkdv_qtile_rows(int d) {
+  switch (d) {
+#define CQSA_KV_QTILE(DD) \
+  case DD:                \
+    return dkdv_qtile<DD>();
+    CQSA_KV_QTILE(32)
+    CQSA_KV_QTILE(64)
+    CQSA_KV_QTILE(96)
+    CQSA_KV_QTILE(128)
+    CQSA_KV_QTILE(160)
+    CQSA_KV_QTILE(192)
+    CQSA_KV_QTILE(224)
+    CQSA_KV_QTILE(256)
+#undef CQSA_KV_QTILE
+  }
+  return 32;
+}
 
 int dkdv_rows_per_wg(int d) {
   switch (d) {

@@ -250,9 +250,10 @@ cqsa_status cqsa_plan_bwd_tile_decisions(const cqsa_plan_t* p, int64_t* dq, int6
     return fail(CQSA_ERR_UNSUPPORTED, "cqsa_plan_bwd_tile_decisions: the backward needs a 16-bit dtype");
   int64_t a[3] = {0, 0, 0}, b[3] = {0, 0, 0};
   const int32_t q_rows = dq_rows_per_wg(p->g.d), k_rows = dkdv_rows_per_wg(p->g.d);
+  const int32_t k_tile = dkdv_qtile_rows(p->g.d);
   for (const Task& t : p->tasks) {
     fwd_tile_decisions(t, p->g.causal != 0, q_rows, a);
-    kv_tile_decisions(t, p->g.causal != 0, k_rows, b);
+    kv_tile_decisions(t, p->g.causal != 0, k_rows, k_tile, b);
   }
   const int64_t bh = int64_t(p->opts.B) * p->g.H;
   for (int i = 0; i < 3; ++i) {

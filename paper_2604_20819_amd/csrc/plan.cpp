@@ -411,8 +411,9 @@ void fwd_tile_decisions(const Task& t, bool causal, int32_t rows, int64_t out[3]
   }
 }
 
-void kv_tile_decisions(const Task& t, bool causal, int32_t rows, int64_t out[3]) {
-  const int64_t L = t.L_local, nqt = (L + 31) / 32;
+void kv_tile_decisions(const Task& t, bool causal, int32_t rows, int32_t qtile, int64_t out[3]) {
+  const int64_t L = t.L_local, nqt = (L + qtile - 1) / qtile;
+  const int64_t per_block = kBlock / qtile;  // query tiles per summary block
   const int64_t ns = (L + rows - 1) / rows;
   std::vector<int64_t> visited;
   for (int64_t s = 0; s < ns; ++s) {
@@ -423,14 +424,15 @@ void kv_tile_decisions(const Task& t, bool causal, int32_t rows, int64_t out[3])
     // first key or sharing a bit of the AND with it
     visited.clear();
     for (int64_t q = 0; q < nqt; ++q)
-      if (!(causal && q * 32 + 31 < first) && (kand & t.blk_and[size_t(q / 2)]) == 0u) visited.push_back(q);
+      if (!(causal && q * qtile + qtile - 1 < first) && (kand & t.blk_and[size_t(q / per_block)]) == 0u)
+        visited.push_back(q);
     for (int64_t k0 = first; k0 <= last; k0 += 32) {
       const int64_t k1 = std::min(k0 + 31, L - 1);
       const uint32_t wor = t.blk_or[size_t(k0 / kBlock)], wand = t.blk_and[size_t(k0 / kBlock)];
       for (int64_t q : visited) {
-        const int64_t q0 = q * 32;
-        const uint32_t qor = t.blk_or[size_t(q / 2)], qand = t.blk_and[size_t(q / 2)];
-        if ((wand & qand) != 0u || (causal && q0 + 31 < k0))
+        const int64_t q0 = q * qtile;
+        const uint32_t qor = t.blk_or[size_t(q / per_block)], qand = t.blk_and[size_t(q / per_block)];
+        if ((wand & qand) != 0u || (causal && q0 + qtile - 1 < k0))
           ++out[0];
         else if ((wor & qor) == 0u && (!causal || q0 >= k1))
           ++out[1];

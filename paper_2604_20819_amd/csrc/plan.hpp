@@ -192,6 +192,8 @@ void pack_groups(const SegmentCover& sc, int32_t H, std::vector<Group>* groups,
 int fwd_rows_per_wg(cqsa_dtype dt, int d);
 int dq_rows_per_wg(int d);
 int dkdv_rows_per_wg(int d);
+// Query rows per tile of the dK/dV kernel (64 or 32).
+int dkdv_qtile_rows(int d);
 
 // Strip orders of one task for its kernels' launch order (longest first):
 // query strips of `rows` rows (a multiple of 64) by the 64-key tiles live for
@@ -209,9 +211,10 @@ std::vector<int32_t> key_strip_order(const Task& t, bool causal, int32_t rows);
 // query.  O(tiles x waves) per task.
 void fwd_tile_decisions(const Task& t, bool causal, int32_t rows, int64_t out[3]);
 // The dK/dV kernel's tile decisions on one (batch element, head) of task t:
-// key strips of `rows` rows, groups of 32 keys, 32-query tiles (tile q's
-// summaries are those of block q / 2); out as for fwd_tile_decisions.
-void kv_tile_decisions(const Task& t, bool causal, int32_t rows, int64_t out[3]);
+// key strips of `rows` rows, groups of 32 keys, query tiles of `qtile` rows
+// (64: tile q's summaries are those of block q; 32: of block q / 2); out as
+// for fwd_tile_decisions.
+void kv_tile_decisions(const Task& t, bool causal, int32_t rows, int32_t qtile, int64_t out[3]);
 
 inline uint64_t align_up(uint64_t x, uint64_t a = 256) { return (x + a - 1) / a * a; }
 

@@ -4,9 +4,9 @@ cqsa_plan_fwd_tile_decisions counts, per (32-query wave, 64-key tile) pair
 that a work group visits, whether the block summaries call it masked for the
 wave, clear or mixed (the inner forward and the dQ kernel, at their
 work-group heights); cqsa_plan_bwd_tile_decisions adds the dK/dV kernel's
-(32-key group, 32-query tile) decisions.  The GPU tests require the kernels'
-own counters to equal these counts.  Here the planner's counts are pinned on
-the CPU:
+(32-key group, query tile of 64 or 32 rows) decisions.  The GPU tests
+require the kernels' own counters to equal these counts.  Here the planner's
+counts are pinned on the CPU:
 
 * against the same rules applied to the oracle planner's tasks;
 * the rules are sound with respect to the paper's pair mask: every pair a
@@ -66,15 +66,17 @@ def rule_counts(tasks, causal, rows, exact_check=False):
     return tuple(out)
 
 
-def kv_rule_counts(tasks, causal, rows, exact_check=False):
-    """The dK/dV kernel's rules: key strips of `rows`, 32-key groups, 32-query
-    tiles whose summaries are those of block q // 2."""
+def kv_rule_counts(tasks, causal, rows, qtile, exact_check=False):
+    """The dK/dV kernel's rules: key strips of `rows`, 32-key groups, query
+    tiles of `qtile` rows (64 or 32) whose summaries are those of block
+    q * qtile // 64."""
+    per_block = BLOCK // qtile
     out = [0, 0, 0]
     for task in tasks:
         bits = task["bits"]
         L = len(bits)
         bor, band = oplan.block_summaries(bits, BLOCK)
-        nqt = (L + 31) // 32
+        nqt = (L + qtile - 1) // qtile
         keep = oplan.local_mask(task, causal) if exact_check else None
         for first in range(0, L, rows):
             last = min(L, first + rows) - 1
@@ -82,24 +84,25 @@ def kv_rule_counts(tasks, causal, rows, exact_check=False):
             for b in range(first // BLOCK, last // BLOCK + 1):
                 kand &= band[b]
             visited = [q for q in range(nqt)
-                       if not (causal and q * 32 + 31 < first) and (kand & band[q // 2]) == 0]
+                       if not (causal and q * qtile + qtile - 1 < first)
+                       and (kand & band[q // per_block]) == 0]
             if exact_check:
                 for q in set(range(nqt)) - set(visited):
-                    assert not keep[q * 32:q * 32 + 32, first:last + 1].any()
+                    assert not keep[q * qtile:q * qtile + qtile, first:last + 1].any()
             for k0 in range(first, last + 1, 32):
                 k1 = min(k0 + 31, L - 1)
                 wor, wand = bor[k0 // BLOCK], band[k0 // BLOCK]
                 for q in visited:
-                    q0 = 32 * q
-                    if (wand & band[q // 2]) != 0 or (causal and q0 + 31 < k0):
+                    q0 = qtile * q
+                    if (wand & band[q // per_block]) != 0 or (causal and q0 + qtile - 1 < k0):
                         v = 0
-                    elif (wor & bor[q // 2]) == 0 and (not causal or q0 >= k1):
+                    elif (wor & bor[q // per_block]) == 0 and (not causal or q0 >= k1):
                         v = 1
                     else:
                         v = 2
                     out[v] += 1
                     if exact_check:
-                        sub = keep[q0:min(q0 + 32, L), k0:k1 + 1]
+                        sub = keep[q0:min(q0 + qtile, L), k0:k1 + 1]
                         if v == 0:
                             assert not sub.any(), (q0, k0)
                         if v == 1:
@@ -117,6 +120,10 @@ def dq_rows(d):
 
 def kv_rows(d):
     return 256 if d in (96, 128) else 128
+
+
+def kv_qtile(d):
+    return 64 if d == 96 else 32
 
 
 @pytest.mark.parametrize("N,itr,causal,d", [(700, 1, False, 128), (700, 1, True, 64),
@@ -178,7 +185,7 @@ def test_undecomposed_closed_forms():
 def test_backward_rules_are_sound_and_match_the_planner(N, itr, causal, d):
     tasks = oplan.build_tasks(N, 7, itr, (0, 1, 3))
     want_q = rule_counts(tasks, causal, dq_rows(d), exact_check=True)
-    want_k = kv_rule_counts(tasks, causal, kv_rows(d), exact_check=True)
+    want_k = kv_rule_counts(tasks, causal, kv_rows(d), kv_qtile(d), exact_check=True)
     for B, H in ((1, 1), (2, 3)):
         p = cq.cqsa_plan(N, H, d, causal, 0, cq.make_opts(B=B, depth=itr, with_backward=True))
         dq, kv = p.bwd_tile_decisions()
