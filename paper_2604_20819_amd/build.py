@@ -4,6 +4,7 @@ Usage: python -m paper_2604_20819_amd.build   (or build() from Python)
 """
 import concurrent.futures
 import os
+import re
 import shutil
 import subprocess
 import sys
@@ -44,6 +45,41 @@ def _compile(src):
     if r.returncode != 0:
         raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
     return obj, r.stderr
+
+
+def device_asm(src):
+    """gfx950 assembly of one .hip source, compiled with the build's flags."""
+    path = os.path.join(CSRC, src)
+    cmd = [hipcc()] + COMMON + ["-x", "hip", "--cuda-device-only", "-S", path, "-o", "-"]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{r.stderr}")
+    return r.stdout
+
+
+def masked_spill_stores(asm):
+    """Kernels of `asm` with a register spill stored right before an exec
+    restore (s_or_b64 exec, exec, ...) in the same basic block: the store then
+    runs under the closing branch's partial exec mask, so lanes (or whole
+    waves) that skipped the branch lose the spilled value.  The compiler has
+    emitted this for a kernel at its register limit; returns {kernel: count}."""
+    out = {}
+    for m in re.finditer(r"\n(_Z\S+):[^\n]*\n(.*?)\.Lfunc_end", asm, re.S):
+        name, lines = m.group(1), m.group(2).split("\n")
+        n = 0
+        for k, line in enumerate(lines):
+            if "scratch_store" not in line:
+                continue
+            for nxt in lines[k + 1:k + 8]:
+                t = nxt.strip()
+                if not t or t.startswith(";") or t.startswith("scratch_store"):
+                    continue
+                if re.match(r"s_or_b64 exec, exec,", t):
+                    n += 1
+                break
+        if n:
+            out[name] = n
+    return out
 
 
 def build(verbose=False):
