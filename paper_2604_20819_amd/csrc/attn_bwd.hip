@@ -59,8 +59,14 @@ __global__ void __launch_bounds__(64 * dq_waves<D>(), (lds_row_elems<D>() > 128 
   constexpr int NBUF = (WAVES == 8 && DP <= 128) ? 3 : 2, AHEAD = NBUF - 1;
   constexpr int TILE_OPS = 2 * NDMA;  // this wave's loads of one tile
   static_assert(NBUF == 2 || TILE_OPS < 16, "vmcnt immediate");
-  __shared__ __attribute__((aligned(1024))) char kst[NBUF][KBYTES];
-  __shared__ __attribute__((aligned(1024))) char vst[NBUF][VBYTES];
+  // each buffer holds the K tile, then the V tile: the V rows lie a constant
+  // offset from the K rows, so their reads share address registers
+  __shared__ __attribute__((aligned(1024))) char kvst[NBUF][KBYTES + VBYTES];
+  // d = 160 and 256: the 16-byte chunk offsets of the LDS reads split into a
+  // swizzled low part and an immediate high part (below), which frees the
+  // registers that these kernels otherwise spilled; elsewhere it measured
+  // neutral or slower, so the plain offsets stay
+  constexpr bool SPLIT_OFF = D == 160 || D == 256;
   __shared__ __attribute__((aligned(16))) uint32_t kbits_s[NBUF][BN];
   __shared__ DevRun runs_s[kMaxRuns];
 
@@ -177,8 +183,8 @@ __global__ void __launch_bounds__(64 * dq_waves<D>(), (lds_row_elems<D>() > 128 
     goff[j] = uint32_t((row * rs + ((lane % CHUNKS) ^ swz(row)) * 8) * 2);
   }
   auto gload = [&](int buf, int kt, int32_t trow) {
-    char* kb = kst[buf];
-    char* vb = vst[buf];
+    char* kb = kvst[buf];
+    char* vb = kb + KBYTES;
     if (trow != kNoRow) {
       // consecutive rows from trow
       const int64_t rows = int64_t(L) - int64_t(kt) * BN;
@@ -282,8 +288,8 @@ __global__ void __launch_bounds__(64 * dq_waves<D>(), (lds_row_elems<D>() > 128 
         n_mixed += wclear ? 0u : 1u;
       }
       const bool use_bits = (qor & kor) != 0u;
-      const char* Kb = kst[buf];
-      const char* Vb = vst[buf];
+      const char* Kb = kvst[buf];
+      const char* Vb = Kb + KBYTES;
       // one 32-key block at a time: S^T, dP^T, dS^T, then its dQ^T products
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
@@ -296,7 +302,10 @@ __global__ void __launch_bounds__(64 * dq_waves<D>(), (lds_row_elems<D>() > 128 
         const int row = 32 * kb + (lane & 31);
 #pragma unroll
         for (int ks = 0; ks < DK; ++ks) {
-          const int slot = ((2 * ks + half) ^ swz(row)) << 4;
+          // 16-byte chunk 2 ks + half of the row: the swizzle changes only
+          // the chunk's low 3 bits, so ks >> 2 may be a separate 128-byte step
+          const int slot = SPLIT_OFF ? (((2 * (ks & 3) + half) ^ swz(row)) << 4) + 128 * (ks >> 2)
+                                     : ((2 * ks + half) ^ swz(row)) << 4;
           const u32x4 ka = *(const u32x4*)(Kb + row * RB + slot);
           s = mfma32<E>(bitcast_u4<vec8>(ka), qf[ks], s);
           const u32x4 va = *(const u32x4*)(Vb + row * RB + slot);
@@ -330,8 +339,13 @@ __global__ void __launch_bounds__(64 * dq_waves<D>(), (lds_row_elems<D>() > 128 
           const int trow = 32 * kb + 16 * sub + 4 * half + ((lane & 15) >> 2);
 #pragma unroll
           for (int db = 0; db < DB; ++db) {
+            // column 32 db + 16 ((lane >> 4) & 1) + 4 (lane & 3) lies in chunk
+            // 4 db + xl; as for the row reads, db >> 1 may be a 128-byte step
             const int col = 32 * db + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
-            const char* p0 = Kb + trow * RB + (((col >> 3) ^ swz(trow)) << 4) + (col & 7) * 2;
+            const int xl = 2 * ((lane >> 4) & 1) + ((lane & 3) >> 1);
+            const int tcol = SPLIT_OFF ? (((4 * (db & 1) + xl) ^ swz(trow)) << 4) + 128 * (db >> 1) + 8 * (lane & 1)
+                                       : (((col >> 3) ^ swz(trow)) << 4) + (col & 7) * 2;
+            const char* p0 = Kb + trow * RB + tcol;
             dq[db] = mfma32<E>(lds_tr_pair<E>(p0, p0 + 8 * RB), bs, dq[db]);
           }
         }
