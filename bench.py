@@ -574,9 +574,13 @@ def fwd_executed_flops(plan, D):
 def bwd_executed_flops(plan, D):
     """FLOPs the backward kernels' products execute: dQ 6 D per pair of its
     computed 32-query x 64-key wave tiles (S, dP, dQ), dK/dV 8 D per pair of
-    its computed 32-key x 32-query tiles (S, dP, dV, dK)."""
+    its computed 32-key x T-query tiles (S, dP, dV, dK; T from
+    cqsa_bwd_kv_query_tile)."""
+    import paper_2604_20819_amd as cq
+
     (_, qc, qm), (_, kc, km) = plan.bwd_tile_decisions()
-    return (qc + qm) * 32 * 64 * 6.0 * D + (kc + km) * 32 * 32 * 8.0 * D
+    t = cq.cqsa_bwd_kv_query_tile(D)
+    return (qc + qm) * 32 * 64 * 6.0 * D + (kc + km) * 32 * t * 8.0 * D
 
 
 def headline(args):

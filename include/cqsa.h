@@ -279,6 +279,10 @@ cqsa_status cqsa_plan_fwd_tile_decisions(const cqsa_plan_t* plan, int64_t* maske
  * causally, the tile starts at or after the group's last key, mixed
  * otherwise.  Summed over tasks times B x H. */
 cqsa_status cqsa_plan_bwd_tile_decisions(const cqsa_plan_t* plan, int64_t* dq, int64_t* kv);
+/* Host only: the query rows T of one dK/dV tile at head dim d (64 at d = 96,
+ * else 32; the unit of the kv counts above), or 0 for a d the kernels do not
+ * take (not a multiple of 32 in [32, 256]). */
+int32_t cqsa_bwd_kv_query_tile(int32_t d);
 void cqsa_plan_destroy(cqsa_plan_t* plan);                 /* NULL is a no-op */
 
 /* Decomposed forward (Alg. 1 computed with the max-shifted merge of App. A.1).

@@ -100,6 +100,7 @@ _SIGS = {
     "cqsa_plan_fwd_tile_decisions": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(ctypes.c_int64),
                                                     ctypes.POINTER(ctypes.c_int64),
                                                     ctypes.POINTER(ctypes.c_int64)]),
+    "cqsa_bwd_kv_query_tile": (ctypes.c_int32, [ctypes.c_int32]),
     "cqsa_plan_bwd_tile_decisions": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(ctypes.c_int64),
                                                     ctypes.POINTER(ctypes.c_int64)]),
     "cqsa_plan_destroy": (None, [ctypes.c_void_p]),
@@ -267,6 +268,11 @@ class Plan:
         dq, kv = (ctypes.c_int64 * 3)(), (ctypes.c_int64 * 3)()
         _check(lib().cqsa_plan_bwd_tile_decisions(self.handle, dq, kv), "cqsa_plan_bwd_tile_decisions")
         return tuple(dq), tuple(kv)
+
+
+def cqsa_bwd_kv_query_tile(d):
+    """Query rows of one dK/dV tile at head dim d (cqsa_bwd_kv_query_tile)."""
+    return lib().cqsa_bwd_kv_query_tile(d)
 
 
 def cqsa_plan(L, H, d, causal, device_budget_bytes=0, opts=None):

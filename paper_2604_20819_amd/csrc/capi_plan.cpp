@@ -242,6 +242,11 @@ cqsa_status cqsa_plan_fwd_tile_decisions(const cqsa_plan_t* p, int64_t* masked, 
   return CQSA_OK;
 }
 
+int32_t cqsa_bwd_kv_query_tile(int32_t d) {
+  if (d < 32 || d > 256 || d % 32 != 0) return 0;
+  return dkdv_qtile_rows(d);
+}
+
 cqsa_status cqsa_plan_bwd_tile_decisions(const cqsa_plan_t* p, int64_t* dq, int64_t* kv) {
   clear_error();
   if (!p || !dq || !kv)

@@ -200,3 +200,10 @@ def test_fp32_plans_are_not_counted():
         with pytest.raises(cq.CqsaError) as e:
             f()
         assert e.value.status == -2
+
+
+def test_kv_query_tile_rows():
+    for d in range(32, 257, 32):
+        assert cq.cqsa_bwd_kv_query_tile(d) == kv_qtile(d)
+    for d in (0, 16, 48, 100, 288, -32):
+        assert cq.cqsa_bwd_kv_query_tile(d) == 0
