@@ -318,10 +318,18 @@ __global__ void __launch_bounds__(64 * fwd_waves<D>(), (lds_row_elems<D>() > 128
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
           for (int r = 0; r < 16; ++r) s[kb][r] = 0.f;
-        // K operands read two steps ahead of their products
+        // K operands read two steps ahead of their products.  Up to d = 192
+        // the 16-byte chunk 2 ks + half is addressed as a swizzled low part
+        // (the swizzle changes only the chunk's low 3 bits) plus ks >> 2 as
+        // an immediate 128-byte step, which needs four per-lane offsets
+        // instead of eight and frees registers; at 224 and 256 (one wave per
+        // SIMD, registers to spare) that measured slower
+        constexpr bool SPLIT_OFF = D <= 192;
         auto kread = [&](int ks, int kb) {
           const int kr = 32 * kb + (lane & 31);
-          return *(const u32x4*)(Kb + kr * RB + (((2 * ks + half) ^ swz(kr)) << 4));
+          const int slot = SPLIT_OFF ? (((2 * (ks & 3) + half) ^ swz(kr)) << 4) + 128 * (ks >> 2)
+                                     : ((2 * ks + half) ^ swz(kr)) << 4;
+          return *(const u32x4*)(Kb + kr * RB + slot);
         };
         u32x4 ka[3][2];
 #pragma unroll
@@ -376,11 +384,10 @@ __global__ void __launch_bounds__(64 * fwd_waves<D>(), (lds_row_elems<D>() > 128
       // shift scales them by a power of two, undone by the final division or
       // the merge).  While some lane has no maximum yet, or when a sum exceeds
       // the bound, the tile takes the exact maximum, with its scores
-      // recomputed if the first try overwrote them.  (At d = 192 the kernel is
-      // at its register limit and always takes the exact maximum.)
+      // recomputed if the first try overwrote them.
       float psum = 0.f;
       bool kept = false;
-      if constexpr (D != 192) {
+      {
         if (__builtin_amdgcn_ballot_w64(m_run == -INFINITY) == 0ull) {
 #pragma unroll
           for (int kb = 0; kb < 2; ++kb)
@@ -437,7 +444,12 @@ __global__ void __launch_bounds__(64 * fwd_waves<D>(), (lds_row_elems<D>() > 128
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
           const int col = 32 * db + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
-          const char* p0 = Vb + row * RB + (((col >> 3) ^ swz(row)) << 4) + (col & 7) * 2;
+          // column col lies in chunk 4 db + xl: as for the K reads, db >> 1
+          // may be a separate 128-byte step
+          const int xl = 2 * ((lane >> 4) & 1) + ((lane & 3) >> 1);
+          const int vcol = D <= 192 ? (((4 * (db & 1) + xl) ^ swz(row)) << 4) + 128 * (db >> 1) + 8 * (lane & 1)
+                                    : (((col >> 3) ^ swz(row)) << 4) + (col & 7) * 2;
+          const char* p0 = Vb + row * RB + vcol;
           const vec8 va = lds_tr_pair<E>(p0, p0 + 8 * RB);
           o[db] = mfma32<E>(va, pb, o[db]);
         }
