@@ -198,7 +198,10 @@ int dkdv_qtile_rows(int d);
 // Strip orders of one task for its kernels' launch order (longest first):
 // query strips of `rows` rows (a multiple of 64) by the 64-key tiles live for
 // them, and key strips of `rows` rows (a multiple of 64) by the 32-query
-// tiles live for them, with the kernels' liveness rule (a tile is skipped
+// tiles live for them (both halves of a 64-token block share its summaries, so
+// counting the dK/dV kernel's 64-query tiles instead, at d = 96, halves the
+// counts up to the causal boundary tile and keeps the order), with the
+// kernels' liveness rule (a tile is skipped
 // when the AND of the strip's block summaries and of the tile's shares a
 // bit, or when it lies causally past the strip).  Ties keep strip order.
 std::vector<int32_t> query_strip_order(const Task& t, bool causal, int32_t rows);
